@@ -1,0 +1,168 @@
+"""Seeded synthetic inputs shaped like the paper's workloads.
+
+This module holds no arithmetic of the method: it only draws token ids and
+gradient rows, so that the GPU path and the CPU oracle are fed the very same
+arrays. The paper's corpora (1-Billion Word, Gutenberg, Tieba) are not
+available, so token streams are drawn from a bounded Zipf law, which is the
+statistic the method exploits (Sec. III: word frequency inversely
+proportional to frequency rank; U grows as a power of the token count,
+Fig. 1).
+
+Recipe
+------
+* Word ids: bounded Zipf over a frequency-ordered vocabulary,
+  p(r) proportional to r**-s for ranks r = 1..V, id = r - 1 (rank 1 is the
+  most frequent word, like "a" = word 1 in the Fig. 2 example). Drawn by
+  inverse CDF: u ~ U[0,1) from PCG64(seed), id = searchsorted(cdf, u,
+  side="right"), clipped to V - 1.
+* Gradient rows: i.i.d. N(0, std^2) fp32, generated in blocks of
+  ``ROW_BLOCK`` rows, block b from PCG64(SeedSequence([seed, b])), so the
+  result does not depend on how many threads fill it. bf16 gradients are the
+  round-to-nearest-even bf16 of those fp32 values, carried as uint16 bits.
+"""
+from __future__ import annotations
+
+import os
+from concurrent.futures import ThreadPoolExecutor
+from dataclasses import dataclass, field
+
+import numpy as np
+
+ROW_BLOCK = 16384
+
+
+def zipf_cdf(V: int, s: float) -> np.ndarray:
+    """Cumulative bounded-Zipf distribution over ranks 1..V (float64)."""
+    r = np.arange(1, V + 1, dtype=np.float64)
+    w = r ** (-float(s))
+    c = np.cumsum(w)
+    return c / c[-1]
+
+
+def zipf_ids(K: int, V: int, s: float, seed: int, dtype=np.int32) -> np.ndarray:
+    """K word ids in [0, V) drawn i.i.d. from the bounded Zipf law."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    u = rng.random(K)
+    ids = np.searchsorted(zipf_cdf(V, s), u, side="right")
+    np.minimum(ids, V - 1, out=ids)
+    return ids.astype(dtype)
+
+
+def _threads() -> int:
+    n = os.cpu_count() or 1
+    return max(1, min(16, n))
+
+
+def normal_rows(K: int, D: int, seed: int, std: float = 1.0) -> np.ndarray:
+    """K x D fp32 rows ~ N(0, std^2), block-seeded (see module docstring)."""
+    out = np.empty((K, D), dtype=np.float32)
+    nblk = (K + ROW_BLOCK - 1) // ROW_BLOCK
+
+    def fill(b: int):
+        lo, hi = b * ROW_BLOCK, min(K, (b + 1) * ROW_BLOCK)
+        rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence([seed, b])))
+        rng.standard_normal(out=out[lo:hi], dtype=np.float32)
+        if std != 1.0:
+            out[lo:hi] *= np.float32(std)
+
+    if nblk <= 1:
+        for b in range(nblk):
+            fill(b)
+    else:
+        with ThreadPoolExecutor(_threads()) as ex:
+            list(ex.map(fill, range(nblk)))
+    return out
+
+
+def bf16_bits(x: np.ndarray) -> np.ndarray:
+    """Round-to-nearest-even bf16 of fp32 values, as uint16 bit patterns."""
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    out = np.empty(x.shape, dtype=np.uint16)
+    flat_in = x.reshape(-1).view(np.uint32)
+    flat_out = out.reshape(-1)
+    step = 1 << 24
+    for lo in range(0, flat_in.size, step):
+        b = flat_in[lo:lo + step]
+        bias = ((b >> np.uint32(16)) & np.uint32(1)) + np.uint32(0x7FFF)
+        flat_out[lo:lo + step] = ((b + bias) >> np.uint32(16)).astype(np.uint16)
+    return out
+
+
+def bf16_to_f32(bits: np.ndarray) -> np.ndarray:
+    """Exact fp32 values of bf16 bit patterns."""
+    return (np.asarray(bits, dtype=np.uint16).astype(np.uint32) << np.uint32(16)).view(np.float32)
+
+
+@dataclass(frozen=True)
+class Workload:
+    """One synthetic workload. ``shards`` > 1 concatenates that many
+    independently seeded batches of K tokens (the G x K gathered index list
+    of Sec. III-A step 3, at real shape on one GPU)."""
+    name: str
+    K: int
+    V: int
+    s: float
+    D: int
+    grad_dtype: str          # "f32" or "bf16"
+    id_dtype: str            # "i32" or "i64"
+    step: str                # what follows Seg-Sum: "scatter", "sgd", "expand", "adam"
+    number: int              # seed base: ids 1000n+1, grads 1000n+2, table 1000n+3, m/v +4/+5
+    shards: int = 1
+    lr: float = 0.0
+    table_std: float = 0.02
+    adam: tuple = field(default=(0.9, 0.999, 1e-8))
+
+    @property
+    def tokens(self) -> int:
+        return self.K * self.shards
+
+    @property
+    def np_id_dtype(self):
+        return np.int64 if self.id_dtype == "i64" else np.int32
+
+    def ids(self) -> np.ndarray:
+        if self.shards == 1:
+            return zipf_ids(self.K, self.V, self.s, 1000 * self.number + 1, self.np_id_dtype)
+        return np.concatenate([self.shard_ids(g) for g in range(self.shards)])
+
+    def shard_ids(self, g: int) -> np.ndarray:
+        return zipf_ids(self.K, self.V, self.s, 1000 * self.number + 100 + g, self.np_id_dtype)
+
+    def grads_f32(self) -> np.ndarray:
+        """fp32 gradients (before any bf16 rounding), K*shards x D."""
+        if self.shards == 1:
+            return normal_rows(self.K, self.D, 1000 * self.number + 2)
+        out = np.empty((self.tokens, self.D), np.float32)
+        for g in range(self.shards):
+            out[g * self.K:(g + 1) * self.K] = normal_rows(
+                self.K, self.D, 1000 * self.number + 200 + g)
+        return out
+
+    def grads(self) -> np.ndarray:
+        """Gradients in the workload's storage dtype (bf16 as uint16 bits)."""
+        g = self.grads_f32()
+        return bf16_bits(g) if self.grad_dtype == "bf16" else g
+
+    def table(self) -> np.ndarray:
+        return normal_rows(self.V, self.D, 1000 * self.number + 3, self.table_std)
+
+
+# The five workloads: per-GPU word-LM batches (Sec. IV-B: 1-Billion Word, 100K
+# and 800K vocabularies, 512/1024-wide embeddings), the post-gather merge over
+# 64 concatenated batches (Sec. III-A step 4 at G = 64), a heavily duplicated
+# character-level vocabulary (Sec. IV-B char LM, Tieba-sized 20K), and a 2M
+# int64 vocabulary updated with Adam.
+WORKLOADS = {
+    "word_tiny_8k": Workload("word_tiny_8k", K=8192, V=100_000, s=1.0, D=512,
+                             grad_dtype="f32", id_dtype="i32", step="scatter", number=1),
+    "word_step_64k": Workload("word_step_64k", K=65536, V=800_000, s=1.0, D=1024,
+                              grad_dtype="f32", id_dtype="i32", step="sgd", number=2, lr=0.1),
+    "merge_64x32k_bf16": Workload("merge_64x32k_bf16", K=32768, V=800_000, s=1.0, D=1024,
+                                  grad_dtype="bf16", id_dtype="i32", step="expand",
+                                  number=3, shards=64),
+    "char_heavy_1m": Workload("char_heavy_1m", K=1_048_576, V=20_000, s=1.2, D=2048,
+                              grad_dtype="f32", id_dtype="i32", step="scatter", number=4),
+    "vocab2m_adam_i64": Workload("vocab2m_adam_i64", K=262_144, V=2_000_000, s=0.9, D=1024,
+                                 grad_dtype="f32", id_dtype="i64", step="adam", number=5,
+                                 lr=1e-3),
+}
