@@ -1,0 +1,256 @@
+"""Throughput of the Zipf gradient-compression hot path on one MI355X.
+
+One step = one pass of the whole path over one batch of synthetic tokens
+already resident in HBM:
+    Unique (lm_unique) -> Seg-Sum (lm_segsum) -> Fill-Values / update
+(SGD or Adam via lm_sparse_apply, SCATTER into a dense table or EXPAND into
+the merged type list via lm_fill_values, by workload). The default workload
+is the per-GPU word-LM step: K = 65,536 Zipf(1.0) token ids over an 800K
+vocabulary, 1024-wide fp32 gradients, SGD (lr 0.1) into an 800K x 1024 fp32
+table. Steps cycle through several independently seeded batches so that the
+gradient rows are not served from the 256 MB Infinity Cache.
+
+Prints one JSON line: tokens/s, ms per step, the Seg-Sum roofline (algorithmic
+bytes per launch / average launch time from HIP events on the launch stream)
+and the CPU oracle timed on a bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+import numpy as np  # noqa: E402
+
+HBM_PEAK_GBPS = 8000.0
+METRIC = "tokens/s through Unique+Seg-Sum+Fill-Values; achieved HBM GB/s vs peak"
+PMC_FILE = os.path.join(ROOT, "profiles", "segsum_pmc_{workload}.json")
+SEGSUM_SRC = os.path.join(ROOT, "paper_1810_10045_amd", "csrc", "segsum.hip")
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def segsum_source_hash() -> str:
+    with open(SEGSUM_SRC, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def segsum_bytes(K, D, U, grad_bytes):
+    """Algorithmic bytes of one Seg-Sum: read every gradient row once, write
+    every type row once, read the permutation and the offsets."""
+    return K * D * grad_bytes + U * D * 4 + K * 4 + (U + 1) * 4
+
+
+class Batch:
+    """One resident batch: ids and gradients on the device (and, for the
+    merge workload, shard 0's own ids and gradients)."""
+
+    def __init__(self, w, torch, dev):
+        self.ids = torch.from_numpy(w.ids()).to(dev)
+        g = w.grads_f32()
+        t = torch.from_numpy(g).to(dev)
+        self.grad = t.to(torch.bfloat16) if w.grad_dtype == "bf16" else t
+        del g
+        if w.step == "expand":
+            self.ids0 = self.ids[:w.K]
+            self.grad0 = self.grad[:w.K]
+
+
+def run_gpu(w, steps, warmup, nbatch, torch, lz):
+    dev = torch.device("cuda:0")
+    log(f"workload {w.name}: K={w.tokens} V={w.V} D={w.D} s={w.s} {w.grad_dtype}/{w.id_dtype} "
+        f"step={w.step}, {nbatch} resident batches")
+    t0 = time.time()
+    batches = [Batch(w.batch(b), torch, dev) for b in range(nbatch)]
+    log(f"inputs generated and copied in {time.time() - t0:.1f}s")
+    K, D = w.tokens, w.D
+    idt = torch.int64 if w.id_dtype == "i64" else torch.int32
+    ures = lz.unique_buffers(K, w.V, idt, dev)
+    ws = lz.Workspace(dev)
+    cap = ures.uniq.numel()
+    out = torch.empty((cap, D), dtype=torch.float32, device=dev)
+    dev_err = ures.dev_err
+    state = {}
+    if w.step in ("sgd", "adam", "scatter"):
+        state["table"] = torch.from_numpy(w.table()).to(dev) if w.step != "scatter" else \
+            torch.zeros((w.V, D), dtype=torch.float32, device=dev)
+    if w.step == "adam":
+        state["m"] = torch.zeros_like(state["table"])
+        state["v"] = torch.zeros_like(state["table"])
+    if w.step == "expand":
+        state["u0"] = lz.unique_buffers(w.K, w.V, idt, dev)
+        state["out0"] = torch.empty((state["u0"].uniq.numel(), D), dtype=torch.float32, device=dev)
+        state["M"] = torch.empty((cap, D), dtype=torch.float32, device=dev)
+    stream = torch.cuda.current_stream()
+
+    def step(b, ev=None):
+        bt = batches[b % nbatch]
+        if ev: ev[0].record(stream)
+        lz.unique(bt.ids, w.V, out=ures, ws=ws)
+        if ev: ev[1].record(stream)
+        lz.segsum(bt.grad, ures.perm, ures.offsets, ures.num_unique, out=out, dev_err=dev_err, ws=ws)
+        if ev: ev[2].record(stream)
+        if w.step == "sgd":
+            lz.sparse_apply(state["table"], ures.uniq, ures.num_unique, out, "sgd", lr=w.lr,
+                            dev_err=dev_err)
+        elif w.step == "adam":
+            b1, b2, eps = w.adam
+            lz.sparse_apply(state["table"], ures.uniq, ures.num_unique, out, "adam", lr=w.lr,
+                            beta1=b1, beta2=b2, eps=eps, step=1 + b, m=state["m"], v=state["v"],
+                            dev_err=dev_err)
+        elif w.step == "scatter":
+            lz.fill_values(out, ures.uniq, ures.num_unique, state["table"], None, None, "scatter",
+                           dev_err=dev_err)
+        elif w.step == "expand":
+            u0 = state["u0"]
+            lz.unique(bt.ids0, w.V, out=u0, ws=ws)
+            lz.segsum(bt.grad0, u0.perm, u0.offsets, u0.num_unique, out=state["out0"],
+                      dev_err=dev_err, ws=ws)
+            lz.fill_values(state["out0"], u0.uniq, u0.num_unique, state["M"], ures.uniq,
+                           ures.num_unique, "expand", dev_err=dev_err)
+        if ev: ev[3].record(stream)
+
+    # Types per batch (read once, outside the timed region).
+    U_of = []
+    for b in range(nbatch):
+        step(b)
+        torch.cuda.synchronize()
+        U_of.append(int(ures.num_unique.item()))
+    lz.check(dev_err)
+    log(f"types per batch: {U_of}")
+    for i in range(warmup):
+        step(i)
+    torch.cuda.synchronize()
+
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(steps)]
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record(stream)
+    for i in range(steps):
+        step(i, evs[i])
+    end.record(stream)
+    torch.cuda.synchronize()
+    lz.check(dev_err)
+    total_ms = start.elapsed_time(end)
+    st = np.array([[e[0].elapsed_time(e[1]), e[1].elapsed_time(e[2]), e[2].elapsed_time(e[3])]
+                   for e in evs])
+    gb = 2 if w.grad_dtype == "bf16" else 4
+    seg_bytes = np.mean([segsum_bytes(K, D, U_of[i % nbatch], gb) for i in range(steps)])
+    seg_ms = float(st[:, 1].mean())
+    return dict(total_ms=total_ms, stage_ms=st.mean(axis=0).tolist(), seg_ms=seg_ms,
+                seg_bytes=float(seg_bytes), U=U_of)
+
+
+def run_cpu_baseline(w, budget_s):
+    """The CPU oracle as it stands, single-threaded, on whole batches of the
+    same workload until about budget_s seconds of work are done."""
+    import oracle
+    wl = w
+    ids = wl.ids()
+    grads = wl.grads() if wl.grad_dtype == "bf16" else wl.grads_f32()
+    table = wl.table() if w.step in ("sgd", "adam") else None
+    done, t_used, toks = 0, 0.0, 0
+    while t_used < budget_s and done < 1000:
+        t0 = time.perf_counter()
+        uniq, counts, offsets, inverse, perm = oracle.unique(ids, w.V)
+        red = oracle.segsum(grads, inverse, len(uniq))
+        if w.step == "sgd":
+            oracle.sgd(table[uniq], red, w.lr)
+        elif w.step == "adam":
+            z = np.zeros((len(uniq), w.D))
+            oracle.adam(table[uniq], z, z, red, w.lr, *w.adam, 0.0, 1)
+        elif w.step == "scatter":
+            oracle.scatter(red, uniq, np.zeros((w.V, w.D)))
+        t_used += time.perf_counter() - t0
+        done += 1
+        toks += len(ids)
+    return dict(value=toks / t_used, unit="tokens/s", cores=1, kind="oracle",
+                sample=f"{done} whole {w.name} batch(es) of {len(ids)} tokens, "
+                       f"unique+segsum+{w.step}, fp64, 1 thread, {t_used:.1f}s")
+
+
+def load_traffic(workload, launches_bytes):
+    """HBM bytes per Seg-Sum launch from committed rocprofv3 counter runs,
+    only while segsum.hip is unchanged since they were taken."""
+    path = PMC_FILE.format(workload=workload)
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        rec = json.load(f)
+    if rec.get("segsum_source_sha256_16") != segsum_source_hash():
+        return None
+    return rec.get("hbm_bytes_per_launch")
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--workload", default="word_step_64k")
+    ap.add_argument("--batches", type=int, default=0, help="resident batches (0: auto)")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle leg")
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU: the multi-GPU collectives of the method are not part "
+              "of this build (run with --gpus 1)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_1810_10045_amd import lmzipf as lz
+    from paper_1810_10045_amd import synth
+
+    w = synth.WORKLOADS[args.workload]
+    gb = 2 if w.grad_dtype == "bf16" else 4
+    batch_bytes = w.tokens * w.D * gb
+    nbatch = args.batches or max(1, min(8, math.ceil((2 << 30) / batch_bytes)))
+    r = run_gpu(w, args.steps, args.warmup, nbatch, torch, lz)
+    ms = r["total_ms"] / args.steps
+    tokens_per_s = w.tokens / (ms / 1e3)
+    achieved = r["seg_bytes"] / (r["seg_ms"] / 1e3) / 1e9
+    rank = int(os.environ.get("RANK", "0"))
+    cpu = None
+    if not args.no_cpu and rank == 0:
+        cpu = run_cpu_baseline(w, args.cpu_seconds)
+    traffic = load_traffic(w.name, r["seg_bytes"])
+    line = {
+        "metric": METRIC,
+        "value": tokens_per_s,
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32" if w.grad_dtype == "f32" else "bf16->f32",
+        "data": "synthetic",
+        "config": {"workload": w.name, "tokens": w.tokens, "V": w.V, "D": w.D, "zipf_s": w.s,
+                   "ids": w.id_dtype, "grad": w.grad_dtype, "after_segsum": w.step,
+                   "resident_batches": nbatch, "types_per_batch": r["U"]},
+        "stages_ms": {"unique": r["stage_ms"][0], "segsum": r["stage_ms"][1],
+                      w.step: r["stage_ms"][2]},
+        "roofline": {"bound": "hbm", "kernel": "lm_segsum (k_segsum + k_segsum_fix)",
+                     "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK_GBPS,
+                     "bytes_per_launch": r["seg_bytes"], "avg_launch_ms": r["seg_ms"],
+                     "traffic": traffic},
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

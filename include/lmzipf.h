@@ -122,8 +122,8 @@ int lm_workspace_clear(void* ws, size_t bytes, void* stream);
  *            LM_UNIQUE_CTRL_BYTES bytes must be zero before the first call
  *            (lm_workspace_clear, or a zero-filled allocation); every
  *            lm_unique leaves them zero when its kernels finish, so a
- *            workspace is reused without clearing. Other calls may use the
- *            rest of the same buffer between lm_unique calls.
+ *            workspace is reused without clearing. No other entry point
+ *            touches those bytes, so one buffer can serve every call.
  * ------------------------------------------------------------------------ */
 #define LM_UNIQUE_CTRL_BYTES ((size_t)8192)
 size_t lm_unique_workspace_bytes(int64_t K, int32_t idtype, int64_t V);
@@ -148,7 +148,8 @@ int lm_unique(const void* ids, int32_t idtype, int64_t K, int64_t V,
  * out        device, u_cap x D fp32, row stride ld_out; rows >= U untouched.
  * dev_err    device int32, zeroed by the caller.
  * ws         device workspace of lm_segsum_workspace_bytes(K, D) bytes,
- *            256-byte aligned; no initial contents are required.
+ *            256-byte aligned; no initial contents are required. Its first
+ *            LM_UNIQUE_CTRL_BYTES bytes are left untouched.
  * ------------------------------------------------------------------------ */
 size_t lm_segsum_workspace_bytes(int64_t K, int64_t D);
 int lm_segsum(const void* grad, int32_t gtype, int64_t K, int64_t D,
@@ -165,14 +166,14 @@ int lm_segsum(const void* grad, int32_t gtype, int64_t K, int64_t D,
  * then -1).
  *
  * sub_ids    device, *n_sub ids (capacity sub_cap) of dtype `idtype`.
- * sup_ids    device, *n_sup ids of the same dtype.
- * n_sub, n_sup  device int64 counts; n_sub may exceed sub_cap only by error
- *            (LM_DEVERR_CAPACITY).
+ * sup_ids    device, *n_sup ids (capacity sup_cap) of the same dtype.
+ * n_sub, n_sup  device int64 counts; a count above its capacity sets
+ *            LM_DEVERR_CAPACITY and is clamped to it.
  * map        device, sub_cap int32.
  * ------------------------------------------------------------------------ */
 int lm_map_ids(const void* sub_ids, const int64_t* n_sub, int64_t sub_cap,
-               const void* sup_ids, const int64_t* n_sup, int32_t idtype,
-               int32_t* map, int32_t* dev_err, void* stream);
+               const void* sup_ids, const int64_t* n_sup, int64_t sup_cap,
+               int32_t idtype, int32_t* map, int32_t* dev_err, void* stream);
 
 /* ------------------------------------------------------------------------
  * Fill-Values — Sec. III-A step 5: move reduced rows into the row space of
@@ -192,10 +193,12 @@ int lm_map_ids(const void* sub_ids, const int64_t* n_sub, int64_t sub_cap,
  * paragraph: unique indices leave no write conflicts).
  *
  * src        device, src_cap x D fp32, row stride ld_src.
- * src_ids    device, *n_src ids of dtype `idtype`.
+ * src_ids    device, at least src_cap ids of dtype `idtype`; the first
+ *            *n_src are used.
  * n_src      device int64 (<= src_cap).
- * dst_ids    device, *n_dst ids of dtype `idtype`, or NULL (SCATTER modes
- *            only: row = id, which must be < dst_rows).
+ * dst_ids    device, at least dst_rows ids of dtype `idtype`, the first
+ *            *n_dst used, or NULL (SCATTER modes only: row = id, which must
+ *            be < dst_rows).
  * n_dst      device int64 (<= dst_rows); ignored when dst_ids is NULL.
  * dst        device, dst_rows x D fp32, row stride ld_dst.
  * A source id missing from dst_ids sets LM_DEVERR_NOT_FOUND; an id

@@ -1,0 +1,232 @@
+// Device-side building blocks shared by the lmzipf kernels (gfx950, wave64).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/lmzipf.h"
+
+namespace lmz {
+
+constexpr int kWave = 64;
+
+// ---------------------------------------------------------------------------
+// Wave-level primitives
+// ---------------------------------------------------------------------------
+
+__device__ __forceinline__ int lane_id() {
+  return __builtin_amdgcn_mbcnt_hi(~0u, __builtin_amdgcn_mbcnt_lo(~0u, 0u));
+}
+
+// Number of set bits of `mask` in lanes below this one.
+__device__ __forceinline__ int popc_below(uint64_t mask) {
+  return __builtin_amdgcn_mbcnt_hi(static_cast<uint32_t>(mask >> 32),
+                                   __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(mask), 0u));
+}
+
+__device__ __forceinline__ uint64_t ballot(bool p) { return __ballot(p); }
+
+__device__ __forceinline__ int read_lane(int v, int lane) {
+  return __builtin_amdgcn_readlane(v, lane);
+}
+
+__device__ __forceinline__ int first_lane(int v) { return __builtin_amdgcn_readfirstlane(v); }
+
+// Inclusive prefix sum over the 64 lanes of a wave.
+template <typename T>
+__device__ __forceinline__ T wave_incl_sum(T v) {
+  const int lane = lane_id();
+#pragma unroll
+  for (int off = 1; off < kWave; off <<= 1) {
+    T t = __shfl_up(v, off, kWave);
+    if (lane >= off) v += t;
+  }
+  return v;
+}
+
+// Inclusive prefix maximum over the 64 lanes of a wave.
+__device__ __forceinline__ int wave_incl_max(int v) {
+  const int lane = lane_id();
+#pragma unroll
+  for (int off = 1; off < kWave; off <<= 1) {
+    int t = __shfl_up(v, off, kWave);
+    if (lane >= off && t > v) v = t;
+  }
+  return v;
+}
+
+// Exclusive prefix sum over a 256-thread block (4 waves). `lds` holds 4
+// entries. Returns this thread's exclusive prefix; `total` gets the block sum.
+template <typename T>
+__device__ __forceinline__ T block256_excl_sum(T v, T* lds, T& total) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  T incl = wave_incl_sum(v);
+  if (lane == 63) lds[wave] = incl;
+  __syncthreads();
+  T w0 = lds[0], w1 = lds[1], w2 = lds[2], w3 = lds[3];
+  __syncthreads();
+  T before = (wave > 0 ? w0 : T(0)) + (wave > 1 ? w1 : T(0)) + (wave > 2 ? w2 : T(0));
+  total = w0 + w1 + w2 + w3;
+  return before + incl - v;
+}
+
+// Exclusive prefix maximum over a 256-thread block (-1 for thread 0).
+__device__ __forceinline__ int block256_excl_max(int v, int* lds, int& total) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  int incl = wave_incl_max(v);
+  int prev = __shfl_up(incl, 1, kWave);
+  if (lane == 0) prev = -1;
+  if (lane == 63) lds[wave] = incl;
+  __syncthreads();
+  int w[4] = {lds[0], lds[1], lds[2], lds[3]};
+  __syncthreads();
+  int before = -1;
+  for (int i = 0; i < wave; ++i) before = w[i] > before ? w[i] : before;
+  total = w[0];
+  for (int i = 1; i < 4; ++i) total = w[i] > total ? w[i] : total;
+  return prev > before ? prev : before;
+}
+
+// ---------------------------------------------------------------------------
+// Inter-workgroup communication. The 8 XCDs of an MI355X each have their own
+// L2, so every flag another workgroup polls is accessed with agent-scope
+// atomics (the compiler then bypasses the non-coherent caches).
+// ---------------------------------------------------------------------------
+
+template <typename T>
+__device__ __forceinline__ T ld_agent(const T* p) {
+  return __hip_atomic_load(const_cast<T*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+template <typename T>
+__device__ __forceinline__ void st_agent(T* p, T v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+template <typename T>
+__device__ __forceinline__ T add_agent(T* p, T v) {
+  return __hip_atomic_fetch_add(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+__device__ __forceinline__ void raise_err(int32_t* dev_err, int bit) {
+  if (dev_err) __hip_atomic_fetch_or(dev_err, bit, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Upper bound on polls of another workgroup's status word before giving up
+// with LM_DEVERR_SPIN (every legitimate wait ends within microseconds).
+constexpr uint32_t kSpinLimit = 1u << 20;
+
+// ---------------------------------------------------------------------------
+// Row loads: VEC consecutive gradient values as fp32.
+// ---------------------------------------------------------------------------
+
+struct bf16_t {
+  uint16_t bits;
+};
+
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ float bf16_to_f32(uint32_t bits16) {
+  return __uint_as_float(bits16 << 16);
+}
+
+template <typename GT, int VEC>
+struct RowVec;
+
+template <>
+struct RowVec<float, 4> {
+  using raw_t = f32x4;
+  static __device__ __forceinline__ raw_t load(const float* p) {
+    return __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(p));
+  }
+  static __device__ __forceinline__ void add(float* acc, const raw_t& r) {
+    acc[0] += r.x; acc[1] += r.y; acc[2] += r.z; acc[3] += r.w;
+  }
+};
+
+template <>
+struct RowVec<float, 1> {
+  using raw_t = float;
+  static __device__ __forceinline__ raw_t load(const float* p) { return __builtin_nontemporal_load(p); }
+  static __device__ __forceinline__ void add(float* acc, const raw_t& r) { acc[0] += r; }
+};
+
+template <>
+struct RowVec<bf16_t, 8> {
+  using raw_t = u32x4;
+  static __device__ __forceinline__ raw_t load(const bf16_t* p) {
+    return __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
+  }
+  static __device__ __forceinline__ void add(float* acc, const raw_t& r) {
+    const uint32_t w[4] = {r.x, r.y, r.z, r.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      acc[2 * i] += __uint_as_float(w[i] << 16);
+      acc[2 * i + 1] += __uint_as_float(w[i] & 0xffff0000u);
+    }
+  }
+};
+
+template <>
+struct RowVec<bf16_t, 1> {
+  using raw_t = uint32_t;
+  static __device__ __forceinline__ raw_t load(const bf16_t* p) {
+    return static_cast<uint32_t>(__builtin_nontemporal_load(&p->bits));
+  }
+  static __device__ __forceinline__ void add(float* acc, const raw_t& r) {
+    acc[0] += bf16_to_f32(r);
+  }
+};
+
+// Store VEC fp32 values (16-byte stores when VEC is a multiple of 4).
+template <int VEC>
+__device__ __forceinline__ void store_vec(float* p, const float* v) {
+  if constexpr (VEC % 4 == 0) {
+#pragma unroll
+    for (int i = 0; i < VEC; i += 4)
+      *reinterpret_cast<float4*>(p + i) = make_float4(v[i], v[i + 1], v[i + 2], v[i + 3]);
+  } else {
+#pragma unroll
+    for (int i = 0; i < VEC; ++i) p[i] = v[i];
+  }
+}
+
+template <int VEC>
+__device__ __forceinline__ void load_vec(const float* p, float* v) {
+  if constexpr (VEC % 4 == 0) {
+#pragma unroll
+    for (int i = 0; i < VEC; i += 4) {
+      float4 t = *reinterpret_cast<const float4*>(p + i);
+      v[i] = t.x; v[i + 1] = t.y; v[i + 2] = t.z; v[i + 3] = t.w;
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < VEC; ++i) v[i] = p[i];
+  }
+}
+
+// Widen a word index of dtype KeyT to int64 / its raw unsigned bits.
+template <typename KeyT>
+__device__ __forceinline__ uint64_t key_bits(KeyT k) {
+  if constexpr (sizeof(KeyT) == 4) return static_cast<uint32_t>(k);
+  else return static_cast<uint64_t>(k);
+}
+
+// First index in [0, n) with a[i] >= x (n if none), over an ascending list.
+template <typename KeyT>
+__device__ __forceinline__ int64_t lower_bound_dev(const KeyT* a, int64_t n, KeyT x) {
+  int64_t lo = 0, hi = n;
+  while (lo < hi) {
+    int64_t mid = lo + ((hi - lo) >> 1);
+    if (a[mid] < x) lo = mid + 1; else hi = mid;
+  }
+  return lo;
+}
+
+}  // namespace lmz
+
+// Host-side launch helpers (defined in lmzipf_api.hip).
+namespace lmz {
+int launch_status(hipError_t e);
+}

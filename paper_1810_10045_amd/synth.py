@@ -24,6 +24,7 @@ from __future__ import annotations
 
 import os
 from concurrent.futures import ThreadPoolExecutor
+import dataclasses
 from dataclasses import dataclass, field
 
 import numpy as np
@@ -115,6 +116,13 @@ class Workload:
     @property
     def tokens(self) -> int:
         return self.K * self.shards
+
+    def batch(self, b: int) -> "Workload":
+        """The b-th independent batch of this workload (b = 0 is the
+        workload itself): every seed moves by 1,000,000 * b."""
+        if b == 0:
+            return self
+        return dataclasses.replace(self, number=self.number + 1000 * b)
 
     @property
     def np_id_dtype(self):

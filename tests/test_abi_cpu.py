@@ -1,0 +1,108 @@
+"""Host-side checks of the C-ABI library (CPU only): it loads, exports every
+entry point the header declares, and rejects bad arguments before any HIP
+call is made (so these run without a GPU)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "lmzipf.h")
+LIB = os.path.join(ROOT, "paper_1810_10045_amd", "liblmzipf.so")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(lm_[a-z_]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(LIB):
+        from paper_1810_10045_amd import build
+        build.build()
+    return ctypes.CDLL(LIB)
+
+
+def test_header_declares_the_boundary():
+    names = declared_functions()
+    for n in ("lm_unique", "lm_segsum", "lm_fill_values", "lm_sparse_apply", "lm_map_ids",
+              "lm_unique_workspace_bytes", "lm_segsum_workspace_bytes", "lm_status_string"):
+        assert n in names
+
+
+def test_library_exports_every_declared_symbol(lib):
+    for n in declared_functions():
+        assert hasattr(lib, n), f"{n} declared in include/lmzipf.h but not exported"
+
+
+def test_binding_names_match_the_header():
+    src = open(os.path.join(ROOT, "paper_1810_10045_amd", "lmzipf.py")).read()
+    for n in declared_functions():
+        assert f'"{n}"' in src, n
+    for n in ("unique", "segsum", "map_ids", "fill_values", "sparse_apply"):
+        assert re.search(rf"^def {n}\(", src, re.M), n
+
+
+def test_status_strings(lib):
+    lib.lm_status_string.restype = ctypes.c_char_p
+    for code in (0, 1, 3, 4, 5, 99):
+        assert lib.lm_status_string(code)
+    assert lib.lm_abi_version() == 100
+
+
+def test_workspace_queries(lib):
+    lib.lm_unique_workspace_bytes.restype = ctypes.c_size_t
+    lib.lm_unique_workspace_bytes.argtypes = [ctypes.c_int64, ctypes.c_int32, ctypes.c_int64]
+    lib.lm_segsum_workspace_bytes.restype = ctypes.c_size_t
+    lib.lm_segsum_workspace_bytes.argtypes = [ctypes.c_int64, ctypes.c_int64]
+    assert lib.lm_unique_workspace_bytes(65536, 0, 800000) >= 8192 + 65536 * 16
+    assert lib.lm_unique_workspace_bytes(65536, 1, 800000) > lib.lm_unique_workspace_bytes(65536, 0, 800000)
+    assert lib.lm_unique_workspace_bytes(-1, 0, 10) == 0
+    assert lib.lm_unique_workspace_bytes(10, 7, 10) == 0
+    assert lib.lm_unique_workspace_bytes(1 << 30, 0, 10) == 0
+    assert lib.lm_segsum_workspace_bytes(65536, 1024) >= 8192
+    assert lib.lm_segsum_workspace_bytes(-1, 4) == 0
+
+
+def _v(x=0x1000):
+    return ctypes.c_void_p(x)
+
+
+def test_argument_errors_return_before_any_launch(lib):
+    P, I64, I32, SZ = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_size_t
+    lib.lm_unique.argtypes = [P, I32, I64, I64, P, P, P, P, P, P, P, P, SZ, P]
+    # unknown id dtype, negative K, V < 1, K too large, NULL workspace, misaligned workspace
+    assert lib.lm_unique(_v(), 7, 10, 10, *([_v()] * 7), _v(), 1 << 20, None) == 5
+    assert lib.lm_unique(_v(), 0, -1, 10, *([_v()] * 7), _v(), 1 << 20, None) == 1
+    assert lib.lm_unique(_v(), 0, 10, 0, *([_v()] * 7), _v(), 1 << 20, None) == 1
+    assert lib.lm_unique(_v(), 0, 1 << 30, 10, *([_v()] * 7), _v(), 1 << 40, None) == 5
+    assert lib.lm_unique(_v(), 0, 10, 10, *([_v()] * 7), None, 1 << 20, None) == 1
+    assert lib.lm_unique(_v(), 0, 10, 10, *([_v()] * 7), _v(0x1010), 1 << 20, None) == 1
+    assert lib.lm_unique(_v(), 0, 10, 10, *([_v()] * 7), _v(), 16, None) == 3
+    lib.lm_segsum.argtypes = [P, I32, I64, I64, I64, P, P, P, I64, P, I64, P, P, SZ, P]
+    assert lib.lm_segsum(_v(), 2, 10, 4, 4, _v(), _v(), _v(), 10, _v(), 4, _v(), _v(), 1 << 20, None) == 5
+    assert lib.lm_segsum(_v(), 0, 10, 4, 3, _v(), _v(), _v(), 10, _v(), 4, _v(), _v(), 1 << 20, None) == 1
+    assert lib.lm_segsum(_v(), 0, 10, 4, 4, _v(), _v(), _v(), 10, _v(), 2, _v(), _v(), 1 << 20, None) == 1
+    assert lib.lm_segsum(None, 0, 10, 4, 4, _v(), _v(), _v(), 10, _v(), 4, _v(), _v(), 1 << 20, None) == 1
+    assert lib.lm_segsum(_v(), 0, 10, 4, 4, _v(), _v(), _v(), 10, _v(), 4, _v(), _v(), 8, None) == 3
+    lib.lm_fill_values.argtypes = [P, I64, P, P, I64, P, P, I32, I64, P, I64, I64, I32, P, P]
+    assert lib.lm_fill_values(_v(), 4, _v(), _v(), 10, _v(), _v(), 0, 4, _v(), 10, 4, 9, _v(), None) == 5
+    assert lib.lm_fill_values(_v(), 4, _v(), _v(), 10, None, None, 0, 4, _v(), 10, 4, 0, _v(), None) == 1
+    assert lib.lm_fill_values(_v(), 2, _v(), _v(), 10, _v(), _v(), 0, 4, _v(), 10, 4, 0, _v(), None) == 1
+    lib.lm_sparse_apply.argtypes = [P, I64, I64, I64, P, I32, P, I64, P, I64, I32] + \
+        [ctypes.c_float] * 5 + [I64, P, P, P, P]
+    assert lib.lm_sparse_apply(_v(), 10, 4, 4, _v(), 0, _v(), 5, _v(), 4, 3, 0.1, 0.9, 0.999, 1e-8, 0.0, 1,
+                               None, None, _v(), None) == 5
+    assert lib.lm_sparse_apply(_v(), 10, 4, 4, _v(), 0, _v(), 5, _v(), 4, 1, 0.1, 0.9, 0.999, 1e-8, 0.0, 0,
+                               _v(), _v(), _v(), None) == 1
+    assert lib.lm_sparse_apply(_v(), 10, 4, 4, _v(), 0, _v(), 5, _v(), 4, 1, 0.1, 0.9, 0.999, 1e-8, 0.0, 1,
+                               None, None, _v(), None) == 1
+    assert lib.lm_sparse_apply(_v(), 10, 4, 4, _v(), 0, _v(), 5, _v(), 4, 1, 0.1, 1.5, 0.999, 1e-8, 0.0, 1,
+                               _v(), _v(), _v(), None) == 1
+    lib.lm_map_ids.argtypes = [P, P, I64, P, P, I64, I32, P, P, P]
+    assert lib.lm_map_ids(_v(), _v(), 4, _v(), _v(), 4, 3, _v(), _v(), None) == 5
+    assert lib.lm_map_ids(None, _v(), 4, _v(), _v(), 4, 0, _v(), _v(), None) == 1
+    assert lib.lm_map_ids(_v(), _v(), 4, _v(), _v(), -1, 0, _v(), _v(), None) == 1

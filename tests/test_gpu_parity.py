@@ -1,0 +1,394 @@
+"""GPU parity: every entry point of liblmzipf.so against the CPU oracle on the
+same seeded inputs, at sizes that span several tiles/chunks plus ragged
+tails, and on the edge cases of the method. Integer outputs bit-exact; fp32
+sums within the per-row tolerance of gpu_helpers."""
+import itertools
+import os
+import sys
+
+import numpy as np
+import pytest
+
+sys.path.insert(0, os.path.dirname(os.path.abspath(__file__)))
+import gpu_helpers as H  # noqa: E402
+import oracle  # noqa: E402
+from paper_1810_10045_amd import synth  # noqa: E402
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+
+@pytest.fixture(scope="module")
+def lz():
+    from paper_1810_10045_amd import lmzipf
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    return lmzipf
+
+
+DEV = "cuda"
+
+
+def _t(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).to(DEV)
+
+
+def _say(msg):
+    print(msg, flush=True)
+
+
+# ---------------------------------------------------------------------------
+# Unique
+# ---------------------------------------------------------------------------
+
+def test_unique_worked_example(lz):
+    for J in ([0, 1, 2, 3, 0, 1], [17, 5, 42, 9, 17, 5]):
+        ids = np.array(J, np.int32)
+        res = lz.unique(_t(ids), 100)
+        torch.cuda.synchronize()
+        lz.check(res.dev_err)
+        o = H.assert_unique_matches(res, ids, 100, oracle, f"J={J}")
+        assert len(o[0]) == 4 and int(o[1].sum()) == 6
+
+
+def test_unique_brute_force(lz):
+    """Every J in [0, V)^K for V <= 4, K <= 6 (bit-exact against the oracle)."""
+    cases = []
+    for V, Kmax in ((1, 4), (2, 5), (3, 5), (4, 6)):
+        for K in range(0, Kmax + 1):
+            for J in itertools.product(range(V), repeat=K):
+                ids = np.array(J, np.int32)
+                cases.append((ids, V, lz.unique(_t(ids), V)))
+    torch.cuda.synchronize()
+    _say(f"brute force: {len(cases)} cases")
+    for ids, V, res in cases:
+        lz.check(res.dev_err)
+        H.assert_unique_matches(res, ids, V, oracle, f"J={ids.tolist()} V={V}")
+
+
+UNIQUE_CASES = [
+    # (K, V, s, id dtype, seed)
+    (1, 10, 1.0, np.int32, 1), (63, 100, 1.0, np.int32, 2), (64, 100, 1.0, np.int32, 3),
+    (65, 7, 1.0, np.int32, 4), (255, 1000, 1.0, np.int32, 5), (257, 1, 1.0, np.int32, 6),
+    (4095, 2, 1.0, np.int32, 7), (4096, 100_000, 1.0, np.int32, 8),
+    (4097, 100_000, 1.0, np.int32, 9), (8205, 100_000, 1.0, np.int32, 10),
+    (65536, 800_000, 1.0, np.int32, 11), (100_003, 20_000, 1.2, np.int32, 12),
+    (262_144 + 77, 2_000_000, 0.9, np.int64, 13), (50_000, 2**31 - 1, 0.8, np.int32, 14),
+    (30_001, 2**40, 0.9, np.int64, 15), (12_345, 256, 0.5, np.int32, 16),
+    (20_000, 257, 1.0, np.int64, 17),
+    # heads on the first item of a thread, tails several threads later (the
+    # case a compiler miscompile of the dedup scan once got wrong)
+    (4096, 50, 1.0, np.int32, 3), (5000, 30, 1.0, np.int32, 8),
+]
+
+
+@pytest.mark.parametrize("K,V,s,dt,seed", UNIQUE_CASES,
+                         ids=[f"K{c[0]}-V{c[1]}-{c[3].__name__}" for c in UNIQUE_CASES])
+def test_unique_random(lz, K, V, s, dt, seed):
+    ids = synth.zipf_ids(K, min(V, 4_000_000), s, seed, dt)
+    if V > 4_000_000:
+        # spread the ranks over the whole id range (and above 2^32 for int64)
+        ids = (ids.astype(np.int64) * (V // 4_000_000) + (V - 4_000_000 * (V // 4_000_000))).astype(dt)
+        assert ids.max() < V
+    _say(f"unique K={K} V={V} dtype={dt.__name__}")
+    res = lz.unique(_t(ids), V)
+    torch.cuda.synchronize()
+    lz.check(res.dev_err)
+    H.assert_unique_matches(res, ids, V, oracle, f"K={K} V={V}")
+
+
+def test_unique_all_same_and_all_distinct(lz):
+    K = 9000
+    same = np.full(K, 4242, np.int32)
+    res = lz.unique(_t(same), 5000)
+    perm_ids = np.random.Generator(np.random.PCG64(5)).permutation(K).astype(np.int32)
+    res2 = lz.unique(_t(perm_ids), K)
+    top = np.full(K, 4999, np.int32)  # every id is V - 1
+    res3 = lz.unique(_t(top), 5000)
+    torch.cuda.synchronize()
+    for r, ids, V in ((res, same, 5000), (res2, perm_ids, K), (res3, top, 5000)):
+        lz.check(r.dev_err)
+        H.assert_unique_matches(r, ids, V, oracle)
+
+
+def test_unique_empty(lz):
+    res = lz.unique(torch.zeros(0, dtype=torch.int32, device=DEV), 10)
+    torch.cuda.synchronize()
+    assert int(res.num_unique.item()) == 0 and int(res.offsets[0].item()) == 0
+
+
+def test_unique_out_of_range_sets_error(lz):
+    ids = np.array([1, 2, 99, 3], np.int32)
+    res = lz.unique(_t(ids), 10)
+    torch.cuda.synchronize()
+    assert int(res.dev_err.item()) & lz.DEVERR_ID_RANGE
+    ids = np.array([1, -4, 3], np.int64)
+    res = lz.unique(_t(ids), 10)
+    torch.cuda.synchronize()
+    assert int(res.dev_err.item()) & lz.DEVERR_ID_RANGE
+
+
+def test_unique_workspace_reuse_and_determinism(lz):
+    """The control block is left zero: back-to-back calls on one workspace,
+    with different sizes, stay exact."""
+    ws = lz.Workspace(DEV)
+    outs = []
+    for K, V, seed in ((70_000, 800_000, 21), (5000, 30, 22), (70_000, 800_000, 21), (1, 3, 23)):
+        ids = synth.zipf_ids(K, V, 1.0, seed, np.int32)
+        outs.append((ids, V, lz.unique(_t(ids), V, ws=ws)))
+    torch.cuda.synchronize()
+    for ids, V, r in outs:
+        lz.check(r.dev_err)
+        H.assert_unique_matches(r, ids, V, oracle)
+    assert torch.equal(outs[0][2].perm, outs[2][2].perm)
+    assert int(ws.buf[:lz.UNIQUE_CTRL_BYTES].count_nonzero().item()) == 0
+
+
+# ---------------------------------------------------------------------------
+# Seg-Sum
+# ---------------------------------------------------------------------------
+
+SEG_CASES = [
+    # (K, V, s, D, grad dtype, seed)
+    (1, 5, 1.0, 16, "f32", 31), (6, 4, 1.0, 3, "f32", 32), (257, 30, 1.0, 1, "f32", 33),
+    (1000, 50, 1.0, 17, "f32", 34), (5000, 100, 1.2, 64, "f32", 35),
+    (20_000, 300, 1.2, 96, "f32", 36), (20_000, 300, 1.2, 1100, "f32", 37),
+    (40_000, 2000, 1.0, 512, "f32", 38), (65_536, 800_000, 1.0, 1024, "f32", 39),
+    (150_000, 20_000, 1.2, 256, "f32", 40), (30_000, 5000, 1.0, 2048, "f32", 41),
+    (3000, 100, 1.0, 4096, "f32", 42),
+    (5000, 100, 1.2, 64, "bf16", 43), (20_000, 300, 1.2, 1024, "bf16", 44),
+    (70_000, 800_000, 1.0, 1024, "bf16", 45), (9000, 500, 1.0, 100, "bf16", 46),
+    (2000, 50, 1.0, 7, "bf16", 47),
+]
+
+
+def _segsum_case(lz, K, V, s, D, gdt, seed, ws=None):
+    ids = synth.zipf_ids(K, V, s, seed, np.int32)
+    g32 = synth.normal_rows(K, D, seed + 1000)
+    grad = synth.bf16_bits(g32) if gdt == "bf16" else g32
+    tgrad = _t(g32).to(torch.bfloat16) if gdt == "bf16" else _t(g32)
+    if gdt == "bf16":  # torch's fp32->bf16 is round-to-nearest-even, like the generator
+        assert np.array_equal(tgrad.view(torch.int16).cpu().numpy().view(np.uint16), grad)
+    res = lz.unique(_t(ids), V, ws=ws)
+    out = lz.segsum(tgrad, res.perm, res.offsets, res.num_unique, dev_err=res.dev_err, ws=ws)
+    return ids, grad, res, out
+
+
+@pytest.mark.parametrize("K,V,s,D,gdt,seed", SEG_CASES,
+                         ids=[f"K{c[0]}-V{c[1]}-D{c[3]}-{c[4]}" for c in SEG_CASES])
+def test_segsum_random(lz, K, V, s, D, gdt, seed):
+    _say(f"segsum K={K} V={V} D={D} {gdt}")
+    ids, grad, res, out = _segsum_case(lz, K, V, s, D, gdt, seed)
+    torch.cuda.synchronize()
+    lz.check(res.dev_err)
+    o = H.assert_unique_matches(res, ids, V, oracle)
+    U = len(o[0])
+    ref = oracle.segsum(grad, o[3], U)
+    got = out[:U].double().cpu().numpy()
+    err = H.row_rel_err(got, ref, H.sum_of_squares(grad, o[3], U, oracle))
+    tol = H.TOL_BF16 if gdt == "bf16" else H.TOL_F32
+    _say(f"  U={U} max row-relative error {err:.3e} (tol {tol})")
+    assert err <= tol
+    ones = o[1] == 1
+    assert np.array_equal(got[ones], ref[ones]), "count-1 rows must be exact copies"
+
+
+def test_segsum_deterministic(lz):
+    a = _segsum_case(lz, 60_000, 500, 1.2, 1024, "f32", 51)[3].clone()
+    b = _segsum_case(lz, 60_000, 500, 1.2, 1024, "f32", 51)[3]
+    torch.cuda.synchronize()
+    assert torch.equal(a, b)
+
+
+def test_segsum_special_rows(lz):
+    """One type: the column sum; every id distinct: the permuted rows."""
+    K, D = 30_000, 160
+    g = synth.normal_rows(K, D, 61)
+    same = np.full(K, 3, np.int32)
+    r1 = lz.unique(_t(same), 10)
+    o1 = lz.segsum(_t(g), r1.perm, r1.offsets, r1.num_unique, dev_err=r1.dev_err)
+    dist = np.random.Generator(np.random.PCG64(62)).permutation(K).astype(np.int32)
+    r2 = lz.unique(_t(dist), K)
+    o2 = lz.segsum(_t(g), r2.perm, r2.offsets, r2.num_unique, dev_err=r2.dev_err)
+    torch.cuda.synchronize()
+    lz.check(r1.dev_err)
+    lz.check(r2.dev_err)
+    colsum = g.astype(np.float64).sum(0, keepdims=True)
+    assert H.row_rel_err(o1[:1].double().cpu().numpy(), colsum) <= H.TOL_F32
+    assert np.array_equal(o2[:K].cpu().numpy(), g[np.argsort(dist)])
+
+
+def test_segsum_strided_and_capacity(lz):
+    """Row strides larger than D (a column slice of a wider matrix), the
+    scalar path (unaligned stride), and u_cap below U."""
+    K, V, D = 9000, 700, 40
+    ids = synth.zipf_ids(K, V, 1.0, 71, np.int32)
+    wide = synth.normal_rows(K, 3 * D + 1, 72)
+    res = lz.unique(_t(ids), V)
+    tw = _t(wide)
+    out_a = lz.segsum(tw[:, 5:5 + D], res.perm, res.offsets, res.num_unique, dev_err=res.dev_err)
+    out_b = lz.segsum(tw[:, 8:8 + D], res.perm, res.offsets, res.num_unique, dev_err=res.dev_err)
+    torch.cuda.synchronize()
+    lz.check(res.dev_err)
+    o = oracle.unique(ids, V)
+    U = len(o[0])
+    for out, c0 in ((out_a, 5), (out_b, 8)):
+        ref = oracle.segsum(np.ascontiguousarray(wide[:, c0:c0 + D]), o[3], U)
+        assert H.row_rel_err(out[:U].double().cpu().numpy(), ref) <= H.TOL_F32
+    err = torch.zeros(1, dtype=torch.int32, device=DEV)
+    small = torch.full((10, D), 7.0, device=DEV)
+    lz.segsum(tw[:, :D], res.perm, res.offsets, res.num_unique, u_cap=10, out=small, dev_err=err)
+    torch.cuda.synchronize()
+    assert int(err.item()) & lz.DEVERR_CAPACITY
+
+
+# ---------------------------------------------------------------------------
+# Map, Fill-Values, the G-shard merge
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("dt", [np.int32, np.int64])
+def test_shard_merge_and_expand(lz, dt):
+    """Steps 1-5 for G shards on one GPU: Unique over the concatenation, the
+    local->global map, EXPAND of each shard's reduction, and the sum of the
+    expansions equals the Seg-Sum of the concatenation (the AllReduce)."""
+    G, K, V, D = 6, 7000, 50_000, 136
+    shards = [synth.zipf_ids(K, V, 1.0, 80 + g, dt) for g in range(G)]
+    grads = [synth.normal_rows(K, D, 90 + g) for g in range(G)]
+    I = np.concatenate(shards)
+    rI = lz.unique(_t(I), V)
+    MI = lz.segsum(_t(np.concatenate(grads)), rI.perm, rI.offsets, rI.num_unique, dev_err=rI.dev_err)
+    total = torch.zeros((rI.uniq.numel(), D), dtype=torch.float64, device=DEV)
+    keep = []
+    for J, g in zip(shards, grads):
+        r = lz.unique(_t(J), V)
+        s = lz.segsum(_t(g), r.perm, r.offsets, r.num_unique, dev_err=r.dev_err)
+        mp = lz.map_ids(r.uniq, r.num_unique, rI.uniq, rI.num_unique, dev_err=r.dev_err)
+        M = torch.full((rI.uniq.numel(), D), float("nan"), device=DEV)
+        lz.fill_values(s, r.uniq, r.num_unique, M, rI.uniq, rI.num_unique, "expand", dev_err=r.dev_err)
+        total += M.double().nan_to_num(0.0)
+        keep.append((J, r, s, mp, M))
+    torch.cuda.synchronize()
+    lz.check(rI.dev_err)
+    oI = H.assert_unique_matches(rI, I, V, oracle)
+    UG = len(oI[0])
+    for J, r, s, mp, M in keep:
+        lz.check(r.dev_err)
+        oj = H.assert_unique_matches(r, J, V, oracle)
+        Ui = len(oj[0])
+        omap, missing = oracle.map_ids(oj[0], oI[0])
+        assert not missing and np.array_equal(mp[:Ui].cpu().numpy(), omap)
+        Mn = M[:UG].cpu().numpy()
+        assert not np.isnan(Mn).any(), "EXPAND must write every row"
+        want = oracle.expand(s[:Ui].double().cpu().numpy(), oj[0], oI[0])
+        assert np.array_equal(Mn.astype(np.float64), want)
+    ref = oracle.segsum(np.concatenate(grads), oI[3], UG)
+    assert H.row_rel_err(total[:UG].cpu().numpy(), ref) <= 2 * H.TOL_F32
+    assert H.row_rel_err(MI[:UG].double().cpu().numpy(), ref) <= H.TOL_F32
+
+
+def test_fill_scatter_modes(lz):
+    K, V, D = 12_000, 3000, 72
+    ids = synth.zipf_ids(K, V, 1.1, 101, np.int32)
+    g = synth.normal_rows(K, D, 102)
+    base = synth.normal_rows(V, D, 103)
+    r = lz.unique(_t(ids), V)
+    s = lz.segsum(_t(g), r.perm, r.offsets, r.num_unique, dev_err=r.dev_err)
+    t1 = _t(base)
+    lz.fill_values(s, r.uniq, r.num_unique, t1, None, None, "scatter", dev_err=r.dev_err)
+    t2 = _t(base)
+    lz.fill_values(s, r.uniq, r.num_unique, t2, None, None, "scatter_add", dev_err=r.dev_err)
+    # scatter into the row space of a superset id list
+    sup = np.unique(np.concatenate([ids, np.arange(0, V, 7)])).astype(np.int32)
+    n_sup = torch.tensor([len(sup)], dtype=torch.int64, device=DEV)
+    t3 = torch.zeros((len(sup), D), device=DEV)
+    lz.fill_values(s, r.uniq, r.num_unique, t3, _t(sup), n_sup, "scatter", dev_err=r.dev_err)
+    torch.cuda.synchronize()
+    lz.check(r.dev_err)
+    o = oracle.unique(ids, V)
+    U = len(o[0])
+    src = s[:U].double().cpu().numpy()
+    assert np.array_equal(t1.cpu().numpy().astype(np.float64), oracle.scatter(src, o[0], base))
+    want_add = oracle.scatter(src, o[0], base, add=True).astype(np.float32)
+    assert np.array_equal(t2.cpu().numpy(), want_add)
+    assert np.array_equal(t3.cpu().numpy().astype(np.float64),
+                          oracle.scatter(src, o[0], np.zeros((len(sup), D)), dst_ids=sup))
+
+
+def test_fill_and_map_errors(lz):
+    ids = _t(np.array([2, 5, 9], np.int32))
+    n3 = torch.tensor([3], dtype=torch.int64, device=DEV)
+    sup = _t(np.array([1, 2, 5, 8], np.int32))
+    n4 = torch.tensor([4], dtype=torch.int64, device=DEV)
+    src = torch.ones((3, 8), device=DEV)
+    e1 = torch.zeros(1, dtype=torch.int32, device=DEV)
+    mp = lz.map_ids(ids, n3, sup, n4, dev_err=e1)
+    e2 = torch.zeros(1, dtype=torch.int32, device=DEV)
+    lz.fill_values(src, ids, n3, torch.zeros((4, 8), device=DEV), sup, n4, "expand", dev_err=e2)
+    e3 = torch.zeros(1, dtype=torch.int32, device=DEV)
+    lz.fill_values(src, ids, n3, torch.zeros((6, 8), device=DEV), None, None, "scatter", dev_err=e3)
+    torch.cuda.synchronize()
+    assert mp.cpu().tolist() == [1, 2, -1]
+    assert int(e1.item()) & lz.DEVERR_NOT_FOUND
+    assert int(e2.item()) & lz.DEVERR_NOT_FOUND
+    assert int(e3.item()) & lz.DEVERR_ID_RANGE
+
+
+# ---------------------------------------------------------------------------
+# Sparse apply (step 7)
+# ---------------------------------------------------------------------------
+
+def _apply_case(lz, opt, dt, K, V, D, seed, step=1, wd=0.0):
+    ids = synth.zipf_ids(K, V, 1.0, seed, dt)
+    g = synth.normal_rows(K, D, seed + 1)
+    p0 = synth.normal_rows(V, D, seed + 2, 0.02)
+    r = lz.unique(_t(ids), V)
+    s = lz.segsum(_t(g), r.perm, r.offsets, r.num_unique, dev_err=r.dev_err)
+    table = _t(p0)
+    kw = {}
+    m0 = v0 = None
+    if opt == "adam":
+        m0 = synth.normal_rows(V, D, seed + 3, 0.01) if step > 1 else np.zeros((V, D), np.float32)
+        v0 = np.abs(synth.normal_rows(V, D, seed + 4, 0.01)) if step > 1 else np.zeros((V, D), np.float32)
+        kw = dict(m=_t(m0), v=_t(v0), step=step)
+    # The kernel receives fp32 hyperparameters; the oracle gets the same
+    # fp32-rounded values (1 - fp32(0.999) differs from 0.001 by 1.3e-5).
+    f32 = lambda x: float(np.float32(x))
+    lr = f32(0.1 if opt == "sgd" else 1e-3)
+    b1, b2, eps = f32(0.9), f32(0.999), f32(1e-8)
+    if opt == "adam":
+        kw["weight_decay"] = f32(wd)
+    lz.sparse_apply(table, r.uniq, r.num_unique, s, opt, lr=lr, beta1=b1, beta2=b2, eps=eps,
+                    dev_err=r.dev_err, **kw)
+    torch.cuda.synchronize()
+    lz.check(r.dev_err)
+    o = oracle.unique(ids, V)
+    U = len(o[0])
+    gs = s[:U].double().cpu().numpy()  # the apply is checked on the GPU's own Seg-Sum
+    rows = o[0]
+    got = table.cpu().numpy()
+    untouched = np.ones(V, bool)
+    untouched[rows] = False
+    assert np.array_equal(got[untouched], p0[untouched]), "untouched rows must be bit-unchanged"
+    if opt == "sgd":
+        ref = oracle.sgd(p0[rows], gs, float(lr))
+        np.testing.assert_allclose(got[rows], ref, rtol=0, atol=float(np.abs(ref).max()) * 2.4e-7)
+    else:
+        pr, mr, vr = oracle.adam(p0[rows], m0[rows], v0[rows], gs, lr, b1, b2, eps, f32(wd), step)
+        dp = np.abs(got[rows] - pr)
+        assert float(dp.max()) <= 2e-6 * float(lr) + 2.4e-7 * float(np.abs(pr).max())
+        np.testing.assert_allclose(kw["m"].cpu().numpy()[rows], mr, rtol=2e-6, atol=1e-9)
+        np.testing.assert_allclose(kw["v"].cpu().numpy()[rows], vr, rtol=2e-6, atol=1e-12)
+
+
+@pytest.mark.parametrize("dt", [np.int32, np.int64])
+def test_apply_sgd(lz, dt):
+    _apply_case(lz, "sgd", dt, 20_000, 30_000, 256, 111)
+
+
+@pytest.mark.parametrize("step,wd", [(1, 0.0), (10, 0.0), (10, 0.01)])
+def test_apply_adam(lz, step, wd):
+    _apply_case(lz, "adam", np.int64, 20_000, 30_000, 200, 121, step, wd)
+
+
+def test_apply_sgd_odd_width(lz):
+    _apply_case(lz, "sgd", np.int32, 3000, 2000, 13, 131)
