@@ -50,6 +50,47 @@ def segsum_bytes(K, D, U, grad_bytes):
     return K * D * grad_bytes + U * D * 4 + K * 4 + (U + 1) * 4
 
 
+class HipEvents:
+    """Timing events created with hipEventDisableSystemFence, recorded on the
+    stream the kernels run on (torch's current stream). Torch's own events
+    add a system-scope cache flush per record, about 5 us of idle GPU each."""
+
+    DISABLE_SYSTEM_FENCE = 0x20000000
+
+    def __init__(self, n):
+        import ctypes
+        self.ct = ctypes
+        self.hip = ctypes.CDLL("libamdhip64.so.7")  # the runtime torch already loaded
+        self.hip.hipEventCreateWithFlags.argtypes = [ctypes.c_void_p, ctypes.c_uint]
+        self.hip.hipEventRecord.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
+        self.hip.hipEventElapsedTime.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
+        self.hip.hipEventDestroy.argtypes = [ctypes.c_void_p]
+        self.ev = []
+        for _ in range(n):
+            h = ctypes.c_void_p()
+            rc = self.hip.hipEventCreateWithFlags(ctypes.byref(h), self.DISABLE_SYSTEM_FENCE)
+            if rc != 0:
+                raise RuntimeError(f"hipEventCreateWithFlags failed ({rc})")
+            self.ev.append(h)
+
+    def record(self, i, stream):
+        rc = self.hip.hipEventRecord(self.ev[i], self.ct.c_void_p(stream.cuda_stream))
+        if rc != 0:
+            raise RuntimeError(f"hipEventRecord failed ({rc})")
+
+    def ms(self, i, j):
+        out = self.ct.c_float()
+        rc = self.hip.hipEventElapsedTime(self.ct.byref(out), self.ev[i], self.ev[j])
+        if rc != 0:
+            raise RuntimeError(f"hipEventElapsedTime failed ({rc})")
+        return out.value
+
+    def close(self):
+        for h in self.ev:
+            self.hip.hipEventDestroy(h)
+        self.ev = []
+
+
 class Batch:
     """One resident batch: ids and gradients on the device (and, for the
     merge workload, shard 0's own ids and gradients)."""
@@ -94,11 +135,11 @@ def run_gpu(w, steps, warmup, nbatch, torch, lz):
 
     def step(b, ev=None):
         bt = batches[b % nbatch]
-        if ev: ev[0].record(stream)
+        if ev: ev(0)
         lz.unique(bt.ids, w.V, out=ures, ws=ws)
-        if ev: ev[1].record(stream)
-        lz.segsum(bt.grad, ures.perm, ures.offsets, ures.num_unique, out=out, dev_err=dev_err, ws=ws)
-        if ev: ev[2].record(stream)
+        if ev: ev(1)
+        lz.segsum(bt.grad, ures.perm, ures.inverse, ures.offsets, ures.num_unique, out=out, dev_err=dev_err, ws=ws)
+        if ev: ev(2)
         if w.step == "sgd":
             lz.sparse_apply(state["table"], ures.uniq, ures.num_unique, out, "sgd", lr=w.lr,
                             dev_err=dev_err)
@@ -113,11 +154,11 @@ def run_gpu(w, steps, warmup, nbatch, torch, lz):
         elif w.step == "expand":
             u0 = state["u0"]
             lz.unique(bt.ids0, w.V, out=u0, ws=ws)
-            lz.segsum(bt.grad0, u0.perm, u0.offsets, u0.num_unique, out=state["out0"],
+            lz.segsum(bt.grad0, u0.perm, u0.inverse, u0.offsets, u0.num_unique, out=state["out0"],
                       dev_err=dev_err, ws=ws)
             lz.fill_values(state["out0"], u0.uniq, u0.num_unique, state["M"], ures.uniq,
                            ures.num_unique, "expand", dev_err=dev_err)
-        if ev: ev[3].record(stream)
+        if ev: ev(3)
 
     # Types per batch (read once, outside the timed region).
     U_of = []
@@ -131,18 +172,18 @@ def run_gpu(w, steps, warmup, nbatch, torch, lz):
         step(i)
     torch.cuda.synchronize()
 
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(steps)]
-    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    ev = HipEvents(4 * steps + 2)
     torch.cuda.synchronize()
-    start.record(stream)
+    ev.record(4 * steps, stream)
     for i in range(steps):
-        step(i, evs[i])
-    end.record(stream)
+        step(i, lambda k, i=i: ev.record(4 * i + k, stream))
+    ev.record(4 * steps + 1, stream)
     torch.cuda.synchronize()
     lz.check(dev_err)
-    total_ms = start.elapsed_time(end)
-    st = np.array([[e[0].elapsed_time(e[1]), e[1].elapsed_time(e[2]), e[2].elapsed_time(e[3])]
-                   for e in evs])
+    total_ms = ev.ms(4 * steps, 4 * steps + 1)
+    st = np.array([[ev.ms(4 * i, 4 * i + 1), ev.ms(4 * i + 1, 4 * i + 2), ev.ms(4 * i + 2, 4 * i + 3)]
+                   for i in range(steps)])
+    ev.close()
     gb = 2 if w.grad_dtype == "bf16" else 4
     seg_bytes = np.mean([segsum_bytes(K, D, U_of[i % nbatch], gb) for i in range(steps)])
     seg_ms = float(st[:, 1].mean())

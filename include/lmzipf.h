@@ -118,14 +118,9 @@ int lm_workspace_clear(void* ws, size_t bytes, void* stream);
  * num_unique [1] int64: U.
  * dev_err    [1] int32, zeroed by the caller.
  * ws         device workspace of at least lm_unique_workspace_bytes(K,
- *            idtype, V) bytes, 256-byte aligned. Its first
- *            LM_UNIQUE_CTRL_BYTES bytes must be zero before the first call
- *            (lm_workspace_clear, or a zero-filled allocation); every
- *            lm_unique leaves them zero when its kernels finish, so a
- *            workspace is reused without clearing. No other entry point
- *            touches those bytes, so one buffer can serve every call.
+ *            idtype, V) bytes, 256-byte aligned; no initial contents are
+ *            required (the first kernel clears what the call needs).
  * ------------------------------------------------------------------------ */
-#define LM_UNIQUE_CTRL_BYTES ((size_t)8192)
 size_t lm_unique_workspace_bytes(int64_t K, int32_t idtype, int64_t V);
 int lm_unique(const void* ids, int32_t idtype, int64_t K, int64_t V,
               void* uniq, int32_t* counts, int32_t* offsets, int32_t* inverse,
@@ -141,22 +136,24 @@ int lm_unique(const void* ids, int32_t idtype, int64_t K, int64_t V,
  *
  * grad       device, K rows of D values of dtype `gtype` (LM_F32 / LM_BF16),
  *            row stride ld_grad elements.
- * perm, offsets, num_unique
- *            device, the CSR produced by lm_unique (perm [K], offsets [U+1]).
+ * perm, inverse, offsets, num_unique
+ *            device, as produced by lm_unique for the same ids: perm [K],
+ *            inverse [K] (inverse[perm[i]] is the type of sorted position
+ *            i), offsets [U+1]. Inconsistent arrays set LM_DEVERR_CAPACITY;
+ *            the kernels still stay inside the buffers.
  * u_cap      rows allocated in `out`; U > u_cap sets LM_DEVERR_CAPACITY
  *            and only the first u_cap rows are written.
  * out        device, u_cap x D fp32, row stride ld_out; rows >= U untouched.
  * dev_err    device int32, zeroed by the caller.
  * ws         device workspace of lm_segsum_workspace_bytes(K, D) bytes,
- *            256-byte aligned; no initial contents are required. Its first
- *            LM_UNIQUE_CTRL_BYTES bytes are left untouched.
+ *            256-byte aligned; no initial contents are required.
  * ------------------------------------------------------------------------ */
 size_t lm_segsum_workspace_bytes(int64_t K, int64_t D);
 int lm_segsum(const void* grad, int32_t gtype, int64_t K, int64_t D,
-              int64_t ld_grad, const int32_t* perm, const int32_t* offsets,
-              const int64_t* num_unique, int64_t u_cap, float* out,
-              int64_t ld_out, int32_t* dev_err, void* ws, size_t ws_bytes,
-              void* stream);
+              int64_t ld_grad, const int32_t* perm, const int32_t* inverse,
+              const int32_t* offsets, const int64_t* num_unique, int64_t u_cap,
+              float* out, int64_t ld_out, int32_t* dev_err, void* ws,
+              size_t ws_bytes, void* stream);
 
 /* ------------------------------------------------------------------------
  * Map — Sec. III-A step 4: the local-to-global map J^ -> I^. Both id lists

@@ -55,36 +55,54 @@ __device__ __forceinline__ int wave_incl_max(int v) {
   return v;
 }
 
-// Exclusive prefix sum over a 256-thread block (4 waves). `lds` holds 4
-// entries. Returns this thread's exclusive prefix; `total` gets the block sum.
-template <typename T>
-__device__ __forceinline__ T block256_excl_sum(T v, T* lds, T& total) {
+// Exclusive prefix sum over a block of NW waves. `lds` holds NW entries.
+// Returns this thread's exclusive prefix; `total` gets the block sum.
+template <int NW, typename T>
+__device__ __forceinline__ T block_excl_sum(T v, T* lds, T& total) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   T incl = wave_incl_sum(v);
   if (lane == 63) lds[wave] = incl;
   __syncthreads();
-  T w0 = lds[0], w1 = lds[1], w2 = lds[2], w3 = lds[3];
+  T before = T(0), all = T(0);
+#pragma unroll
+  for (int w = 0; w < NW; ++w) {
+    const T x = lds[w];
+    before += w < wave ? x : T(0);
+    all += x;
+  }
   __syncthreads();
-  T before = (wave > 0 ? w0 : T(0)) + (wave > 1 ? w1 : T(0)) + (wave > 2 ? w2 : T(0));
-  total = w0 + w1 + w2 + w3;
+  total = all;
   return before + incl - v;
 }
 
-// Exclusive prefix maximum over a 256-thread block (-1 for thread 0).
-__device__ __forceinline__ int block256_excl_max(int v, int* lds, int& total) {
+template <typename T>
+__device__ __forceinline__ T block256_excl_sum(T v, T* lds, T& total) {
+  return block_excl_sum<4, T>(v, lds, total);
+}
+
+// Exclusive prefix maximum over a block of NW waves (-1 for thread 0).
+template <int NW>
+__device__ __forceinline__ int block_excl_max(int v, int* lds, int& total) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   int incl = wave_incl_max(v);
   int prev = __shfl_up(incl, 1, kWave);
   if (lane == 0) prev = -1;
   if (lane == 63) lds[wave] = incl;
   __syncthreads();
-  int w[4] = {lds[0], lds[1], lds[2], lds[3]};
+  int before = -1, all = -1;
+#pragma unroll
+  for (int w = 0; w < NW; ++w) {
+    const int x = lds[w];
+    if (w < wave && x > before) before = x;
+    if (x > all) all = x;
+  }
   __syncthreads();
-  int before = -1;
-  for (int i = 0; i < wave; ++i) before = w[i] > before ? w[i] : before;
-  total = w[0];
-  for (int i = 1; i < 4; ++i) total = w[i] > total ? w[i] : total;
+  total = all;
   return prev > before ? prev : before;
+}
+
+__device__ __forceinline__ int block256_excl_max(int v, int* lds, int& total) {
+  return block_excl_max<4>(v, lds, total);
 }
 
 // ---------------------------------------------------------------------------
@@ -127,6 +145,19 @@ struct bf16_t {
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
+// Gradient rows are read exactly once: stream them past the caches.
+#ifndef LMZ_STREAM_LOADS
+#define LMZ_STREAM_LOADS 1
+#endif
+template <typename T>
+__device__ __forceinline__ T stream_load(const T* p) {
+#if LMZ_STREAM_LOADS
+  return __builtin_nontemporal_load(p);
+#else
+  return *p;
+#endif
+}
+
 __device__ __forceinline__ float bf16_to_f32(uint32_t bits16) {
   return __uint_as_float(bits16 << 16);
 }
@@ -138,7 +169,7 @@ template <>
 struct RowVec<float, 4> {
   using raw_t = f32x4;
   static __device__ __forceinline__ raw_t load(const float* p) {
-    return __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(p));
+    return stream_load(reinterpret_cast<const f32x4*>(p));
   }
   static __device__ __forceinline__ void add(float* acc, const raw_t& r) {
     acc[0] += r.x; acc[1] += r.y; acc[2] += r.z; acc[3] += r.w;
@@ -148,7 +179,7 @@ struct RowVec<float, 4> {
 template <>
 struct RowVec<float, 1> {
   using raw_t = float;
-  static __device__ __forceinline__ raw_t load(const float* p) { return __builtin_nontemporal_load(p); }
+  static __device__ __forceinline__ raw_t load(const float* p) { return stream_load(p); }
   static __device__ __forceinline__ void add(float* acc, const raw_t& r) { acc[0] += r; }
 };
 
@@ -156,7 +187,7 @@ template <>
 struct RowVec<bf16_t, 8> {
   using raw_t = u32x4;
   static __device__ __forceinline__ raw_t load(const bf16_t* p) {
-    return __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
+    return stream_load(reinterpret_cast<const u32x4*>(p));
   }
   static __device__ __forceinline__ void add(float* acc, const raw_t& r) {
     const uint32_t w[4] = {r.x, r.y, r.z, r.w};
@@ -172,7 +203,7 @@ template <>
 struct RowVec<bf16_t, 1> {
   using raw_t = uint32_t;
   static __device__ __forceinline__ raw_t load(const bf16_t* p) {
-    return static_cast<uint32_t>(__builtin_nontemporal_load(&p->bits));
+    return static_cast<uint32_t>(stream_load(&p->bits));
   }
   static __device__ __forceinline__ void add(float* acc, const raw_t& r) {
     acc[0] += bf16_to_f32(r);

@@ -2,36 +2,59 @@
 // sorted positions i of type u, accumulated in fp32 in a fixed order.
 //
 // Work partition (no float atomics, run-to-run bit-identical):
-//   The K sorted positions are cut into chunks of R positions, one chunk per
-//   wave (and per column tile of up to 1024 columns). A segment (the
-//   positions of one type) shorter than kLongRows rows belongs entirely to
-//   the chunk that holds its first position, even when it runs past the
-//   chunk end; a longer one — the heads of the Zipf distribution — is cut at
-//   chunk boundaries, each chunk summing its piece into a partial row:
+//   The K sorted positions are cut into chunks of R positions (R = 32..512,
+//   growing with K), one chunk per wave and per column tile of up to 1024
+//   columns. The segment (type) of a position is inverse[perm[i]], so a wave
+//   learns every segment boundary of its chunk from two gathers and a ballot,
+//   without searching. A segment shorter than T = min(R, 64) rows belongs
+//   entirely to the chunk holding its first position, even where it runs
+//   past the chunk end; a longer one — a head of the Zipf distribution — is
+//   cut at chunk boundaries and every chunk sums its piece into a partial
+//   row:
 //     part_start[c]  the piece of a long segment that starts in chunk c and
 //                    continues past it (desc[c] names that segment),
 //     part_cont[c]   the piece of a long segment that started before chunk c.
-//   k_segsum_fix then adds, for every desc[c] >= 0, part_start[c] and the
-//   part_cont rows of the following chunks the segment covers, in chunk
-//   order. A chunk therefore reads at most R + kLongRows - 1 rows, and a
-//   head holding 20% of a million tokens is spread over ~400 waves.
-//   Each wave gathers whole 16-byte column vectors of RF rows at a time
-//   (RF x NV x 1 KiB in flight), adds them in fp32 registers and writes a row
-//   as soon as its segment ends; grad is streamed with non-temporal loads.
+//   k_segsum_fix then sums, for each desc[c] >= 0, part_start[c] and the
+//   part_cont rows of the chunks the segment covers, in order: one wave for
+//   a segment of few pieces, 16 waves (fixed stride split of the pieces,
+//   fixed-order combine in LDS) for a head.
+// A chunk reads at most R + T - 1 rows; a segment is split into at most
+// K / R pieces.
+//
+// Each wave gathers whole 16-byte column vectors of RF rows at a time
+// (RF x NV x 1 KiB in flight), adds them in fp32 registers and writes a row
+// as soon as its segment ends; grad is streamed with non-temporal loads.
 #include "common.hpp"
 
 namespace lmz {
 
+// Tuning knobs (overridable at build time).
+#ifndef LMZ_SEG_TARGET_CHUNKS
+#define LMZ_SEG_TARGET_CHUNKS 2048   // K is cut into about this many chunks
+#endif
+#ifndef LMZ_SEG_RF4
+#define LMZ_SEG_RF4 4                // rows per gather batch with 4 vectors per lane
+#endif
+#ifndef LMZ_SEG_RF2
+#define LMZ_SEG_RF2 8                // rows per gather batch with <= 2 vectors per lane
+#endif
+#ifndef LMZ_SEG_NV_MAX
+#define LMZ_SEG_NV_MAX 4             // 16-byte vectors per lane per row (fp32)
+#endif
+#ifndef LMZ_SEG_FIX_RF
+#define LMZ_SEG_FIX_RF 4             // partial rows per wave per batch in the fix-up
+#endif
+
 constexpr int kSegThreads = 256;
 constexpr int kSegWaves = kSegThreads / kWave;
-constexpr int kLongRows = 64;
-constexpr int kTargetChunks = 2048;
+constexpr int kMinR = 32, kMaxR = 512;
 
 struct SegArgs {
   const void* grad;
   int64_t ld_grad;
   int K, D;
   const int32_t* perm;
+  const int32_t* inverse;
   const int32_t* offsets;
   const int64_t* num_unique;
   int64_t u_cap;
@@ -53,11 +76,12 @@ static inline size_t a256(size_t x) { return (x + 255) & ~size_t(255); }
 
 static SegLayout seg_layout(int64_t K, int64_t D) {
   SegLayout L{};
-  int64_t r = (K + kTargetChunks - 1) / kTargetChunks;
-  r = (r + 63) / 64 * 64;
-  L.R = static_cast<int>(r < 64 ? 64 : r);
-  L.nchunks = static_cast<int>((K + L.R - 1) / L.R);
-  size_t off = LM_UNIQUE_CTRL_BYTES;  // reserved for lm_unique's control block
+  const int64_t want = (K + LMZ_SEG_TARGET_CHUNKS - 1) / LMZ_SEG_TARGET_CHUNKS;
+  int R = kMinR;
+  while (R < want && R < kMaxR) R *= 2;
+  L.R = R;
+  L.nchunks = static_cast<int>((K + R - 1) / R);
+  size_t off = 0;
   L.cont = off;  off += a256(size_t(L.nchunks) * D * 4);
   L.start = off; off += a256(size_t(L.nchunks) * D * 4);
   L.desc = off;  off += a256(size_t(L.nchunks) * 4);
@@ -67,86 +91,123 @@ static SegLayout seg_layout(int64_t K, int64_t D) {
 
 size_t segsum_workspace_bytes(int64_t K, int64_t D) { return seg_layout(K, D).total; }
 
-// Largest s in [0, U) with offsets[s] <= target (offsets ascending, offsets[0]
-// = 0). A 64-ary search by the whole wave: ceil(log64 U) dependent loads.
-__device__ __forceinline__ int seg_search(const int32_t* __restrict__ offsets, int U, int target) {
-  const int lane = lane_id();
-  int lo = 0, hi = U;
-  while (hi - lo > 1) {
-    const int stride = (hi - lo + kWave - 1) / kWave;
-    const int idx = lo + lane * stride;
-    const bool pred = idx < hi && offsets[idx] <= target;
-    int t = __popcll(ballot(pred));
-    if (t < 1) t = 1;  // only reachable with non-monotone offsets
-    const int nlo = lo + (t - 1) * stride;
-    const int nhi = lo + t * stride;
-    lo = nlo;
-    hi = nhi < hi ? nhi : hi;
-  }
-  return lo;
-}
+// Windows of positions a wave loads up front: [p0 - 1, p0 - 1 + 64 * NW)
+// must cover p0 - 1 (to see whether the first segment started earlier), the
+// whole walk (at most R + T - 1 rows from p0) and one position past it (to
+// see whether the last row ends its segment).
+template <int R>
+constexpr int windows_for() { return (R + (R < 64 ? R : 64)) / 64 + 1; }
 
-template <typename GT, int VEC, int NV, int RF>
+template <typename GT, int VEC, int NV, int RF, int R>
 __global__ __launch_bounds__(kSegThreads) void k_segsum(SegArgs a) {
   using RV = RowVec<GT, VEC>;
   using raw_t = typename RV::raw_t;
   constexpr int kColsPerVec = kWave * VEC;
   constexpr int CT = NV * kColsPerVec;
+  constexpr int NW = windows_for<R>();
+  constexpr int T = R < 64 ? R : 64;
 
   const int lane = lane_id();
-  const int c = blockIdx.x * kSegWaves + (threadIdx.x >> 6);
+  const int c = first_lane(blockIdx.x * kSegWaves + (threadIdx.x >> 6));  // one chunk per wave
   if (c >= a.nchunks) return;
   const int ct = blockIdx.y;
-  const int K = a.K, D = a.D, R = a.R;
-
-  int64_t U64 = *a.num_unique;
-  if (U64 > a.u_cap) {
-    if (c == 0 && ct == 0 && lane == 0) raise_err(a.dev_err, LM_DEVERR_CAPACITY);
-  }
-  const int U = static_cast<int>(U64 < K ? U64 : K);
+  const int K = a.K, D = a.D;
   const int p0 = c * R;
   const int p1 = p0 + R < K ? p0 + R : K;
-  if (U <= 0 || p0 >= K) {
-    if (ct == 0 && lane == 0) a.desc[c] = -1;
-    return;
-  }
-  const int32_t* __restrict__ offsets = a.offsets;
-  const int32_t* __restrict__ perm = a.perm;
 
-  const int s_f = seg_search(offsets, U, p0);
-  const int s_l = seg_search(offsets, U, p1 - 1);
-  const int a_f = offsets[s_f], b_f = offsets[s_f + 1];
-  const int a_l = offsets[s_l], b_l = offsets[s_l + 1];
-  const bool long_l = b_l - a_l >= kLongRows;
-  int s = s_f, q = p0;
-  if (a_f < p0 && b_f - a_f < kLongRows) {
-    s = s_f + 1;  // a short segment owned by the previous chunk
-    q = b_f;
+  // 1. Gather the permutation and the segment of every position in the
+  //    windows (sentinels: -2 before position 0, -1 from position K on).
+  int pw[NW], sw[NW];
+  bool bad = false;
+#pragma unroll
+  for (int w = 0; w < NW; ++w) {
+    const int pos = p0 - 1 + w * kWave + lane;
+    pw[w] = (pos >= 0 && pos < K) ? a.perm[pos] : 0;
   }
-  int q_end = long_l ? p1 : b_l;
-  if (q_end > K) q_end = K;
-  if (ct == 0 && lane == 0) a.desc[c] = (long_l && a_l >= p0 && b_l > p1) ? s_l : -1;
-  if (q >= q_end) return;
+#pragma unroll
+  for (int w = 0; w < NW; ++w) {
+    const int pos = p0 - 1 + w * kWave + lane;
+    const bool ok = pos >= 0 && pos < K;
+    const bool kin = static_cast<uint32_t>(pw[w]) < static_cast<uint32_t>(K);
+    bad |= ok && !kin;
+    if (!kin) pw[w] = 0;
+    sw[w] = ok ? a.inverse[pw[w]] : (pos < 0 ? -2 : -1);
+  }
+  // ends[w] bit j: position p0-1+64w+j is the last of its segment.
+  uint64_t ends[NW];
+#pragma unroll
+  for (int w = 0; w < NW; ++w) {
+    int nxt = __shfl_down(sw[w], 1, kWave);
+    if (lane == kWave - 1) nxt = w + 1 < NW ? read_lane(sw[w + 1 < NW ? w + 1 : w], 0) : -3;
+    ends[w] = ballot(sw[w] != nxt);
+  }
+  const int64_t U64 = *a.num_unique;
+  if (U64 > a.u_cap && c == 0 && ct == 0 && lane == 0) raise_err(a.dev_err, LM_DEVERR_CAPACITY);
+  const int U = first_lane(static_cast<int>(U64 < K ? U64 : K));
 
-  // Columns of this lane.
+  // 2. First and last segment of the chunk and, where needed, their lengths.
+  const int s_f = read_lane(sw[0], 1);                     // segment of p0
+  const bool started_before = read_lane(sw[0], 0) == s_f;  // p0 - 1 in the same segment
+  const int il = p1 - p0;                                  // window index of p1 - 1
+  int s_l = 0;
+  bool cont_after = false;                                 // p1 in the segment of p1 - 1
+#pragma unroll
+  for (int w = 0; w < NW; ++w) {
+    if (il / kWave == w) s_l = read_lane(sw[w], il % kWave);
+  }
+#pragma unroll
+  for (int w = 0; w < NW; ++w) {
+    if ((il + 1) / kWave == w) cont_after = read_lane(sw[w], (il + 1) % kWave) == s_l;
+  }
+  const bool sf_ok = s_f >= 0 && s_f < U, sl_ok = s_l >= 0 && s_l < U;
+  bad |= !sf_ok || !sl_ok;
+  const int len_f = first_lane(sf_ok && started_before ? a.offsets[s_f + 1] - a.offsets[s_f] : 0);
+  const int b_l = first_lane(sl_ok && cont_after ? a.offsets[s_l + 1] : p1);
+  const int len_l = first_lane(sl_ok && cont_after ? b_l - a.offsets[s_l] : 0);
+  const bool long_f = started_before && len_f >= T;
+  const bool long_l = cont_after && len_l >= T;
+  if (ct == 0 && lane == 0)
+    a.desc[c] = (long_l && !(started_before && s_l == s_f)) ? s_l : -1;
+
+  // Rows this chunk sums: skip a short segment owned by the previous chunk,
+  // run a short last segment to its end, stop a long one at p1.
+  int q = p0;
+  if (started_before && !long_f) {
+    int first_end = K;  // first end bit at or after p0
+#pragma unroll
+    for (int w = NW - 1; w >= 0; --w) {
+      uint64_t m = ends[w];
+      if (w == 0) m &= ~uint64_t(1);
+      if (m) first_end = p0 - 1 + w * kWave + __builtin_ctzll(m);
+    }
+    q = first_end + 1;
+  }
+  int q_end = cont_after && !long_l ? b_l : p1;
+  const int walk_max = p0 - 1 + NW * kWave - 1;  // last position whose end bit is known
+  if (q_end > walk_max) {
+    bad = true;  // only inconsistent offsets get here: never walk past the windows
+    q_end = walk_max;
+  }
+  if (ballot(bad) && lane == 0) raise_err(a.dev_err, LM_DEVERR_CAPACITY);
+  // Every lane holds the same walk bounds: tell the compiler, so the row
+  // loop below is scalar control flow and the gathers of a batch stay in
+  // flight together.
+  q = first_lane(q);
+  q_end = first_lane(q_end);
+
+  // 3. Walk rows q .. q_end - 1, window by window. Lanes past the last column
+  //    load a valid vector of the same row (col_ld) and never store it, so
+  //    the loads need no per-lane guard.
   const int col0 = ct * CT + lane * VEC;
   bool col_ok[NV];
+  int col_ld[NV];
 #pragma unroll
-  for (int v = 0; v < NV; ++v) col_ok[v] = col0 + v * kColsPerVec < D;
-
-  const GT* __restrict__ grad = static_cast<const GT*>(a.grad) + col0;
-
-  // Windows: perm_cur/perm_nxt hold perm[pw .. pw+128); ends holds
-  // offsets[ow+1 .. ow+65) (the end of segments ow .. ow+63).
-  int pw = q;
-  int perm_cur = pw + lane < K ? perm[pw + lane] : 0;
-  int perm_nxt = pw + kWave + lane < K ? perm[pw + kWave + lane] : 0;
-  int ow = s;
-  int ends = ow + 1 + lane <= U ? offsets[ow + 1 + lane] : K;
-
-  int seg_a = s < U ? offsets[s] : K;
-  int seg_b = s < U ? read_lane(ends, 0) : K;
-  int run_end = seg_b < q_end ? seg_b : q_end;
+  for (int v = 0; v < NV; ++v) {
+    const int col = col0 + v * kColsPerVec;
+    col_ok[v] = col < D;
+    col_ld[v] = col < D ? col : D - VEC;
+  }
+  const GT* __restrict__ grad = static_cast<const GT*>(a.grad);
 
   float acc[NV][VEC];
 #pragma unroll
@@ -154,107 +215,194 @@ __global__ __launch_bounds__(kSegThreads) void k_segsum(SegArgs a) {
 #pragma unroll
     for (int e = 0; e < VEC; ++e) acc[v][e] = 0.f;
 
-  bool bad_row = false;
-  while (q < q_end) {
-    const int n = q_end - q < RF ? q_end - q : RF;
-    raw_t buf[RF][NV];
 #pragma unroll
-    for (int r = 0; r < RF; ++r) {
-      if (r < n) {
-        const int idx = q + r - pw;
-        int k = idx < kWave ? read_lane(perm_cur, idx) : read_lane(perm_nxt, idx - kWave);
-        if (static_cast<uint32_t>(k) >= static_cast<uint32_t>(K)) { bad_row = true; k = 0; }
+  for (int w = 0; w < NW; ++w) {
+    const int wbase = p0 - 1 + w * kWave;
+    const int lo = q > wbase ? q - wbase : 0;
+    const int hi = q_end - wbase < kWave ? q_end - wbase : kWave;
+    for (int j0 = lo; j0 < hi; j0 += RF) {
+      const int n = hi - j0 < RF ? hi - j0 : RF;
+      // Always RF row loads (rows past n repeat row n-1, a cache hit): a load
+      // under a condition makes the compiler wait for every earlier load.
+      raw_t buf[RF][NV];
+#pragma unroll
+      for (int r = 0; r < RF; ++r) {
+        const int k = read_lane(pw[w], j0 + (r < n ? r : n - 1));
         const GT* row = grad + static_cast<int64_t>(k) * a.ld_grad;
 #pragma unroll
-        for (int v = 0; v < NV; ++v)
-          if (col_ok[v]) buf[r][v] = RV::load(row + v * kColsPerVec);
-          else buf[r][v] = raw_t{};
+        for (int v = 0; v < NV; ++v) buf[r][v] = RV::load(row + col_ld[v]);
       }
-    }
 #pragma unroll
-    for (int r = 0; r < RF; ++r) {
-      if (r < n) {
+      for (int r = 0; r < RF; ++r) {
+        if (r < n) {
 #pragma unroll
-        for (int v = 0; v < NV; ++v) RV::add(acc[v], buf[r][v]);
-        if (q + r + 1 == run_end) {
-          // Segment s (or its piece in this chunk) is complete.
-          const bool is_long = seg_b - seg_a >= kLongRows;
-          float* dst;
-          if (is_long && seg_a < p0) dst = a.part_cont + static_cast<int64_t>(c) * D;
-          else if (is_long && seg_b > p1) dst = a.part_start + static_cast<int64_t>(c) * D;
-          else dst = s < a.u_cap ? a.out + static_cast<int64_t>(s) * a.ld_out : nullptr;
-          if (dst) {
+          for (int v = 0; v < NV; ++v) RV::add(acc[v], buf[r][v]);
+          const int j = j0 + r;
+          const bool is_end = (ends[w] >> j) & 1u;
+          if (is_end || wbase + j == q_end - 1) {
+            // is_end false here means a long last segment stopped at p1.
+            const int s = read_lane(sw[w], j);
+            float* dst;
+            if (s == s_f && started_before) dst = a.part_cont + static_cast<int64_t>(c) * D;
+            else if (!is_end) dst = a.part_start + static_cast<int64_t>(c) * D;
+            else dst = (s >= 0 && s < a.u_cap) ? a.out + static_cast<int64_t>(s) * a.ld_out : nullptr;
+            if (dst) {
+#pragma unroll
+              for (int v = 0; v < NV; ++v)
+                if (col_ok[v]) store_vec<VEC>(dst + col0 + v * kColsPerVec, acc[v]);
+            }
 #pragma unroll
             for (int v = 0; v < NV; ++v)
-              if (col_ok[v]) store_vec<VEC>(dst + col0 + v * kColsPerVec, acc[v]);
-          }
 #pragma unroll
-          for (int v = 0; v < NV; ++v)
-#pragma unroll
-            for (int e = 0; e < VEC; ++e) acc[v][e] = 0.f;
-          ++s;
-          if (s < U) {
-            seg_a = seg_b;
-            if (s - ow >= kWave) {
-              ow = s;
-              ends = ow + 1 + lane <= U ? offsets[ow + 1 + lane] : K;
-            }
-            seg_b = read_lane(ends, s - ow);
-          } else {
-            seg_a = seg_b = K;
+              for (int e = 0; e < VEC; ++e) acc[v][e] = 0.f;
           }
-          run_end = seg_b < q_end ? seg_b : q_end;
         }
       }
     }
-    q += n;
-    if (q - pw >= kWave) {
-      pw += kWave;
-      perm_cur = perm_nxt;
-      perm_nxt = pw + kWave + lane < K ? perm[pw + kWave + lane] : 0;
-    }
   }
-  if (ballot(bad_row) && lane == 0) raise_err(a.dev_err, LM_DEVERR_CAPACITY);
 }
 
-// Sum the pieces of every long segment that spans chunks, in chunk order.
-// One wave per (starting chunk, 64*VEC columns).
-template <int VEC, int RF>
-__global__ __launch_bounds__(kSegThreads) void k_segsum_fix(SegArgs a) {
+// Sum the pieces of every long segment that spans chunks (piece 0 is
+// part_start[c], piece t >= 1 is part_cont[c + t], added in order of t).
+// One 1024-thread workgroup per 16 chunks, wave w looking after chunk
+// 16*blockIdx + w. A segment of at most kFixSmall pieces is summed by that
+// wave alone; a longer one (the heads of the Zipf law) by all 16 waves of
+// the workgroup, wave v adding pieces v, v+16, v+32, ... in order, the 16
+// partial rows then added in wave order through LDS. Columns go in passes
+// of 64 * VEC * NV.
+constexpr int kFixThreads = 1024;
+constexpr int kFixWaves = kFixThreads / kWave;
+constexpr int kFixSmall = 16;
+
+template <int VEC, int NV, int RF>
+__global__ __launch_bounds__(kFixThreads) void k_segsum_fix(SegArgs a) {
+  constexpr int kPass = kWave * VEC * NV;  // columns per pass
+  __shared__ float s_part[kFixWaves][kPass];
+  __shared__ int s_big[kFixWaves];
   const int lane = lane_id();
-  const int c = blockIdx.x * kSegWaves + (threadIdx.x >> 6);
-  if (c >= a.nchunks) return;
-  const int s = a.desc[c];
-  if (s < 0) return;
-  const int U = static_cast<int>(*a.num_unique);
-  if (s >= U) return;
-  const int b = a.offsets[s + 1];
-  int c1 = (b - 1) / a.R;
-  if (c1 >= a.nchunks) c1 = a.nchunks - 1;
+  const int wave = first_lane(static_cast<int>(threadIdx.x >> 6));
   const int D = a.D;
-  const int col = blockIdx.y * (kWave * VEC) + lane * VEC;
-  if (col >= D) return;
-  float acc[VEC];
-  load_vec<VEC>(a.part_start + static_cast<int64_t>(c) * D + col, acc);
-  for (int cc = c + 1; cc <= c1; cc += RF) {
-    float buf[RF][VEC];
-#pragma unroll
-    for (int r = 0; r < RF; ++r)
-      if (cc + r <= c1) load_vec<VEC>(a.part_cont + static_cast<int64_t>(cc + r) * D + col, buf[r]);
-#pragma unroll
-    for (int r = 0; r < RF; ++r)
-      if (cc + r <= c1)
-#pragma unroll
-        for (int e = 0; e < VEC; ++e) acc[e] += buf[r][e];
+  const int U = first_lane(static_cast<int>(*a.num_unique));
+  const int c = blockIdx.x * kFixWaves + wave;
+
+  int s = c < a.nchunks ? first_lane(a.desc[c]) : -1;
+  if (!(s >= 0 && s < U && s < a.u_cap)) s = -1;
+  int P = -1;
+  if (s >= 0) {
+    int c1 = first_lane((a.offsets[s + 1] - 1) / a.R);
+    if (c1 >= a.nchunks) c1 = a.nchunks - 1;
+    P = c1 - c;
   }
-  if (s < a.u_cap) store_vec<VEC>(a.out + static_cast<int64_t>(s) * a.ld_out + col, acc);
+  auto piece = [&](int cs, int t) {
+    return t == 0 ? a.part_start + static_cast<int64_t>(cs) * D
+                  : a.part_cont + static_cast<int64_t>(cs + t) * D;
+  };
+
+  // Segments of few pieces: this wave alone.
+  if (s >= 0 && P <= kFixSmall) {
+    float* dst = a.out + static_cast<int64_t>(s) * a.ld_out;
+    for (int cb = 0; cb < D; cb += kPass) {
+      float acc[NV][VEC];
+#pragma unroll
+      for (int v = 0; v < NV; ++v)
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) acc[v][e] = 0.f;
+      int col[NV], col_ld[NV];
+#pragma unroll
+      for (int v = 0; v < NV; ++v) {
+        col[v] = cb + v * kWave * VEC + lane * VEC;
+        col_ld[v] = col[v] < D ? col[v] : D - VEC;  // past the end: a valid, unstored vector
+      }
+      for (int t0 = 0; t0 <= P; t0 += RF) {
+        float buf[RF][NV][VEC];
+#pragma unroll
+        for (int r = 0; r < RF; ++r) {
+          const float* row = piece(c, t0 + r <= P ? t0 + r : t0);
+#pragma unroll
+          for (int v = 0; v < NV; ++v) load_vec<VEC>(row + col_ld[v], buf[r][v]);
+        }
+#pragma unroll
+        for (int r = 0; r < RF; ++r)
+          if (t0 + r <= P)
+#pragma unroll
+            for (int v = 0; v < NV; ++v)
+#pragma unroll
+              for (int e = 0; e < VEC; ++e) acc[v][e] += buf[r][v][e];
+      }
+#pragma unroll
+      for (int v = 0; v < NV; ++v)
+        if (col[v] < D) store_vec<VEC>(dst + col[v], acc[v]);
+    }
+  }
+
+  // Segments of many pieces: the whole workgroup, one after the other.
+  if (lane == 0) s_big[wave] = (s >= 0 && P > kFixSmall) ? s : -1;
+  __syncthreads();
+  for (int bw = 0; bw < kFixWaves; ++bw) {
+    const int sb = s_big[bw];
+    if (sb < 0) continue;  // the same in every thread
+    const int cs = blockIdx.x * kFixWaves + bw;
+    int c1 = first_lane((a.offsets[sb + 1] - 1) / a.R);
+    if (c1 >= a.nchunks) c1 = a.nchunks - 1;
+    const int PB = c1 - cs;
+    float* dst = a.out + static_cast<int64_t>(sb) * a.ld_out;
+    for (int cb = 0; cb < D; cb += kPass) {
+      float acc[NV][VEC];
+#pragma unroll
+      for (int v = 0; v < NV; ++v)
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) acc[v][e] = 0.f;
+      int col_ld[NV];
+#pragma unroll
+      for (int v = 0; v < NV; ++v) {
+        const int col = cb + v * kWave * VEC + lane * VEC;
+        col_ld[v] = col < D ? col : D - VEC;
+      }
+      for (int t0 = wave; t0 <= PB; t0 += kFixWaves * RF) {
+        float buf[RF][NV][VEC];
+#pragma unroll
+        for (int r = 0; r < RF; ++r) {
+          const int t = t0 + r * kFixWaves;
+          const float* row = piece(cs, t <= PB ? t : t0);
+#pragma unroll
+          for (int v = 0; v < NV; ++v) load_vec<VEC>(row + col_ld[v], buf[r][v]);
+        }
+#pragma unroll
+        for (int r = 0; r < RF; ++r)
+          if (t0 + r * kFixWaves <= PB)
+#pragma unroll
+            for (int v = 0; v < NV; ++v)
+#pragma unroll
+              for (int e = 0; e < VEC; ++e) acc[v][e] += buf[r][v][e];
+      }
+#pragma unroll
+      for (int v = 0; v < NV; ++v)
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) s_part[wave][v * kWave * VEC + lane * VEC + e] = acc[v][e];
+      __syncthreads();
+      // Thread x adds column cb + x over the 16 waves in order.
+      for (int x = threadIdx.x; x < kPass && cb + x < D; x += kFixThreads) {
+        float sum = 0.f;
+#pragma unroll
+        for (int w = 0; w < kFixWaves; ++w) sum += s_part[w][x];
+        dst[cb + x] = sum;
+      }
+      __syncthreads();
+    }
+  }
 }
 
 template <typename GT, int VEC, int NV, int RF>
-static hipError_t launch_main(const SegArgs& a, hipStream_t st) {
+static hipError_t launch_r(const SegArgs& a, hipStream_t st) {
   constexpr int CT = NV * kWave * VEC;
   dim3 grid((a.nchunks + kSegWaves - 1) / kSegWaves, (a.D + CT - 1) / CT);
-  k_segsum<GT, VEC, NV, RF><<<grid, kSegThreads, 0, st>>>(a);
+  switch (a.R) {
+    case 32: k_segsum<GT, VEC, NV, RF, 32><<<grid, kSegThreads, 0, st>>>(a); break;
+    case 64: k_segsum<GT, VEC, NV, RF, 64><<<grid, kSegThreads, 0, st>>>(a); break;
+    case 128: k_segsum<GT, VEC, NV, RF, 128><<<grid, kSegThreads, 0, st>>>(a); break;
+    case 256: k_segsum<GT, VEC, NV, RF, 256><<<grid, kSegThreads, 0, st>>>(a); break;
+    default: k_segsum<GT, VEC, NV, RF, 512><<<grid, kSegThreads, 0, st>>>(a); break;
+  }
   return hipGetLastError();
 }
 
@@ -263,18 +411,18 @@ static hipError_t dispatch_nv(const SegArgs& a, int nv_max, hipStream_t st) {
   const int per = kWave * VEC;
   int nv = (a.D + per - 1) / per;
   if (nv > nv_max) nv = nv_max;
-  if (nv <= 1) return launch_main<GT, VEC, 1, 8>(a, st);
-  if (nv == 2) return launch_main<GT, VEC, 2, 8>(a, st);
-  if constexpr (sizeof(GT) == 4 || VEC == 1) return launch_main<GT, VEC, 4, 4>(a, st);
-  return launch_main<GT, VEC, 2, 8>(a, st);
+  if (nv <= 1) return launch_r<GT, VEC, 1, LMZ_SEG_RF2>(a, st);
+  if (nv == 2) return launch_r<GT, VEC, 2, LMZ_SEG_RF2>(a, st);
+  if constexpr (sizeof(GT) == 4 || VEC == 1) return launch_r<GT, VEC, 4, LMZ_SEG_RF4>(a, st);
+  return launch_r<GT, VEC, 2, LMZ_SEG_RF2>(a, st);
 }
 
 static bool al16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
 
 int segsum_run(const void* grad, int gtype, int64_t K, int64_t D, int64_t ld_grad,
-               const int32_t* perm, const int32_t* offsets, const int64_t* num_unique,
-               int64_t u_cap, float* out, int64_t ld_out, int32_t* dev_err, void* ws,
-               size_t ws_bytes, hipStream_t st) {
+               const int32_t* perm, const int32_t* inverse, const int32_t* offsets,
+               const int64_t* num_unique, int64_t u_cap, float* out, int64_t ld_out,
+               int32_t* dev_err, void* ws, size_t ws_bytes, hipStream_t st) {
   const SegLayout L = seg_layout(K, D);
   if (ws_bytes < L.total) return LM_E_WORKSPACE;
   if (K == 0 || D == 0 || u_cap == 0) return LM_OK;
@@ -285,6 +433,7 @@ int segsum_run(const void* grad, int gtype, int64_t K, int64_t D, int64_t ld_gra
   a.K = static_cast<int>(K);
   a.D = static_cast<int>(D);
   a.perm = perm;
+  a.inverse = inverse;
   a.offsets = offsets;
   a.num_unique = num_unique;
   a.u_cap = u_cap;
@@ -301,20 +450,18 @@ int segsum_run(const void* grad, int gtype, int64_t K, int64_t D, int64_t ld_gra
   hipError_t e;
   if (gtype == LM_F32) {
     const bool vec = out_vec && al16(grad) && ld_grad % 4 == 0;
-    e = vec ? dispatch_nv<float, 4>(a, 4, st) : dispatch_nv<float, 1>(a, 4, st);
+    e = vec ? dispatch_nv<float, 4>(a, LMZ_SEG_NV_MAX, st) : dispatch_nv<float, 1>(a, 4, st);
   } else {
     const bool vec = out_vec && al16(grad) && ld_grad % 8 == 0 && D % 8 == 0;
-    e = vec ? dispatch_nv<bf16_t, 8>(a, 2, st) : dispatch_nv<bf16_t, 1>(a, 4, st);
+    e = vec ? dispatch_nv<bf16_t, 8>(a, LMZ_SEG_NV_MAX < 2 ? LMZ_SEG_NV_MAX : 2, st)
+            : dispatch_nv<bf16_t, 1>(a, 4, st);
   }
   if (e != hipSuccess) return launch_status(e);
-
-  if (D % 4 == 0) {
-    dim3 grid((L.nchunks + kSegWaves - 1) / kSegWaves, (a.D + 255) / 256);
-    k_segsum_fix<4, 16><<<grid, kSegThreads, 0, st>>>(a);
-  } else {
-    dim3 grid((L.nchunks + kSegWaves - 1) / kSegWaves, (a.D + 63) / 64);
-    k_segsum_fix<1, 16><<<grid, kSegThreads, 0, st>>>(a);
-  }
+  const uint32_t fix_blocks = static_cast<uint32_t>((L.nchunks + kFixWaves - 1) / kFixWaves);
+  if (D % 4 == 0)
+    k_segsum_fix<4, 4, LMZ_SEG_FIX_RF><<<fix_blocks, kFixThreads, 0, st>>>(a);
+  else
+    k_segsum_fix<1, 4, LMZ_SEG_FIX_RF><<<fix_blocks, kFixThreads, 0, st>>>(a);
   return launch_status(hipGetLastError());
 }
 

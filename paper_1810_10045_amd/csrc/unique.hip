@@ -2,49 +2,66 @@
 // ascending order, with counts, CSR offsets, the token->type map and the
 // stable sort permutation.
 //
-// Pipeline (all on one stream, no host sync):
-//   k_hist      digit histograms of every radix pass in one read of the ids;
-//               also clears this call's look-back status words and tickets.
-//   k_onesweep  one LSD radix pass per 8-bit digit over only ceil(log2 V) key
-//               bits: each 256-thread workgroup ranks a tile of keys with
-//               wave64 ballot matching, gets its global digit offsets through
-//               a decoupled look-back over tile status words, reorders the
-//               tile in LDS and writes it out in digit runs.
-//   k_dedup     run-head flags on the sorted keys, a block scan plus a
-//               decoupled look-back that carries (number of heads, position of
-//               the last head), and writes uniq, offsets, counts, inverse and
-//               num_unique; it also re-zeroes the histogram control block.
-// Tiles take their index from an atomic ticket, so a tile only ever waits on
-// tiles that already hold a workgroup: the look-back always makes progress.
+// Pipeline (all on one stream, no host sync; the only atomics are the tile
+// tickets):
+//   k_hist      digit histograms of every radix pass in one read of the ids,
+//               one row per workgroup (4096 ids each, at most 64 rows); also
+//               clears this call's tile tickets and look-back status words.
+//   k_onesweep  one LSD radix pass over a digit of up to 8 bits (the
+//               ceil(log2 V) key bits are split evenly over the fewest
+//               passes; 8-bit digits measured faster per key bit than 10- or
+//               11-bit ones, whose counters and look-back cost twice as
+//               much per pass). A 1024-thread
+//               workgroup ranks a tile of 4096 keys (4 per thread) with
+//               wave64 ballot matching, publishes its per-digit counts,
+//               learns the counts of the tiles before it through a decoupled
+//               look-back, reorders the tile in LDS and writes it out in
+//               digit runs.
+//   k_dedup     run heads on the sorted keys (4 per thread, one 16-byte load
+//               each), a block scan plus a wave-wide decoupled look-back (64
+//               predecessors per round) carrying (number of heads, position of
+//               the last head), then writes uniq, offsets, counts, inverse and
+//               num_unique.
+// Tiles take their index from an atomic ticket, so a tile only waits on
+// tiles that already hold a workgroup: every look-back makes progress. A
+// tile's inputs are fetched for tile = blockIdx.x while the ticket is in
+// flight (workgroups are dispatched in order, so the guess almost always
+// holds) and fetched again when it does not.
 #include "common.hpp"
 
 namespace lmz {
 
-constexpr int kSortThreads = 256;
-constexpr int kSortWaves = kSortThreads / kWave;
-constexpr int kRadix = 256;
-constexpr int kMaxPasses = 8;             // 64-bit keys
-constexpr int kSortItems = 16;            // keys per thread in a sort tile
-constexpr int kSortTile = kSortThreads * kSortItems;
-constexpr int kDedupItems = 16;
-constexpr int kDedupTile = kSortThreads * kDedupItems;
+constexpr int kThreads = 1024;
+constexpr int kWaves = kThreads / kWave;
+#ifndef LMZ_UNIQUE_DIGIT_BITS
+#define LMZ_UNIQUE_DIGIT_BITS 8
+#endif
+constexpr int kMaxDigitBits = LMZ_UNIQUE_DIGIT_BITS;
+constexpr int kMaxRadix = 1 << kMaxDigitBits;
+constexpr int kMaxPasses = 8;              // ceil(64 / 8)
+constexpr int kItems = 4;                  // keys per thread in a tile
+constexpr int kTile = kThreads * kItems;   // 4096
+constexpr int kHistItems = 16;             // keys per thread per histogram round
+constexpr int kHistKeysPerBlock = 1 << 12;
+constexpr int kMaxHistBlocks = 64;
 
 // Status words of the sort look-back: 2-bit flag | 30-bit count.
 constexpr uint32_t kFlagAgg = 1u << 30, kFlagPrefix = 2u << 30, kValMask = (1u << 30) - 1;
 // Status words of the dedup look-back: flag (2) | heads (31) | last head + 1 (31).
-constexpr uint64_t kDFlagAgg = 1ull << 62, kDFlagPrefix = 2ull << 62;
+constexpr uint64_t kDFlagAgg = 1ull << 62, kDFlagPrefix = 2ull << 62, kDFlags = 3ull << 62;
 constexpr uint64_t kD31 = (1ull << 31) - 1;
 
 struct UniqueLayout {
-  size_t hist, tickets, status, dstatus, keys0, keys1, vals0, vals1, total;
-  int passes, bits, tiles, dtiles;
+  size_t bhist, tickets, status, dstatus, keys0, keys1, vals0, vals1, total;
+  int passes, bits, tiles, hist_blocks;
+  int shift[kMaxPasses], nbits[kMaxPasses];
 };
 
 static inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
 static inline int key_bits_for(int64_t V) {
   if (V <= 1) return 0;
-  uint64_t m = static_cast<uint64_t>(V - 1);
+  const uint64_t m = static_cast<uint64_t>(V - 1);
   return 64 - __builtin_clzll(m);
 }
 
@@ -52,14 +69,23 @@ static UniqueLayout unique_layout(int64_t K, int idtype, int64_t V) {
   UniqueLayout L{};
   const size_t ks = idtype == LM_I64 ? 8 : 4;
   L.bits = key_bits_for(V);
-  L.passes = L.bits == 0 ? 1 : (L.bits + 7) / 8;
-  L.tiles = static_cast<int>((K + kSortTile - 1) / kSortTile);
-  L.dtiles = static_cast<int>((K + kDedupTile - 1) / kDedupTile);
+  L.passes = L.bits == 0 ? 1 : (L.bits + kMaxDigitBits - 1) / kMaxDigitBits;
+  // Split the key bits evenly: the low passes take the extra bit.
+  int sh = 0;
+  for (int p = 0; p < L.passes; ++p) {
+    const int nb = L.bits / L.passes + (p < L.bits % L.passes ? 1 : 0);
+    L.shift[p] = sh;
+    L.nbits[p] = nb;
+    sh += nb;
+  }
+  L.tiles = static_cast<int>((K + kTile - 1) / kTile);
+  const int64_t hb = (K + kHistKeysPerBlock - 1) / kHistKeysPerBlock;
+  L.hist_blocks = static_cast<int>(hb < 1 ? 1 : (hb > kMaxHistBlocks ? kMaxHistBlocks : hb));
   size_t off = 0;
-  L.hist = off;    off += LM_UNIQUE_CTRL_BYTES;                      // zero between calls
+  L.bhist = off;   off += align256(size_t(L.hist_blocks) * L.passes * kMaxRadix * 4);
   L.tickets = off; off += 256;
-  L.status = off;  off += align256(size_t(L.passes) * L.tiles * kRadix * 4);
-  L.dstatus = off; off += align256(size_t(L.dtiles) * 8);
+  L.status = off;  off += align256(size_t(L.passes) * L.tiles * kMaxRadix * 4);
+  L.dstatus = off; off += align256(size_t(L.tiles) * 8);
   L.keys0 = off;   off += align256(size_t(K) * ks);
   L.keys1 = off;   off += align256(size_t(K) * ks);
   L.vals0 = off;   off += align256(size_t(K) * 4);
@@ -68,252 +94,380 @@ static UniqueLayout unique_layout(int64_t K, int idtype, int64_t V) {
   return L;
 }
 
+struct PassBits {
+  int shift[kMaxPasses], nbits[kMaxPasses];
+};
+
+template <typename KeyT>
+__device__ __forceinline__ uint32_t digit_of(KeyT k, int shift, uint32_t mask) {
+  return static_cast<uint32_t>(key_bits(k) >> shift) & mask;
+}
+
 // ---------------------------------------------------------------------------
-// k_hist
+// k_hist: bhist[b][p][d] = number of keys read by workgroup b whose digit of
+// pass p is d (rows of kMaxRadix per pass). Also clears the tickets and the
+// look-back status words of this call.
 // ---------------------------------------------------------------------------
 template <typename KeyT>
-__global__ __launch_bounds__(kSortThreads) void k_hist(
-    const KeyT* __restrict__ keys, int K, uint64_t V, int passes, int bits,
-    uint32_t* __restrict__ hist, uint32_t* __restrict__ clear, int64_t clear_words,
+__global__ __launch_bounds__(kThreads) void k_hist(
+    const KeyT* __restrict__ keys, int K, uint64_t V, int passes, PassBits pb,
+    uint32_t* __restrict__ bhist, uint32_t* __restrict__ clear, int64_t clear_words,
     int32_t* __restrict__ dev_err) {
-  __shared__ uint32_t sh[kMaxPasses][kRadix];
-  for (int i = threadIdx.x; i < kMaxPasses * kRadix; i += kSortThreads) (&sh[0][0])[i] = 0;
-  // Clear this call's look-back status words and tile tickets.
-  for (int64_t i = blockIdx.x * int64_t(kSortThreads) + threadIdx.x; i < clear_words;
-       i += int64_t(gridDim.x) * kSortThreads)
+  extern __shared__ uint32_t sh[];  // passes * kMaxRadix
+  for (int i = threadIdx.x; i < passes * kMaxRadix; i += kThreads) sh[i] = 0;
+  for (int64_t i = blockIdx.x * int64_t(kThreads) + threadIdx.x; i < clear_words;
+       i += int64_t(gridDim.x) * kThreads)
     clear[i] = 0;
   __syncthreads();
   bool bad = false;
-  for (int64_t i = blockIdx.x * int64_t(kSortThreads) + threadIdx.x; i < K;
-       i += int64_t(gridDim.x) * kSortThreads) {
-    const uint64_t kb = key_bits(keys[i]);
-    bad |= kb >= V;
-    for (int p = 0; p < passes; ++p) {
-      const int shift = 8 * p;
-      const int nb = bits - shift < 8 ? bits - shift : 8;
-      const uint32_t d = nb > 0 ? static_cast<uint32_t>(kb >> shift) & ((1u << nb) - 1) : 0u;
-      atomicAdd(&sh[p][d], 1u);
+  const int64_t stride = int64_t(gridDim.x) * kThreads;
+  for (int64_t i0 = blockIdx.x * int64_t(kThreads) + threadIdx.x; i0 < K;
+       i0 += stride * kHistItems) {
+    KeyT kv[kHistItems];  // all loads of a round in flight together
+#pragma unroll
+    for (int j = 0; j < kHistItems; ++j) {
+      const int64_t i = i0 + j * stride;
+      kv[j] = i < K ? keys[i] : KeyT(0);
+    }
+#pragma unroll
+    for (int j = 0; j < kHistItems; ++j) {
+      if (i0 + j * stride < K) {
+        const uint64_t kb = key_bits(kv[j]);
+        bad |= kb >= V;
+        for (int p = 0; p < passes; ++p) {
+          const uint32_t d = static_cast<uint32_t>(kb >> pb.shift[p]) & ((1u << pb.nbits[p]) - 1);
+          atomicAdd(&sh[p * kMaxRadix + d], 1u);
+        }
+      }
     }
   }
   if (ballot(bad) && lane_id() == 0) raise_err(dev_err, LM_DEVERR_ID_RANGE);
   __syncthreads();
-  for (int i = threadIdx.x; i < passes * kRadix; i += kSortThreads) {
-    const uint32_t c = (&sh[0][0])[i];
-    if (c) add_agent(&hist[i], c);
-  }
+  uint32_t* row = bhist + size_t(blockIdx.x) * passes * kMaxRadix;
+  for (int i = threadIdx.x; i < passes * kMaxRadix; i += kThreads) row[i] = sh[i];
 }
 
 // ---------------------------------------------------------------------------
-// k_onesweep: one stable LSD pass over the digit (key >> shift) & (2^nbits-1).
+// k_onesweep: one stable LSD pass over the digit (key >> shift) & (2^nbits-1),
+// nbits <= RB. Thread t answers for digits t*DPT .. t*DPT+DPT-1 (DPT = 2 for
+// 11-bit digits; for 8-bit digits threads 0..255 answer for one each).
 // ---------------------------------------------------------------------------
-template <typename KeyT>
-__global__ __launch_bounds__(kSortThreads) void k_onesweep(
+template <typename KeyT, int RB>
+__global__ __launch_bounds__(kThreads) void k_onesweep(
     const KeyT* __restrict__ keys_in, const int32_t* __restrict__ vals_in,
     KeyT* __restrict__ keys_out, int32_t* __restrict__ vals_out, int K, int shift, int nbits,
-    const uint32_t* __restrict__ hist, uint32_t* __restrict__ status,
-    uint32_t* __restrict__ ticket, int32_t* __restrict__ dev_err) {
-  __shared__ KeyT s_keys[kSortTile];
-  __shared__ int32_t s_vals[kSortTile];
-  __shared__ uint32_t s_cnt[kSortWaves][kRadix];  // per-wave digit counts, then offsets
-  __shared__ int32_t s_local[kRadix];             // tile-local start of each digit
-  __shared__ int32_t s_shift[kRadix];             // global position - local position
-  __shared__ uint32_t s_scan[4];
+    const uint32_t* __restrict__ bhist, int hist_blocks, int hist_stride,
+    uint32_t* __restrict__ status, uint32_t* __restrict__ ticket, int32_t* __restrict__ dev_err) {
+  constexpr int kRadix = 1 << RB;
+  constexpr int DPT = kRadix >= kThreads ? kRadix / kThreads : 1;
+  constexpr int kDigitThreads = kRadix / DPT;        // threads that own digits
+  constexpr int W = 16;                              // predecessors per look-back round
+  __shared__ KeyT s_keys[kTile];
+  __shared__ int32_t s_vals[kTile];
+  __shared__ uint16_t s_cnt[kWaves][kRadix];         // per-wave digit counts, then offsets
+  __shared__ int32_t s_shift[kRadix];                // global position - local position
+  __shared__ int32_t s_local[kRadix];                // tile-local start of each digit
+  __shared__ uint32_t s_scan[kWaves];
   __shared__ uint32_t s_tile;
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = first_lane(tid >> 6);
+  const bool owner = tid < kDigitThreads;
   if (tid == 0) s_tile = add_agent(ticket, 1u);
-  for (int i = tid; i < kSortWaves * kRadix; i += kSortThreads) (&s_cnt[0][0])[i] = 0;
-  __syncthreads();
-  const int tile = static_cast<int>(s_tile);
-  const int64_t base = int64_t(tile) * kSortTile;
   const uint32_t mask = nbits > 0 ? (1u << nbits) - 1 : 0u;
 
-  // Wave w owns tile items [w*16*64, (w+1)*16*64); item i of a lane is
-  // base + w*1024 + i*64 + lane, so (wave, i, lane) order is position order.
-  KeyT key[kSortItems];
-  int32_t val[kSortItems];
-  uint32_t dig[kSortItems];
+  // Item i of a lane is base + wave*256 + i*64 + lane: (wave, i, lane) order
+  // is position order. Fetched for tile blockIdx.x while the ticket flies.
+  KeyT key[kItems];
+  int32_t val[kItems];
+  auto fetch = [&](int64_t base) {
 #pragma unroll
-  for (int i = 0; i < kSortItems; ++i) {
-    const int64_t pos = base + int64_t(wave) * (kSortItems * kWave) + i * kWave + lane;
-    const bool ok = pos < K;
-    key[i] = ok ? keys_in[pos] : KeyT(0);
-    val[i] = ok ? (vals_in ? vals_in[pos] : static_cast<int32_t>(pos)) : 0;
-    dig[i] = ok ? static_cast<uint32_t>(key_bits(key[i]) >> shift) & mask : kRadix;
+    for (int i = 0; i < kItems; ++i) {
+      const int64_t pos = base + int64_t(wave) * (kItems * kWave) + i * kWave + lane;
+      const bool ok = pos < K;
+      key[i] = ok ? keys_in[pos] : KeyT(0);
+      val[i] = ok ? (vals_in ? vals_in[pos] : static_cast<int32_t>(pos)) : 0;
+    }
+  };
+  fetch(int64_t(blockIdx.x) * kTile);
+  // Totals of this thread's digits over the whole input.
+  uint32_t dig_total[DPT];
+#pragma unroll
+  for (int i = 0; i < DPT; ++i) dig_total[i] = 0;
+  if (owner) {
+    for (int b = 0; b < hist_blocks; b += 4) {
+      uint32_t h[4][DPT];
+#pragma unroll
+      for (int r = 0; r < 4; ++r)
+#pragma unroll
+        for (int i = 0; i < DPT; ++i)
+          h[r][i] = b + r < hist_blocks ? bhist[size_t(b + r) * hist_stride + tid * DPT + i] : 0u;
+#pragma unroll
+      for (int r = 0; r < 4; ++r)
+#pragma unroll
+        for (int i = 0; i < DPT; ++i) dig_total[i] += h[r][i];
+    }
+  }
+  for (int i = tid; i < kWaves * kRadix / 2; i += kThreads)
+    reinterpret_cast<uint32_t*>(&s_cnt[0][0])[i] = 0;
+  __syncthreads();
+  const int tile = first_lane(static_cast<int>(s_tile));
+  const int64_t base = int64_t(tile) * kTile;
+  if (tile != static_cast<int>(blockIdx.x)) fetch(base);
+
+  uint32_t dig[kItems];
+#pragma unroll
+  for (int i = 0; i < kItems; ++i) {
+    const int64_t pos = base + int64_t(wave) * (kItems * kWave) + i * kWave + lane;
+    dig[i] = pos < K ? digit_of(key[i], shift, mask) : kRadix;
   }
 
   // Rank every key among the equal-digit keys before it in its wave.
-  uint32_t rank[kSortItems];
+  uint32_t rank[kItems];
 #pragma unroll
-  for (int i = 0; i < kSortItems; ++i) {
+  for (int i = 0; i < kItems; ++i) {
     const bool ok = dig[i] < kRadix;
     uint64_t peers = ballot(ok);
-    for (int b = 0; b < nbits; ++b) {
-      const bool bit = (dig[i] >> b) & 1u;
-      const uint64_t bb = ballot(bit);
-      peers &= bit ? bb : ~bb;
+#pragma unroll
+    for (int b = 0; b < RB; ++b) {
+      if (b < nbits) {
+        const bool bit = (dig[i] >> b) & 1u;
+        const uint64_t bb = ballot(bit);
+        peers &= bit ? bb : ~bb;
+      }
     }
     uint32_t prior = 0;
     if (ok) prior = s_cnt[wave][dig[i]];
-    rank[i] = prior + popc_below(peers);
-    if (ok && popc_below(peers) == 0) s_cnt[wave][dig[i]] = prior + __popcll(peers);
+    const uint32_t below = popc_below(peers);
+    rank[i] = prior + below;
+    if (ok && below == 0) s_cnt[wave][dig[i]] = static_cast<uint16_t>(prior + __popcll(peers));
   }
   __syncthreads();
 
-  // Thread d: per-wave exclusive offsets of digit d, tile total of digit d.
-  const int d = tid;
-  uint32_t tot = 0;
+  // Per-wave exclusive offsets and tile counts of this thread's digits,
+  // published at once for the tiles after this one.
+  uint32_t tot[DPT];
+  uint32_t tsum = 0, gsum = 0;
 #pragma unroll
-  for (int w = 0; w < kSortWaves; ++w) {
-    const uint32_t c = s_cnt[w][d];
-    s_cnt[w][d] = tot;
-    tot += c;
+  for (int i = 0; i < DPT; ++i) {
+    tot[i] = 0;
+    if (owner) {
+      const int d = tid * DPT + i;
+      uint32_t t = 0;
+#pragma unroll
+      for (int w = 0; w < kWaves; ++w) {
+        const uint32_t c = s_cnt[w][d];
+        s_cnt[w][d] = static_cast<uint16_t>(t);
+        t += c;
+      }
+      tot[i] = t;
+      tsum += t;
+      gsum += dig_total[i];
+      st_agent(status + size_t(tile) * kRadix + d, (tile == 0 ? kFlagPrefix : kFlagAgg) | t);
+    }
   }
-  uint32_t tile_sum;
-  const uint32_t local = block256_excl_sum<uint32_t>(tot, s_scan, tile_sum);
-  uint32_t hist_sum;
-  const uint32_t gbase = block256_excl_sum<uint32_t>(hist[d], s_scan, hist_sum);
-  s_local[d] = static_cast<int32_t>(local);
+  uint32_t tile_sum, all_sum;
+  uint32_t local = block_excl_sum<kWaves, uint32_t>(tsum, s_scan, tile_sum);
+  uint32_t gbase = block_excl_sum<kWaves, uint32_t>(gsum, s_scan, all_sum);
 
-  // Decoupled look-back for digit d.
-  uint32_t* my = status + size_t(tile) * kRadix + d;
-  uint32_t excl = 0;
-  if (tile == 0) {
-    st_agent(my, kFlagPrefix | tot);
-  } else {
-    st_agent(my, kFlagAgg | tot);
-    int j = tile - 1;
+  // Decoupled look-back for this thread's digits, W predecessors per round.
+  uint32_t excl[DPT];
+#pragma unroll
+  for (int i = 0; i < DPT; ++i) excl[i] = 0;
+  if (tile > 0 && owner) {
+    int j[DPT];
+    bool done[DPT];
+#pragma unroll
+    for (int i = 0; i < DPT; ++i) { j[i] = tile - 1; done[i] = false; }
     uint32_t spins = 0;
     while (true) {
-      const uint32_t s = ld_agent(status + size_t(j) * kRadix + d);
-      const uint32_t f = s & ~kValMask;
-      if (f == 0) {
+      bool all_done = true, stalled = false;
+      uint32_t s[DPT][W];
+#pragma unroll
+      for (int i = 0; i < DPT; ++i)
+#pragma unroll
+        for (int r = 0; r < W; ++r)
+          s[i][r] = (!done[i] && j[i] - r >= 0)
+                        ? ld_agent(status + size_t(j[i] - r) * kRadix + tid * DPT + i)
+                        : kFlagPrefix;
+#pragma unroll
+      for (int i = 0; i < DPT; ++i) {
+        if (done[i]) continue;
+        bool stop = false;
+        int used = 0;
+#pragma unroll
+        for (int r = 0; r < W; ++r) {
+          if (!stop) {
+            const uint32_t f = s[i][r] & ~kValMask;
+            if (f == 0) {
+              stop = true;
+              stalled = true;
+            } else {
+              excl[i] += s[i][r] & kValMask;
+              ++used;
+              if (f == kFlagPrefix) { stop = true; done[i] = true; }
+            }
+          }
+        }
+        j[i] -= used;
+        all_done &= done[i];
+      }
+      if (all_done) break;
+      if (stalled) {
         if (++spins > kSpinLimit) { raise_err(dev_err, LM_DEVERR_SPIN); break; }
         __builtin_amdgcn_s_sleep(1);
-        continue;
       }
-      excl += s & kValMask;
-      if (f == kFlagPrefix || j == 0) break;
-      --j;
     }
-    st_agent(my, kFlagPrefix | ((excl + tot) & kValMask));
+#pragma unroll
+    for (int i = 0; i < DPT; ++i)
+      st_agent(status + size_t(tile) * kRadix + tid * DPT + i,
+               kFlagPrefix | ((excl[i] + tot[i]) & kValMask));
   }
-  s_shift[d] = static_cast<int32_t>(gbase + excl) - static_cast<int32_t>(local);
+  if (owner) {
+#pragma unroll
+    for (int i = 0; i < DPT; ++i) {
+      const int d = tid * DPT + i;
+      s_local[d] = static_cast<int32_t>(local);
+      s_shift[d] = static_cast<int32_t>(gbase + excl[i]) - static_cast<int32_t>(local);
+      local += tot[i];
+      gbase += dig_total[i];
+    }
+  }
   __syncthreads();
 
   // Reorder the tile in LDS by digit (stable), then write digit runs out.
 #pragma unroll
-  for (int i = 0; i < kSortItems; ++i) {
+  for (int i = 0; i < kItems; ++i) {
     if (dig[i] < kRadix) {
-      const int lp = s_local[dig[i]] + static_cast<int>(s_cnt[wave][dig[i]] + rank[i]);
+      const int lp = s_local[dig[i]] + static_cast<int>(s_cnt[wave][dig[i]]) + static_cast<int>(rank[i]);
       s_keys[lp] = key[i];
       s_vals[lp] = val[i];
     }
   }
   __syncthreads();
-  const int n = static_cast<int>(K - base < kSortTile ? K - base : kSortTile);
-  for (int j = tid; j < n; j += kSortThreads) {
-    const KeyT k = s_keys[j];
-    const uint32_t dd = static_cast<uint32_t>(key_bits(k) >> shift) & mask;
-    const int gp = s_shift[dd] + j;
-    // Only a failed look-back (LM_DEVERR_SPIN already raised) leaves gp out
-    // of range; never write outside the buffers.
-    if (static_cast<uint32_t>(gp) < static_cast<uint32_t>(K)) {
-      keys_out[gp] = k;
-      vals_out[gp] = s_vals[j];
+  const int n = static_cast<int>(K - base < kTile ? K - base : kTile);
+#pragma unroll
+  for (int i = 0; i < kItems; ++i) {
+    const int jj = tid + i * kThreads;
+    if (jj < n) {
+      const KeyT k = s_keys[jj];
+      const int gp = s_shift[digit_of(k, shift, mask)] + jj;
+      // Only a look-back that gave up (LM_DEVERR_SPIN) leaves gp out of
+      // range; never write outside the buffers.
+      if (static_cast<uint32_t>(gp) < static_cast<uint32_t>(K)) {
+        keys_out[gp] = k;
+        vals_out[gp] = s_vals[jj];
+      }
     }
   }
 }
 
 // ---------------------------------------------------------------------------
-// k_dedup
+// k_dedup: thread t of tile `tile` owns the 4 sorted positions
+// base + 4t .. base + 4t + 3.
 // ---------------------------------------------------------------------------
 template <typename KeyT>
-__global__ __launch_bounds__(kSortThreads) void k_dedup(
+__global__ __launch_bounds__(kThreads) void k_dedup(
     const KeyT* __restrict__ skeys, const int32_t* __restrict__ perm, int K, int cap,
     KeyT* __restrict__ uniq, int32_t* __restrict__ counts, int32_t* __restrict__ offsets,
     int32_t* __restrict__ inverse, int64_t* __restrict__ num_unique,
-    uint64_t* __restrict__ status, uint32_t* __restrict__ ticket,
-    uint32_t* __restrict__ hist, int hist_words, int32_t* __restrict__ dev_err) {
-  __shared__ KeyT s_keys[kDedupTile + 2];  // [0]: key before the tile, [n+1]: key after
-  __shared__ uint32_t s_scan[4];
-  __shared__ int s_maxs[4];
+    uint64_t* __restrict__ status, uint32_t* __restrict__ ticket, int32_t* __restrict__ dev_err) {
+  __shared__ uint32_t s_scan[kWaves];
+  __shared__ int s_maxs[kWaves];
   __shared__ uint32_t s_tile;
   __shared__ uint32_t s_excl_heads;
   __shared__ int s_excl_last;
 
-  const int tid = threadIdx.x;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = first_lane(tid >> 6);
   if (tid == 0) s_tile = add_agent(ticket, 1u);
+  KeyT k[kItems], kprev, knext;
+  int32_t src[kItems];
+  auto fetch = [&](int64_t base) {
+    const int64_t p0 = base + int64_t(tid) * kItems;
+#pragma unroll
+    for (int i = 0; i < kItems; ++i) {
+      const bool ok = p0 + i < K;
+      k[i] = ok ? skeys[p0 + i] : KeyT(0);
+      src[i] = ok ? perm[p0 + i] : 0;
+    }
+    kprev = p0 > 0 && p0 - 1 < K ? skeys[p0 - 1] : KeyT(0);
+    knext = p0 + kItems < K ? skeys[p0 + kItems] : KeyT(0);
+  };
+  fetch(int64_t(blockIdx.x) * kTile);
   __syncthreads();
-  const int tile = static_cast<int>(s_tile);
-  const int64_t base = int64_t(tile) * kDedupTile;
-  const int n = static_cast<int>(K - base < kDedupTile ? K - base : kDedupTile);
+  const int tile = first_lane(static_cast<int>(s_tile));
+  const int64_t base = int64_t(tile) * kTile;
+  if (tile != static_cast<int>(blockIdx.x)) fetch(base);
+  const int64_t p0 = base + int64_t(tid) * kItems;
 
-  // The histogram control block is no longer needed by this call: leave it
-  // zero for the next one.
-  if (tile == 0)
-    for (int i = tid; i < hist_words; i += kSortThreads) hist[i] = 0;
-
-  for (int j = tid; j < n; j += kSortThreads) s_keys[j + 1] = skeys[base + j];
-  if (tid == 0) s_keys[0] = base > 0 ? skeys[base - 1] : KeyT(0);
-  if (tid == 1) s_keys[n + 1] = base + n < K ? skeys[base + n] : KeyT(0);
-  __syncthreads();
-
-  // Thread t owns positions base + t*16 + i. Run heads and tails become
-  // bit masks first (bit i: item i), evaluated without short-circuit
-  // branches: ROCm 7.2's compiler dropped `last = p` on the branchy form
-  // of this loop when the head was a thread's first item.
-  const int first = tid * kDedupItems;
+  // Run heads and tails as bit masks (bit i: item i), evaluated without
+  // short-circuit branches: ROCm 7.2's compiler dropped `last = p` on the
+  // branchy form of this loop when the head was a thread's first item.
   uint32_t hmask = 0, tmask = 0;
 #pragma unroll
-  for (int i = 0; i < kDedupItems; ++i) {
-    const int j = first + i;
-    if (j < n) {
-      const int64_t p = base + j;
-      const KeyT k = s_keys[j + 1];
-      const bool head = (p == 0) | (k != s_keys[j]);
-      const bool tail = (p == K - 1) | (s_keys[j + 2] != k);
+  for (int i = 0; i < kItems; ++i) {
+    const int64_t p = p0 + i;
+    if (p < K) {
+      const KeyT prev = i == 0 ? kprev : k[i - 1];
+      const KeyT next = i + 1 < kItems ? k[i + 1] : knext;
+      const bool head = (p == 0) | (k[i] != prev);
+      const bool tail = (p == K - 1) | (next != k[i]);
       hmask |= static_cast<uint32_t>(head) << i;
       tmask |= static_cast<uint32_t>(tail) << i;
     }
   }
   const uint32_t nheads = static_cast<uint32_t>(__popc(hmask));
-  const int last_head =
-      hmask ? static_cast<int>(base) + first + (31 - __clz(static_cast<int>(hmask))) : -1;
+  const int last_head = hmask ? static_cast<int>(p0) + (31 - __clz(static_cast<int>(hmask))) : -1;
   uint32_t tile_heads;
-  const uint32_t heads_before = block256_excl_sum<uint32_t>(nheads, s_scan, tile_heads);
+  const uint32_t heads_before = block_excl_sum<kWaves, uint32_t>(nheads, s_scan, tile_heads);
   int tile_last;
-  const int last_before = block256_excl_max(last_head, s_maxs, tile_last);
+  const int last_before = block_excl_max<kWaves>(last_head, s_maxs, tile_last);
 
-  if (tid == 0) {
+  // Wave 0: publish the tile aggregate, then look back 64 tiles per round.
+  if (wave == 0) {
     uint64_t* my = status + tile;
+    const uint64_t agg = (uint64_t(tile_heads) << 31) | uint64_t(tile_last + 1);
+    if (lane == 0) st_agent(my, (tile == 0 ? kDFlagPrefix : kDFlagAgg) | agg);
     uint32_t eh = 0;
     int el = -1;
-    if (tile == 0) {
-      st_agent(my, kDFlagPrefix | (uint64_t(tile_heads) << 31) | uint64_t(tile_last + 1));
-    } else {
-      st_agent(my, kDFlagAgg | (uint64_t(tile_heads) << 31) | uint64_t(tile_last + 1));
+    if (tile > 0) {
       int j = tile - 1;
       uint32_t spins = 0;
       while (true) {
-        const uint64_t s = ld_agent(status + j);
-        const uint64_t f = s & (3ull << 62);
-        if (f == 0) {
+        const int pos = j - lane;
+        const uint64_t s = pos >= 0 ? ld_agent(status + pos) : kDFlagPrefix;
+        const uint64_t f = s & kDFlags;
+        const uint64_t notready = ballot(f == 0);
+        const uint64_t prefix = ballot(f == kDFlagPrefix);
+        const int first_nr = notready ? __builtin_ctzll(notready) : kWave;
+        const int first_px = prefix ? __builtin_ctzll(prefix) : kWave;
+        const bool done = first_px < first_nr;
+        const int take = done ? first_px + 1 : first_nr;  // lanes [0, take) are consumed
+        const bool mine = lane < take;
+        uint32_t h = mine ? static_cast<uint32_t>((s >> 31) & kD31) : 0u;
+#pragma unroll
+        for (int off = 32; off >= 1; off >>= 1) h += __shfl_xor(h, off, kWave);
+        eh += h;
+        // the nearest consumed predecessor that has a head holds the last one
+        const int pl = static_cast<int>(s & kD31) - 1;
+        const uint64_t has = ballot(mine && pl >= 0);
+        if (el < 0 && has) el = read_lane(pl, __builtin_ctzll(has));
+        if (done) break;
+        j -= take;
+        if (take == 0) {
           if (++spins > kSpinLimit) { raise_err(dev_err, LM_DEVERR_SPIN); break; }
           __builtin_amdgcn_s_sleep(1);
-          continue;
         }
-        eh += static_cast<uint32_t>((s >> 31) & kD31);
-        const int pl = static_cast<int>(s & kD31) - 1;
-        if (el < 0) el = pl;
-        if (f == kDFlagPrefix || j == 0) break;
-        --j;
       }
       const int incl_last = tile_last >= 0 ? tile_last : el;
-      st_agent(my, kDFlagPrefix | (uint64_t(eh + tile_heads) << 31) | uint64_t(incl_last + 1));
+      if (lane == 0)
+        st_agent(my, kDFlagPrefix | (uint64_t(eh + tile_heads) << 31) | uint64_t(incl_last + 1));
     }
-    s_excl_heads = eh;
-    s_excl_last = el;
+    if (lane == 0) {
+      s_excl_heads = eh;
+      s_excl_last = el;
+    }
   }
   __syncthreads();
 
@@ -323,23 +477,20 @@ __global__ __launch_bounds__(kSortThreads) void k_dedup(
   int hp = last_before >= 0 ? last_before : s_excl_last;
   bool over = false;
 #pragma unroll
-  for (int i = 0; i < kDedupItems; ++i) {
-    const int j = first + i;
-    if (j < n) {
-      const int64_t p = base + j;
-      const KeyT k = s_keys[j + 1];
+  for (int i = 0; i < kItems; ++i) {
+    const int64_t p = p0 + i;
+    if (p < K) {
       const bool head = (hmask >> i) & 1u;
       seg += head ? 1 : 0;
       hp = head ? static_cast<int>(p) : hp;
       const bool in_cap = static_cast<uint32_t>(seg) < static_cast<uint32_t>(cap);
       over |= !in_cap;
       if (head && in_cap) {
-        uniq[seg] = k;
+        uniq[seg] = k[i];
         offsets[seg] = static_cast<int32_t>(p);
       }
       if (((tmask >> i) & 1u) && in_cap) counts[seg] = static_cast<int32_t>(p + 1 - hp);
-      const int32_t src = perm[p];
-      if (static_cast<uint32_t>(src) < static_cast<uint32_t>(K)) inverse[src] = seg;
+      if (static_cast<uint32_t>(src[i]) < static_cast<uint32_t>(K)) inverse[src[i]] = seg;
       else over = true;
       if (p == K - 1) {
         *num_unique = seg + 1 < cap ? seg + 1 : cap;
@@ -364,6 +515,18 @@ size_t unique_workspace_bytes(int64_t K, int idtype, int64_t V) {
   return unique_layout(K, idtype, V).total;
 }
 
+template <typename KeyT, int RB>
+static hipError_t launch_pass(const UniqueLayout& L, int p, const KeyT* kin, const int32_t* vin,
+                              KeyT* kout, int32_t* vout, int K, uint32_t* bhist,
+                              uint32_t* status, uint32_t* tickets, int32_t* dev_err,
+                              hipStream_t st) {
+  k_onesweep<KeyT, RB><<<L.tiles, kThreads, 0, st>>>(
+      kin, vin, kout, vout, K, L.shift[p], L.nbits[p], bhist + size_t(p) * kMaxRadix,
+      L.hist_blocks, L.passes * kMaxRadix, status + size_t(p) * L.tiles * kMaxRadix, tickets + p,
+      dev_err);
+  return hipGetLastError();
+}
+
 template <typename KeyT>
 static int run_unique(const KeyT* ids, int K, int64_t V, KeyT* uniq, int32_t* counts,
                       int32_t* offsets, int32_t* inverse, int32_t* perm, int64_t* num_unique,
@@ -372,41 +535,39 @@ static int run_unique(const KeyT* ids, int K, int64_t V, KeyT* uniq, int32_t* co
     k_unique_empty<<<1, 64, 0, st>>>(num_unique, offsets);
     return launch_status(hipGetLastError());
   }
-  uint32_t* hist = reinterpret_cast<uint32_t*>(ws + L.hist);
+  uint32_t* bhist = reinterpret_cast<uint32_t*>(ws + L.bhist);
   uint32_t* tickets = reinterpret_cast<uint32_t*>(ws + L.tickets);
   uint32_t* status = reinterpret_cast<uint32_t*>(ws + L.status);
   uint64_t* dstatus = reinterpret_cast<uint64_t*>(ws + L.dstatus);
   KeyT* kb[2] = {reinterpret_cast<KeyT*>(ws + L.keys0), reinterpret_cast<KeyT*>(ws + L.keys1)};
   int32_t* vb[2] = {reinterpret_cast<int32_t*>(ws + L.vals0), reinterpret_cast<int32_t*>(ws + L.vals1)};
 
-  // tickets .. end of dstatus is contiguous: clear it in k_hist.
+  PassBits pb{};
+  for (int p = 0; p < L.passes; ++p) {
+    pb.shift[p] = L.shift[p];
+    pb.nbits[p] = L.nbits[p];
+  }
+  // tickets .. end of dstatus is contiguous: k_hist clears it.
   const int64_t clear_words = static_cast<int64_t>((L.keys0 - L.tickets) / 4);
-  int hist_blocks = (K + kSortThreads * 16 - 1) / (kSortThreads * 16);
-  if (hist_blocks > 1024) hist_blocks = 1024;
-  const int64_t clear_blocks = (clear_words + kSortThreads * 8 - 1) / (kSortThreads * 8);
-  if (hist_blocks < clear_blocks) hist_blocks = static_cast<int>(clear_blocks < 1024 ? clear_blocks : 1024);
-  k_hist<KeyT><<<hist_blocks, kSortThreads, 0, st>>>(ids, K, static_cast<uint64_t>(V), L.passes,
-                                                     L.bits, hist, tickets, clear_words, dev_err);
+  const size_t hist_lds = size_t(L.passes) * kMaxRadix * 4;
+  k_hist<KeyT><<<L.hist_blocks, kThreads, hist_lds, st>>>(
+      ids, K, static_cast<uint64_t>(V), L.passes, pb, bhist, tickets, clear_words, dev_err);
   if (hipError_t e = hipGetLastError(); e != hipSuccess) return launch_status(e);
 
   const KeyT* kin = ids;
   const int32_t* vin = nullptr;
   for (int p = 0; p < L.passes; ++p) {
-    const int shift = 8 * p;
-    const int nb = L.bits - shift < 8 ? L.bits - shift : 8;
     KeyT* kout = kb[p & 1];
     int32_t* vout = p == L.passes - 1 ? perm : vb[p & 1];
-    k_onesweep<KeyT><<<L.tiles, kSortThreads, 0, st>>>(
-        kin, vin, kout, vout, K, shift, nb < 0 ? 0 : nb, hist + p * kRadix,
-        status + size_t(p) * L.tiles * kRadix, tickets + p, dev_err);
-    if (hipError_t e = hipGetLastError(); e != hipSuccess) return launch_status(e);
+    const hipError_t e = launch_pass<KeyT, kMaxDigitBits>(L, p, kin, vin, kout, vout, K, bhist,
+                                                          status, tickets, dev_err, st);
+    if (e != hipSuccess) return launch_status(e);
     kin = kout;
     vin = vout;
   }
-  k_dedup<KeyT><<<L.dtiles, kSortThreads, 0, st>>>(
+  k_dedup<KeyT><<<L.tiles, kThreads, 0, st>>>(
       kin, perm, K, static_cast<int>(K < V ? K : V), uniq, counts, offsets, inverse, num_unique,
-      dstatus, tickets + kMaxPasses,
-      hist, L.passes * kRadix, dev_err);
+      dstatus, tickets + kMaxPasses, dev_err);
   return launch_status(hipGetLastError());
 }
 

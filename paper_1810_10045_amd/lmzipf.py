@@ -25,7 +25,6 @@ I32, I64 = 0, 1
 F32, BF16 = 0, 1
 FILL_EXPAND, FILL_SCATTER, FILL_SCATTER_ADD = 0, 1, 2
 OPT_SGD, OPT_ADAM = 0, 1
-UNIQUE_CTRL_BYTES = 8192
 MAX_K = 1 << 30
 
 EXPORTS = ("lm_status_string", "lm_abi_version", "lm_workspace_clear",
@@ -58,7 +57,7 @@ def _load():
     L.lm_unique.argtypes = [P, I32_, I64_, I64_, P, P, P, P, P, P, P, P, SZ, P]
     L.lm_segsum_workspace_bytes.argtypes = [I64_, I64_]
     L.lm_segsum_workspace_bytes.restype = SZ
-    L.lm_segsum.argtypes = [P, I32_, I64_, I64_, I64_, P, P, P, I64_, P, I64_, P, P, SZ, P]
+    L.lm_segsum.argtypes = [P, I32_, I64_, I64_, I64_, P, P, P, P, I64_, P, I64_, P, P, SZ, P]
     L.lm_map_ids.argtypes = [P, P, I64_, P, P, I64_, I32_, P, P, P]
     L.lm_fill_values.argtypes = [P, I64_, P, P, I64_, P, P, I32_, I64_, P, I64_, I64_, I32_, P, P]
     L.lm_sparse_apply.argtypes = [P, I64_, I64_, I64_, P, I32_, P, I64_, P, I64_, I32_,
@@ -122,17 +121,18 @@ def _dev(t: torch.Tensor, what: str):
 
 
 class Workspace:
-    """A device scratch buffer that grows on demand. The unique control block
-    (its first 8 KiB) starts zero and every lm_unique leaves it zero."""
+    """A device scratch buffer that grows on demand (no entry point needs
+    particular initial contents). Torch's allocator returns 512-byte aligned
+    blocks, above the 256 bytes the library asks for."""
 
     def __init__(self, device=None):
         self.device = torch.device(device or "cuda")
-        self.buf = torch.zeros(0, dtype=torch.uint8, device=self.device)
+        self.buf = torch.empty(0, dtype=torch.uint8, device=self.device)
 
     def get(self, nbytes: int) -> torch.Tensor:
-        nbytes = max(int(nbytes), UNIQUE_CTRL_BYTES)
+        nbytes = max(int(nbytes), 256)
         if self.buf.numel() < nbytes:
-            self.buf = torch.zeros(nbytes + 256, dtype=torch.uint8, device=self.device)
+            self.buf = torch.empty(nbytes, dtype=torch.uint8, device=self.device)
         return self.buf
 
 
@@ -198,7 +198,7 @@ def unique(ids: torch.Tensor, V: int, out: Optional[UniqueResult] = None,
     return out
 
 
-def segsum(grad: torch.Tensor, perm: torch.Tensor, offsets: torch.Tensor,
+def segsum(grad: torch.Tensor, perm: torch.Tensor, inverse: torch.Tensor, offsets: torch.Tensor,
            num_unique: torch.Tensor, u_cap: Optional[int] = None,
            out: Optional[torch.Tensor] = None, dev_err: Optional[torch.Tensor] = None,
            ws: Optional[Workspace] = None, stream=None) -> torch.Tensor:
@@ -209,8 +209,8 @@ def segsum(grad: torch.Tensor, perm: torch.Tensor, offsets: torch.Tensor,
     ld = _rows(grad, "grad")
     if u_cap is None:
         u_cap = offsets.numel() - 1
-    if perm.numel() < K or offsets.numel() < 1:
-        raise LmError("perm must hold K entries")
+    if perm.numel() < K or inverse.numel() < K or offsets.numel() < 1:
+        raise LmError("perm and inverse must hold K entries")
     if out is None:
         out = torch.empty((max(u_cap, 1), D), dtype=torch.float32, device=grad.device)
     if out.shape[0] < u_cap or out.shape[1] != D:
@@ -220,7 +220,7 @@ def segsum(grad: torch.Tensor, perm: torch.Tensor, offsets: torch.Tensor,
         dev_err = torch.zeros(1, dtype=torch.int32, device=grad.device)
     ws = ws or default_workspace(grad.device)
     buf = ws.get(_lib.lm_segsum_workspace_bytes(K, D))
-    _call(_lib.lm_segsum(_ptr(grad), _gtype(grad), K, D, ld, _ptr(perm), _ptr(offsets),
+    _call(_lib.lm_segsum(_ptr(grad), _gtype(grad), K, D, ld, _ptr(perm), _ptr(inverse), _ptr(offsets),
                          _ptr(num_unique), u_cap, _ptr(out), ld_out, _ptr(dev_err), _ptr(buf),
                          buf.numel(), _stream(stream)), "lm_segsum")
     return out

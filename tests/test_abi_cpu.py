@@ -82,12 +82,12 @@ def test_argument_errors_return_before_any_launch(lib):
     assert lib.lm_unique(_v(), 0, 10, 10, *([_v()] * 7), None, 1 << 20, None) == 1
     assert lib.lm_unique(_v(), 0, 10, 10, *([_v()] * 7), _v(0x1010), 1 << 20, None) == 1
     assert lib.lm_unique(_v(), 0, 10, 10, *([_v()] * 7), _v(), 16, None) == 3
-    lib.lm_segsum.argtypes = [P, I32, I64, I64, I64, P, P, P, I64, P, I64, P, P, SZ, P]
-    assert lib.lm_segsum(_v(), 2, 10, 4, 4, _v(), _v(), _v(), 10, _v(), 4, _v(), _v(), 1 << 20, None) == 5
-    assert lib.lm_segsum(_v(), 0, 10, 4, 3, _v(), _v(), _v(), 10, _v(), 4, _v(), _v(), 1 << 20, None) == 1
-    assert lib.lm_segsum(_v(), 0, 10, 4, 4, _v(), _v(), _v(), 10, _v(), 2, _v(), _v(), 1 << 20, None) == 1
-    assert lib.lm_segsum(None, 0, 10, 4, 4, _v(), _v(), _v(), 10, _v(), 4, _v(), _v(), 1 << 20, None) == 1
-    assert lib.lm_segsum(_v(), 0, 10, 4, 4, _v(), _v(), _v(), 10, _v(), 4, _v(), _v(), 8, None) == 3
+    lib.lm_segsum.argtypes = [P, I32, I64, I64, I64, P, P, P, P, I64, P, I64, P, P, SZ, P]
+    assert lib.lm_segsum(_v(), 2, 10, 4, 4, _v(), _v(), _v(), _v(), 10, _v(), 4, _v(), _v(), 1 << 20, None) == 5
+    assert lib.lm_segsum(_v(), 0, 10, 4, 3, _v(), _v(), _v(), _v(), 10, _v(), 4, _v(), _v(), 1 << 20, None) == 1
+    assert lib.lm_segsum(_v(), 0, 10, 4, 4, _v(), _v(), _v(), _v(), 10, _v(), 2, _v(), _v(), 1 << 20, None) == 1
+    assert lib.lm_segsum(None, 0, 10, 4, 4, _v(), _v(), _v(), _v(), 10, _v(), 4, _v(), _v(), 1 << 20, None) == 1
+    assert lib.lm_segsum(_v(), 0, 10, 4, 4, _v(), _v(), _v(), _v(), 10, _v(), 4, _v(), _v(), 8, None) == 3
     lib.lm_fill_values.argtypes = [P, I64, P, P, I64, P, P, I32, I64, P, I64, I64, I32, P, P]
     assert lib.lm_fill_values(_v(), 4, _v(), _v(), 10, _v(), _v(), 0, 4, _v(), 10, 4, 9, _v(), None) == 5
     assert lib.lm_fill_values(_v(), 4, _v(), _v(), 10, None, None, 0, 4, _v(), 10, 4, 0, _v(), None) == 1
