@@ -95,15 +95,74 @@ class Batch:
     """One resident batch: ids and gradients on the device (and, for the
     merge workload, shard 0's own ids and gradients)."""
 
-    def __init__(self, w, torch, dev):
-        self.ids = torch.from_numpy(w.ids()).to(dev)
-        g = w.grads_f32()
-        t = torch.from_numpy(g).to(dev)
-        self.grad = t.to(torch.bfloat16) if w.grad_dtype == "bf16" else t
-        del g
+    def __init__(self, w, torch, dev, ids=None, grads=None):
+        self.ids = torch.from_numpy(w.ids() if ids is None else ids).to(dev)
+        # bf16 arrives as its uint16 bit patterns, the oracle's very input
+        g = w.grads() if grads is None else grads
+        t = torch.from_numpy(g)
+        self.grad = (t.view(torch.bfloat16) if w.grad_dtype == "bf16" else t).to(dev)
+        del g, t
         if w.step == "expand":
             self.ids0 = self.ids[:w.K]
             self.grad0 = self.grad[:w.K]
+
+
+class Pipeline:
+    """The timed step: device buffers for one workload and the calls of one
+    pass of the hot path over resident batch b. The full-size parity tests
+    drive this same class, so they check the launches that are timed here."""
+
+    def __init__(self, w, batches, torch, lz, dev, table=None):
+        self.w, self.batches, self.lz = w, batches, lz
+        K, D = w.tokens, w.D
+        idt = torch.int64 if w.id_dtype == "i64" else torch.int32
+        self.ures = lz.unique_buffers(K, w.V, idt, dev)
+        self.ws = lz.Workspace(dev)
+        cap = self.ures.uniq.numel()
+        self.out = torch.empty((cap, D), dtype=torch.float32, device=dev)
+        self.dev_err = self.ures.dev_err
+        self.state = {}
+        st = self.state
+        if w.step in ("sgd", "adam"):
+            st["table"] = torch.from_numpy(w.table() if table is None else table).to(dev)
+        elif w.step == "scatter":
+            st["table"] = torch.zeros((w.V, D), dtype=torch.float32, device=dev)
+        if w.step == "adam":
+            st["m"] = torch.zeros_like(st["table"])
+            st["v"] = torch.zeros_like(st["table"])
+        if w.step == "expand":
+            st["u0"] = lz.unique_buffers(w.K, w.V, idt, dev)
+            st["out0"] = torch.empty((st["u0"].uniq.numel(), D), dtype=torch.float32, device=dev)
+            st["M"] = torch.empty((cap, D), dtype=torch.float32, device=dev)
+
+    def step(self, b, ev=None):
+        w, lz, st, ures, err = self.w, self.lz, self.state, self.ures, self.dev_err
+        bt = self.batches[b % len(self.batches)]
+        if ev: ev(0)
+        lz.unique(bt.ids, w.V, out=ures, ws=self.ws)
+        if ev: ev(1)
+        lz.segsum(bt.grad, ures.perm, ures.inverse, ures.offsets, ures.num_unique, out=self.out,
+                  dev_err=err, ws=self.ws)
+        if ev: ev(2)
+        if w.step == "sgd":
+            lz.sparse_apply(st["table"], ures.uniq, ures.num_unique, self.out, "sgd", lr=w.lr,
+                            dev_err=err)
+        elif w.step == "adam":
+            b1, b2, eps = w.adam
+            lz.sparse_apply(st["table"], ures.uniq, ures.num_unique, self.out, "adam", lr=w.lr,
+                            beta1=b1, beta2=b2, eps=eps, step=1 + b, m=st["m"], v=st["v"],
+                            dev_err=err)
+        elif w.step == "scatter":
+            lz.fill_values(self.out, ures.uniq, ures.num_unique, st["table"], None, None,
+                           "scatter", dev_err=err)
+        elif w.step == "expand":
+            u0 = st["u0"]
+            lz.unique(bt.ids0, w.V, out=u0, ws=self.ws)
+            lz.segsum(bt.grad0, u0.perm, u0.inverse, u0.offsets, u0.num_unique, out=st["out0"],
+                      dev_err=err, ws=self.ws)
+            lz.fill_values(st["out0"], u0.uniq, u0.num_unique, st["M"], ures.uniq,
+                           ures.num_unique, "expand", dev_err=err)
+        if ev: ev(3)
 
 
 def run_gpu(w, steps, warmup, nbatch, torch, lz):
@@ -114,51 +173,9 @@ def run_gpu(w, steps, warmup, nbatch, torch, lz):
     batches = [Batch(w.batch(b), torch, dev) for b in range(nbatch)]
     log(f"inputs generated and copied in {time.time() - t0:.1f}s")
     K, D = w.tokens, w.D
-    idt = torch.int64 if w.id_dtype == "i64" else torch.int32
-    ures = lz.unique_buffers(K, w.V, idt, dev)
-    ws = lz.Workspace(dev)
-    cap = ures.uniq.numel()
-    out = torch.empty((cap, D), dtype=torch.float32, device=dev)
-    dev_err = ures.dev_err
-    state = {}
-    if w.step in ("sgd", "adam", "scatter"):
-        state["table"] = torch.from_numpy(w.table()).to(dev) if w.step != "scatter" else \
-            torch.zeros((w.V, D), dtype=torch.float32, device=dev)
-    if w.step == "adam":
-        state["m"] = torch.zeros_like(state["table"])
-        state["v"] = torch.zeros_like(state["table"])
-    if w.step == "expand":
-        state["u0"] = lz.unique_buffers(w.K, w.V, idt, dev)
-        state["out0"] = torch.empty((state["u0"].uniq.numel(), D), dtype=torch.float32, device=dev)
-        state["M"] = torch.empty((cap, D), dtype=torch.float32, device=dev)
+    pipe = Pipeline(w, batches, torch, lz, dev)
+    ures, dev_err, step = pipe.ures, pipe.dev_err, pipe.step
     stream = torch.cuda.current_stream()
-
-    def step(b, ev=None):
-        bt = batches[b % nbatch]
-        if ev: ev(0)
-        lz.unique(bt.ids, w.V, out=ures, ws=ws)
-        if ev: ev(1)
-        lz.segsum(bt.grad, ures.perm, ures.inverse, ures.offsets, ures.num_unique, out=out, dev_err=dev_err, ws=ws)
-        if ev: ev(2)
-        if w.step == "sgd":
-            lz.sparse_apply(state["table"], ures.uniq, ures.num_unique, out, "sgd", lr=w.lr,
-                            dev_err=dev_err)
-        elif w.step == "adam":
-            b1, b2, eps = w.adam
-            lz.sparse_apply(state["table"], ures.uniq, ures.num_unique, out, "adam", lr=w.lr,
-                            beta1=b1, beta2=b2, eps=eps, step=1 + b, m=state["m"], v=state["v"],
-                            dev_err=dev_err)
-        elif w.step == "scatter":
-            lz.fill_values(out, ures.uniq, ures.num_unique, state["table"], None, None, "scatter",
-                           dev_err=dev_err)
-        elif w.step == "expand":
-            u0 = state["u0"]
-            lz.unique(bt.ids0, w.V, out=u0, ws=ws)
-            lz.segsum(bt.grad0, u0.perm, u0.inverse, u0.offsets, u0.num_unique, out=state["out0"],
-                      dev_err=dev_err, ws=ws)
-            lz.fill_values(state["out0"], u0.uniq, u0.num_unique, state["M"], ures.uniq,
-                           ures.num_unique, "expand", dev_err=dev_err)
-        if ev: ev(3)
 
     # Types per batch (read once, outside the timed region).
     U_of = []

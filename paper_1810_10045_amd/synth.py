@@ -49,29 +49,54 @@ def zipf_ids(K: int, V: int, s: float, seed: int, dtype=np.int32) -> np.ndarray:
     return ids.astype(dtype)
 
 
+def distinct_ids(n: int, V: int, seed: int, dtype=np.int32) -> np.ndarray:
+    """n distinct word ids in [0, V), drawn uniformly without replacement and
+    listed in ascending order (a stand-in for a type list, as the row list
+    of an update or the source ids of a fill)."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    return np.sort(rng.choice(V, size=n, replace=False)).astype(dtype)
+
+
 def _threads() -> int:
     n = os.cpu_count() or 1
     return max(1, min(16, n))
 
 
+def _fill_normal(out: np.ndarray, seed: int, b: int, std: float):
+    """Rows [b * ROW_BLOCK, (b + 1) * ROW_BLOCK) of a block-seeded matrix."""
+    lo, hi = b * ROW_BLOCK, min(out.shape[0], (b + 1) * ROW_BLOCK)
+    rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence([seed, b])))
+    rng.standard_normal(out=out[lo:hi], dtype=np.float32)
+    if std != 1.0:
+        out[lo:hi] *= np.float32(std)
+
+
+def _blocks(K: int) -> int:
+    return (K + ROW_BLOCK - 1) // ROW_BLOCK
+
+
 def normal_rows(K: int, D: int, seed: int, std: float = 1.0) -> np.ndarray:
     """K x D fp32 rows ~ N(0, std^2), block-seeded (see module docstring)."""
     out = np.empty((K, D), dtype=np.float32)
-    nblk = (K + ROW_BLOCK - 1) // ROW_BLOCK
-
-    def fill(b: int):
-        lo, hi = b * ROW_BLOCK, min(K, (b + 1) * ROW_BLOCK)
-        rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence([seed, b])))
-        rng.standard_normal(out=out[lo:hi], dtype=np.float32)
-        if std != 1.0:
-            out[lo:hi] *= np.float32(std)
-
+    nblk = _blocks(K)
     if nblk <= 1:
         for b in range(nblk):
-            fill(b)
+            _fill_normal(out, seed, b, std)
     else:
         with ThreadPoolExecutor(_threads()) as ex:
-            list(ex.map(fill, range(nblk)))
+            list(ex.map(lambda b: _fill_normal(out, seed, b, std), range(nblk)))
+    return out
+
+
+def stacked_normal_rows(K: int, D: int, seeds) -> np.ndarray:
+    """Concatenation of normal_rows(K, D, seed) over ``seeds``, filled by one
+    thread pool over every (part, block) pair."""
+    seeds = list(seeds)
+    out = np.empty((K * len(seeds), D), dtype=np.float32)
+    parts = [out[g * K:(g + 1) * K] for g in range(len(seeds))]
+    jobs = [(g, b) for g in range(len(seeds)) for b in range(_blocks(K))]
+    with ThreadPoolExecutor(_threads()) as ex:
+        list(ex.map(lambda j: _fill_normal(parts[j[0]], seeds[j[0]], j[1], 1.0), jobs))
     return out
 
 
@@ -81,11 +106,20 @@ def bf16_bits(x: np.ndarray) -> np.ndarray:
     out = np.empty(x.shape, dtype=np.uint16)
     flat_in = x.reshape(-1).view(np.uint32)
     flat_out = out.reshape(-1)
-    step = 1 << 24
-    for lo in range(0, flat_in.size, step):
+    step = 1 << 22
+
+    def conv(lo: int):
         b = flat_in[lo:lo + step]
         bias = ((b >> np.uint32(16)) & np.uint32(1)) + np.uint32(0x7FFF)
         flat_out[lo:lo + step] = ((b + bias) >> np.uint32(16)).astype(np.uint16)
+
+    starts = range(0, flat_in.size, step)
+    if len(starts) <= 1:
+        for lo in starts:
+            conv(lo)
+    else:
+        with ThreadPoolExecutor(_threads()) as ex:
+            list(ex.map(conv, starts))
     return out
 
 
@@ -140,11 +174,8 @@ class Workload:
         """fp32 gradients (before any bf16 rounding), K*shards x D."""
         if self.shards == 1:
             return normal_rows(self.K, self.D, 1000 * self.number + 2)
-        out = np.empty((self.tokens, self.D), np.float32)
-        for g in range(self.shards):
-            out[g * self.K:(g + 1) * self.K] = normal_rows(
-                self.K, self.D, 1000 * self.number + 200 + g)
-        return out
+        return stacked_normal_rows(self.K, self.D,
+                                   [1000 * self.number + 200 + g for g in range(self.shards)])
 
     def grads(self) -> np.ndarray:
         """Gradients in the workload's storage dtype (bf16 as uint16 bits)."""

@@ -60,3 +60,50 @@ def sum_of_squares(grad, inverse, U, oracle):
     g = np.asarray(grad)
     vals = (g.astype(np.uint32) << np.uint32(16)).view(np.float32) if g.dtype == np.uint16 else g
     return oracle.segsum(np.square(vals, dtype=np.float32), inverse, U)
+
+
+# ---------------------------------------------------------------------------
+# End-to-end bounds: the GPU's update computed from its own Seg-Sum against
+# the oracle's update computed from the oracle's Seg-Sum. delta[u] bounds
+# |S_gpu[u,d] - S_ref[u,d]| (the Seg-Sum tolerance times the row scale); the
+# rest is fp32 rounding of the update itself, with unit roundoff U32.
+# ---------------------------------------------------------------------------
+U32 = 2.0 ** -24
+
+
+def row_delta(S_ref, tol, sumsq=None):
+    """Per-row bound on the Seg-Sum error allowed by the row tolerance."""
+    scale = np.abs(S_ref).max(axis=1)
+    if sumsq is not None:
+        scale = np.maximum(scale, np.sqrt(np.asarray(sumsq, np.float64).mean(axis=1)))
+    return tol * scale
+
+
+def assert_sgd_rows(got, ref, S_ref, lr, delta):
+    """ref = oracle.sgd(p0, S_ref, lr). The GPU subtracts fl(lr * S_gpu)
+    from p0 and rounds: |got - ref| <= lr*delta + 2u(|ref| + lr|S_ref|)."""
+    got = np.asarray(got, np.float64)
+    bound = (lr * delta[:, None] + 2 * U32 * (np.abs(ref) + lr * (np.abs(S_ref) + delta[:, None])))
+    bad = np.abs(got - ref) > bound * 1.01 + 1e-30
+    assert not bad.any(), f"SGD rows: {int(bad.sum())} values outside the bound, first at {np.argwhere(bad)[0]}"
+
+
+def assert_adam_first_step(got_p, got_m, got_v, ref_p, ref_m, ref_v, S_ref, lr, b1, b2, eps, delta):
+    """First lazy-Adam step from zero moments (t = 1, no weight decay):
+    m = (1-b1) g, v = (1-b2) g^2 and the update lr * g / (|g| + eps).
+    Where |g| > 2 delta the update moves by at most lr*delta*eps/(|g|-delta)^2
+    under a perturbation of g by delta; where |g| <= 2 delta its sign is not
+    determined by the tolerance and any update in [-lr, lr] is accepted."""
+    d = delta[:, None]
+    g = np.abs(S_ref)
+    got_p, got_m, got_v = (np.asarray(a, np.float64) for a in (got_p, got_m, got_v))
+    bm = (1 - b1) * d + 8 * U32 * np.abs(ref_m)
+    assert (np.abs(got_m - ref_m) <= bm * 1.01 + 1e-38).all(), "Adam m"
+    bv = (1 - b2) * (2 * g * d + d * d) + 8 * U32 * np.abs(ref_v)
+    assert (np.abs(got_v - ref_v) <= bv * 1.01 + 1e-38).all(), "Adam v"
+    sure = g > 2 * d
+    gap = np.where(sure, g - d, 1.0)
+    bp = np.where(sure, lr * (d * eps / (gap * gap) + 16 * U32), 2 * lr * (1 + 16 * U32))
+    bp = bp + 2 * U32 * np.abs(ref_p)
+    bad = np.abs(got_p - ref_p) > bp * 1.01
+    assert not bad.any(), f"Adam p: {int(bad.sum())} values outside the bound"

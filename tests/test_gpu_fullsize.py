@@ -1,0 +1,217 @@
+"""GPU parity at the full sizes of the five synthetic workloads, through the
+very launches that bench.py times (its Batch and Pipeline, batch 0).
+
+* Unique: every integer output bit-exact against the oracle, whole input.
+* Seg-Sum: per-row tolerance against the oracle's fp64 sums, on every row
+  where the oracle finishes in seconds; on the merge (2M tokens) and the 2M
+  vocabulary a sample of rows (the heaviest types, which span the most
+  chunks and go through the fix-up, plus seeded random types and the first
+  and last), each evaluated by oracle.segsum_select over the tokens of the
+  sampled types only.
+* What follows Seg-Sum, end to end from the oracle's own sums: SCATTER into a
+  dense table (against the dense per-token scatter-add for the 100K x 512
+  case), SGD, the first lazy-Adam step (moments too), EXPAND of shard 0 into
+  the merged type list; rows the step must not touch are compared exactly.
+"""
+import os
+import sys
+
+import numpy as np
+import pytest
+
+sys.path.insert(0, os.path.dirname(os.path.abspath(__file__)))
+import gpu_helpers as H  # noqa: E402
+import oracle  # noqa: E402
+from paper_1810_10045_amd import synth  # noqa: E402
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+N_HEADS, N_RANDOM = 16, 240
+
+
+@pytest.fixture(scope="module")
+def lz():
+    from paper_1810_10045_amd import lmzipf
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    return lmzipf
+
+
+def _say(msg):
+    print(msg, flush=True)
+
+
+def _f32(x):
+    return float(np.float32(x))
+
+
+def _run(lz, w, ids, grads, table=None):
+    """One bench step over batch 0 of workload w (inputs given as host arrays)."""
+    import bench
+    dev = torch.device("cuda:0")
+    _say(f"[fullsize] {w.name}: K={w.tokens} V={w.V} D={w.D} {w.grad_dtype}/{w.id_dtype} {w.step}")
+    pipe = bench.Pipeline(w, [bench.Batch(w, torch, dev, ids=ids, grads=grads)], torch, lz, dev,
+                          table=table)
+    pipe.step(0)
+    torch.cuda.synchronize()
+    lz.check(pipe.dev_err)
+    return pipe
+
+
+def _release(pipe):
+    del pipe
+    torch.cuda.empty_cache()
+
+
+def _as_f32(g):
+    return synth.bf16_to_f32(g) if g.dtype == np.uint16 else g
+
+
+def _sample_types(counts, seed):
+    """Row positions: the N_HEADS heaviest types, N_RANDOM seeded random
+    ones, the first and the last (ascending, distinct)."""
+    U = len(counts)
+    heads = np.argsort(-counts, kind="stable")[:N_HEADS]
+    rnd = np.random.default_rng(seed).choice(U, min(U, N_RANDOM), replace=False)
+    return np.unique(np.concatenate([heads, rnd, [0, U - 1]]))
+
+
+def _sampled_sums(ids, grads, sel_ids):
+    """Oracle Seg-Sum rows (and sums of squares) of the word ids sel_ids,
+    from only the tokens that carry them (the others add nothing)."""
+    keep = np.isin(ids, sel_ids)
+    sub_ids, sub_g = ids[keep], grads[keep]
+    S = oracle.segsum_select(sub_g, sub_ids, sel_ids)
+    sq = oracle.segsum_select(np.square(_as_f32(sub_g)), sub_ids, sel_ids)
+    return S, sq
+
+
+def test_full_word_tiny_8k(lz):
+    """8,192 tokens over 100K words, D = 512: Seg-Sum on every row and the
+    dense V x 512 table filled by SCATTER against the per-token scatter-add."""
+    w = synth.WORKLOADS["word_tiny_8k"]
+    ids, g = w.ids(), w.grads()
+    pipe = _run(lz, w, ids, g)
+    o = H.assert_unique_matches(pipe.ures, ids, w.V, oracle, w.name)
+    U = len(o[0])
+    S = oracle.segsum(g, o[3], U)
+    sq = H.sum_of_squares(g, o[3], U, oracle)
+    assert H.row_rel_err(pipe.out[:U].cpu().numpy(), S, sq) <= H.TOL_F32
+    dense = oracle.dense_scatter(g, ids, w.V)
+    T = pipe.state["table"].cpu().numpy()
+    others = np.ones(w.V, bool)
+    others[o[0]] = False
+    assert np.array_equal(T[others], dense[others]) and not T[others].any()
+    assert H.row_rel_err(T[o[0]], dense[o[0]], sq) <= H.TOL_F32
+    _release(pipe)
+
+
+def test_full_word_step_64k(lz):
+    """The per-GPU word-LM step: 65,536 tokens over 800K words, D = 1024,
+    every Seg-Sum row, then SGD (lr 0.1) into the 800K x 1024 table."""
+    w = synth.WORKLOADS["word_step_64k"]
+    ids, g, table0 = w.ids(), w.grads(), w.table()
+    pipe = _run(lz, w, ids, g, table0)
+    o = H.assert_unique_matches(pipe.ures, ids, w.V, oracle, w.name)
+    U = len(o[0])
+    S = oracle.segsum(g, o[3], U)
+    sq = H.sum_of_squares(g, o[3], U, oracle)
+    assert H.row_rel_err(pipe.out[:U].cpu().numpy(), S, sq) <= H.TOL_F32
+    lr = _f32(w.lr)
+    ref = oracle.sgd(table0[o[0]], S, lr)
+    table = pipe.state["table"]
+    rows_t = torch.from_numpy(o[0]).to(table.device)
+    H.assert_sgd_rows(table[rows_t].cpu().numpy(), ref, S, lr, H.row_delta(S, H.TOL_F32, sq))
+    others = torch.ones(w.V, dtype=torch.bool, device=table.device)
+    others[rows_t] = False
+    t0 = torch.from_numpy(table0).to(table.device)
+    assert torch.equal(table[others], t0[others]), "untouched rows must be bit-unchanged"
+    del t0
+    _release(pipe)
+
+
+def test_full_merge_64x32k_bf16(lz):
+    """64 concatenated shards of 32,768 tokens (2,097,152), bf16 gradients:
+    Unique of the concatenation and of shard 0, sampled Seg-Sum rows of the
+    concatenation, every Seg-Sum row of shard 0 and its EXPAND into the
+    merged type list."""
+    w = synth.WORKLOADS["merge_64x32k_bf16"]
+    ids, g = w.ids(), w.grads()
+    pipe = _run(lz, w, ids, g)
+    o = H.assert_unique_matches(pipe.ures, ids, w.V, oracle, w.name)
+    UG = len(o[0])
+    pos = _sample_types(o[1], 31)
+    S, sq = _sampled_sums(ids, g, o[0][pos])
+    got = pipe.out[torch.from_numpy(pos).to(pipe.out.device)].cpu().numpy()
+    assert H.row_rel_err(got, S, sq) <= H.TOL_BF16
+    # shard 0: steps 1-2 on its own tokens, step 5 into the merged rows
+    ids0, g0 = ids[:w.K], g[:w.K]
+    u0 = pipe.state["u0"]
+    o0 = H.assert_unique_matches(u0, ids0, w.V, oracle, w.name + " shard 0")
+    U0 = len(o0[0])
+    S0 = oracle.segsum(g0, o0[3], U0)
+    sq0 = H.sum_of_squares(g0, o0[3], U0, oracle)
+    assert H.row_rel_err(pipe.state["out0"][:U0].cpu().numpy(), S0, sq0) <= H.TOL_BF16
+    mp, missing = oracle.map_ids(o0[0], o[0])
+    assert not missing
+    want = oracle.expand(S0, o0[0], o[0])
+    M = pipe.state["M"][:UG].cpu().numpy()
+    others = np.ones(UG, bool)
+    others[mp] = False
+    assert not M[others].any() and not want[others].any(), "EXPAND must zero the other rows"
+    assert H.row_rel_err(M[mp], want[mp], sq0) <= H.TOL_BF16
+    _release(pipe)
+
+
+def test_full_char_heavy_1m(lz):
+    """1,048,576 tokens over 20K characters (Zipf 1.2, the top type holds
+    about a fifth of the tokens), D = 2048: every Seg-Sum row, then SCATTER
+    into the dense 20K x 2048 table. No floor on the row scale here: with
+    2048 columns the largest |sum| always exceeds the rms of the summands."""
+    w = synth.WORKLOADS["char_heavy_1m"]
+    ids, g = w.ids(), w.grads()
+    pipe = _run(lz, w, ids, g)
+    o = H.assert_unique_matches(pipe.ures, ids, w.V, oracle, w.name)
+    U = len(o[0])
+    S = oracle.segsum(g, o[3], U)
+    assert H.row_rel_err(pipe.out[:U].cpu().numpy(), S) <= H.TOL_F32
+    T = pipe.state["table"].cpu().numpy()
+    others = np.ones(w.V, bool)
+    others[o[0]] = False
+    assert not T[others].any()
+    assert H.row_rel_err(T[o[0]], S) <= H.TOL_F32
+    _release(pipe)
+
+
+def test_full_vocab2m_adam_i64(lz):
+    """262,144 int64 ids over a 2M vocabulary (Zipf 0.9), D = 1024: sampled
+    Seg-Sum rows, then the first lazy-Adam step (beta1 0.9, beta2 0.999,
+    eps 1e-8, lr 1e-3, zero moments) on the touched rows of the 2M x 1024
+    param, m and v tables; every untouched row is compared exactly."""
+    w = synth.WORKLOADS["vocab2m_adam_i64"]
+    ids, g, table0 = w.ids(), w.grads(), w.table()
+    pipe = _run(lz, w, ids, g, table0)
+    o = H.assert_unique_matches(pipe.ures, ids, w.V, oracle, w.name)
+    pos = _sample_types(o[1], 51)
+    sel = o[0][pos]
+    S, sq = _sampled_sums(ids, g, sel)
+    dev = pipe.out.device
+    got = pipe.out[torch.from_numpy(pos).to(dev)].cpu().numpy()
+    assert H.row_rel_err(got, S, sq) <= H.TOL_F32
+    lr, (b1, b2, eps) = _f32(w.lr), (_f32(x) for x in w.adam)
+    z = np.zeros_like(S)
+    rp, rm, rv = oracle.adam(table0[sel], z, z, S, lr, b1, b2, eps, 0.0, 1)
+    sel_t = torch.from_numpy(sel).to(dev)
+    st = pipe.state
+    H.assert_adam_first_step(st["table"][sel_t].cpu().numpy(), st["m"][sel_t].cpu().numpy(),
+                             st["v"][sel_t].cpu().numpy(), rp, rm, rv, S, lr, b1, b2, eps,
+                             H.row_delta(S, H.TOL_F32, sq))
+    others = torch.ones(w.V, dtype=torch.bool, device=dev)
+    others[torch.from_numpy(o[0]).to(dev)] = False
+    t0 = torch.from_numpy(table0).to(dev)
+    assert torch.equal(st["table"][others], t0[others]), "untouched rows must be bit-unchanged"
+    del t0
+    assert int(torch.count_nonzero(st["m"][others])) == 0
+    assert int(torch.count_nonzero(st["v"][others])) == 0
+    _release(pipe)

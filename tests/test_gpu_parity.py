@@ -271,7 +271,7 @@ def test_shard_merge_and_expand(lz, dt):
     lz.check(rI.dev_err)
     oI = H.assert_unique_matches(rI, I, V, oracle)
     UG = len(oI[0])
-    for J, r, s, mp, M in keep:
+    for (J, r, s, mp, M), g in zip(keep, grads):
         lz.check(r.dev_err)
         oj = H.assert_unique_matches(r, J, V, oracle)
         Ui = len(oj[0])
@@ -279,39 +279,50 @@ def test_shard_merge_and_expand(lz, dt):
         assert not missing and np.array_equal(mp[:Ui].cpu().numpy(), omap)
         Mn = M[:UG].cpu().numpy()
         assert not np.isnan(Mn).any(), "EXPAND must write every row"
-        want = oracle.expand(s[:Ui].double().cpu().numpy(), oj[0], oI[0])
-        assert np.array_equal(Mn.astype(np.float64), want)
+        # the oracle's steps 2 and 5 on the same shard
+        want = oracle.expand(oracle.segsum(g, oj[3], Ui), oj[0], oI[0])
+        others = np.ones(UG, bool)
+        others[omap] = False
+        assert not Mn[others].any() and not want[others].any()
+        assert H.row_rel_err(Mn[omap], want[omap]) <= H.TOL_F32
     ref = oracle.segsum(np.concatenate(grads), oI[3], UG)
     assert H.row_rel_err(total[:UG].cpu().numpy(), ref) <= 2 * H.TOL_F32
     assert H.row_rel_err(MI[:UG].double().cpu().numpy(), ref) <= H.TOL_F32
 
 
-def test_fill_scatter_modes(lz):
-    K, V, D = 12_000, 3000, 72
-    ids = synth.zipf_ids(K, V, 1.1, 101, np.int32)
-    g = synth.normal_rows(K, D, 102)
+@pytest.mark.parametrize("dt", [np.int32, np.int64])
+def test_fill_modes(lz, dt):
+    """Step 5 and the row scatters on seeded source rows (the same arrays go
+    to the oracle): every mode is a copy or one fp32 add, so bit-exact."""
+    U, V, D = 3000, 40_000, 72
+    src_ids = synth.distinct_ids(U, V, 101, dt)
+    src = synth.normal_rows(U, D, 102)
     base = synth.normal_rows(V, D, 103)
-    r = lz.unique(_t(ids), V)
-    s = lz.segsum(_t(g), r.perm, r.inverse, r.offsets, r.num_unique, dev_err=r.dev_err)
+    n_src = torch.tensor([U], dtype=torch.int64, device=DEV)
+    sid, s = _t(src_ids), _t(src)
+    err = torch.zeros(1, dtype=torch.int32, device=DEV)
     t1 = _t(base)
-    lz.fill_values(s, r.uniq, r.num_unique, t1, None, None, "scatter", dev_err=r.dev_err)
+    lz.fill_values(s, sid, n_src, t1, None, None, "scatter", dev_err=err)
     t2 = _t(base)
-    lz.fill_values(s, r.uniq, r.num_unique, t2, None, None, "scatter_add", dev_err=r.dev_err)
-    # scatter into the row space of a superset id list
-    sup = np.unique(np.concatenate([ids, np.arange(0, V, 7)])).astype(np.int32)
+    lz.fill_values(s, sid, n_src, t2, None, None, "scatter_add", dev_err=err)
+    # the row space of a superset id list: scatter, and EXPAND (zero fill)
+    sup = np.union1d(src_ids, synth.distinct_ids(9000, V, 104, dt)).astype(dt)
     n_sup = torch.tensor([len(sup)], dtype=torch.int64, device=DEV)
     t3 = torch.zeros((len(sup), D), device=DEV)
-    lz.fill_values(s, r.uniq, r.num_unique, t3, _t(sup), n_sup, "scatter", dev_err=r.dev_err)
+    lz.fill_values(s, sid, n_src, t3, _t(sup), n_sup, "scatter", dev_err=err)
+    t4 = torch.full((len(sup) + 5, D), float("nan"), device=DEV)
+    lz.fill_values(s, sid, n_src, t4, _t(sup), n_sup, "expand", dev_err=err)
     torch.cuda.synchronize()
-    lz.check(r.dev_err)
-    o = oracle.unique(ids, V)
-    U = len(o[0])
-    src = s[:U].double().cpu().numpy()
-    assert np.array_equal(t1.cpu().numpy().astype(np.float64), oracle.scatter(src, o[0], base))
-    want_add = oracle.scatter(src, o[0], base, add=True).astype(np.float32)
+    lz.check(err)
+    s64 = src.astype(np.float64)
+    assert np.array_equal(t1.cpu().numpy().astype(np.float64), oracle.scatter(s64, src_ids, base))
+    want_add = oracle.scatter(s64, src_ids, base, add=True).astype(np.float32)
     assert np.array_equal(t2.cpu().numpy(), want_add)
     assert np.array_equal(t3.cpu().numpy().astype(np.float64),
-                          oracle.scatter(src, o[0], np.zeros((len(sup), D)), dst_ids=sup))
+                          oracle.scatter(s64, src_ids, np.zeros((len(sup), D)), dst_ids=sup))
+    got4 = t4.cpu().numpy()
+    assert np.array_equal(got4[:len(sup)].astype(np.float64), oracle.expand(s64, src_ids, sup))
+    assert np.isnan(got4[len(sup):]).all(), "EXPAND wrote past the merged rows"
 
 
 def test_fill_and_map_errors(lz):
@@ -337,12 +348,14 @@ def test_fill_and_map_errors(lz):
 # Sparse apply (step 7)
 # ---------------------------------------------------------------------------
 
-def _apply_case(lz, opt, dt, K, V, D, seed, step=1, wd=0.0):
-    ids = synth.zipf_ids(K, V, 1.0, seed, dt)
-    g = synth.normal_rows(K, D, seed + 1)
+def _apply_case(lz, opt, dt, U, V, D, seed, step=1, wd=0.0):
+    """Step 7 on seeded touched rows and update values (the same arrays go to
+    the oracle, which works in fp64)."""
+    rows = synth.distinct_ids(U, V, seed, dt)
+    g = synth.normal_rows(U, D, seed + 1)
     p0 = synth.normal_rows(V, D, seed + 2, 0.02)
-    r = lz.unique(_t(ids), V)
-    s = lz.segsum(_t(g), r.perm, r.inverse, r.offsets, r.num_unique, dev_err=r.dev_err)
+    n_rows = torch.tensor([U], dtype=torch.int64, device=DEV)
+    err = torch.zeros(1, dtype=torch.int32, device=DEV)
     table = _t(p0)
     kw = {}
     m0 = v0 = None
@@ -357,38 +370,41 @@ def _apply_case(lz, opt, dt, K, V, D, seed, step=1, wd=0.0):
     b1, b2, eps = f32(0.9), f32(0.999), f32(1e-8)
     if opt == "adam":
         kw["weight_decay"] = f32(wd)
-    lz.sparse_apply(table, r.uniq, r.num_unique, s, opt, lr=lr, beta1=b1, beta2=b2, eps=eps,
-                    dev_err=r.dev_err, **kw)
+    lz.sparse_apply(table, _t(rows), n_rows, _t(g), opt, lr=lr, beta1=b1, beta2=b2, eps=eps,
+                    dev_err=err, **kw)
     torch.cuda.synchronize()
-    lz.check(r.dev_err)
-    o = oracle.unique(ids, V)
-    U = len(o[0])
-    gs = s[:U].double().cpu().numpy()  # the apply is checked on the GPU's own Seg-Sum
-    rows = o[0]
+    lz.check(err)
     got = table.cpu().numpy()
     untouched = np.ones(V, bool)
     untouched[rows] = False
     assert np.array_equal(got[untouched], p0[untouched]), "untouched rows must be bit-unchanged"
     if opt == "sgd":
-        ref = oracle.sgd(p0[rows], gs, float(lr))
+        ref = oracle.sgd(p0[rows], g, float(lr))
         np.testing.assert_allclose(got[rows], ref, rtol=0, atol=float(np.abs(ref).max()) * 2.4e-7)
     else:
-        pr, mr, vr = oracle.adam(p0[rows], m0[rows], v0[rows], gs, lr, b1, b2, eps, f32(wd), step)
+        pr, mr, vr = oracle.adam(p0[rows], m0[rows], v0[rows], g, lr, b1, b2, eps, f32(wd), step)
         dp = np.abs(got[rows] - pr)
         assert float(dp.max()) <= 2e-6 * float(lr) + 2.4e-7 * float(np.abs(pr).max())
-        np.testing.assert_allclose(kw["m"].cpu().numpy()[rows], mr, rtol=2e-6, atol=1e-9)
-        np.testing.assert_allclose(kw["v"].cpu().numpy()[rows], vr, rtol=2e-6, atol=1e-12)
+        # Each moment is a two-term fp32 update: its rounding error is bounded
+        # by the size of the terms, not of the (possibly cancelling) result.
+        u = 2.0 ** -24
+        bm = 3 * u * (b1 * np.abs(m0[rows]) + (1 - b1) * np.abs(g.astype(np.float64)))
+        bv = 4 * u * (b2 * v0[rows] + (1 - b2) * np.square(g.astype(np.float64)))
+        assert (np.abs(kw["m"].cpu().numpy()[rows] - mr) <= bm).all(), "Adam m"
+        assert (np.abs(kw["v"].cpu().numpy()[rows] - vr) <= bv).all(), "Adam v"
+        assert np.array_equal(kw["m"].cpu().numpy()[untouched], m0[untouched])
+        assert np.array_equal(kw["v"].cpu().numpy()[untouched], v0[untouched])
 
 
 @pytest.mark.parametrize("dt", [np.int32, np.int64])
 def test_apply_sgd(lz, dt):
-    _apply_case(lz, "sgd", dt, 20_000, 30_000, 256, 111)
+    _apply_case(lz, "sgd", dt, 7_000, 30_000, 256, 111)
 
 
 @pytest.mark.parametrize("step,wd", [(1, 0.0), (10, 0.0), (10, 0.01)])
 def test_apply_adam(lz, step, wd):
-    _apply_case(lz, "adam", np.int64, 20_000, 30_000, 200, 121, step, wd)
+    _apply_case(lz, "adam", np.int64, 7_000, 30_000, 200, 121, step, wd)
 
 
 def test_apply_sgd_odd_width(lz):
-    _apply_case(lz, "sgd", np.int32, 3000, 2000, 13, 131)
+    _apply_case(lz, "sgd", np.int32, 900, 2000, 13, 131)
