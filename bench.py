@@ -31,8 +31,10 @@ import numpy as np  # noqa: E402
 
 HBM_PEAK_GBPS = 8000.0
 METRIC = "tokens/s through Unique+Seg-Sum+Fill-Values; achieved HBM GB/s vs peak"
-PMC_FILE = os.path.join(ROOT, "profiles", "segsum_pmc_{workload}.json")
-SEGSUM_SRC = os.path.join(ROOT, "paper_1810_10045_amd", "csrc", "segsum.hip")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "segsum_traffic_{workload}.md")
+SEGSUM_SRCS = [os.path.join(ROOT, "paper_1810_10045_amd", "csrc", f)
+               for f in ("segsum.hip", "common.hpp")]
+COPY_BYTES = 1 << 30  # the plain copy that scales the HBM byte counters
 
 
 def log(msg):
@@ -40,8 +42,11 @@ def log(msg):
 
 
 def segsum_source_hash() -> str:
-    with open(SEGSUM_SRC, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+    h = hashlib.sha256()
+    for path in SEGSUM_SRCS:
+        with open(path, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
 
 
 def segsum_bytes(K, D, U, grad_bytes):
@@ -236,17 +241,38 @@ def run_cpu_baseline(w, budget_s):
                        f"unique+segsum+{w.step}, fp64, 1 thread, {t_used:.1f}s")
 
 
-def load_traffic(workload, launches_bytes):
-    """HBM bytes per Seg-Sum launch from committed rocprofv3 counter runs,
-    only while segsum.hip is unchanged since they were taken."""
-    path = PMC_FILE.format(workload=workload)
+def load_traffic(workload):
+    """HBM bytes per Seg-Sum launch from the committed rocprofv3 counter
+    summary (FETCH_SIZE + WRITE_SIZE, scaled by a plain copy), only while the
+    Seg-Sum sources are unchanged since the counters were taken."""
+    path = TRAFFIC_FILE.format(workload=workload)
     if not os.path.exists(path):
         return None
+    rec = {}
     with open(path) as f:
-        rec = json.load(f)
-    if rec.get("segsum_source_sha256_16") != segsum_source_hash():
+        for line in f:
+            if line.startswith("- ") and ": " in line:
+                k, v = line[2:].strip().split(": ", 1)
+                rec[k.strip("`")] = v.strip("`")
+    if rec.get("segsum_sources_sha256_16") != segsum_source_hash():
         return None
-    return rec.get("hbm_bytes_per_launch")
+    try:
+        return float(rec["hbm_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def copy_calibration(torch, reps=3):
+    """Plain device copies of COPY_BYTES (read COPY_BYTES, write COPY_BYTES)
+    whose counter readings scale FETCH_SIZE / WRITE_SIZE to bytes."""
+    src = torch.ones(COPY_BYTES // 4, dtype=torch.float32, device="cuda:0")
+    dst = torch.empty_like(src)
+    for _ in range(reps):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    log(f"copy calibration: {reps} copies of {COPY_BYTES} bytes")
+    del src, dst
+    torch.cuda.empty_cache()
 
 
 def main():
@@ -258,6 +284,8 @@ def main():
     ap.add_argument("--batches", type=int, default=0, help="resident batches (0: auto)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle leg")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="first run plain 1 GiB copies (scale for HBM byte counters)")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -269,6 +297,8 @@ def main():
     from paper_1810_10045_amd import lmzipf as lz
     from paper_1810_10045_amd import synth
 
+    if args.copy_calibration:
+        copy_calibration(torch)
     w = synth.WORKLOADS[args.workload]
     gb = 2 if w.grad_dtype == "bf16" else 4
     batch_bytes = w.tokens * w.D * gb
@@ -281,7 +311,7 @@ def main():
     cpu = None
     if not args.no_cpu and rank == 0:
         cpu = run_cpu_baseline(w, args.cpu_seconds)
-    traffic = load_traffic(w.name, r["seg_bytes"])
+    traffic = load_traffic(w.name)
     line = {
         "metric": METRIC,
         "value": tokens_per_s,
