@@ -194,15 +194,26 @@ def run_gpu(w, steps, warmup, nbatch, torch, lz):
         step(i)
     torch.cuda.synchronize()
 
-    ev = HipEvents(4 * steps + 2)
+    # Pass 1, the headline: K steps between two events and nothing else on
+    # the stream (an event record costs the GPU a few microseconds).
+    ev = HipEvents(2)
     torch.cuda.synchronize()
-    ev.record(4 * steps, stream)
+    ev.record(0, stream)
     for i in range(steps):
-        step(i, lambda k, i=i: ev.record(4 * i + k, stream))
-    ev.record(4 * steps + 1, stream)
+        step(i)
+    ev.record(1, stream)
     torch.cuda.synchronize()
     lz.check(dev_err)
-    total_ms = ev.ms(4 * steps, 4 * steps + 1)
+    total_ms = ev.ms(0, 1)
+    ev.close()
+    # Pass 2, the same K steps with an event around every entry point: the
+    # per-stage times and the Seg-Sum launch time of the roofline.
+    ev = HipEvents(4 * steps)
+    torch.cuda.synchronize()
+    for i in range(steps):
+        step(i, lambda k, i=i: ev.record(4 * i + k, stream))
+    torch.cuda.synchronize()
+    lz.check(dev_err)
     st = np.array([[ev.ms(4 * i, 4 * i + 1), ev.ms(4 * i + 1, 4 * i + 2), ev.ms(4 * i + 2, 4 * i + 3)]
                    for i in range(steps)])
     ev.close()

@@ -15,9 +15,9 @@
 //                    continues past it (desc[c] names that segment),
 //     part_cont[c]   the piece of a long segment that started before chunk c.
 //   k_segsum_fix then sums, for each desc[c] >= 0, part_start[c] and the
-//   part_cont rows of the chunks the segment covers, in order: one wave for
-//   a segment of few pieces, 16 waves (fixed stride split of the pieces,
-//   fixed-order combine in LDS) for a head.
+//   part_cont rows of the chunks the segment covers, in order: one wave per
+//   column tile for a segment of at most 16 pieces, 16 waves (fixed stride
+//   split of the pieces, fixed-order combine in LDS) for a head.
 // A chunk reads at most R + T - 1 rows; a segment is split into at most
 // K / R pieces.
 //
@@ -42,7 +42,7 @@ namespace lmz {
 #define LMZ_SEG_NV_MAX 4             // 16-byte vectors per lane per row (fp32)
 #endif
 #ifndef LMZ_SEG_FIX_RF
-#define LMZ_SEG_FIX_RF 4             // partial rows per wave per batch in the fix-up
+#define LMZ_SEG_FIX_RF 16            // partial rows per wave in flight in the fix-up
 #endif
 
 constexpr int kSegThreads = 256;
@@ -264,131 +264,116 @@ __global__ __launch_bounds__(kSegThreads) void k_segsum(SegArgs a) {
 
 // Sum the pieces of every long segment that spans chunks (piece 0 is
 // part_start[c], piece t >= 1 is part_cont[c + t], added in order of t).
-// One 1024-thread workgroup per 16 chunks, wave w looking after chunk
-// 16*blockIdx + w. A segment of at most kFixSmall pieces is summed by that
-// wave alone; a longer one (the heads of the Zipf law) by all 16 waves of
-// the workgroup, wave v adding pieces v, v+16, v+32, ... in order, the 16
-// partial rows then added in wave order through LDS. Columns go in passes
-// of 64 * VEC * NV.
-constexpr int kFixThreads = 1024;
-constexpr int kFixWaves = kFixThreads / kWave;
-constexpr int kFixSmall = 16;
+// Grid: one workgroup of kFixWaves waves per kFixChunks chunks and per
+// column tile of 64 * VEC columns. Few chunks start such a segment, so a workgroup reads
+// the desc entries of its chunks with one coalesced load and a ballot, and
+// only waves with work touch the partial rows (launching a wave per chunk
+// cost more than the sums). The partial rows were just written, so the sums
+// are bound by load latency: a wave keeps RF pieces in flight at once. A
+// segment of at most RF pieces is summed by one wave in one round; a longer
+// one (a head of the Zipf law) by all kFixWaves waves, wave v adding pieces
+// v, v + kFixWaves, ... in order, their partial rows then added in wave
+// order through LDS.
+#ifndef LMZ_SEG_FIX_WAVES
+#define LMZ_SEG_FIX_WAVES 8          // waves of a fix-up workgroup
+#endif
+#ifndef LMZ_SEG_FIX_CHUNKS
+#define LMZ_SEG_FIX_CHUNKS 8         // chunks a fix-up workgroup looks after (<= 64)
+#endif
+constexpr int kFixWaves = LMZ_SEG_FIX_WAVES;
+constexpr int kFixThreads = kFixWaves * kWave;
+constexpr int kFixChunks = LMZ_SEG_FIX_CHUNKS;
+static_assert(kFixChunks <= kWave, "one desc entry per lane");
 
-template <int VEC, int NV, int RF>
+template <int VEC, int RF>
 __global__ __launch_bounds__(kFixThreads) void k_segsum_fix(SegArgs a) {
-  constexpr int kPass = kWave * VEC * NV;  // columns per pass
-  __shared__ float s_part[kFixWaves][kPass];
-  __shared__ int s_big[kFixWaves];
+  constexpr int kCols = kWave * VEC;  // columns of a tile
+  __shared__ float s_part[kFixWaves][kCols];
   const int lane = lane_id();
   const int wave = first_lane(static_cast<int>(threadIdx.x >> 6));
   const int D = a.D;
   const int U = first_lane(static_cast<int>(*a.num_unique));
-  const int c = blockIdx.x * kFixWaves + wave;
+  const int c0 = blockIdx.x * kFixChunks;
+  const int col = blockIdx.y * kCols + lane * VEC;
+  const int col_ld = col < D ? col : D - VEC;  // past the end: a valid, unstored vector
 
-  int s = c < a.nchunks ? first_lane(a.desc[c]) : -1;
-  if (!(s >= 0 && s < U && s < a.u_cap)) s = -1;
-  int P = -1;
-  if (s >= 0) {
+  // Chunks c0 + i that start a long segment, as a mask over i (the same in
+  // every wave).
+  const int ci = c0 + lane;
+  int sd = (lane < kFixChunks && ci < a.nchunks) ? a.desc[ci] : -1;
+  const bool has = sd >= 0 && sd < U && sd < a.u_cap;
+  const uint64_t todo = ballot(has);
+  auto piece = [&](int cs, int t) {
+    return (t == 0 ? a.part_start + static_cast<int64_t>(cs) * D
+                   : a.part_cont + static_cast<int64_t>(cs + t) * D) + col_ld;
+  };
+  auto pieces_after = [&](int cs, int s) {  // chunks past cs holding rows of s
     int c1 = first_lane((a.offsets[s + 1] - 1) / a.R);
     if (c1 >= a.nchunks) c1 = a.nchunks - 1;
-    P = c1 - c;
-  }
-  auto piece = [&](int cs, int t) {
-    return t == 0 ? a.part_start + static_cast<int64_t>(cs) * D
-                  : a.part_cont + static_cast<int64_t>(cs + t) * D;
+    return c1 - cs;
   };
 
-  // Segments of few pieces: this wave alone.
-  if (s >= 0 && P <= kFixSmall) {
-    float* dst = a.out + static_cast<int64_t>(s) * a.ld_out;
-    for (int cb = 0; cb < D; cb += kPass) {
-      float acc[NV][VEC];
+  // Pass 1: segments of at most RF pieces, the j-th of the mask by wave
+  // j % kFixWaves.
+  uint64_t m = todo;
+  for (int j = 0; m; ++j, m &= m - 1) {
+    if (j % kFixWaves != wave) continue;
+    const int i = __builtin_ctzll(m);
+    const int cs = c0 + i;
+    const int s = read_lane(sd, i);
+    const int P = pieces_after(cs, s);
+    if (P >= RF) continue;
+    float buf[RF][VEC];
 #pragma unroll
-      for (int v = 0; v < NV; ++v)
+    for (int r = 0; r < RF; ++r) load_vec<VEC>(piece(cs, r <= P ? r : 0), buf[r]);
+    float acc[VEC];
 #pragma unroll
-        for (int e = 0; e < VEC; ++e) acc[v][e] = 0.f;
-      int col[NV], col_ld[NV];
+    for (int e = 0; e < VEC; ++e) acc[e] = buf[0][e];
 #pragma unroll
-      for (int v = 0; v < NV; ++v) {
-        col[v] = cb + v * kWave * VEC + lane * VEC;
-        col_ld[v] = col[v] < D ? col[v] : D - VEC;  // past the end: a valid, unstored vector
-      }
-      for (int t0 = 0; t0 <= P; t0 += RF) {
-        float buf[RF][NV][VEC];
+    for (int r = 1; r < RF; ++r)
+      if (r <= P)
 #pragma unroll
-        for (int r = 0; r < RF; ++r) {
-          const float* row = piece(c, t0 + r <= P ? t0 + r : t0);
-#pragma unroll
-          for (int v = 0; v < NV; ++v) load_vec<VEC>(row + col_ld[v], buf[r][v]);
-        }
-#pragma unroll
-        for (int r = 0; r < RF; ++r)
-          if (t0 + r <= P)
-#pragma unroll
-            for (int v = 0; v < NV; ++v)
-#pragma unroll
-              for (int e = 0; e < VEC; ++e) acc[v][e] += buf[r][v][e];
-      }
-#pragma unroll
-      for (int v = 0; v < NV; ++v)
-        if (col[v] < D) store_vec<VEC>(dst + col[v], acc[v]);
-    }
+        for (int e = 0; e < VEC; ++e) acc[e] += buf[r][e];
+    if (col < D) store_vec<VEC>(a.out + static_cast<int64_t>(s) * a.ld_out + col, acc);
   }
 
-  // Segments of many pieces: the whole workgroup, one after the other.
-  if (lane == 0) s_big[wave] = (s >= 0 && P > kFixSmall) ? s : -1;
-  __syncthreads();
-  for (int bw = 0; bw < kFixWaves; ++bw) {
-    const int sb = s_big[bw];
-    if (sb < 0) continue;  // the same in every thread
-    const int cs = blockIdx.x * kFixWaves + bw;
-    int c1 = first_lane((a.offsets[sb + 1] - 1) / a.R);
-    if (c1 >= a.nchunks) c1 = a.nchunks - 1;
-    const int PB = c1 - cs;
-    float* dst = a.out + static_cast<int64_t>(sb) * a.ld_out;
-    for (int cb = 0; cb < D; cb += kPass) {
-      float acc[NV][VEC];
+  // Pass 2: segments of more pieces, one after the other, all waves.
+  for (m = todo; m; m &= m - 1) {
+    const int i = __builtin_ctzll(m);
+    const int cs = c0 + i;
+    const int sb = read_lane(sd, i);
+    const int PB = pieces_after(cs, sb);
+    if (PB < RF) continue;  // the same in every thread
+    float acc[VEC];
 #pragma unroll
-      for (int v = 0; v < NV; ++v)
+    for (int e = 0; e < VEC; ++e) acc[e] = 0.f;
+    for (int t0 = wave; t0 <= PB; t0 += kFixWaves * RF) {
+      float buf[RF][VEC];
 #pragma unroll
-        for (int e = 0; e < VEC; ++e) acc[v][e] = 0.f;
-      int col_ld[NV];
-#pragma unroll
-      for (int v = 0; v < NV; ++v) {
-        const int col = cb + v * kWave * VEC + lane * VEC;
-        col_ld[v] = col < D ? col : D - VEC;
-      }
-      for (int t0 = wave; t0 <= PB; t0 += kFixWaves * RF) {
-        float buf[RF][NV][VEC];
-#pragma unroll
-        for (int r = 0; r < RF; ++r) {
-          const int t = t0 + r * kFixWaves;
-          const float* row = piece(cs, t <= PB ? t : t0);
-#pragma unroll
-          for (int v = 0; v < NV; ++v) load_vec<VEC>(row + col_ld[v], buf[r][v]);
-        }
-#pragma unroll
-        for (int r = 0; r < RF; ++r)
-          if (t0 + r * kFixWaves <= PB)
-#pragma unroll
-            for (int v = 0; v < NV; ++v)
-#pragma unroll
-              for (int e = 0; e < VEC; ++e) acc[v][e] += buf[r][v][e];
+      for (int r = 0; r < RF; ++r) {
+        const int t = t0 + r * kFixWaves;
+        load_vec<VEC>(piece(cs, t <= PB ? t : t0), buf[r]);
       }
 #pragma unroll
-      for (int v = 0; v < NV; ++v)
+      for (int r = 0; r < RF; ++r)
+        if (t0 + r * kFixWaves <= PB)
 #pragma unroll
-        for (int e = 0; e < VEC; ++e) s_part[wave][v * kWave * VEC + lane * VEC + e] = acc[v][e];
-      __syncthreads();
-      // Thread x adds column cb + x over the 16 waves in order.
-      for (int x = threadIdx.x; x < kPass && cb + x < D; x += kFixThreads) {
+          for (int e = 0; e < VEC; ++e) acc[e] += buf[r][e];
+    }
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) s_part[wave][lane * VEC + e] = acc[e];
+    __syncthreads();
+    // Thread x adds column x of the tile over the waves in order.
+    for (int x = threadIdx.x; x < kCols; x += kFixThreads) {
+      const int cx = blockIdx.y * kCols + x;
+      if (cx < D) {
         float sum = 0.f;
 #pragma unroll
         for (int w = 0; w < kFixWaves; ++w) sum += s_part[w][x];
-        dst[cb + x] = sum;
+        a.out[static_cast<int64_t>(sb) * a.ld_out + cx] = sum;
       }
-      __syncthreads();
     }
+    __syncthreads();
   }
 }
 
@@ -457,11 +442,11 @@ int segsum_run(const void* grad, int gtype, int64_t K, int64_t D, int64_t ld_gra
             : dispatch_nv<bf16_t, 1>(a, 4, st);
   }
   if (e != hipSuccess) return launch_status(e);
-  const uint32_t fix_blocks = static_cast<uint32_t>((L.nchunks + kFixWaves - 1) / kFixWaves);
+  const uint32_t fix_blocks = static_cast<uint32_t>((L.nchunks + kFixChunks - 1) / kFixChunks);
   if (D % 4 == 0)
-    k_segsum_fix<4, 4, LMZ_SEG_FIX_RF><<<fix_blocks, kFixThreads, 0, st>>>(a);
+    k_segsum_fix<4, LMZ_SEG_FIX_RF><<<dim3(fix_blocks, (D + 255) / 256), kFixThreads, 0, st>>>(a);
   else
-    k_segsum_fix<1, 4, LMZ_SEG_FIX_RF><<<fix_blocks, kFixThreads, 0, st>>>(a);
+    k_segsum_fix<1, LMZ_SEG_FIX_RF><<<dim3(fix_blocks, (D + 63) / 64), kFixThreads, 0, st>>>(a);
   return launch_status(hipGetLastError());
 }
 

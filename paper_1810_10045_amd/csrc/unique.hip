@@ -11,8 +11,10 @@
 //               ceil(log2 V) key bits are split evenly over the fewest
 //               passes; 8-bit digits measured faster per key bit than 10- or
 //               11-bit ones, whose counters and look-back cost twice as
-//               much per pass). A 1024-thread
-//               workgroup ranks a tile of 4096 keys (4 per thread) with
+//               much per pass). A workgroup of NT threads (256 for inputs
+//               of up to LMZ_UNIQUE_SMALL_TILE_MAX_K keys, so that they
+//               spread over more CUs, else 1024) ranks a tile of 4 * NT
+//               keys (4 per thread) with
 //               wave64 ballot matching, publishes its per-digit counts,
 //               learns the counts of the tiles before it through a decoupled
 //               look-back, reorders the tile in LDS and writes it out in
@@ -31,8 +33,10 @@
 
 namespace lmz {
 
-constexpr int kThreads = 1024;
-constexpr int kWaves = kThreads / kWave;
+constexpr int kHistThreads = 1024;
+#ifndef LMZ_UNIQUE_SMALL_TILE_MAX_K
+#define LMZ_UNIQUE_SMALL_TILE_MAX_K (1 << 17)  // up to this K, 256-thread tiles
+#endif
 #ifndef LMZ_UNIQUE_DIGIT_BITS
 #define LMZ_UNIQUE_DIGIT_BITS 8
 #endif
@@ -40,7 +44,6 @@ constexpr int kMaxDigitBits = LMZ_UNIQUE_DIGIT_BITS;
 constexpr int kMaxRadix = 1 << kMaxDigitBits;
 constexpr int kMaxPasses = 8;              // ceil(64 / 8)
 constexpr int kItems = 4;                  // keys per thread in a tile
-constexpr int kTile = kThreads * kItems;   // 4096
 constexpr int kHistItems = 16;             // keys per thread per histogram round
 constexpr int kHistKeysPerBlock = 1 << 12;
 constexpr int kMaxHistBlocks = 64;
@@ -53,7 +56,7 @@ constexpr uint64_t kD31 = (1ull << 31) - 1;
 
 struct UniqueLayout {
   size_t bhist, tickets, status, dstatus, keys0, keys1, vals0, vals1, total;
-  int passes, bits, tiles, hist_blocks;
+  int passes, bits, tiles, hist_blocks, nt;
   int shift[kMaxPasses], nbits[kMaxPasses];
 };
 
@@ -78,7 +81,12 @@ static UniqueLayout unique_layout(int64_t K, int idtype, int64_t V) {
     L.nbits[p] = nb;
     sh += nb;
   }
-  L.tiles = static_cast<int>((K + kTile - 1) / kTile);
+  // Workgroups of 256 threads (tiles of 1024 keys) spread a small input over
+  // more CUs; large inputs take 1024-thread tiles, which keep the look-back
+  // status arrays (one word per digit and tile) 4x smaller.
+  L.nt = K <= LMZ_UNIQUE_SMALL_TILE_MAX_K ? 256 : 1024;
+  const int64_t tile_keys = int64_t(L.nt) * kItems;
+  L.tiles = static_cast<int>((K + tile_keys - 1) / tile_keys);
   const int64_t hb = (K + kHistKeysPerBlock - 1) / kHistKeysPerBlock;
   L.hist_blocks = static_cast<int>(hb < 1 ? 1 : (hb > kMaxHistBlocks ? kMaxHistBlocks : hb));
   size_t off = 0;
@@ -109,19 +117,19 @@ __device__ __forceinline__ uint32_t digit_of(KeyT k, int shift, uint32_t mask) {
 // look-back status words of this call.
 // ---------------------------------------------------------------------------
 template <typename KeyT>
-__global__ __launch_bounds__(kThreads) void k_hist(
+__global__ __launch_bounds__(kHistThreads) void k_hist(
     const KeyT* __restrict__ keys, int K, uint64_t V, int passes, PassBits pb,
     uint32_t* __restrict__ bhist, uint32_t* __restrict__ clear, int64_t clear_words,
     int32_t* __restrict__ dev_err) {
   extern __shared__ uint32_t sh[];  // passes * kMaxRadix
-  for (int i = threadIdx.x; i < passes * kMaxRadix; i += kThreads) sh[i] = 0;
-  for (int64_t i = blockIdx.x * int64_t(kThreads) + threadIdx.x; i < clear_words;
-       i += int64_t(gridDim.x) * kThreads)
+  for (int i = threadIdx.x; i < passes * kMaxRadix; i += kHistThreads) sh[i] = 0;
+  for (int64_t i = blockIdx.x * int64_t(kHistThreads) + threadIdx.x; i < clear_words;
+       i += int64_t(gridDim.x) * kHistThreads)
     clear[i] = 0;
   __syncthreads();
   bool bad = false;
-  const int64_t stride = int64_t(gridDim.x) * kThreads;
-  for (int64_t i0 = blockIdx.x * int64_t(kThreads) + threadIdx.x; i0 < K;
+  const int64_t stride = int64_t(gridDim.x) * kHistThreads;
+  for (int64_t i0 = blockIdx.x * int64_t(kHistThreads) + threadIdx.x; i0 < K;
        i0 += stride * kHistItems) {
     KeyT kv[kHistItems];  // all loads of a round in flight together
 #pragma unroll
@@ -144,7 +152,7 @@ __global__ __launch_bounds__(kThreads) void k_hist(
   if (ballot(bad) && lane_id() == 0) raise_err(dev_err, LM_DEVERR_ID_RANGE);
   __syncthreads();
   uint32_t* row = bhist + size_t(blockIdx.x) * passes * kMaxRadix;
-  for (int i = threadIdx.x; i < passes * kMaxRadix; i += kThreads) row[i] = sh[i];
+  for (int i = threadIdx.x; i < passes * kMaxRadix; i += kHistThreads) row[i] = sh[i];
 }
 
 // ---------------------------------------------------------------------------
@@ -152,14 +160,16 @@ __global__ __launch_bounds__(kThreads) void k_hist(
 // nbits <= RB. Thread t answers for digits t*DPT .. t*DPT+DPT-1 (DPT = 2 for
 // 11-bit digits; for 8-bit digits threads 0..255 answer for one each).
 // ---------------------------------------------------------------------------
-template <typename KeyT, int RB>
-__global__ __launch_bounds__(kThreads) void k_onesweep(
+template <typename KeyT, int RB, int NT>
+__global__ __launch_bounds__(NT) void k_onesweep(
     const KeyT* __restrict__ keys_in, const int32_t* __restrict__ vals_in,
     KeyT* __restrict__ keys_out, int32_t* __restrict__ vals_out, int K, int shift, int nbits,
     const uint32_t* __restrict__ bhist, int hist_blocks, int hist_stride,
     uint32_t* __restrict__ status, uint32_t* __restrict__ ticket, int32_t* __restrict__ dev_err) {
+  constexpr int kWaves = NT / kWave;
+  constexpr int kTile = NT * kItems;
   constexpr int kRadix = 1 << RB;
-  constexpr int DPT = kRadix >= kThreads ? kRadix / kThreads : 1;
+  constexpr int DPT = kRadix >= NT ? kRadix / NT : 1;
   constexpr int kDigitThreads = kRadix / DPT;        // threads that own digits
   constexpr int W = 16;                              // predecessors per look-back round
   __shared__ KeyT s_keys[kTile];
@@ -195,20 +205,23 @@ __global__ __launch_bounds__(kThreads) void k_onesweep(
 #pragma unroll
   for (int i = 0; i < DPT; ++i) dig_total[i] = 0;
   if (owner) {
-    for (int b = 0; b < hist_blocks; b += 4) {
-      uint32_t h[4][DPT];
+    // 16 rows in flight per round: one round for up to 64K keys.
+    for (int b = 0; b < hist_blocks; b += 16) {
+      uint32_t h[16][DPT];
 #pragma unroll
-      for (int r = 0; r < 4; ++r)
+      for (int r = 0; r < 16; ++r)
 #pragma unroll
-        for (int i = 0; i < DPT; ++i)
-          h[r][i] = b + r < hist_blocks ? bhist[size_t(b + r) * hist_stride + tid * DPT + i] : 0u;
+        for (int i = 0; i < DPT; ++i) {
+          const int br = b + r < hist_blocks ? b + r : b;  // repeat a valid row, unused
+          h[r][i] = bhist[size_t(br) * hist_stride + tid * DPT + i];
+        }
 #pragma unroll
-      for (int r = 0; r < 4; ++r)
+      for (int r = 0; r < 16; ++r)
 #pragma unroll
-        for (int i = 0; i < DPT; ++i) dig_total[i] += h[r][i];
+        for (int i = 0; i < DPT; ++i) dig_total[i] += b + r < hist_blocks ? h[r][i] : 0u;
     }
   }
-  for (int i = tid; i < kWaves * kRadix / 2; i += kThreads)
+  for (int i = tid; i < kWaves * kRadix / 2; i += NT)
     reinterpret_cast<uint32_t*>(&s_cnt[0][0])[i] = 0;
   __syncthreads();
   const int tile = first_lane(static_cast<int>(s_tile));
@@ -348,7 +361,7 @@ __global__ __launch_bounds__(kThreads) void k_onesweep(
   const int n = static_cast<int>(K - base < kTile ? K - base : kTile);
 #pragma unroll
   for (int i = 0; i < kItems; ++i) {
-    const int jj = tid + i * kThreads;
+    const int jj = tid + i * NT;
     if (jj < n) {
       const KeyT k = s_keys[jj];
       const int gp = s_shift[digit_of(k, shift, mask)] + jj;
@@ -366,12 +379,14 @@ __global__ __launch_bounds__(kThreads) void k_onesweep(
 // k_dedup: thread t of tile `tile` owns the 4 sorted positions
 // base + 4t .. base + 4t + 3.
 // ---------------------------------------------------------------------------
-template <typename KeyT>
-__global__ __launch_bounds__(kThreads) void k_dedup(
+template <typename KeyT, int NT>
+__global__ __launch_bounds__(NT) void k_dedup(
     const KeyT* __restrict__ skeys, const int32_t* __restrict__ perm, int K, int cap,
     KeyT* __restrict__ uniq, int32_t* __restrict__ counts, int32_t* __restrict__ offsets,
     int32_t* __restrict__ inverse, int64_t* __restrict__ num_unique,
     uint64_t* __restrict__ status, uint32_t* __restrict__ ticket, int32_t* __restrict__ dev_err) {
+  constexpr int kWaves = NT / kWave;
+  constexpr int kTile = NT * kItems;
   __shared__ uint32_t s_scan[kWaves];
   __shared__ int s_maxs[kWaves];
   __shared__ uint32_t s_tile;
@@ -515,12 +530,12 @@ size_t unique_workspace_bytes(int64_t K, int idtype, int64_t V) {
   return unique_layout(K, idtype, V).total;
 }
 
-template <typename KeyT, int RB>
+template <typename KeyT, int RB, int NT>
 static hipError_t launch_pass(const UniqueLayout& L, int p, const KeyT* kin, const int32_t* vin,
                               KeyT* kout, int32_t* vout, int K, uint32_t* bhist,
                               uint32_t* status, uint32_t* tickets, int32_t* dev_err,
                               hipStream_t st) {
-  k_onesweep<KeyT, RB><<<L.tiles, kThreads, 0, st>>>(
+  k_onesweep<KeyT, RB, NT><<<L.tiles, NT, 0, st>>>(
       kin, vin, kout, vout, K, L.shift[p], L.nbits[p], bhist + size_t(p) * kMaxRadix,
       L.hist_blocks, L.passes * kMaxRadix, status + size_t(p) * L.tiles * kMaxRadix, tickets + p,
       dev_err);
@@ -550,7 +565,7 @@ static int run_unique(const KeyT* ids, int K, int64_t V, KeyT* uniq, int32_t* co
   // tickets .. end of dstatus is contiguous: k_hist clears it.
   const int64_t clear_words = static_cast<int64_t>((L.keys0 - L.tickets) / 4);
   const size_t hist_lds = size_t(L.passes) * kMaxRadix * 4;
-  k_hist<KeyT><<<L.hist_blocks, kThreads, hist_lds, st>>>(
+  k_hist<KeyT><<<L.hist_blocks, kHistThreads, hist_lds, st>>>(
       ids, K, static_cast<uint64_t>(V), L.passes, pb, bhist, tickets, clear_words, dev_err);
   if (hipError_t e = hipGetLastError(); e != hipSuccess) return launch_status(e);
 
@@ -559,15 +574,23 @@ static int run_unique(const KeyT* ids, int K, int64_t V, KeyT* uniq, int32_t* co
   for (int p = 0; p < L.passes; ++p) {
     KeyT* kout = kb[p & 1];
     int32_t* vout = p == L.passes - 1 ? perm : vb[p & 1];
-    const hipError_t e = launch_pass<KeyT, kMaxDigitBits>(L, p, kin, vin, kout, vout, K, bhist,
-                                                          status, tickets, dev_err, st);
+    const hipError_t e =
+        L.nt == 256 ? launch_pass<KeyT, kMaxDigitBits, 256>(L, p, kin, vin, kout, vout, K, bhist,
+                                                             status, tickets, dev_err, st)
+                    : launch_pass<KeyT, kMaxDigitBits, 1024>(L, p, kin, vin, kout, vout, K, bhist,
+                                                              status, tickets, dev_err, st);
     if (e != hipSuccess) return launch_status(e);
     kin = kout;
     vin = vout;
   }
-  k_dedup<KeyT><<<L.tiles, kThreads, 0, st>>>(
-      kin, perm, K, static_cast<int>(K < V ? K : V), uniq, counts, offsets, inverse, num_unique,
-      dstatus, tickets + kMaxPasses, dev_err);
+  const int cap = static_cast<int>(K < V ? K : V);
+  if (L.nt == 256)
+    k_dedup<KeyT, 256><<<L.tiles, 256, 0, st>>>(kin, perm, K, cap, uniq, counts, offsets, inverse,
+                                                num_unique, dstatus, tickets + kMaxPasses, dev_err);
+  else
+    k_dedup<KeyT, 1024><<<L.tiles, 1024, 0, st>>>(kin, perm, K, cap, uniq, counts, offsets,
+                                                  inverse, num_unique, dstatus,
+                                                  tickets + kMaxPasses, dev_err);
   return launch_status(hipGetLastError());
 }
 
