@@ -2,24 +2,33 @@
 // sorted positions i of type u, accumulated in fp32 in a fixed order.
 //
 // Work partition (no float atomics, run-to-run bit-identical):
-//   The K sorted positions are cut into chunks of R positions (R = 32..512,
-//   growing with K), one chunk per wave and per column tile of up to 1024
-//   columns. The segment (type) of a position is inverse[perm[i]], so a wave
-//   learns every segment boundary of its chunk from two gathers and a ballot,
-//   without searching. A segment shorter than T = min(R, 64) rows belongs
-//   entirely to the chunk holding its first position, even where it runs
-//   past the chunk end; a longer one — a head of the Zipf distribution — is
-//   cut at chunk boundaries and every chunk sums its piece into a partial
-//   row:
+//   The K sorted positions are cut into N chunks of equal cost, one chunk per
+//   wave and per column tile of up to 1024 columns. A position costs one row
+//   read (rw) and a segment end one row write (ww, weighted for writes
+//   costing more than reads of the same size), so the cost before position p
+//   of segment u is rw * p + ww * u; chunk c starts where that reaches c * Q,
+//   Q = ceil((rw * K + ww * U) / N). Reads and writes
+//   thus balance across waves wherever the heads and the tail of the Zipf
+//   law fall in the sorted order (equal-length chunks left the waves of the
+//   tail, one write per row, twice as long as those of the heads). A wave
+//   finds its bounds with a 32-ary search of offsets, two targets at once.
+//   The segment (type) of a position is inverse[perm[i]], so a wave learns
+//   every segment boundary of its chunk from two gathers and a ballot,
+//   without searching. A segment shorter than T rows belongs entirely to the
+//   chunk holding its first position, even where it runs past the chunk
+//   end; a longer one is cut at chunk boundaries and every chunk sums its
+//   piece into a partial row:
 //     part_start[c]  the piece of a long segment that starts in chunk c and
 //                    continues past it (desc[c] names that segment),
-//     part_cont[c]   the piece of a long segment that started before chunk c.
+//     part_cont[c]   the piece of a long segment that started before chunk c
+//                    (cont_seg[c] names that segment).
 //   k_segsum_fix then sums, for each desc[c] >= 0, part_start[c] and the
-//   part_cont rows of the chunks the segment covers, in order: one wave per
-//   column tile for a segment of at most 16 pieces, 16 waves (fixed stride
-//   split of the pieces, fixed-order combine in LDS) for a head.
-// A chunk reads at most R + T - 1 rows; a segment is split into at most
-// K / R pieces.
+//   part_cont rows of the chunks after c that name the same segment, in
+//   order: one wave per column tile for a segment of at most 16 pieces,
+//   all waves of a workgroup (fixed stride split of the pieces, fixed-order
+//   combine in LDS) for a head.
+// A chunk holds at most R positions (N is sized for U = min(K, u_cap)) and
+// reads at most R + T - 1 rows.
 //
 // Each wave gathers whole 16-byte column vectors of RF rows at a time
 // (RF x NV x 1 KiB in flight), adds them in fp32 registers and writes a row
@@ -30,7 +39,13 @@ namespace lmz {
 
 // Tuning knobs (overridable at build time).
 #ifndef LMZ_SEG_TARGET_CHUNKS
-#define LMZ_SEG_TARGET_CHUNKS 2048   // K is cut into about this many chunks
+#define LMZ_SEG_TARGET_CHUNKS 1024   // R = the power of two near K / this (32..512)
+#endif
+#ifndef LMZ_SEG_WRITE_X2
+#define LMZ_SEG_WRITE_X2 4           // cost of a row written / a row read, times 2
+#endif
+#ifndef LMZ_SEG_TDIV
+#define LMZ_SEG_TDIV 4               // long-segment threshold T = R / this (1..64)
 #endif
 #ifndef LMZ_SEG_RF4
 #define LMZ_SEG_RF4 4                // rows per gather batch with 4 vectors per lane
@@ -63,16 +78,27 @@ struct SegArgs {
   float* part_cont;
   float* part_start;
   int32_t* desc;
-  int R, nchunks;
+  int32_t* cont_seg;
+  int R, nchunks, rw, ww;  // cost of a position / of a segment end
   int32_t* dev_err;
 };
 
 struct SegLayout {
-  int R, nchunks;
-  size_t cont, start, desc, total;
+  int R, max_chunks;
+  size_t cont, start, desc, cont_seg, total;
 };
 
 static inline size_t a256(size_t x) { return (x + 255) & ~size_t(255); }
+
+// Costs: a sorted position (a row read) costs rw = 2 * sizeof(grad) per
+// column, a segment end (a row written) ww = 4 * LMZ_SEG_WRITE_X2. A call
+// has at most rw * K + ww * min(K, u_cap) of it, at most rw * R per chunk.
+static inline int read_cost(int gtype) { return gtype == LM_BF16 ? 4 : 8; }
+constexpr int kWriteCost = 4 * LMZ_SEG_WRITE_X2;
+static inline int64_t chunks_for(int64_t K, int R, int rw, int64_t u_cap) {
+  const int64_t ub = u_cap < K ? u_cap : K;
+  return (int64_t(rw) * K + int64_t(kWriteCost) * ub + int64_t(rw) * R - 1) / (int64_t(rw) * R);
+}
 
 static SegLayout seg_layout(int64_t K, int64_t D) {
   SegLayout L{};
@@ -80,11 +106,13 @@ static SegLayout seg_layout(int64_t K, int64_t D) {
   int R = kMinR;
   while (R < want && R < kMaxR) R *= 2;
   L.R = R;
-  L.nchunks = static_cast<int>((K + R - 1) / R);
+  L.max_chunks = static_cast<int>(chunks_for(K, R, 4, K));  // any dtype and capacity
+  const size_t n = size_t(L.max_chunks);
   size_t off = 0;
-  L.cont = off;  off += a256(size_t(L.nchunks) * D * 4);
-  L.start = off; off += a256(size_t(L.nchunks) * D * 4);
-  L.desc = off;  off += a256(size_t(L.nchunks) * 4);
+  L.cont = off;     off += a256(n * D * 4);
+  L.start = off;    off += a256(n * D * 4);
+  L.desc = off;     off += a256(n * 4);
+  L.cont_seg = off; off += a256(n * 4);
   L.total = off;
   return L;
 }
@@ -95,25 +123,94 @@ size_t segsum_workspace_bytes(int64_t K, int64_t D) { return seg_layout(K, D).to
 // must cover p0 - 1 (to see whether the first segment started earlier), the
 // whole walk (at most R + T - 1 rows from p0) and one position past it (to
 // see whether the last row ends its segment).
-template <int R>
-constexpr int windows_for() { return (R + (R < 64 ? R : 64)) / 64 + 1; }
+template <int R, int T>
+constexpr int windows_for() { return (R + T) / 64 + 1; }
 
-template <typename GT, int VEC, int NV, int RF, int R>
+// Chunk bounds: the number of sorted positions whose running cost is below
+// t (the cost before position p of segment u is rw * p + ww * u), for
+// t = tA in lanes 0..31 and t = tB in lanes 32..63. A 32-ary search per
+// half-wave for the largest u < U with f(u) = rw * offsets[u] + ww * u <= t
+// (f(0) = 0), then b = offsets[u] + min(ceil((t - f(u)) / rw), len(u));
+// b = K once t >= rw * K + ww * U. Every value the search keeps is
+// wave-uniform.
+__device__ __forceinline__ void chunk_bounds(const int32_t* __restrict__ offsets, int U, int rw,
+                                             int ww, int K, int64_t tA, int64_t tB, int& bA,
+                                             int& bB) {
+  const int lane = lane_id();
+  const bool hi = lane >= 32;
+  const int hl = lane & 31;
+  int loA = 0, nA = U, loB = 0, nB = U;
+  while (nA > 1 || nB > 1) {
+    const int sA = (nA + 31) / 32, sB = (nB + 31) / 32;
+    const int lo = hi ? loB : loA, n = hi ? nB : nA, st = hi ? sB : sA;
+    const int64_t t = hi ? tB : tA;
+    const int u = lo + (hl + 1) * st;
+    bool le = false;
+    if (n > 1 && u < lo + n) le = int64_t(rw) * offsets[u] + int64_t(ww) * u <= t;
+    const uint64_t m = ballot(le);
+    const int cA = __popcll(m & 0xffffffffull), cB = __popcll(m >> 32);
+    if (nA > 1) {
+      loA += cA * sA;
+      nA = nA - cA * sA < sA ? nA - cA * sA : sA;
+    }
+    if (nB > 1) {
+      loB += cB * sB;
+      nB = nB - cB * sB < sB ? nB - cB * sB : sB;
+    }
+  }
+  const int u = hi ? loB : loA;
+  const int64_t t = hi ? tB : tA;
+  const int o0 = offsets[u], o1 = offsets[u + 1];
+  const int64_t into = (t - (int64_t(rw) * o0 + int64_t(ww) * u) + rw - 1) / rw;
+  int b = int64_t(o0) + into < int64_t(o1) ? static_cast<int>(int64_t(o0) + into) : o1;
+  if (t >= int64_t(rw) * K + int64_t(ww) * U) b = K;
+  bA = first_lane(b);
+  bB = read_lane(b, 32);
+}
+
+template <typename GT, int VEC, int NV, int RF, int R, int T>
 __global__ __launch_bounds__(kSegThreads) void k_segsum(SegArgs a) {
   using RV = RowVec<GT, VEC>;
   using raw_t = typename RV::raw_t;
   constexpr int kColsPerVec = kWave * VEC;
   constexpr int CT = NV * kColsPerVec;
-  constexpr int NW = windows_for<R>();
-  constexpr int T = R < 64 ? R : 64;
+  constexpr int NW = windows_for<R, T>();
 
   const int lane = lane_id();
   const int c = first_lane(blockIdx.x * kSegWaves + (threadIdx.x >> 6));  // one chunk per wave
   if (c >= a.nchunks) return;
   const int ct = blockIdx.y;
   const int K = a.K, D = a.D;
-  const int p0 = c * R;
-  const int p1 = p0 + R < K ? p0 + R : K;
+
+  // 0. This chunk's positions [p0, p1): equal shares of the cost rw * K + ww * U.
+  const int64_t U64 = *a.num_unique;
+  if (U64 > a.u_cap && c == 0 && ct == 0 && lane == 0) raise_err(a.dev_err, LM_DEVERR_CAPACITY);
+  const int U = first_lane(static_cast<int>(U64 < K ? U64 : K));
+  if (U < 1) {  // K > 0 always has a type: only a bad count gets here
+    if (ct == 0 && lane == 0) {
+      a.desc[c] = -1;
+      a.cont_seg[c] = -1;
+      if (c == 0) raise_err(a.dev_err, LM_DEVERR_CAPACITY);
+    }
+    return;
+  }
+  const int Ub = U < a.u_cap ? U : static_cast<int>(a.u_cap);
+  const int64_t cost = int64_t(a.rw) * K + int64_t(a.ww) * Ub;
+  const int64_t Q = (cost + a.nchunks - 1) / a.nchunks;
+  int p0, p1;
+  chunk_bounds(a.offsets, U, a.rw, a.ww, K, int64_t(c) * Q, int64_t(c + 1) * Q, p0, p1);
+  if (c == a.nchunks - 1) p1 = K;
+  if (p1 - p0 > R) {  // only inconsistent offsets: never walk past the windows
+    if (lane == 0) raise_err(a.dev_err, LM_DEVERR_CAPACITY);
+    p1 = p0 + R;
+  }
+  if (p1 <= p0) {  // an empty chunk (a segment end cost more than Q)
+    if (ct == 0 && lane == 0) {
+      a.desc[c] = -1;
+      a.cont_seg[c] = -1;
+    }
+    return;
+  }
 
   // 1. Gather the permutation and the segment of every position in the
   //    windows (sentinels: -2 before position 0, -1 from position K on).
@@ -141,10 +238,6 @@ __global__ __launch_bounds__(kSegThreads) void k_segsum(SegArgs a) {
     if (lane == kWave - 1) nxt = w + 1 < NW ? read_lane(sw[w + 1 < NW ? w + 1 : w], 0) : -3;
     ends[w] = ballot(sw[w] != nxt);
   }
-  const int64_t U64 = *a.num_unique;
-  if (U64 > a.u_cap && c == 0 && ct == 0 && lane == 0) raise_err(a.dev_err, LM_DEVERR_CAPACITY);
-  const int U = first_lane(static_cast<int>(U64 < K ? U64 : K));
-
   // 2. First and last segment of the chunk and, where needed, their lengths.
   const int s_f = read_lane(sw[0], 1);                     // segment of p0
   const bool started_before = read_lane(sw[0], 0) == s_f;  // p0 - 1 in the same segment
@@ -166,8 +259,10 @@ __global__ __launch_bounds__(kSegThreads) void k_segsum(SegArgs a) {
   const int len_l = first_lane(sl_ok && cont_after ? b_l - a.offsets[s_l] : 0);
   const bool long_f = started_before && len_f >= T;
   const bool long_l = cont_after && len_l >= T;
-  if (ct == 0 && lane == 0)
+  if (ct == 0 && lane == 0) {
     a.desc[c] = (long_l && !(started_before && s_l == s_f)) ? s_l : -1;
+    a.cont_seg[c] = long_f ? s_f : -1;
+  }
 
   // Rows this chunk sums: skip a short segment owned by the previous chunk,
   // run a short last segment to its end, stop a long one at p1.
@@ -307,10 +402,17 @@ __global__ __launch_bounds__(kFixThreads) void k_segsum_fix(SegArgs a) {
     return (t == 0 ? a.part_start + static_cast<int64_t>(cs) * D
                    : a.part_cont + static_cast<int64_t>(cs + t) * D) + col_ld;
   };
-  auto pieces_after = [&](int cs, int s) {  // chunks past cs holding rows of s
-    int c1 = first_lane((a.offsets[s + 1] - 1) / a.R);
-    if (c1 >= a.nchunks) c1 = a.nchunks - 1;
-    return c1 - cs;
+  auto pieces_after = [&](int cs, int s) {  // chunks after cs that hold a piece of s
+    int P = 0;
+    while (true) {
+      const int cc = cs + 1 + P + lane;
+      const bool same = cc < a.nchunks && a.cont_seg[cc] == s;
+      const uint64_t m = ballot(same);
+      const int run = ~m ? __builtin_ctzll(~m) : kWave;
+      P += run;
+      if (run < kWave) break;
+    }
+    return P;
   };
 
   // Pass 1: segments of at most RF pieces, the j-th of the mask by wave
@@ -377,16 +479,22 @@ __global__ __launch_bounds__(kFixThreads) void k_segsum_fix(SegArgs a) {
   }
 }
 
+template <int R>
+constexpr int t_for() {
+  constexpr int t = R / LMZ_SEG_TDIV;
+  return t < 1 ? 1 : (t > 64 ? 64 : t);
+}
+
 template <typename GT, int VEC, int NV, int RF>
 static hipError_t launch_r(const SegArgs& a, hipStream_t st) {
   constexpr int CT = NV * kWave * VEC;
   dim3 grid((a.nchunks + kSegWaves - 1) / kSegWaves, (a.D + CT - 1) / CT);
   switch (a.R) {
-    case 32: k_segsum<GT, VEC, NV, RF, 32><<<grid, kSegThreads, 0, st>>>(a); break;
-    case 64: k_segsum<GT, VEC, NV, RF, 64><<<grid, kSegThreads, 0, st>>>(a); break;
-    case 128: k_segsum<GT, VEC, NV, RF, 128><<<grid, kSegThreads, 0, st>>>(a); break;
-    case 256: k_segsum<GT, VEC, NV, RF, 256><<<grid, kSegThreads, 0, st>>>(a); break;
-    default: k_segsum<GT, VEC, NV, RF, 512><<<grid, kSegThreads, 0, st>>>(a); break;
+    case 32: k_segsum<GT, VEC, NV, RF, 32, t_for<32>()><<<grid, kSegThreads, 0, st>>>(a); break;
+    case 64: k_segsum<GT, VEC, NV, RF, 64, t_for<64>()><<<grid, kSegThreads, 0, st>>>(a); break;
+    case 128: k_segsum<GT, VEC, NV, RF, 128, t_for<128>()><<<grid, kSegThreads, 0, st>>>(a); break;
+    case 256: k_segsum<GT, VEC, NV, RF, 256, t_for<256>()><<<grid, kSegThreads, 0, st>>>(a); break;
+    default: k_segsum<GT, VEC, NV, RF, 512, t_for<512>()><<<grid, kSegThreads, 0, st>>>(a); break;
   }
   return hipGetLastError();
 }
@@ -427,8 +535,11 @@ int segsum_run(const void* grad, int gtype, int64_t K, int64_t D, int64_t ld_gra
   a.part_cont = reinterpret_cast<float*>(w + L.cont);
   a.part_start = reinterpret_cast<float*>(w + L.start);
   a.desc = reinterpret_cast<int32_t*>(w + L.desc);
+  a.cont_seg = reinterpret_cast<int32_t*>(w + L.cont_seg);
   a.R = L.R;
-  a.nchunks = L.nchunks;
+  a.rw = read_cost(gtype);
+  a.ww = kWriteCost;
+  a.nchunks = static_cast<int>(chunks_for(K, L.R, a.rw, u_cap));
   a.dev_err = dev_err;
 
   const bool out_vec = al16(out) && ld_out % 4 == 0 && D % 4 == 0;
@@ -442,7 +553,7 @@ int segsum_run(const void* grad, int gtype, int64_t K, int64_t D, int64_t ld_gra
             : dispatch_nv<bf16_t, 1>(a, 4, st);
   }
   if (e != hipSuccess) return launch_status(e);
-  const uint32_t fix_blocks = static_cast<uint32_t>((L.nchunks + kFixChunks - 1) / kFixChunks);
+  const uint32_t fix_blocks = static_cast<uint32_t>((a.nchunks + kFixChunks - 1) / kFixChunks);
   if (D % 4 == 0)
     k_segsum_fix<4, LMZ_SEG_FIX_RF><<<dim3(fix_blocks, (D + 255) / 256), kFixThreads, 0, st>>>(a);
   else
