@@ -32,6 +32,22 @@ __device__ __forceinline__ int read_lane(int v, int lane) {
 
 __device__ __forceinline__ int first_lane(int v) { return __builtin_amdgcn_readfirstlane(v); }
 
+__device__ __forceinline__ int first_lane(unsigned v) { return first_lane(static_cast<int>(v)); }
+
+__device__ __forceinline__ int64_t read_lane(int64_t v, int lane) {
+  const uint64_t u = static_cast<uint64_t>(v);
+  const uint32_t lo = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(u), lane));
+  const uint32_t hi = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(u >> 32), lane));
+  return static_cast<int64_t>((uint64_t(hi) << 32) | lo);
+}
+
+__device__ __forceinline__ int64_t first_lane(int64_t v) {
+  const uint64_t u = static_cast<uint64_t>(v);
+  const uint32_t lo = static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<int>(u)));
+  const uint32_t hi = static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<int>(u >> 32)));
+  return static_cast<int64_t>((uint64_t(hi) << 32) | lo);
+}
+
 // Inclusive prefix sum over the 64 lanes of a wave.
 template <typename T>
 __device__ __forceinline__ T wave_incl_sum(T v) {
@@ -223,6 +239,21 @@ __device__ __forceinline__ void store_vec(float* p, const float* v) {
   }
 }
 
+// Streaming store (non-temporal): for rows nothing reads back soon.
+template <int VEC>
+__device__ __forceinline__ void store_vec_nt(float* p, const float* v) {
+  if constexpr (VEC % 4 == 0) {
+#pragma unroll
+    for (int i = 0; i < VEC; i += 4) {
+      f32x4 t = {v[i], v[i + 1], v[i + 2], v[i + 3]};
+      __builtin_nontemporal_store(t, reinterpret_cast<f32x4*>(p + i));
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < VEC; ++i) __builtin_nontemporal_store(v[i], p + i);
+  }
+}
+
 template <int VEC>
 __device__ __forceinline__ void load_vec(const float* p, float* v) {
   if constexpr (VEC % 4 == 0) {
@@ -251,6 +282,25 @@ __device__ __forceinline__ int64_t lower_bound_dev(const KeyT* a, int64_t n, Key
   while (lo < hi) {
     int64_t mid = lo + ((hi - lo) >> 1);
     if (a[mid] < x) lo = mid + 1; else hi = mid;
+  }
+  return lo;
+}
+
+// lower_bound for a wave-uniform key x: the 64 lanes probe 64 evenly spaced
+// positions per round (log64 n rounds of one gather instead of log2 n
+// dependent loads). Every lane returns the same first index i with a[i] >= x.
+template <typename KeyT>
+__device__ __forceinline__ int64_t lower_bound_wave(const KeyT* a, int64_t n, KeyT x) {
+  const int lane = lane_id();
+  int64_t lo = 0, len = n;  // answer in [lo, lo + len]
+  while (len > 0) {
+    const int64_t step = (len + kWave) / (kWave + 1) > 0 ? (len + kWave) / (kWave + 1) : 1;
+    const int64_t pos = lo + (lane + 1) * step - 1;  // probe a[pos] < x
+    const bool lt = pos < lo + len && a[pos] < x;
+    const int cnt = __popcll(ballot(lt));
+    lo += int64_t(cnt) * step;
+    const int64_t rem = len - int64_t(cnt) * step;
+    len = cnt < kWave ? (step - 1 < rem ? step - 1 : rem) : rem;
   }
   return lo;
 }

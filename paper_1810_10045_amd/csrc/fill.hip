@@ -3,15 +3,32 @@
 // ascending, so every destination row is owned by exactly one wave: plain
 // row stores, no atomics and no locks.
 //
-// Layout: one wave per row, lanes across the columns in 16-byte vectors
-// (64 x 4 floats = 256 columns per vector step), NV vector steps unrolled so
-// a lane keeps NV loads of every operand in flight.
+// Layout: lanes across the columns in 16-byte vectors (64 x VEC floats per
+// vector step), NV vector steps per pass so a lane keeps NV loads of every
+// operand in flight. Loop bounds and row indices are wave-uniform and loads
+// are unconditional (a column past D loads a valid clamped column and is not
+// stored): a load under a lane condition makes the compiler wait for every
+// earlier load.
 #include "common.hpp"
 
 namespace lmz {
 
 constexpr int kFillThreads = 256;
 constexpr int kFillWaves = kFillThreads / kWave;
+#ifndef LMZ_FILL_ROWS_PER_WAVE
+#define LMZ_FILL_ROWS_PER_WAVE 1     // rows of a scatter / an update per wave
+#endif
+constexpr int kRowsPerWave = LMZ_FILL_ROWS_PER_WAVE;
+#ifndef LMZ_ZERO_ROWS
+#define LMZ_ZERO_ROWS 8              // rows a wave of the EXPAND zero fill stores
+#endif
+constexpr int kZeroRows = LMZ_ZERO_ROWS;
+#ifndef LMZ_ZERO_NT
+#define LMZ_ZERO_NT 1                // non-temporal stores for the zero fill
+#endif
+#ifndef LMZ_ADAM_HW_MATH
+#define LMZ_ADAM_HW_MATH 0
+#endif
 
 template <typename KeyT>
 __device__ __forceinline__ int64_t find_row(const KeyT* __restrict__ ids, int64_t n, KeyT x) {
@@ -50,19 +67,33 @@ __global__ __launch_bounds__(kFillThreads) void k_map_ids(
 }
 
 // ---------------------------------------------------------------------------
-// Row helpers: lanes cover columns [lane*VEC + j*64*VEC] for j < steps.
+// Columns of one pass: lane vectors at cb + j*64*VEC + lane*VEC, j < NV.
 // ---------------------------------------------------------------------------
+template <int VEC, int NV>
+struct PassCols {
+  int col[NV], ld[NV];
+  bool ok[NV];
+  __device__ __forceinline__ PassCols(int cb, int lane, int D) {
+#pragma unroll
+    for (int j = 0; j < NV; ++j) {
+      col[j] = cb + j * kWave * VEC + lane * VEC;
+      ok[j] = col[j] < D;
+      ld[j] = ok[j] ? col[j] : D - VEC;  // a valid column, loaded and not stored
+    }
+  }
+};
+
 template <int VEC, int NV>
 __device__ __forceinline__ void copy_row(float* __restrict__ dst, const float* __restrict__ src,
                                          int D, int lane) {
-  for (int c0 = lane * VEC; c0 < D; c0 += NV * kWave * VEC) {
+  for (int cb = 0; cb < D; cb += NV * kWave * VEC) {
+    const PassCols<VEC, NV> pc(cb, lane, D);
     float v[NV][VEC];
 #pragma unroll
-    for (int j = 0; j < NV; ++j)
-      if (c0 + j * kWave * VEC < D) load_vec<VEC>(src + c0 + j * kWave * VEC, v[j]);
+    for (int j = 0; j < NV; ++j) load_vec<VEC>(src + pc.ld[j], v[j]);
 #pragma unroll
     for (int j = 0; j < NV; ++j)
-      if (c0 + j * kWave * VEC < D) store_vec<VEC>(dst + c0 + j * kWave * VEC, v[j]);
+      if (pc.ok[j]) store_vec<VEC>(dst + pc.col[j], v[j]);
   }
 }
 
@@ -71,62 +102,64 @@ __device__ __forceinline__ void zero_row(float* __restrict__ dst, int D, int lan
   float z[VEC];
 #pragma unroll
   for (int e = 0; e < VEC; ++e) z[e] = 0.f;
-  for (int c0 = lane * VEC; c0 < D; c0 += kWave * VEC) store_vec<VEC>(dst + c0, z);
+  for (int cb = 0; cb < D; cb += NV * kWave * VEC) {
+    const PassCols<VEC, NV> pc(cb, lane, D);
+#pragma unroll
+    for (int j = 0; j < NV; ++j)
+      if (pc.ok[j]) {
+#if LMZ_ZERO_NT
+        store_vec_nt<VEC>(dst + pc.col[j], z);
+#else
+        store_vec<VEC>(dst + pc.col[j], z);
+#endif
+      }
+  }
 }
 
 template <int VEC, int NV>
 __device__ __forceinline__ void add_row(float* __restrict__ dst, const float* __restrict__ src,
                                         int D, int lane) {
-  for (int c0 = lane * VEC; c0 < D; c0 += NV * kWave * VEC) {
+  for (int cb = 0; cb < D; cb += NV * kWave * VEC) {
+    const PassCols<VEC, NV> pc(cb, lane, D);
     float v[NV][VEC], t[NV][VEC];
 #pragma unroll
-    for (int j = 0; j < NV; ++j)
-      if (c0 + j * kWave * VEC < D) {
-        load_vec<VEC>(src + c0 + j * kWave * VEC, v[j]);
-        load_vec<VEC>(dst + c0 + j * kWave * VEC, t[j]);
-      }
+    for (int j = 0; j < NV; ++j) {
+      load_vec<VEC>(src + pc.ld[j], v[j]);
+      load_vec<VEC>(dst + pc.ld[j], t[j]);
+    }
 #pragma unroll
-    for (int j = 0; j < NV; ++j)
-      if (c0 + j * kWave * VEC < D) {
+    for (int j = 0; j < NV; ++j) {
 #pragma unroll
-        for (int e = 0; e < VEC; ++e) t[j][e] += v[j][e];
-        store_vec<VEC>(dst + c0 + j * kWave * VEC, t[j]);
-      }
+      for (int e = 0; e < VEC; ++e) t[j][e] += v[j][e];
+      if (pc.ok[j]) store_vec<VEC>(dst + pc.col[j], t[j]);
+    }
   }
 }
 
 // ---------------------------------------------------------------------------
-// EXPAND: one wave per destination row r < n_dst: dst[r] = src[u] where
-// src_ids[u] == dst_ids[r], else zeros. The same waves also check that every
-// source id occurs in dst_ids (LM_DEVERR_NOT_FOUND otherwise).
+// EXPAND (step 5): the zero fill of rows [0, n_dst) of dst, then the SCATTER
+// of the source rows into the rows of dst_ids (k_scatter, which also flags a
+// source id missing from dst_ids). The fill is a pure store stream: a wave
+// zeroes kZeroRows consecutive rows (most of the merged rows have no source
+// on a given shard). Writing the few present rows twice is cheaper than
+// interleaving their loads with the fill, whose stores a later load would
+// have to wait for.
 // ---------------------------------------------------------------------------
-template <typename KeyT, int VEC, int NV>
-__global__ __launch_bounds__(kFillThreads) void k_expand(
-    const float* __restrict__ src, int64_t ld_src, const KeyT* __restrict__ src_ids,
-    const int64_t* __restrict__ n_src, int64_t src_cap, const KeyT* __restrict__ dst_ids,
+template <int VEC, int NV>
+__global__ __launch_bounds__(kFillThreads) void k_zero_rows(
     const int64_t* __restrict__ n_dst, int64_t dst_rows, int D, float* __restrict__ dst,
     int64_t ld_dst, int64_t nwaves, int32_t* __restrict__ dev_err) {
   const int lane = lane_id();
-  const int64_t w = blockIdx.x * int64_t(kFillWaves) + (threadIdx.x >> 6);
-  const bool first = w == 0 && lane == 0;
-  const int64_t ns = clamp_count(n_src, src_cap, dev_err, first);
-  const int64_t nd = clamp_count(n_dst, dst_rows, dev_err, first);
-  // Source-side check: lanes of the waves cover the source ids.
-  bool missing = false;
-  for (int64_t u = w * kWave + lane; u < ns; u += nwaves * kWave)
-    missing |= find_row(dst_ids, nd, src_ids[u]) < 0;
-  if (ballot(missing) && lane == 0) raise_err(dev_err, LM_DEVERR_NOT_FOUND);
-
-  for (int64_t r = w; r < nd; r += nwaves) {
-    const int64_t u = find_row(src_ids, ns, dst_ids[r]);  // uniform: same r in every lane
-    float* d = dst + r * ld_dst;
-    if (u >= 0) copy_row<VEC, NV>(d, src + u * ld_src, D, lane);
-    else zero_row<VEC, NV>(d, D, lane);
+  const int64_t w = first_lane(static_cast<int64_t>(blockIdx.x) * kFillWaves + (threadIdx.x >> 6));
+  const int64_t nd = first_lane(clamp_count(n_dst, dst_rows, dev_err, w == 0 && lane == 0));
+  for (int64_t r0 = w * kZeroRows; r0 < nd; r0 += nwaves * kZeroRows) {
+    const int nr = nd - r0 < kZeroRows ? static_cast<int>(nd - r0) : kZeroRows;
+    for (int j = 0; j < nr; ++j) zero_row<VEC, NV>(dst + (r0 + j) * ld_dst, D, lane);
   }
 }
 
 // ---------------------------------------------------------------------------
-// SCATTER / SCATTER_ADD: one wave per source row.
+// SCATTER / SCATTER_ADD: kRowsPerWave source rows per wave (grid-stride).
 // ---------------------------------------------------------------------------
 template <typename KeyT, int VEC, int NV, bool ADD>
 __global__ __launch_bounds__(kFillThreads) void k_scatter(
@@ -135,15 +168,16 @@ __global__ __launch_bounds__(kFillThreads) void k_scatter(
     const int64_t* __restrict__ n_dst, int64_t dst_rows, int D, float* __restrict__ dst,
     int64_t ld_dst, int64_t nwaves, int32_t* __restrict__ dev_err) {
   const int lane = lane_id();
-  const int64_t w = blockIdx.x * int64_t(kFillWaves) + (threadIdx.x >> 6);
+  const int64_t w = first_lane(static_cast<int64_t>(blockIdx.x) * kFillWaves + (threadIdx.x >> 6));
   const bool first = w == 0 && lane == 0;
-  const int64_t ns = clamp_count(n_src, src_cap, dev_err, first);
-  const int64_t nd = dst_ids ? clamp_count(n_dst, dst_rows, dev_err, first) : dst_rows;
+  const int64_t ns = first_lane(clamp_count(n_src, src_cap, dev_err, first));
+  const int64_t nd = dst_ids ? first_lane(clamp_count(n_dst, dst_rows, dev_err, first)) : dst_rows;
   for (int64_t u = w; u < ns; u += nwaves) {
-    const KeyT id = src_ids[u];
+    const KeyT id = first_lane(src_ids[u]);
     int64_t row;
     if (dst_ids) {
-      row = find_row(dst_ids, nd, id);
+      const int64_t lb = lower_bound_wave(dst_ids, nd, id);
+      row = (lb < nd && first_lane(dst_ids[lb]) == id) ? lb : -1;
       if (row < 0 && lane == 0) raise_err(dev_err, LM_DEVERR_NOT_FOUND);
     } else {
       row = (id >= 0 && static_cast<int64_t>(id) < dst_rows) ? static_cast<int64_t>(id) : -1;
@@ -169,10 +203,10 @@ __global__ __launch_bounds__(kFillThreads) void k_apply(
     int64_t ld_vals, OptParams o, float* __restrict__ m, float* __restrict__ v, int64_t nwaves,
     int32_t* __restrict__ dev_err) {
   const int lane = lane_id();
-  const int64_t w = blockIdx.x * int64_t(kFillWaves) + (threadIdx.x >> 6);
-  const int64_t n = clamp_count(n_rows, rows_cap, dev_err, w == 0 && lane == 0);
+  const int64_t w = first_lane(static_cast<int64_t>(blockIdx.x) * kFillWaves + (threadIdx.x >> 6));
+  const int64_t n = first_lane(clamp_count(n_rows, rows_cap, dev_err, w == 0 && lane == 0));
   for (int64_t u = w; u < n; u += nwaves) {
-    const KeyT id = rows[u];
+    const KeyT id = first_lane(rows[u]);
     if (!(id >= 0 && static_cast<int64_t>(id) < V)) {
       if (lane == 0) raise_err(dev_err, LM_DEVERR_ID_RANGE);
       continue;
@@ -181,41 +215,45 @@ __global__ __launch_bounds__(kFillThreads) void k_apply(
     const float* g = vals + u * ld_vals;
     float* mm = ADAM ? m + static_cast<int64_t>(id) * ld_table : nullptr;
     float* vv = ADAM ? v + static_cast<int64_t>(id) * ld_table : nullptr;
-    for (int c0 = lane * VEC; c0 < D; c0 += NV * kWave * VEC) {
+    for (int cb = 0; cb < D; cb += NV * kWave * VEC) {
+      const PassCols<VEC, NV> pc(cb, lane, D);
       float gr[NV][VEC], pr[NV][VEC], mr[NV][VEC], vr[NV][VEC];
 #pragma unroll
       for (int j = 0; j < NV; ++j) {
-        const int c = c0 + j * kWave * VEC;
-        if (c < D) {
-          load_vec<VEC>(g + c, gr[j]);
-          load_vec<VEC>(p + c, pr[j]);
-          if constexpr (ADAM) {
-            load_vec<VEC>(mm + c, mr[j]);
-            load_vec<VEC>(vv + c, vr[j]);
-          }
+        load_vec<VEC>(g + pc.ld[j], gr[j]);
+        load_vec<VEC>(p + pc.ld[j], pr[j]);
+        if constexpr (ADAM) {
+          load_vec<VEC>(mm + pc.ld[j], mr[j]);
+          load_vec<VEC>(vv + pc.ld[j], vr[j]);
         }
       }
 #pragma unroll
       for (int j = 0; j < NV; ++j) {
-        const int c = c0 + j * kWave * VEC;
-        if (c < D) {
 #pragma unroll
-          for (int e = 0; e < VEC; ++e) {
-            if constexpr (ADAM) {
-              const float gg = gr[j][e];
-              mr[j][e] = o.b1 * mr[j][e] + (1.f - o.b1) * gg;
-              vr[j][e] = o.b2 * vr[j][e] + (1.f - o.b2) * gg * gg;
-              const float mhat = mr[j][e] * o.inv_c1;
-              const float vhat = vr[j][e] * o.inv_c2;
-              pr[j][e] -= o.lr * (mhat / (sqrtf(vhat) + o.eps) + o.wd * pr[j][e]);
-            } else {
-              pr[j][e] -= o.lr * gr[j][e];
-            }
-          }
-          store_vec<VEC>(p + c, pr[j]);
+        for (int e = 0; e < VEC; ++e) {
           if constexpr (ADAM) {
-            store_vec<VEC>(mm + c, mr[j]);
-            store_vec<VEC>(vv + c, vr[j]);
+            const float gg = gr[j][e];
+            mr[j][e] = o.b1 * mr[j][e] + (1.f - o.b1) * gg;
+            vr[j][e] = o.b2 * vr[j][e] + (1.f - o.b2) * gg * gg;
+            const float mhat = mr[j][e] * o.inv_c1;
+            const float vhat = vr[j][e] * o.inv_c2;
+#if LMZ_ADAM_HW_MATH
+            // v_sqrt_f32 and v_rcp_f32 (about 1 ulp each) instead of the
+            // correctly rounded sequences.
+            const float den = __builtin_amdgcn_sqrtf(vhat) + o.eps;
+            pr[j][e] -= o.lr * (mhat * __builtin_amdgcn_rcpf(den) + o.wd * pr[j][e]);
+#else
+            pr[j][e] -= o.lr * (mhat / (sqrtf(vhat) + o.eps) + o.wd * pr[j][e]);
+#endif
+          } else {
+            pr[j][e] -= o.lr * gr[j][e];
+          }
+        }
+        if (pc.ok[j]) {
+          store_vec<VEC>(p + pc.col[j], pr[j]);
+          if constexpr (ADAM) {
+            store_vec<VEC>(mm + pc.col[j], mr[j]);
+            store_vec<VEC>(vv + pc.col[j], vr[j]);
           }
         }
       }
@@ -228,9 +266,11 @@ __global__ __launch_bounds__(kFillThreads) void k_apply(
 // ---------------------------------------------------------------------------
 static bool a16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
 
-static int64_t grid_waves(int64_t rows) {
-  int64_t w = rows < 1 ? 1 : rows;
-  const int64_t cap = int64_t(1) << 20;  // grid-stride beyond a million waves
+// Waves for `rows` rows at `per` rows per wave (grid-stride beyond a million).
+static int64_t grid_waves(int64_t rows, int per) {
+  int64_t w = (rows + per - 1) / per;
+  if (w < 1) w = 1;
+  const int64_t cap = int64_t(1) << 20;
   return w < cap ? w : cap;
 }
 
@@ -262,13 +302,18 @@ static hipError_t fill_launch(const float* src, int64_t ld_src, const void* src_
   const KeyT* si = static_cast<const KeyT*>(src_ids);
   const KeyT* di = static_cast<const KeyT*>(dst_ids);
   if (mode == LM_FILL_EXPAND) {
-    const int64_t waves = grid_waves(dst_rows);
+    const int64_t waves = grid_waves(dst_rows, kZeroRows);
     const uint32_t blocks = static_cast<uint32_t>((waves + kFillWaves - 1) / kFillWaves);
-    k_expand<KeyT, VEC, 4><<<blocks, kFillThreads, 0, st>>>(
+    k_zero_rows<VEC, 4><<<blocks, kFillThreads, 0, st>>>(
+        n_dst, dst_rows, static_cast<int>(D), dst, ld_dst, int64_t(blocks) * kFillWaves, dev_err);
+    if (src_cap == 0) return hipGetLastError();
+    const int64_t swaves = grid_waves(src_cap, kRowsPerWave);
+    const uint32_t sblocks = static_cast<uint32_t>((swaves + kFillWaves - 1) / kFillWaves);
+    k_scatter<KeyT, VEC, 4, false><<<sblocks, kFillThreads, 0, st>>>(
         src, ld_src, si, n_src, src_cap, di, n_dst, dst_rows, static_cast<int>(D), dst, ld_dst,
-        int64_t(blocks) * kFillWaves, dev_err);
+        int64_t(sblocks) * kFillWaves, dev_err);
   } else {
-    const int64_t waves = grid_waves(src_cap);
+    const int64_t waves = grid_waves(src_cap, kRowsPerWave);
     const uint32_t blocks = static_cast<uint32_t>((waves + kFillWaves - 1) / kFillWaves);
     if (mode == LM_FILL_SCATTER)
       k_scatter<KeyT, VEC, 4, false><<<blocks, kFillThreads, 0, st>>>(
@@ -308,7 +353,7 @@ static hipError_t apply_launch(float* table, int64_t V, int64_t D, int64_t ld_ta
                                const void* rows, const int64_t* n_rows, int64_t rows_cap,
                                const float* vals, int64_t ld_vals, bool adam, const OptParams& o,
                                float* m, float* v, int32_t* dev_err, hipStream_t st) {
-  const int64_t waves = grid_waves(rows_cap);
+  const int64_t waves = grid_waves(rows_cap, kRowsPerWave);
   const uint32_t blocks = static_cast<uint32_t>((waves + kFillWaves - 1) / kFillWaves);
   const KeyT* r = static_cast<const KeyT*>(rows);
   if (adam)
