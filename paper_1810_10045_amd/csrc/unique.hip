@@ -38,10 +38,13 @@ constexpr int kHistThreads = 1024;
 #define LMZ_UNIQUE_SMALL_TILE_MAX_K (1 << 17)  // up to this K, 256-thread tiles
 #endif
 #ifndef LMZ_UNIQUE_DIGIT_BITS
-#define LMZ_UNIQUE_DIGIT_BITS 8
+#define LMZ_UNIQUE_DIGIT_BITS 8        // widest digit with 256-thread tiles
 #endif
-constexpr int kMaxDigitBits = LMZ_UNIQUE_DIGIT_BITS;
-constexpr int kMaxRadix = 1 << kMaxDigitBits;
+#ifndef LMZ_UNIQUE_DIGIT_BITS_LARGE
+#define LMZ_UNIQUE_DIGIT_BITS_LARGE 10 // widest digit with 1024-thread tiles
+#endif
+constexpr int kSmallDigitBits = LMZ_UNIQUE_DIGIT_BITS;
+constexpr int kLargeDigitBits = LMZ_UNIQUE_DIGIT_BITS_LARGE;
 constexpr int kMaxPasses = 8;              // ceil(64 / 8)
 constexpr int kItems = 4;                  // keys per thread in a tile
 constexpr int kHistItems = 16;             // keys per thread per histogram round
@@ -57,6 +60,7 @@ constexpr uint64_t kD31 = (1ull << 31) - 1;
 struct UniqueLayout {
   size_t bhist, tickets, status, dstatus, keys0, keys1, vals0, vals1, total;
   int passes, bits, tiles, hist_blocks, nt;
+  int rstride;  // digit slots per pass in the histogram rows and status arrays
   int shift[kMaxPasses], nbits[kMaxPasses];
 };
 
@@ -72,7 +76,15 @@ static UniqueLayout unique_layout(int64_t K, int idtype, int64_t V) {
   UniqueLayout L{};
   const size_t ks = idtype == LM_I64 ? 8 : 4;
   L.bits = key_bits_for(V);
-  L.passes = L.bits == 0 ? 1 : (L.bits + kMaxDigitBits - 1) / kMaxDigitBits;
+  // Workgroups of 256 threads (tiles of 1024 keys) spread a small input over
+  // more CUs; large inputs take 1024-thread tiles, which keep the look-back
+  // status arrays (one word per digit and tile) 4x smaller and can afford
+  // wider digits where that saves a pass.
+  L.nt = K <= LMZ_UNIQUE_SMALL_TILE_MAX_K ? 256 : 1024;
+  const int narrow = kSmallDigitBits < kLargeDigitBits ? kSmallDigitBits : kLargeDigitBits;
+  const int widest = L.nt == 256 ? kSmallDigitBits : kLargeDigitBits;
+  const int p_narrow = (L.bits + narrow - 1) / narrow, p_wide = (L.bits + widest - 1) / widest;
+  L.passes = L.bits == 0 ? 1 : (p_wide < p_narrow ? p_wide : p_narrow);
   // Split the key bits evenly: the low passes take the extra bit.
   int sh = 0;
   for (int p = 0; p < L.passes; ++p) {
@@ -81,18 +93,17 @@ static UniqueLayout unique_layout(int64_t K, int idtype, int64_t V) {
     L.nbits[p] = nb;
     sh += nb;
   }
-  // Workgroups of 256 threads (tiles of 1024 keys) spread a small input over
-  // more CUs; large inputs take 1024-thread tiles, which keep the look-back
-  // status arrays (one word per digit and tile) 4x smaller.
-  L.nt = K <= LMZ_UNIQUE_SMALL_TILE_MAX_K ? 256 : 1024;
   const int64_t tile_keys = int64_t(L.nt) * kItems;
   L.tiles = static_cast<int>((K + tile_keys - 1) / tile_keys);
   const int64_t hb = (K + kHistKeysPerBlock - 1) / kHistKeysPerBlock;
   L.hist_blocks = static_cast<int>(hb < 1 ? 1 : (hb > kMaxHistBlocks ? kMaxHistBlocks : hb));
   size_t off = 0;
-  L.bhist = off;   off += align256(size_t(L.hist_blocks) * L.passes * kMaxRadix * 4);
+  L.rstride = 1 << kSmallDigitBits;
+  for (int p = 0; p < L.passes; ++p)
+    if (L.nbits[p] > kSmallDigitBits) L.rstride = 1 << kLargeDigitBits;
+  L.bhist = off;   off += align256(size_t(L.hist_blocks) * L.passes * L.rstride * 4);
   L.tickets = off; off += 256;
-  L.status = off;  off += align256(size_t(L.passes) * L.tiles * kMaxRadix * 4);
+  L.status = off;  off += align256(size_t(L.passes) * L.tiles * L.rstride * 4);
   L.dstatus = off; off += align256(size_t(L.tiles) * 8);
   L.keys0 = off;   off += align256(size_t(K) * ks);
   L.keys1 = off;   off += align256(size_t(K) * ks);
@@ -113,16 +124,16 @@ __device__ __forceinline__ uint32_t digit_of(KeyT k, int shift, uint32_t mask) {
 
 // ---------------------------------------------------------------------------
 // k_hist: bhist[b][p][d] = number of keys read by workgroup b whose digit of
-// pass p is d (rows of kMaxRadix per pass). Also clears the tickets and the
+// pass p is d (rows of rstride slots per pass). Also clears the tickets and the
 // look-back status words of this call.
 // ---------------------------------------------------------------------------
 template <typename KeyT>
 __global__ __launch_bounds__(kHistThreads) void k_hist(
-    const KeyT* __restrict__ keys, int K, uint64_t V, int passes, PassBits pb,
+    const KeyT* __restrict__ keys, int K, uint64_t V, int passes, int rstride, PassBits pb,
     uint32_t* __restrict__ bhist, uint32_t* __restrict__ clear, int64_t clear_words,
     int32_t* __restrict__ dev_err) {
-  extern __shared__ uint32_t sh[];  // passes * kMaxRadix
-  for (int i = threadIdx.x; i < passes * kMaxRadix; i += kHistThreads) sh[i] = 0;
+  extern __shared__ uint32_t sh[];  // passes * rstride
+  for (int i = threadIdx.x; i < passes * rstride; i += kHistThreads) sh[i] = 0;
   for (int64_t i = blockIdx.x * int64_t(kHistThreads) + threadIdx.x; i < clear_words;
        i += int64_t(gridDim.x) * kHistThreads)
     clear[i] = 0;
@@ -144,15 +155,15 @@ __global__ __launch_bounds__(kHistThreads) void k_hist(
         bad |= kb >= V;
         for (int p = 0; p < passes; ++p) {
           const uint32_t d = static_cast<uint32_t>(kb >> pb.shift[p]) & ((1u << pb.nbits[p]) - 1);
-          atomicAdd(&sh[p * kMaxRadix + d], 1u);
+          atomicAdd(&sh[p * rstride + d], 1u);
         }
       }
     }
   }
   if (ballot(bad) && lane_id() == 0) raise_err(dev_err, LM_DEVERR_ID_RANGE);
   __syncthreads();
-  uint32_t* row = bhist + size_t(blockIdx.x) * passes * kMaxRadix;
-  for (int i = threadIdx.x; i < passes * kMaxRadix; i += kHistThreads) row[i] = sh[i];
+  uint32_t* row = bhist + size_t(blockIdx.x) * passes * rstride;
+  for (int i = threadIdx.x; i < passes * rstride; i += kHistThreads) row[i] = sh[i];
 }
 
 // ---------------------------------------------------------------------------
@@ -536,8 +547,8 @@ static hipError_t launch_pass(const UniqueLayout& L, int p, const KeyT* kin, con
                               uint32_t* status, uint32_t* tickets, int32_t* dev_err,
                               hipStream_t st) {
   k_onesweep<KeyT, RB, NT><<<L.tiles, NT, 0, st>>>(
-      kin, vin, kout, vout, K, L.shift[p], L.nbits[p], bhist + size_t(p) * kMaxRadix,
-      L.hist_blocks, L.passes * kMaxRadix, status + size_t(p) * L.tiles * kMaxRadix, tickets + p,
+      kin, vin, kout, vout, K, L.shift[p], L.nbits[p], bhist + size_t(p) * L.rstride,
+      L.hist_blocks, L.passes * L.rstride, status + size_t(p) * L.tiles * L.rstride, tickets + p,
       dev_err);
   return hipGetLastError();
 }
@@ -564,9 +575,10 @@ static int run_unique(const KeyT* ids, int K, int64_t V, KeyT* uniq, int32_t* co
   }
   // tickets .. end of dstatus is contiguous: k_hist clears it.
   const int64_t clear_words = static_cast<int64_t>((L.keys0 - L.tickets) / 4);
-  const size_t hist_lds = size_t(L.passes) * kMaxRadix * 4;
+  const size_t hist_lds = size_t(L.passes) * L.rstride * 4;
   k_hist<KeyT><<<L.hist_blocks, kHistThreads, hist_lds, st>>>(
-      ids, K, static_cast<uint64_t>(V), L.passes, pb, bhist, tickets, clear_words, dev_err);
+      ids, K, static_cast<uint64_t>(V), L.passes, L.rstride, pb, bhist, tickets, clear_words,
+      dev_err);
   if (hipError_t e = hipGetLastError(); e != hipSuccess) return launch_status(e);
 
   const KeyT* kin = ids;
@@ -574,11 +586,19 @@ static int run_unique(const KeyT* ids, int K, int64_t V, KeyT* uniq, int32_t* co
   for (int p = 0; p < L.passes; ++p) {
     KeyT* kout = kb[p & 1];
     int32_t* vout = p == L.passes - 1 ? perm : vb[p & 1];
-    const hipError_t e =
-        L.nt == 256 ? launch_pass<KeyT, kMaxDigitBits, 256>(L, p, kin, vin, kout, vout, K, bhist,
+    // The narrowest compiled digit that holds this pass's bits.
+    const bool narrow = L.nbits[p] <= kSmallDigitBits;
+    hipError_t e;
+    if (L.nt == 256)
+      e = narrow ? launch_pass<KeyT, kSmallDigitBits, 256>(L, p, kin, vin, kout, vout, K, bhist,
+                                                            status, tickets, dev_err, st)
+                 : launch_pass<KeyT, kLargeDigitBits, 256>(L, p, kin, vin, kout, vout, K, bhist,
+                                                            status, tickets, dev_err, st);
+    else
+      e = narrow ? launch_pass<KeyT, kSmallDigitBits, 1024>(L, p, kin, vin, kout, vout, K, bhist,
                                                              status, tickets, dev_err, st)
-                    : launch_pass<KeyT, kMaxDigitBits, 1024>(L, p, kin, vin, kout, vout, K, bhist,
-                                                              status, tickets, dev_err, st);
+                 : launch_pass<KeyT, kLargeDigitBits, 1024>(L, p, kin, vin, kout, vout, K, bhist,
+                                                             status, tickets, dev_err, st);
     if (e != hipSuccess) return launch_status(e);
     kin = kout;
     vin = vout;
