@@ -49,6 +49,16 @@ def zipf_ids(K: int, V: int, s: float, seed: int, dtype=np.int32) -> np.ndarray:
     return ids.astype(dtype)
 
 
+def zipf_ids_permuted(K: int, V: int, s: float, seed: int, perm_seed: int,
+                      dtype=np.int32) -> np.ndarray:
+    """Bounded-Zipf ids whose ranks are spread over the vocabulary by a fixed
+    random permutation (id = perm[rank - 1]): the same counts as zipf_ids,
+    but the frequent words no longer sit at the smallest ids, so in sorted
+    order the long runs are scattered among the short ones."""
+    perm = np.random.Generator(np.random.PCG64(perm_seed)).permutation(V)
+    return perm[zipf_ids(K, V, s, seed, np.int64)].astype(dtype)
+
+
 def distinct_ids(n: int, V: int, seed: int, dtype=np.int32) -> np.ndarray:
     """n distinct word ids in [0, V), drawn uniformly without replacement and
     listed in ascending order (a stand-in for a type list, as the row list
@@ -143,6 +153,7 @@ class Workload:
     step: str                # what follows Seg-Sum: "scatter", "sgd", "expand", "adam"
     number: int              # seed base: ids 1000n+1, grads 1000n+2, table 1000n+3, m/v +4/+5
     shards: int = 1
+    perm_seed: int = 0       # > 0: ranks spread over the ids by a fixed permutation
     lr: float = 0.0
     table_std: float = 0.02
     adam: tuple = field(default=(0.9, 0.999, 1e-8))
@@ -162,13 +173,18 @@ class Workload:
     def np_id_dtype(self):
         return np.int64 if self.id_dtype == "i64" else np.int32
 
+    def _draw(self, seed: int) -> np.ndarray:
+        if self.perm_seed:
+            return zipf_ids_permuted(self.K, self.V, self.s, seed, self.perm_seed, self.np_id_dtype)
+        return zipf_ids(self.K, self.V, self.s, seed, self.np_id_dtype)
+
     def ids(self) -> np.ndarray:
         if self.shards == 1:
-            return zipf_ids(self.K, self.V, self.s, 1000 * self.number + 1, self.np_id_dtype)
+            return self._draw(1000 * self.number + 1)
         return np.concatenate([self.shard_ids(g) for g in range(self.shards)])
 
     def shard_ids(self, g: int) -> np.ndarray:
-        return zipf_ids(self.K, self.V, self.s, 1000 * self.number + 100 + g, self.np_id_dtype)
+        return self._draw(1000 * self.number + 100 + g)
 
     def grads_f32(self) -> np.ndarray:
         """fp32 gradients (before any bf16 rounding), K*shards x D."""
@@ -204,4 +220,9 @@ WORKLOADS = {
     "vocab2m_adam_i64": Workload("vocab2m_adam_i64", K=262_144, V=2_000_000, s=0.9, D=1024,
                                  grad_dtype="f32", id_dtype="i64", step="adam", number=5,
                                  lr=1e-3),
+    # The per-GPU word step with the word ranks permuted over the vocabulary
+    # (the robustness variant: heads no longer first in sorted order).
+    "word_step_64k_perm": Workload("word_step_64k_perm", K=65536, V=800_000, s=1.0, D=1024,
+                                   grad_dtype="f32", id_dtype="i32", step="sgd", number=2,
+                                   lr=0.1, perm_seed=77),
 }

@@ -107,10 +107,12 @@ def test_full_word_tiny_8k(lz):
     _release(pipe)
 
 
-def test_full_word_step_64k(lz):
+@pytest.mark.parametrize("name", ["word_step_64k", "word_step_64k_perm"])
+def test_full_word_step_64k(lz, name):
     """The per-GPU word-LM step: 65,536 tokens over 800K words, D = 1024,
-    every Seg-Sum row, then SGD (lr 0.1) into the 800K x 1024 table."""
-    w = synth.WORKLOADS["word_step_64k"]
+    every Seg-Sum row, then SGD (lr 0.1) into the 800K x 1024 table; also
+    with the word ranks permuted over the vocabulary."""
+    w = synth.WORKLOADS[name]
     ids, g, table0 = w.ids(), w.grads(), w.table()
     pipe = _run(lz, w, ids, g, table0)
     o = H.assert_unique_matches(pipe.ures, ids, w.V, oracle, w.name)

@@ -167,8 +167,9 @@ SEG_CASES = [
 ]
 
 
-def _segsum_case(lz, K, V, s, D, gdt, seed, ws=None):
-    ids = synth.zipf_ids(K, V, s, seed, np.int32)
+def _segsum_case(lz, K, V, s, D, gdt, seed, ws=None, perm_seed=0):
+    ids = (synth.zipf_ids_permuted(K, V, s, seed, perm_seed, np.int32) if perm_seed
+           else synth.zipf_ids(K, V, s, seed, np.int32))
     g32 = synth.normal_rows(K, D, seed + 1000)
     grad = synth.bf16_bits(g32) if gdt == "bf16" else g32
     tgrad = _t(g32).to(torch.bfloat16) if gdt == "bf16" else _t(g32)
@@ -181,9 +182,9 @@ def _segsum_case(lz, K, V, s, D, gdt, seed, ws=None):
 
 @pytest.mark.parametrize("K,V,s,D,gdt,seed", SEG_CASES,
                          ids=[f"K{c[0]}-V{c[1]}-D{c[3]}-{c[4]}" for c in SEG_CASES])
-def test_segsum_random(lz, K, V, s, D, gdt, seed):
-    _say(f"segsum K={K} V={V} D={D} {gdt}")
-    ids, grad, res, out = _segsum_case(lz, K, V, s, D, gdt, seed)
+def test_segsum_random(lz, K, V, s, D, gdt, seed, perm_seed=0):
+    _say(f"segsum K={K} V={V} D={D} {gdt} perm_seed={perm_seed}")
+    ids, grad, res, out = _segsum_case(lz, K, V, s, D, gdt, seed, perm_seed=perm_seed)
     torch.cuda.synchronize()
     lz.check(res.dev_err)
     o = H.assert_unique_matches(res, ids, V, oracle)
@@ -196,6 +197,20 @@ def test_segsum_random(lz, K, V, s, D, gdt, seed):
     assert err <= tol
     ones = o[1] == 1
     assert np.array_equal(got[ones], ref[ones]), "count-1 rows must be exact copies"
+
+
+PERM_CASES = [
+    # Zipf ranks spread over the ids by a fixed permutation: the long runs of
+    # the heads fall anywhere in the sorted order, among short ones.
+    (65_536, 800_000, 1.0, 1024, "f32", 51), (150_000, 20_000, 1.2, 256, "f32", 52),
+    (70_000, 800_000, 1.0, 1024, "bf16", 53), (20_000, 300, 1.2, 96, "f32", 54),
+]
+
+
+@pytest.mark.parametrize("K,V,s,D,gdt,seed", PERM_CASES,
+                         ids=[f"K{c[0]}-V{c[1]}-D{c[3]}-{c[4]}" for c in PERM_CASES])
+def test_segsum_permuted_ids(lz, K, V, s, D, gdt, seed):
+    test_segsum_random(lz, K, V, s, D, gdt, seed, perm_seed=seed + 500)
 
 
 def test_segsum_deterministic(lz):
