@@ -17,6 +17,12 @@ Parity status per routine (what pins it lives in ``tests/test_oracle_pins.py``):
   scatter         pinned (worked two-GPU example, numpy, invariants)
   sgd, adam       pinned (closed forms: t = 1 with zero moments, one step by
                   hand, bias-correction limits)
+  f16_from_f32,
+  f32_from_f16,
+  compress,
+  decompress      pinned (numpy's float16 conversion, every binary16 pattern
+                  round-tripped, overflow / subnormal / tie cases, power-of-two
+                  scales exact)
 """
 from __future__ import annotations
 
@@ -51,9 +57,14 @@ def _declare(L):
     L.orc_scatter.argtypes = [P, I, I, P, P, I, P, I, ctypes.c_int]
     L.orc_sgd.argtypes = [P, P, I, I, ctypes.c_double]
     L.orc_adam.argtypes = [P, P, P, P, I, I] + [ctypes.c_double] * 5 + [I]
+    L.orc_f16_from_f32.argtypes = [P, I, P]
+    L.orc_f32_from_f16.argtypes = [P, I, P]
+    L.orc_compress.argtypes = [P, I, I, ctypes.c_float, P]
+    L.orc_decompress.argtypes = [P, I, I, ctypes.c_float, P]
     for f in ("orc_unique", "orc_segsum", "orc_segsum_select",
               "orc_dense_scatter", "orc_map", "orc_expand", "orc_scatter",
-              "orc_sgd", "orc_adam"):
+              "orc_sgd", "orc_adam", "orc_f16_from_f32", "orc_f32_from_f16",
+              "orc_compress", "orc_decompress"):
         getattr(L, f).restype = ctypes.c_int
     return L
 
@@ -221,3 +232,37 @@ def adam(p, m, v, g, lr, beta1, beta2, eps, weight_decay, step):
     _check(lib().orc_adam(_p(p), _p(m), _p(v), _p(g), n, D, lr, beta1, beta2,
                           eps, weight_decay, step), "adam")
     return p, m, v
+
+
+def f16_from_f32(x) -> np.ndarray:
+    """Sec. III-C: binary16 bits of fp32 values, round to nearest even."""
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    out = np.full(x.shape, 0xDEAD, np.uint16)
+    _check(lib().orc_f16_from_f32(_p(x), x.size, _p(out)), "f16_from_f32")
+    return out
+
+
+def f32_from_f16(h) -> np.ndarray:
+    """Exact fp32 values of binary16 bit patterns."""
+    h = np.ascontiguousarray(h, dtype=np.uint16)
+    out = np.full(h.shape, np.nan, np.float32)
+    _check(lib().orc_f32_from_f16(_p(h), h.size, _p(out)), "f32_from_f16")
+    return out
+
+
+def compress(x, scale: float) -> np.ndarray:
+    """Sec. III-C compression of an n x D payload: binary16(fp32(x) * F)."""
+    x = np.ascontiguousarray(x, dtype=np.float64)
+    n, D = x.shape
+    out = np.full((n, D), 0xDEAD, np.uint16)
+    _check(lib().orc_compress(_p(x), n, D, float(scale), _p(out)), "compress")
+    return out
+
+
+def decompress(h, inv_scale: float) -> np.ndarray:
+    """Sec. III-C decompression: fp32(binary16) * (1/F), as fp64."""
+    h = np.ascontiguousarray(h, dtype=np.uint16)
+    n, D = h.shape
+    out = np.full((n, D), np.nan)
+    _check(lib().orc_decompress(_p(h), n, D, float(inv_scale), _p(out)), "decompress")
+    return out

@@ -266,3 +266,99 @@ int orc_adam(double* p, double* m, double* v, const double* g, int64_t n,
   }
   return ORC_OK;
 }
+
+/*
+ * Sec. III-C (lower precision): the payload that the GPUs exchange is cast
+ * to IEEE binary16 after multiplying it by a compression scale F, and cast
+ * back and divided by F at the receiving end. The kernels multiply in fp32
+ * and round once to binary16, so the oracle does the same here.
+ *
+ * f16_bits: the binary16 encoding of an fp32 value, rounded to nearest with
+ * ties to even, written out from the two formats (1 sign, 5 exponent bits
+ * biased by 15, 10 fraction bits; subnormals below 2^-14 in units of 2^-24;
+ * magnitudes that round past 65504 become infinity).
+ */
+static uint16_t f16_bits(float f) {
+  uint32_t x;
+  memcpy(&x, &f, sizeof x);
+  const uint32_t sign = (x >> 16) & 0x8000u;
+  const int exp32 = (int)((x >> 23) & 0xffu);
+  const uint32_t frac = x & 0x7fffffu;
+  if (exp32 == 0xff) return (uint16_t)(sign | (frac ? 0x7e00u : 0x7c00u));
+  const int e = exp32 - 127 + 15; /* exponent field of binary16 */
+  if (e >= 31) return (uint16_t)(sign | 0x7c00u);
+  if (e >= 1) {
+    /* normal: keep 10 of the 23 fraction bits, round on the other 13 */
+    uint32_t h = ((uint32_t)e << 10) | (frac >> 13);
+    const uint32_t rest = frac & 0x1fffu;
+    if (rest > 0x1000u || (rest == 0x1000u && (h & 1u))) h += 1; /* a carry may reach infinity */
+    return (uint16_t)(sign | h);
+  }
+  /* subnormal or zero: the value is M * 2^(e - 14) units of 2^-24, M the
+     24-bit significand with its leading one */
+  if (e < -10) return (uint16_t)sign; /* below half the smallest subnormal */
+  const uint32_t M = frac | 0x800000u;
+  const int s = 14 - e; /* bits dropped, 14..24 */
+  uint32_t m = M >> s;
+  const uint32_t rest = M & ((1u << s) - 1u), half = 1u << (s - 1);
+  if (rest > half || (rest == half && (m & 1u))) m += 1; /* 1024 is the smallest normal */
+  return (uint16_t)(sign | m);
+}
+
+/* The fp32 value of a binary16 encoding (exact). */
+static float f16_value(uint16_t h) {
+  const uint32_t sign = (uint32_t)(h & 0x8000u) << 16;
+  const uint32_t e = (h >> 10) & 0x1fu, m = h & 0x3ffu;
+  uint32_t x;
+  if (e == 31) {
+    x = sign | 0x7f800000u | (m << 13);
+  } else if (e == 0) {
+    if (m == 0) {
+      x = sign;
+    } else { /* subnormal: m * 2^-24 */
+      float f = (float)m * 0x1p-24f;
+      memcpy(&x, &f, sizeof x);
+      x |= sign;
+    }
+  } else {
+    x = sign | ((e - 15 + 127) << 23) | (m << 13);
+  }
+  float f;
+  memcpy(&f, &x, sizeof f);
+  return f;
+}
+
+/* Element-wise conversions, for the pins. */
+int orc_f16_from_f32(const float* x, int64_t n, uint16_t* out) {
+  for (int64_t i = 0; i < n; ++i) out[i] = f16_bits(x[i]);
+  return ORC_OK;
+}
+
+int orc_f32_from_f16(const uint16_t* h, int64_t n, float* out) {
+  for (int64_t i = 0; i < n; ++i) out[i] = f16_value(h[i]);
+  return ORC_OK;
+}
+
+/*
+ * Compression: out = binary16(fp32(fp32(x) * scale)), n x D. x arrives in
+ * fp64 and is first rounded to fp32, the precision the kernels hold it in.
+ */
+int orc_compress(const double* x, int64_t n, int64_t D, float scale, uint16_t* out) {
+  if (n < 0 || D < 0) return ORC_BADARG;
+  for (int64_t i = 0; i < n * D; ++i) {
+    const float x32 = (float)x[i];
+    const float t = x32 * scale;
+    out[i] = f16_bits(t);
+  }
+  return ORC_OK;
+}
+
+/* Decompression: out = fp32(fp32(h) * inv_scale), returned as fp64. */
+int orc_decompress(const uint16_t* h, int64_t n, int64_t D, float inv_scale, double* out) {
+  if (n < 0 || D < 0) return ORC_BADARG;
+  for (int64_t i = 0; i < n * D; ++i) {
+    const float g = f16_value(h[i]) * inv_scale;
+    out[i] = (double)g;
+  }
+  return ORC_OK;
+}

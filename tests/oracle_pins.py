@@ -359,10 +359,64 @@ def check_memory_example():
     assert round(ag / un) == g["paper_saving_x"]
 
 
+def check_f16_conversion():
+    """Sec. III-C binary16 casts against numpy's (IEEE round to nearest even):
+    every binary16 pattern widens to numpy's value and narrows back to itself;
+    random fp32 values over 57 binades, and the exact midpoints between
+    neighbouring binary16 values (normal and subnormal), narrow like numpy."""
+    allh = np.arange(1 << 16, dtype=np.uint32).astype(np.uint16)
+    wide = oracle.f32_from_f16(allh)
+    ref = allh.view(np.float16).astype(np.float32)
+    nan = np.isnan(ref)
+    assert np.array_equal(np.isnan(wide), nan)
+    assert np.array_equal(wide[~nan].view(np.uint32), ref[~nan].view(np.uint32))
+    back = oracle.f16_from_f32(wide)
+    assert np.array_equal(back[~nan], allh[~nan])
+    assert np.all((back[nan] & 0x7C00) == 0x7C00) and np.all((back[nan] & 0x3FF) != 0)
+    rng = np.random.default_rng(61)
+    mag = np.exp2(rng.uniform(-40, 17, size=200_000)).astype(np.float32)
+    x = np.where(rng.random(mag.size) < 0.5, -mag, mag).astype(np.float32)
+    with np.errstate(over="ignore"):
+        want = x.astype(np.float16).view(np.uint16)
+    assert np.array_equal(oracle.f16_from_f32(x), want)
+    # exact midpoints: ties go to the even neighbour
+    fin = ref[np.isfinite(ref) & (ref >= 0)]
+    fin = np.unique(fin)
+    mid = ((fin[:-1].astype(np.float64) + fin[1:].astype(np.float64)) / 2).astype(np.float32)
+    assert np.array_equal(mid.astype(np.float64), (fin[:-1].astype(np.float64) + fin[1:]) / 2)
+    with np.errstate(over="ignore"):
+        assert np.array_equal(oracle.f16_from_f32(mid), mid.astype(np.float16).view(np.uint16))
+
+
+def check_compression():
+    """Sec. III-C compression-scaling: with a power-of-two F the product is
+    exact, so the payload equals numpy's binary16 of x*F and the round trip
+    errs by at most 2^-11 |x| while |x F| stays in the normal range; past
+    65504 the code saturates to infinity; with any other F the product is
+    rounded to fp32 before the cast."""
+    rng = np.random.default_rng(62)
+    x32 = (rng.standard_normal((300, 40)) * 0.01).astype(np.float32)
+    for F in (1.0, 256.0, 1024.0):
+        h = oracle.compress(x32.astype(np.float64), F)
+        assert np.array_equal(h, (x32 * np.float32(F)).astype(np.float16).view(np.uint16))
+        back = oracle.decompress(h, 1.0 / F)
+        big = np.abs(x32 * F) >= 2.0 ** -14
+        assert np.all(np.abs(back - x32)[big] <= 2.0 ** -11 * np.abs(x32)[big])
+        assert np.all(np.abs(back - x32)[~big] <= 2.0 ** -25 / F)
+    F = 3.0
+    prod = x32 * np.float32(F)
+    assert np.array_equal(oracle.compress(x32.astype(np.float64), F),
+                          prod.astype(np.float16).view(np.uint16))
+    over = np.array([[65519.0 / 256, 65521.0 / 256, -70000.0 / 256, 1e9]], np.float64)
+    h = oracle.compress(over, 256.0)
+    assert h.tolist() == [[0x7BFF, 0x7C00, 0xFC00, 0x7C00]]
+    assert np.all(np.isinf(oracle.decompress(h[:, 1:], 1 / 256.0)))
+
+
 ALL_CHECKS = [
     check_to_be_or_not_to_be, check_numpy_unique, check_brute_force_unique,
     check_unique_invariants, check_unique_rejects_out_of_range,
     check_fig2_i_want_a_pen_and_a, check_segsum_numpy, check_segsum_special_cases,
     check_segsum_select, check_fig3_two_gpus, check_shards_merge, check_map_and_fill,
-    check_sgd, check_adam_closed_forms,
+    check_sgd, check_adam_closed_forms, check_f16_conversion, check_compression,
 ]

@@ -14,6 +14,15 @@ SRC = os.path.join(os.path.dirname(oracle.__file__), "lmoracle.c")
 
 # (name, text in lmoracle.c, replacement)
 MUTANTS = [
+    ("f16_ties_away", "if (rest > 0x1000u || (rest == 0x1000u && (h & 1u))) h += 1;",
+     "if (rest >= 0x1000u) h += 1;"),
+    ("f16_truncates", "if (rest > 0x1000u || (rest == 0x1000u && (h & 1u))) h += 1;", ""),
+    ("f16_subnormal_shift", "const int s = 14 - e; /* bits dropped, 14..24 */",
+     "const int s = 13 - e; /* bits dropped, 14..24 */"),
+    ("f16_exponent_bias", "const int e = exp32 - 127 + 15;", "const int e = exp32 - 127 + 16;"),
+    ("compress_scale_dropped", "const float t = x32 * scale;", "const float t = x32;"),
+    ("decompress_scale_inverted", "const float g = f16_value(h[i]) * inv_scale;",
+     "const float g = f16_value(h[i]) / inv_scale;"),
     ("ties_reversed", "if (x->k != y->k) return x->k < y->k ? -1 : 1;",
      "if (x->k != y->k) return x->k < y->k ? 1 : -1;"),
     ("last_token_dropped", "for (int64_t i = 0; i < K; ++i) {\n    if (i == 0",
