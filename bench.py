@@ -107,7 +107,7 @@ class Batch:
         t = torch.from_numpy(g)
         self.grad = (t.view(torch.bfloat16) if w.grad_dtype == "bf16" else t).to(dev)
         del g, t
-        if w.step == "expand":
+        if w.step in ("expand", "expand_f16"):
             self.ids0 = self.ids[:w.K]
             self.grad0 = self.grad[:w.K]
 
@@ -135,10 +135,11 @@ class Pipeline:
         if w.step == "adam":
             st["m"] = torch.zeros_like(st["table"])
             st["v"] = torch.zeros_like(st["table"])
-        if w.step == "expand":
+        if w.step in ("expand", "expand_f16"):
             st["u0"] = lz.unique_buffers(w.K, w.V, idt, dev)
             st["out0"] = torch.empty((st["u0"].uniq.numel(), D), dtype=torch.float32, device=dev)
-            st["M"] = torch.empty((cap, D), dtype=torch.float32, device=dev)
+            mdt = torch.float16 if w.step == "expand_f16" else torch.float32
+            st["M"] = torch.empty((cap, D), dtype=mdt, device=dev)
 
     def step(self, b, ev=None):
         w, lz, st, ures, err = self.w, self.lz, self.state, self.ures, self.dev_err
@@ -160,13 +161,17 @@ class Pipeline:
         elif w.step == "scatter":
             lz.fill_values(self.out, ures.uniq, ures.num_unique, st["table"], None, None,
                            "scatter", dev_err=err)
-        elif w.step == "expand":
+        elif w.step in ("expand", "expand_f16"):
             u0 = st["u0"]
             lz.unique(bt.ids0, w.V, out=u0, ws=self.ws)
             lz.segsum(bt.grad0, u0.perm, u0.inverse, u0.offsets, u0.num_unique, out=st["out0"],
                       dev_err=err, ws=self.ws)
-            lz.fill_values(st["out0"], u0.uniq, u0.num_unique, st["M"], ures.uniq,
-                           ures.num_unique, "expand", dev_err=err)
+            if w.step == "expand":
+                lz.fill_values(st["out0"], u0.uniq, u0.num_unique, st["M"], ures.uniq,
+                               ures.num_unique, "expand", dev_err=err)
+            else:
+                lz.fill_values_f16(st["out0"], u0.uniq, u0.num_unique, st["M"], ures.uniq,
+                                   ures.num_unique, "expand", scale=w.scale, dev_err=err)
         if ev: ev(3)
 
 

@@ -63,7 +63,8 @@ enum {
   LM_DEVERR_ID_RANGE = 1,   /* an id outside [0, V) (or outside the dense table) */
   LM_DEVERR_NOT_FOUND = 2,  /* a source id that the destination id list lacks */
   LM_DEVERR_CAPACITY = 4,   /* a device-side count above its buffer's capacity */
-  LM_DEVERR_SPIN = 8        /* a bounded inter-workgroup wait gave up */
+  LM_DEVERR_SPIN = 8,       /* a bounded inter-workgroup wait gave up */
+  LM_DEVERR_NONFINITE = 16  /* a compressed (binary16) value is infinite or NaN */
 };
 
 /* Index dtypes: word indices are int32 or int64; every position, count and
@@ -234,6 +235,41 @@ int lm_sparse_apply(float* table, int64_t V, int64_t D, int64_t ld_table,
                     int32_t opt, float lr, float beta1, float beta2, float eps,
                     float weight_decay, int64_t step, float* m, float* v,
                     int32_t* dev_err, void* stream);
+
+/* ------------------------------------------------------------------------
+ * Compressed payload — Sec. III-C (lower precision): the U_g x D matrix the
+ * GPUs all-reduce in step 6 travels as IEEE binary16 after a multiplication
+ * by a compression scale F, and is multiplied by 1/F after the up-cast at the
+ * receiving end. These two entry points are the two ends, fused into the
+ * steps that write and read the payload (the collective itself is not part
+ * of this library). A power-of-two F makes both scalings exact.
+ *
+ * lm_fill_values_f16: as lm_fill_values, but dst is binary16 and each value
+ * written is binary16(fp32(src * scale)) (round to nearest even; EXPAND's
+ * zero rows are +0). Modes LM_FILL_EXPAND and LM_FILL_SCATTER;
+ * LM_FILL_SCATTER_ADD returns LM_E_UNSUPPORTED.
+ * dst        device, dst_rows x D binary16 (uint16 bit patterns), row
+ *            stride ld_dst (in elements).
+ * scale      the compression scale F (finite, nonzero).
+ * A written value that is infinite or NaN (|src * scale| rounds above
+ * 65504, the binary16 maximum) sets LM_DEVERR_NONFINITE, the signal a
+ * caller uses to lower F; the value is still written.
+ * ------------------------------------------------------------------------ */
+int lm_fill_values_f16(const float* src, int64_t ld_src, const void* src_ids,
+                       const int64_t* n_src, int64_t src_cap, const void* dst_ids,
+                       const int64_t* n_dst, int32_t idtype, int64_t D, uint16_t* dst,
+                       int64_t dst_rows, int64_t ld_dst, int32_t mode, float scale,
+                       int32_t* dev_err, void* stream);
+
+/* lm_sparse_apply_f16: as lm_sparse_apply, but vals is the binary16 payload
+ * (rows_cap x D uint16 bit patterns, row stride ld_vals) and each gradient
+ * value is fp32(vals) * inv_scale (inv_scale = 1/F; finite, nonzero). */
+int lm_sparse_apply_f16(float* table, int64_t V, int64_t D, int64_t ld_table,
+                        const void* rows, int32_t idtype, const int64_t* n_rows,
+                        int64_t rows_cap, const uint16_t* vals, int64_t ld_vals,
+                        float inv_scale, int32_t opt, float lr, float beta1, float beta2,
+                        float eps, float weight_decay, int64_t step, float* m, float* v,
+                        int32_t* dev_err, void* stream);
 
 #ifdef __cplusplus
 }

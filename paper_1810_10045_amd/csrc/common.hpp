@@ -239,6 +239,84 @@ __device__ __forceinline__ void store_vec(float* p, const float* v) {
   }
 }
 
+// ---------------------------------------------------------------------------
+// binary16 payload (Sec. III-C): VEC values per lane, 8 per 16-byte vector.
+// The casts are v_cvt_f16_f32 (round to nearest even, binary16 subnormals
+// kept) and v_cvt_f32_f16 (exact). The scaling is an fp32 multiply whose
+// result is held opaque (mul_rounded): folded into the cast
+// (v_fma_mixlo_f16), the product would be rounded once to binary16 instead
+// of first to fp32.
+// ---------------------------------------------------------------------------
+typedef _Float16 h16x8 __attribute__((ext_vector_type(8)));
+
+__device__ __forceinline__ bool half_nonfinite(uint16_t b) { return (b & 0x7c00u) == 0x7c00u; }
+
+// p[i] = binary16(v[i] * s); returns true if any stored value is inf or NaN.
+// fp32 product of a and b, rounded to fp32 and opaque to the optimizer (an
+// empty asm statement holds it in a VGPR), so no later cast can absorb it.
+__device__ __forceinline__ float mul_rounded(float a, float b) {
+  float t = __fmul_rn(a, b);
+  asm volatile("" : "+v"(t));
+  return t;
+}
+
+template <int VEC>
+__device__ __forceinline__ bool store_half_scaled(uint16_t* p, const float* v, float s) {
+  bool bad = false;
+  if constexpr (VEC % 8 == 0) {
+#pragma unroll
+    for (int i = 0; i < VEC; i += 8) {
+      h16x8 h;
+#pragma unroll
+      for (int k = 0; k < 8; ++k) h[k] = static_cast<_Float16>(mul_rounded(v[i + k], s));
+      const u32x4 w = __builtin_bit_cast(u32x4, h);
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        bad |= half_nonfinite(static_cast<uint16_t>(w[k]));
+        bad |= half_nonfinite(static_cast<uint16_t>(w[k] >> 16));
+      }
+      *reinterpret_cast<u32x4*>(p + i) = w;
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < VEC; ++i) {
+      const uint16_t b = __builtin_bit_cast(uint16_t, static_cast<_Float16>(mul_rounded(v[i], s)));
+      bad |= half_nonfinite(b);
+      p[i] = b;
+    }
+  }
+  return bad;
+}
+
+// v[i] = fp32(p[i]) * s.
+template <int VEC>
+__device__ __forceinline__ void load_half_scaled(const uint16_t* p, float* v, float s) {
+  if constexpr (VEC % 8 == 0) {
+#pragma unroll
+    for (int i = 0; i < VEC; i += 8) {
+      const h16x8 h = __builtin_bit_cast(h16x8, *reinterpret_cast<const u32x4*>(p + i));
+#pragma unroll
+      for (int k = 0; k < 8; ++k) v[i + k] = mul_rounded(static_cast<float>(h[k]), s);
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < VEC; ++i)
+      v[i] = mul_rounded(static_cast<float>(__builtin_bit_cast(_Float16, p[i])), s);
+  }
+}
+
+template <int VEC>
+__device__ __forceinline__ void store_half_zero(uint16_t* p) {
+  if constexpr (VEC % 8 == 0) {
+    const u32x4 z = {0u, 0u, 0u, 0u};
+#pragma unroll
+    for (int i = 0; i < VEC; i += 8) __builtin_nontemporal_store(z, reinterpret_cast<u32x4*>(p + i));
+  } else {
+#pragma unroll
+    for (int i = 0; i < VEC; ++i) p[i] = 0;
+  }
+}
+
 // Streaming store (non-temporal): for rows nothing reads back soon.
 template <int VEC>
 __device__ __forceinline__ void store_vec_nt(float* p, const float* v) {

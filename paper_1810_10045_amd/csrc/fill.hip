@@ -190,16 +190,83 @@ __global__ __launch_bounds__(kFillThreads) void k_scatter(
 }
 
 // ---------------------------------------------------------------------------
+// binary16 payload (Sec. III-C): EXPAND / SCATTER of fp32 rows into a
+// binary16 matrix, each value multiplied by the compression scale in fp32
+// and rounded once. A stored inf or NaN raises LM_DEVERR_NONFINITE.
+// ---------------------------------------------------------------------------
+template <int VEC, int NV>
+__global__ __launch_bounds__(kFillThreads) void k_zero_rows_h(
+    const int64_t* __restrict__ n_dst, int64_t dst_rows, int D, uint16_t* __restrict__ dst,
+    int64_t ld_dst, int64_t nwaves, int32_t* __restrict__ dev_err) {
+  const int lane = lane_id();
+  const int64_t w = first_lane(static_cast<int64_t>(blockIdx.x) * kFillWaves + (threadIdx.x >> 6));
+  const int64_t nd = first_lane(clamp_count(n_dst, dst_rows, dev_err, w == 0 && lane == 0));
+  for (int64_t r0 = w * kZeroRows; r0 < nd; r0 += nwaves * kZeroRows) {
+    const int nr = nd - r0 < kZeroRows ? static_cast<int>(nd - r0) : kZeroRows;
+    for (int j = 0; j < nr; ++j) {
+      uint16_t* row = dst + (r0 + j) * ld_dst;
+      for (int cb = 0; cb < D; cb += NV * kWave * VEC) {
+        const PassCols<VEC, NV> pc(cb, lane, D);
+#pragma unroll
+        for (int k = 0; k < NV; ++k)
+          if (pc.ok[k]) store_half_zero<VEC>(row + pc.col[k]);
+      }
+    }
+  }
+}
+
+template <typename KeyT, int VEC, int NV>
+__global__ __launch_bounds__(kFillThreads) void k_scatter_h(
+    const float* __restrict__ src, int64_t ld_src, const KeyT* __restrict__ src_ids,
+    const int64_t* __restrict__ n_src, int64_t src_cap, const KeyT* __restrict__ dst_ids,
+    const int64_t* __restrict__ n_dst, int64_t dst_rows, int D, uint16_t* __restrict__ dst,
+    int64_t ld_dst, float scale, int64_t nwaves, int32_t* __restrict__ dev_err) {
+  const int lane = lane_id();
+  const int64_t w = first_lane(static_cast<int64_t>(blockIdx.x) * kFillWaves + (threadIdx.x >> 6));
+  const bool first = w == 0 && lane == 0;
+  const int64_t ns = first_lane(clamp_count(n_src, src_cap, dev_err, first));
+  const int64_t nd = dst_ids ? first_lane(clamp_count(n_dst, dst_rows, dev_err, first)) : dst_rows;
+  bool bad = false;
+  for (int64_t u = w; u < ns; u += nwaves) {
+    const KeyT id = first_lane(src_ids[u]);
+    int64_t row;
+    if (dst_ids) {
+      const int64_t lb = lower_bound_wave(dst_ids, nd, id);
+      row = (lb < nd && first_lane(dst_ids[lb]) == id) ? lb : -1;
+      if (row < 0 && lane == 0) raise_err(dev_err, LM_DEVERR_NOT_FOUND);
+    } else {
+      row = (id >= 0 && static_cast<int64_t>(id) < dst_rows) ? static_cast<int64_t>(id) : -1;
+      if (row < 0 && lane == 0) raise_err(dev_err, LM_DEVERR_ID_RANGE);
+    }
+    if (row < 0) continue;
+    const float* srow = src + u * ld_src;
+    uint16_t* drow = dst + row * ld_dst;
+    for (int cb = 0; cb < D; cb += NV * kWave * VEC) {
+      const PassCols<VEC, NV> pc(cb, lane, D);
+      float v[NV][VEC];
+#pragma unroll
+      for (int k = 0; k < NV; ++k) load_vec<VEC>(srow + pc.ld[k], v[k]);
+#pragma unroll
+      for (int k = 0; k < NV; ++k)
+        if (pc.ok[k]) bad |= store_half_scaled<VEC>(drow + pc.col[k], v[k], scale);
+    }
+  }
+  if (ballot(bad) && lane == 0) raise_err(dev_err, LM_DEVERR_NONFINITE);
+}
+
+// ---------------------------------------------------------------------------
 // Sparse apply (step 7): one wave per touched row.
 // ---------------------------------------------------------------------------
 struct OptParams {
-  float lr, b1, b2, eps, wd, inv_c1, inv_c2;
+  float lr, b1, b2, eps, wd, inv_c1, inv_c2, g_scale;
 };
 
-template <typename KeyT, int VEC, int NV, bool ADAM>
+// ValT float: fp32 gradients; ValT uint16_t: the binary16 payload of
+// Sec. III-C, each value multiplied by o.g_scale (1/F) after the up-cast.
+template <typename KeyT, typename ValT, int VEC, int NV, bool ADAM>
 __global__ __launch_bounds__(kFillThreads) void k_apply(
     float* __restrict__ table, int64_t V, int D, int64_t ld_table, const KeyT* __restrict__ rows,
-    const int64_t* __restrict__ n_rows, int64_t rows_cap, const float* __restrict__ vals,
+    const int64_t* __restrict__ n_rows, int64_t rows_cap, const ValT* __restrict__ vals,
     int64_t ld_vals, OptParams o, float* __restrict__ m, float* __restrict__ v, int64_t nwaves,
     int32_t* __restrict__ dev_err) {
   const int lane = lane_id();
@@ -212,7 +279,7 @@ __global__ __launch_bounds__(kFillThreads) void k_apply(
       continue;
     }
     float* p = table + static_cast<int64_t>(id) * ld_table;
-    const float* g = vals + u * ld_vals;
+    const ValT* g = vals + u * ld_vals;
     float* mm = ADAM ? m + static_cast<int64_t>(id) * ld_table : nullptr;
     float* vv = ADAM ? v + static_cast<int64_t>(id) * ld_table : nullptr;
     for (int cb = 0; cb < D; cb += NV * kWave * VEC) {
@@ -220,7 +287,8 @@ __global__ __launch_bounds__(kFillThreads) void k_apply(
       float gr[NV][VEC], pr[NV][VEC], mr[NV][VEC], vr[NV][VEC];
 #pragma unroll
       for (int j = 0; j < NV; ++j) {
-        load_vec<VEC>(g + pc.ld[j], gr[j]);
+        if constexpr (sizeof(ValT) == 2) load_half_scaled<VEC>(g + pc.ld[j], gr[j], o.g_scale);
+        else load_vec<VEC>(g + pc.ld[j], gr[j]);
         load_vec<VEC>(p + pc.ld[j], pr[j]);
         if constexpr (ADAM) {
           load_vec<VEC>(mm + pc.ld[j], mr[j]);
@@ -348,23 +416,40 @@ int fill_run(const float* src, int64_t ld_src, const void* src_ids, const int64_
   return launch_status(e);
 }
 
-template <typename KeyT, int VEC>
+template <typename KeyT, typename ValT, int VEC, int NV>
 static hipError_t apply_launch(float* table, int64_t V, int64_t D, int64_t ld_table,
                                const void* rows, const int64_t* n_rows, int64_t rows_cap,
-                               const float* vals, int64_t ld_vals, bool adam, const OptParams& o,
+                               const ValT* vals, int64_t ld_vals, bool adam, const OptParams& o,
                                float* m, float* v, int32_t* dev_err, hipStream_t st) {
   const int64_t waves = grid_waves(rows_cap, kRowsPerWave);
   const uint32_t blocks = static_cast<uint32_t>((waves + kFillWaves - 1) / kFillWaves);
   const KeyT* r = static_cast<const KeyT*>(rows);
   if (adam)
-    k_apply<KeyT, VEC, 4, true><<<blocks, kFillThreads, 0, st>>>(
+    k_apply<KeyT, ValT, VEC, NV, true><<<blocks, kFillThreads, 0, st>>>(
         table, V, static_cast<int>(D), ld_table, r, n_rows, rows_cap, vals, ld_vals, o, m, v,
         int64_t(blocks) * kFillWaves, dev_err);
   else
-    k_apply<KeyT, VEC, 4, false><<<blocks, kFillThreads, 0, st>>>(
+    k_apply<KeyT, ValT, VEC, NV, false><<<blocks, kFillThreads, 0, st>>>(
         table, V, static_cast<int>(D), ld_table, r, n_rows, rows_cap, vals, ld_vals, o, m, v,
         int64_t(blocks) * kFillWaves, dev_err);
   return hipGetLastError();
+}
+
+static OptParams opt_params(int opt, float lr, float beta1, float beta2, float eps,
+                            float weight_decay, int64_t step, float g_scale) {
+  OptParams o{};
+  o.lr = lr;
+  o.b1 = beta1;
+  o.b2 = beta2;
+  o.eps = eps;
+  o.wd = weight_decay;
+  o.g_scale = g_scale;
+  if (opt == LM_OPT_ADAM) {
+    // Bias corrections 1 - beta^t, computed once on the host in double.
+    o.inv_c1 = static_cast<float>(1.0 / (1.0 - __builtin_pow(static_cast<double>(beta1), static_cast<double>(step))));
+    o.inv_c2 = static_cast<float>(1.0 / (1.0 - __builtin_pow(static_cast<double>(beta2), static_cast<double>(step))));
+  }
+  return o;
 }
 
 int apply_run(float* table, int64_t V, int64_t D, int64_t ld_table, const void* rows, int idtype,
@@ -373,30 +458,90 @@ int apply_run(float* table, int64_t V, int64_t D, int64_t ld_table, const void* 
               int64_t step, float* m, float* v, int32_t* dev_err, hipStream_t st) {
   if (D == 0 || rows_cap == 0) return LM_OK;
   const bool adam = opt == LM_OPT_ADAM;
-  OptParams o{};
-  o.lr = lr;
-  o.b1 = beta1;
-  o.b2 = beta2;
-  o.eps = eps;
-  o.wd = weight_decay;
-  if (adam) {
-    // Bias corrections 1 - beta^t, computed once on the host in double.
-    o.inv_c1 = static_cast<float>(1.0 / (1.0 - __builtin_pow(static_cast<double>(beta1), static_cast<double>(step))));
-    o.inv_c2 = static_cast<float>(1.0 / (1.0 - __builtin_pow(static_cast<double>(beta2), static_cast<double>(step))));
-  }
+  const OptParams o = opt_params(opt, lr, beta1, beta2, eps, weight_decay, step, 1.f);
   bool vec = a16(table) && a16(vals) && ld_table % 4 == 0 && ld_vals % 4 == 0 && D % 4 == 0;
   if (adam) vec = vec && a16(m) && a16(v);
   hipError_t e;
   if (idtype == LM_I64)
-    e = vec ? apply_launch<int64_t, 4>(table, V, D, ld_table, rows, n_rows, rows_cap, vals, ld_vals,
-                                       adam, o, m, v, dev_err, st)
-            : apply_launch<int64_t, 1>(table, V, D, ld_table, rows, n_rows, rows_cap, vals, ld_vals,
-                                       adam, o, m, v, dev_err, st);
+    e = vec ? apply_launch<int64_t, float, 4, 4>(table, V, D, ld_table, rows, n_rows, rows_cap,
+                                                 vals, ld_vals, adam, o, m, v, dev_err, st)
+            : apply_launch<int64_t, float, 1, 4>(table, V, D, ld_table, rows, n_rows, rows_cap,
+                                                 vals, ld_vals, adam, o, m, v, dev_err, st);
   else
-    e = vec ? apply_launch<int32_t, 4>(table, V, D, ld_table, rows, n_rows, rows_cap, vals, ld_vals,
-                                       adam, o, m, v, dev_err, st)
-            : apply_launch<int32_t, 1>(table, V, D, ld_table, rows, n_rows, rows_cap, vals, ld_vals,
-                                       adam, o, m, v, dev_err, st);
+    e = vec ? apply_launch<int32_t, float, 4, 4>(table, V, D, ld_table, rows, n_rows, rows_cap,
+                                                 vals, ld_vals, adam, o, m, v, dev_err, st)
+            : apply_launch<int32_t, float, 1, 4>(table, V, D, ld_table, rows, n_rows, rows_cap,
+                                                 vals, ld_vals, adam, o, m, v, dev_err, st);
+  return launch_status(e);
+}
+
+int apply_run_f16(float* table, int64_t V, int64_t D, int64_t ld_table, const void* rows,
+                  int idtype, const int64_t* n_rows, int64_t rows_cap, const uint16_t* vals,
+                  int64_t ld_vals, float inv_scale, int opt, float lr, float beta1, float beta2,
+                  float eps, float weight_decay, int64_t step, float* m, float* v,
+                  int32_t* dev_err, hipStream_t st) {
+  if (D == 0 || rows_cap == 0) return LM_OK;
+  const bool adam = opt == LM_OPT_ADAM;
+  const OptParams o = opt_params(opt, lr, beta1, beta2, eps, weight_decay, step, inv_scale);
+  // 8 columns per lane: one 16-byte payload vector, two of every fp32 table.
+  bool vec = a16(table) && a16(vals) && ld_table % 4 == 0 && ld_vals % 8 == 0 && D % 8 == 0;
+  if (adam) vec = vec && a16(m) && a16(v);
+  hipError_t e;
+  if (idtype == LM_I64)
+    e = vec ? apply_launch<int64_t, uint16_t, 8, 2>(table, V, D, ld_table, rows, n_rows, rows_cap,
+                                                    vals, ld_vals, adam, o, m, v, dev_err, st)
+            : apply_launch<int64_t, uint16_t, 1, 4>(table, V, D, ld_table, rows, n_rows, rows_cap,
+                                                    vals, ld_vals, adam, o, m, v, dev_err, st);
+  else
+    e = vec ? apply_launch<int32_t, uint16_t, 8, 2>(table, V, D, ld_table, rows, n_rows, rows_cap,
+                                                    vals, ld_vals, adam, o, m, v, dev_err, st)
+            : apply_launch<int32_t, uint16_t, 1, 4>(table, V, D, ld_table, rows, n_rows, rows_cap,
+                                                    vals, ld_vals, adam, o, m, v, dev_err, st);
+  return launch_status(e);
+}
+
+template <typename KeyT, int VEC>
+static hipError_t fill_launch_f16(const float* src, int64_t ld_src, const void* src_ids,
+                                  const int64_t* n_src, int64_t src_cap, const void* dst_ids,
+                                  const int64_t* n_dst, int64_t D, uint16_t* dst,
+                                  int64_t dst_rows, int64_t ld_dst, int mode, float scale,
+                                  int32_t* dev_err, hipStream_t st) {
+  constexpr int NV = VEC == 8 ? 2 : 4;
+  const KeyT* si = static_cast<const KeyT*>(src_ids);
+  const KeyT* di = static_cast<const KeyT*>(dst_ids);
+  if (mode == LM_FILL_EXPAND) {
+    const int64_t waves = grid_waves(dst_rows, kZeroRows);
+    const uint32_t blocks = static_cast<uint32_t>((waves + kFillWaves - 1) / kFillWaves);
+    k_zero_rows_h<VEC, NV><<<blocks, kFillThreads, 0, st>>>(
+        n_dst, dst_rows, static_cast<int>(D), dst, ld_dst, int64_t(blocks) * kFillWaves, dev_err);
+    if (src_cap == 0) return hipGetLastError();
+  }
+  const int64_t swaves = grid_waves(src_cap, kRowsPerWave);
+  const uint32_t sblocks = static_cast<uint32_t>((swaves + kFillWaves - 1) / kFillWaves);
+  k_scatter_h<KeyT, VEC, NV><<<sblocks, kFillThreads, 0, st>>>(
+      src, ld_src, si, n_src, src_cap, di, n_dst, dst_rows, static_cast<int>(D), dst, ld_dst,
+      scale, int64_t(sblocks) * kFillWaves, dev_err);
+  return hipGetLastError();
+}
+
+int fill_run_f16(const float* src, int64_t ld_src, const void* src_ids, const int64_t* n_src,
+                 int64_t src_cap, const void* dst_ids, const int64_t* n_dst, int idtype,
+                 int64_t D, uint16_t* dst, int64_t dst_rows, int64_t ld_dst, int mode,
+                 float scale, int32_t* dev_err, hipStream_t st) {
+  if (D == 0) return LM_OK;
+  if (mode == LM_FILL_EXPAND ? dst_rows == 0 : src_cap == 0) return LM_OK;
+  const bool vec = a16(src) && a16(dst) && ld_src % 4 == 0 && ld_dst % 8 == 0 && D % 8 == 0;
+  hipError_t e;
+  if (idtype == LM_I64)
+    e = vec ? fill_launch_f16<int64_t, 8>(src, ld_src, src_ids, n_src, src_cap, dst_ids, n_dst, D,
+                                          dst, dst_rows, ld_dst, mode, scale, dev_err, st)
+            : fill_launch_f16<int64_t, 1>(src, ld_src, src_ids, n_src, src_cap, dst_ids, n_dst, D,
+                                          dst, dst_rows, ld_dst, mode, scale, dev_err, st);
+  else
+    e = vec ? fill_launch_f16<int32_t, 8>(src, ld_src, src_ids, n_src, src_cap, dst_ids, n_dst, D,
+                                          dst, dst_rows, ld_dst, mode, scale, dev_err, st)
+            : fill_launch_f16<int32_t, 1>(src, ld_src, src_ids, n_src, src_cap, dst_ids, n_dst, D,
+                                          dst, dst_rows, ld_dst, mode, scale, dev_err, st);
   return launch_status(e);
 }
 

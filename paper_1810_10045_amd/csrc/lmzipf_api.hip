@@ -26,7 +26,19 @@ int apply_run(float* table, int64_t V, int64_t D, int64_t ld_table, const void* 
               int opt, float lr, float beta1, float beta2, float eps, float weight_decay,
               int64_t step, float* m, float* v, int32_t* dev_err, hipStream_t st);
 
+int fill_run_f16(const float* src, int64_t ld_src, const void* src_ids, const int64_t* n_src,
+                 int64_t src_cap, const void* dst_ids, const int64_t* n_dst, int idtype,
+                 int64_t D, uint16_t* dst, int64_t dst_rows, int64_t ld_dst, int mode,
+                 float scale, int32_t* dev_err, hipStream_t st);
+int apply_run_f16(float* table, int64_t V, int64_t D, int64_t ld_table, const void* rows,
+                  int idtype, const int64_t* n_rows, int64_t rows_cap, const uint16_t* vals,
+                  int64_t ld_vals, float inv_scale, int opt, float lr, float beta1, float beta2,
+                  float eps, float weight_decay, int64_t step, float* m, float* v,
+                  int32_t* dev_err, hipStream_t st);
+
 int launch_status(hipError_t e) { return e == hipSuccess ? LM_OK : LM_E_HIP; }
+
+static bool finite_nonzero(float x) { return x == x && x != 0.f && x - x == 0.f; }
 
 __global__ __launch_bounds__(256) void k_clear(uint32_t* p, int64_t words, uint8_t* tail,
                                                int tail_bytes) {
@@ -55,7 +67,7 @@ const char* lm_status_string(int status) {
   }
 }
 
-int lm_abi_version(void) { return 100; }
+int lm_abi_version(void) { return 101; }
 
 int lm_workspace_clear(void* ws, size_t bytes, void* stream) {
   if (bytes == 0) return LM_OK;
@@ -159,6 +171,47 @@ int lm_sparse_apply(float* table, int64_t V, int64_t D, int64_t ld_table, const 
   return apply_run(table, V, D, ld_table, rows, idtype, n_rows, rows_cap, vals, ld_vals, opt, lr,
                    beta1, beta2, eps, weight_decay, step, m, v, dev_err,
                    static_cast<hipStream_t>(stream));
+}
+
+int lm_fill_values_f16(const float* src, int64_t ld_src, const void* src_ids,
+                       const int64_t* n_src, int64_t src_cap, const void* dst_ids,
+                       const int64_t* n_dst, int32_t idtype, int64_t D, uint16_t* dst,
+                       int64_t dst_rows, int64_t ld_dst, int32_t mode, float scale,
+                       int32_t* dev_err, void* stream) {
+  if (!valid_idtype(idtype)) return LM_E_UNSUPPORTED;
+  if (mode != LM_FILL_EXPAND && mode != LM_FILL_SCATTER) return LM_E_UNSUPPORTED;
+  if (!finite_nonzero(scale)) return LM_E_INVAL;
+  if (D < 0 || src_cap < 0 || dst_rows < 0 || ld_src < D || ld_dst < D) return LM_E_INVAL;
+  if (D > (int64_t(1) << 24)) return LM_E_UNSUPPORTED;
+  if (mode == LM_FILL_EXPAND && (!dst_ids || !n_dst)) return LM_E_INVAL;
+  if (dst_ids && !n_dst) return LM_E_INVAL;
+  if ((src_cap > 0 || dst_rows > 0) && D > 0 && (!src_ids || !n_src || !dev_err)) return LM_E_INVAL;
+  if (src_cap > 0 && D > 0 && !src) return LM_E_INVAL;
+  if (dst_rows > 0 && D > 0 && !dst) return LM_E_INVAL;
+  return fill_run_f16(src, ld_src, src_ids, n_src, src_cap, dst_ids, n_dst, idtype, D, dst,
+                      dst_rows, ld_dst, mode, scale, dev_err, static_cast<hipStream_t>(stream));
+}
+
+int lm_sparse_apply_f16(float* table, int64_t V, int64_t D, int64_t ld_table, const void* rows,
+                        int32_t idtype, const int64_t* n_rows, int64_t rows_cap,
+                        const uint16_t* vals, int64_t ld_vals, float inv_scale, int32_t opt,
+                        float lr, float beta1, float beta2, float eps, float weight_decay,
+                        int64_t step, float* m, float* v, int32_t* dev_err, void* stream) {
+  if (!valid_idtype(idtype)) return LM_E_UNSUPPORTED;
+  if (opt != LM_OPT_SGD && opt != LM_OPT_ADAM) return LM_E_UNSUPPORTED;
+  if (!finite_nonzero(inv_scale)) return LM_E_INVAL;
+  if (V < 0 || D < 0 || rows_cap < 0 || ld_table < D || ld_vals < D) return LM_E_INVAL;
+  if (D > (int64_t(1) << 24)) return LM_E_UNSUPPORTED;
+  if (rows_cap > 0 && D > 0 && (!table || !rows || !n_rows || !vals || !dev_err))
+    return LM_E_INVAL;
+  if (opt == LM_OPT_ADAM) {
+    if (step < 1) return LM_E_INVAL;
+    if (rows_cap > 0 && D > 0 && (!m || !v)) return LM_E_INVAL;
+    if (!(beta1 >= 0.f && beta1 < 1.f && beta2 >= 0.f && beta2 < 1.f)) return LM_E_INVAL;
+  }
+  return apply_run_f16(table, V, D, ld_table, rows, idtype, n_rows, rows_cap, vals, ld_vals,
+                       inv_scale, opt, lr, beta1, beta2, eps, weight_decay, step, m, v, dev_err,
+                       static_cast<hipStream_t>(stream));
 }
 
 }  // extern "C"

@@ -21,6 +21,7 @@ LIB_PATH = os.path.join(HERE, "liblmzipf.so")
 
 OK, E_INVAL, E_WORKSPACE, E_HIP, E_UNSUPPORTED = 0, 1, 3, 4, 5
 DEVERR_ID_RANGE, DEVERR_NOT_FOUND, DEVERR_CAPACITY, DEVERR_SPIN = 1, 2, 4, 8
+DEVERR_NONFINITE = 16
 I32, I64 = 0, 1
 F32, BF16 = 0, 1
 FILL_EXPAND, FILL_SCATTER, FILL_SCATTER_ADD = 0, 1, 2
@@ -29,7 +30,8 @@ MAX_K = 1 << 30
 
 EXPORTS = ("lm_status_string", "lm_abi_version", "lm_workspace_clear",
            "lm_unique_workspace_bytes", "lm_unique", "lm_segsum_workspace_bytes",
-           "lm_segsum", "lm_map_ids", "lm_fill_values", "lm_sparse_apply")
+           "lm_segsum", "lm_map_ids", "lm_fill_values", "lm_sparse_apply",
+           "lm_fill_values_f16", "lm_sparse_apply_f16")
 
 
 class LmError(RuntimeError):
@@ -62,8 +64,12 @@ def _load():
     L.lm_fill_values.argtypes = [P, I64_, P, P, I64_, P, P, I32_, I64_, P, I64_, I64_, I32_, P, P]
     L.lm_sparse_apply.argtypes = [P, I64_, I64_, I64_, P, I32_, P, I64_, P, I64_, I32_,
                                   F, F, F, F, F, I64_, P, P, P, P]
+    L.lm_fill_values_f16.argtypes = [P, I64_, P, P, I64_, P, P, I32_, I64_, P, I64_, I64_, I32_,
+                                     F, P, P]
+    L.lm_sparse_apply_f16.argtypes = [P, I64_, I64_, I64_, P, I32_, P, I64_, P, I64_, F, I32_,
+                                      F, F, F, F, F, I64_, P, P, P, P]
     for f in ("lm_abi_version", "lm_workspace_clear", "lm_unique", "lm_segsum", "lm_map_ids",
-              "lm_fill_values", "lm_sparse_apply"):
+              "lm_fill_values", "lm_sparse_apply", "lm_fill_values_f16", "lm_sparse_apply_f16"):
         getattr(L, f).restype = ctypes.c_int
     return L
 
@@ -153,7 +159,8 @@ def check(dev_err: torch.Tensor):
         names = [n for b, n in ((DEVERR_ID_RANGE, "id out of range"),
                                 (DEVERR_NOT_FOUND, "id not found"),
                                 (DEVERR_CAPACITY, "capacity exceeded"),
-                                (DEVERR_SPIN, "inter-workgroup wait gave up")) if v & b]
+                                (DEVERR_SPIN, "inter-workgroup wait gave up"),
+                                (DEVERR_NONFINITE, "compressed value not finite")) if v & b]
         raise DeviceError(f"device error 0x{v:x}: {', '.join(names)}")
 
 
@@ -292,4 +299,60 @@ def sparse_apply(table: torch.Tensor, rows: torch.Tensor, n_rows: torch.Tensor,
                                _rows(vals, "vals"), kind, lr, beta1, beta2, eps, weight_decay,
                                step, _ptr(m), _ptr(v), _ptr(dev_err), _stream(stream)),
           "lm_sparse_apply")
+    return table
+
+
+def _payload(t: torch.Tensor, what: str):
+    if t.dtype not in (torch.float16, torch.int16, torch.uint16):
+        raise LmError(f"{what} must hold binary16 (float16, or its bits as int16/uint16)")
+
+
+def fill_values_f16(src: torch.Tensor, src_ids: torch.Tensor, n_src: torch.Tensor,
+                    dst: torch.Tensor, dst_ids: Optional[torch.Tensor] = None,
+                    n_dst: Optional[torch.Tensor] = None, mode: str = "expand",
+                    scale: float = 1.0, dev_err: Optional[torch.Tensor] = None,
+                    stream=None) -> torch.Tensor:
+    """lm_fill_values_f16: Sec. III-C, EXPAND / SCATTER into a binary16 payload
+    dst = binary16(src * scale)."""
+    D = src.shape[1]
+    _payload(dst, "dst")
+    if dst.shape[1] != D:
+        raise LmError("src and dst widths differ")
+    if dst_ids is not None and dst_ids.dtype != src_ids.dtype:
+        raise LmError("src_ids and dst_ids must share a dtype")
+    if dev_err is None:
+        dev_err = torch.zeros(1, dtype=torch.int32, device=src.device)
+    src_cap = min(src.shape[0], src_ids.numel())
+    dst_rows = dst.shape[0] if dst_ids is None else min(dst.shape[0], dst_ids.numel())
+    _call(_lib.lm_fill_values_f16(_ptr(src), _rows(src, "src"), _ptr(src_ids), _ptr(n_src),
+                                  src_cap, _ptr(dst_ids), _ptr(n_dst), _idtype(src_ids), D,
+                                  _ptr(dst), dst_rows, _rows(dst, "dst"), _MODES[mode], scale,
+                                  _ptr(dev_err), _stream(stream)), "lm_fill_values_f16")
+    return dst
+
+
+def sparse_apply_f16(table: torch.Tensor, rows: torch.Tensor, n_rows: torch.Tensor,
+                     vals: torch.Tensor, inv_scale: float = 1.0, opt: str = "sgd",
+                     lr: float = 0.1, beta1: float = 0.9, beta2: float = 0.999, eps: float = 1e-8,
+                     weight_decay: float = 0.0, step: int = 1, m: Optional[torch.Tensor] = None,
+                     v: Optional[torch.Tensor] = None, dev_err: Optional[torch.Tensor] = None,
+                     stream=None) -> torch.Tensor:
+    """lm_sparse_apply_f16: step 7 from a binary16 payload, g = fp32(vals) * inv_scale."""
+    V, D = table.shape
+    _payload(vals, "vals")
+    if vals.shape[1] != D:
+        raise LmError("vals and table widths differ")
+    kind = {"sgd": OPT_SGD, "adam": OPT_ADAM}[opt]
+    if kind == OPT_ADAM:
+        for t, n in ((m, "m"), (v, "v")):
+            if t is None or t.shape != table.shape or t.stride() != table.stride():
+                raise LmError(f"Adam needs {n} shaped and strided like the table")
+    if dev_err is None:
+        dev_err = torch.zeros(1, dtype=torch.int32, device=table.device)
+    rows_cap = min(rows.numel(), vals.shape[0])
+    _call(_lib.lm_sparse_apply_f16(_ptr(table), V, D, _rows(table, "table"), _ptr(rows),
+                                   _idtype(rows), _ptr(n_rows), rows_cap, _ptr(vals),
+                                   _rows(vals, "vals"), inv_scale, kind, lr, beta1, beta2, eps,
+                                   weight_decay, step, _ptr(m), _ptr(v), _ptr(dev_err),
+                                   _stream(stream)), "lm_sparse_apply_f16")
     return table

@@ -154,6 +154,7 @@ class Workload:
     number: int              # seed base: ids 1000n+1, grads 1000n+2, table 1000n+3, m/v +4/+5
     shards: int = 1
     perm_seed: int = 0       # > 0: ranks spread over the ids by a fixed permutation
+    scale: float = 1.0       # compression scale F of a binary16 payload (Sec. III-C)
     lr: float = 0.0
     table_std: float = 0.02
     adam: tuple = field(default=(0.9, 0.999, 1e-8))
@@ -220,6 +221,12 @@ WORKLOADS = {
     "vocab2m_adam_i64": Workload("vocab2m_adam_i64", K=262_144, V=2_000_000, s=0.9, D=1024,
                                  grad_dtype="f32", id_dtype="i64", step="adam", number=5,
                                  lr=1e-3),
+    # The merge with the step-5 payload compressed to binary16 (Sec. III-C),
+    # same inputs as merge_64x32k_bf16; F = 64 keeps the largest per-word
+    # sums of these N(0,1) rows (about +-240) inside binary16's range.
+    "merge_64x32k_f16": Workload("merge_64x32k_f16", K=32768, V=800_000, s=1.0, D=1024,
+                                 grad_dtype="bf16", id_dtype="i32", step="expand_f16",
+                                 number=3, shards=64, scale=64.0),
     # The per-GPU word step with the word ranks permuted over the vocabulary
     # (the robustness variant: heads no longer first in sorted order).
     "word_step_64k_perm": Workload("word_step_64k_perm", K=65536, V=800_000, s=1.0, D=1024,

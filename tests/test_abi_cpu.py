@@ -42,7 +42,8 @@ def test_binding_names_match_the_header():
     src = open(os.path.join(ROOT, "paper_1810_10045_amd", "lmzipf.py")).read()
     for n in declared_functions():
         assert f'"{n}"' in src, n
-    for n in ("unique", "segsum", "map_ids", "fill_values", "sparse_apply"):
+    for n in ("unique", "segsum", "map_ids", "fill_values", "sparse_apply", "fill_values_f16",
+              "sparse_apply_f16"):
         assert re.search(rf"^def {n}\(", src, re.M), n
 
 
@@ -50,7 +51,7 @@ def test_status_strings(lib):
     lib.lm_status_string.restype = ctypes.c_char_p
     for code in (0, 1, 3, 4, 5, 99):
         assert lib.lm_status_string(code)
-    assert lib.lm_abi_version() == 100
+    assert lib.lm_abi_version() == 101
 
 
 def test_workspace_queries(lib):
@@ -102,6 +103,21 @@ def test_argument_errors_return_before_any_launch(lib):
                                None, None, _v(), None) == 1
     assert lib.lm_sparse_apply(_v(), 10, 4, 4, _v(), 0, _v(), 5, _v(), 4, 1, 0.1, 1.5, 0.999, 1e-8, 0.0, 1,
                                _v(), _v(), _v(), None) == 1
+    F = ctypes.c_float
+    lib.lm_fill_values_f16.argtypes = [P, I64, P, P, I64, P, P, I32, I64, P, I64, I64, I32, F, P, P]
+    # SCATTER_ADD into a binary16 payload, a zero or non-finite scale, ld_dst < D
+    assert lib.lm_fill_values_f16(_v(), 8, _v(), _v(), 10, _v(), _v(), 0, 8, _v(), 10, 8, 2, 256.0, _v(), None) == 5
+    assert lib.lm_fill_values_f16(_v(), 8, _v(), _v(), 10, _v(), _v(), 0, 8, _v(), 10, 8, 0, 0.0, _v(), None) == 1
+    assert lib.lm_fill_values_f16(_v(), 8, _v(), _v(), 10, _v(), _v(), 0, 8, _v(), 10, 8, 0, float("inf"), _v(), None) == 1
+    assert lib.lm_fill_values_f16(_v(), 8, _v(), _v(), 10, _v(), _v(), 0, 8, _v(), 10, 4, 0, 256.0, _v(), None) == 1
+    lib.lm_sparse_apply_f16.argtypes = [P, I64, I64, I64, P, I32, P, I64, P, I64, F, I32] + \
+        [F] * 5 + [I64, P, P, P, P]
+    assert lib.lm_sparse_apply_f16(_v(), 10, 8, 8, _v(), 0, _v(), 5, _v(), 8, float("nan"), 0, 0.1, 0.9,
+                                   0.999, 1e-8, 0.0, 1, None, None, _v(), None) == 1
+    assert lib.lm_sparse_apply_f16(_v(), 10, 8, 8, _v(), 0, _v(), 5, _v(), 8, 1 / 256, 4, 0.1, 0.9,
+                                   0.999, 1e-8, 0.0, 1, None, None, _v(), None) == 5
+    assert lib.lm_sparse_apply_f16(_v(), 10, 8, 8, _v(), 0, _v(), 5, _v(), 8, 1 / 256, 1, 0.1, 0.9,
+                                   0.999, 1e-8, 0.0, 1, None, None, _v(), None) == 1
     lib.lm_map_ids.argtypes = [P, P, I64, P, P, I64, I32, P, P, P]
     assert lib.lm_map_ids(_v(), _v(), 4, _v(), _v(), 4, 3, _v(), _v(), None) == 5
     assert lib.lm_map_ids(None, _v(), 4, _v(), _v(), 4, 0, _v(), _v(), None) == 1
