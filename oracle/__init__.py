@@ -23,6 +23,9 @@ Parity status per routine (what pins it lives in ``tests/test_oracle_pins.py``):
   decompress      pinned (numpy's float16 conversion, every binary16 pattern
                   round-tripped, overflow / subnormal / tie cases, power-of-two
                   scales exact)
+  sample_ids      pinned (V a power of two: the top bits; exact run lengths of
+                  every id for small V over an evenly spaced sweep of r;
+                  monotone in r; Python's exact integer product)
 """
 from __future__ import annotations
 
@@ -61,10 +64,11 @@ def _declare(L):
     L.orc_f32_from_f16.argtypes = [P, I, P]
     L.orc_compress.argtypes = [P, I, I, ctypes.c_float, P]
     L.orc_decompress.argtypes = [P, I, I, ctypes.c_float, P]
+    L.orc_sample_ids.argtypes = [P, I, I, P]
     for f in ("orc_unique", "orc_segsum", "orc_segsum_select",
               "orc_dense_scatter", "orc_map", "orc_expand", "orc_scatter",
               "orc_sgd", "orc_adam", "orc_f16_from_f32", "orc_f32_from_f16",
-              "orc_compress", "orc_decompress"):
+              "orc_compress", "orc_decompress", "orc_sample_ids"):
         getattr(L, f).restype = ctypes.c_int
     return L
 
@@ -265,4 +269,12 @@ def decompress(h, inv_scale: float) -> np.ndarray:
     n, D = h.shape
     out = np.full((n, D), np.nan)
     _check(lib().orc_decompress(_p(h), n, D, float(inv_scale), _p(out)), "decompress")
+    return out
+
+
+def sample_ids(r, V: int) -> np.ndarray:
+    """Sec. III-B sampler: ids floor(r * V / 2^64) of 64-bit random words."""
+    r = np.ascontiguousarray(r, dtype=np.uint64)
+    out = np.full(r.shape, -7, np.int64)
+    _check(lib().orc_sample_ids(_p(r), r.size, V, _p(out)), "sample_ids")
     return out

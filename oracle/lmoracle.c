@@ -362,3 +362,19 @@ int orc_decompress(const uint16_t* h, int64_t n, int64_t D, float inv_scale, dou
   }
   return ORC_OK;
 }
+
+/*
+ * Sec. II-A / III-B (sampled softmax): the output embedding is updated only
+ * at a random subset of the vocabulary, drawn uniformly. Given 64-bit random
+ * words r (drawn by the caller from its seed), the id of each is
+ * floor(r * V / 2^64): the high word of the 128-bit product, which splits
+ * [0, 2^64) into V runs of equal length (to within one).
+ */
+int orc_sample_ids(const uint64_t* r, int64_t n, int64_t V, int64_t* ids) {
+  if (n < 0 || V < 1) return ORC_BADARG;
+  for (int64_t i = 0; i < n; ++i) {
+    const unsigned __int128 p = (unsigned __int128)r[i] * (unsigned __int128)(uint64_t)V;
+    ids[i] = (int64_t)(uint64_t)(p >> 64);
+  }
+  return ORC_OK;
+}

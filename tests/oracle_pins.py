@@ -413,10 +413,32 @@ def check_compression():
     assert np.all(np.isinf(oracle.decompress(h[:, 1:], 1 / 256.0)))
 
 
+def check_sample_ids():
+    """Sec. III-B uniform candidate sampler: with V = 2^k an id is the top k
+    bits of r; 40 V values of r spaced evenly over [0, 2^64) land 40 +- 1
+    times on every id, monotonically; and each id equals the exact integer
+    floor(r * V / 2^64) (Python's big integers)."""
+    rng = np.random.default_rng(71)
+    r = rng.integers(0, 2**63, size=5000, dtype=np.uint64) * np.uint64(2) + \
+        rng.integers(0, 2, size=5000, dtype=np.uint64)
+    for k in (1, 7, 20, 33):
+        assert np.array_equal(oracle.sample_ids(r, 1 << k), (r >> np.uint64(64 - k)).astype(np.int64))
+    for V in (3, 10, 97, 800_000):
+        sweep = (np.arange(V * 40, dtype=np.uint64) * np.uint64((2**64 - 1) // (V * 40)))
+        ids = oracle.sample_ids(sweep, V)
+        assert np.all(np.diff(ids) >= 0) and ids.min() == 0 and ids.max() == V - 1
+        c = np.bincount(ids, minlength=V)
+        assert np.all(np.abs(c - 40) <= 1)
+        exact = [(int(x) * V) >> 64 for x in r[:300]]
+        assert oracle.sample_ids(r[:300], V).tolist() == exact
+    assert oracle.sample_ids(np.array([0, 2**64 - 1], np.uint64), 5).tolist() == [0, 4]
+
+
 ALL_CHECKS = [
     check_to_be_or_not_to_be, check_numpy_unique, check_brute_force_unique,
     check_unique_invariants, check_unique_rejects_out_of_range,
     check_fig2_i_want_a_pen_and_a, check_segsum_numpy, check_segsum_special_cases,
     check_segsum_select, check_fig3_two_gpus, check_shards_merge, check_map_and_fill,
     check_sgd, check_adam_closed_forms, check_f16_conversion, check_compression,
+    check_sample_ids,
 ]

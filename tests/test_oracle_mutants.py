@@ -14,6 +14,9 @@ SRC = os.path.join(os.path.dirname(oracle.__file__), "lmoracle.c")
 
 # (name, text in lmoracle.c, replacement)
 MUTANTS = [
+    ("sample_low_word", "ids[i] = (int64_t)(uint64_t)(p >> 64);", "ids[i] = (int64_t)(uint64_t)p % V;"),
+    ("sample_modulo_bias", "const unsigned __int128 p = (unsigned __int128)r[i] * (unsigned __int128)(uint64_t)V;",
+     "const unsigned __int128 p = (unsigned __int128)(r[i] >> 1) * (unsigned __int128)(uint64_t)V;"),
     ("f16_ties_away", "if (rest > 0x1000u || (rest == 0x1000u && (h & 1u))) h += 1;",
      "if (rest >= 0x1000u) h += 1;"),
     ("f16_truncates", "if (rest > 0x1000u || (rest == 0x1000u && (h & 1u))) h += 1;", ""),
