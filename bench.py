@@ -100,8 +100,19 @@ class Batch:
     """One resident batch: ids and gradients on the device (and, for the
     merge workload, shard 0's own ids and gradients)."""
 
-    def __init__(self, w, torch, dev, ids=None, grads=None):
-        self.ids = torch.from_numpy(w.ids() if ids is None else ids).to(dev)
+    def __init__(self, w, torch, dev, ids=None, grads=None, words=None):
+        if w.samples:
+            # sampled softmax: the shards' random words (sampled on the GPU
+            # into the front of ids each step), then their batches' own words
+            from paper_1810_10045_amd import seeding
+            if words is None:
+                words = w.sampler_words(seeding.seed_of_gpus(w.shards, w.seed_rule))
+            self.words = torch.from_numpy(words.view(np.int64)).to(dev)
+            true = w.ids() if ids is None else ids[w.shards * w.samples:]
+            self.ids = torch.empty(w.tokens, dtype=torch.int32, device=dev)
+            self.ids[w.shards * w.samples:] = torch.from_numpy(true).to(dev)
+        else:
+            self.ids = torch.from_numpy(w.ids() if ids is None else ids).to(dev)
         # bf16 arrives as its uint16 bit patterns, the oracle's very input
         g = w.grads() if grads is None else grads
         t = torch.from_numpy(g)
@@ -128,7 +139,7 @@ class Pipeline:
         self.dev_err = self.ures.dev_err
         self.state = {}
         st = self.state
-        if w.step in ("sgd", "adam"):
+        if w.step in ("sgd", "adam", "softmax_sgd"):
             st["table"] = torch.from_numpy(w.table() if table is None else table).to(dev)
         elif w.step == "scatter":
             st["table"] = torch.zeros((w.V, D), dtype=torch.float32, device=dev)
@@ -145,12 +156,14 @@ class Pipeline:
         w, lz, st, ures, err = self.w, self.lz, self.state, self.ures, self.dev_err
         bt = self.batches[b % len(self.batches)]
         if ev: ev(0)
+        if w.samples:
+            lz.sample_ids(bt.words, w.V, out=bt.ids[:w.shards * w.samples])
         lz.unique(bt.ids, w.V, out=ures, ws=self.ws)
         if ev: ev(1)
         lz.segsum(bt.grad, ures.perm, ures.inverse, ures.offsets, ures.num_unique, out=self.out,
                   dev_err=err, ws=self.ws)
         if ev: ev(2)
-        if w.step == "sgd":
+        if w.step in ("sgd", "softmax_sgd"):
             lz.sparse_apply(st["table"], ures.uniq, ures.num_unique, self.out, "sgd", lr=w.lr,
                             dev_err=err)
         elif w.step == "adam":
@@ -235,14 +248,18 @@ def run_cpu_baseline(w, budget_s):
     import oracle
     wl = w
     ids = wl.ids()
+    if w.samples:
+        from paper_1810_10045_amd import seeding
+        words = w.sampler_words(seeding.seed_of_gpus(w.shards, w.seed_rule))
+        ids = np.concatenate([oracle.sample_ids(words, w.V), ids])
     grads = wl.grads() if wl.grad_dtype == "bf16" else wl.grads_f32()
-    table = wl.table() if w.step in ("sgd", "adam") else None
+    table = wl.table() if w.step in ("sgd", "adam", "softmax_sgd") else None
     done, t_used, toks = 0, 0.0, 0
     while t_used < budget_s and done < 1000:
         t0 = time.perf_counter()
         uniq, counts, offsets, inverse, perm = oracle.unique(ids, w.V)
         red = oracle.segsum(grads, inverse, len(uniq))
-        if w.step == "sgd":
+        if w.step in ("sgd", "softmax_sgd"):
             oracle.sgd(table[uniq], red, w.lr)
         elif w.step == "adam":
             z = np.zeros((len(uniq), w.D))
@@ -343,6 +360,8 @@ def main():
         "data": "synthetic",
         "config": {"workload": w.name, "tokens": w.tokens, "V": w.V, "D": w.D, "zipf_s": w.s,
                    "ids": w.id_dtype, "grad": w.grad_dtype, "after_segsum": w.step,
+                   **({"gpus_simulated": w.shards, "samples_per_gpu": w.samples,
+                       "seed_rule": w.seed_rule} if w.samples else {}),
                    "resident_batches": nbatch, "types_per_batch": r["U"]},
         "stages_ms": {"unique": r["stage_ms"][0], "segsum": r["stage_ms"][1],
                       w.step: r["stage_ms"][2]},

@@ -271,6 +271,20 @@ int lm_sparse_apply_f16(float* table, int64_t V, int64_t D, int64_t ld_table,
                         float eps, float weight_decay, int64_t step, float* m, float* v,
                         int32_t* dev_err, void* stream);
 
+/* ------------------------------------------------------------------------
+ * Candidate sampler — Sec. II-A (sampled softmax) and Sec. III-B
+ * (controlled randomness): the output embedding is updated at a random,
+ * uniformly drawn subset of the vocabulary plus the batch's own words.
+ * Groups of GPUs share a seed so that their subsets coincide; the random
+ * words are drawn by the caller from its group's seed and passed in.
+ *   ids[i] = floor(r[i] * V / 2^64)   (the high word of the product)
+ * r          device, n uint64 random words.
+ * V          vocabulary size (>= 1; <= 2^31 for int32 ids).
+ * ids        device, n ids of dtype `idtype`, written.
+ * ------------------------------------------------------------------------ */
+int lm_sample_ids(const uint64_t* r, int64_t n, int64_t V, void* ids, int32_t idtype,
+                  void* stream);
+
 #ifdef __cplusplus
 }
 #endif

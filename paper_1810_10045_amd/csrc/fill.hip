@@ -546,3 +546,35 @@ int fill_run_f16(const float* src, int64_t ld_src, const void* src_ids, const in
 }
 
 }  // namespace lmz
+
+// ---------------------------------------------------------------------------
+// Candidate sampler of the sampled softmax (Sec. II-A, Sec. III-B): the id of
+// a 64-bit random word r is floor(r * V / 2^64), the high word of the
+// product, so every id in [0, V) is equally likely. The random words come
+// from the caller (one stream per seed group of GPUs).
+// ---------------------------------------------------------------------------
+namespace lmz {
+
+template <typename KeyT>
+__global__ __launch_bounds__(kFillThreads) void k_sample_ids(const uint64_t* __restrict__ r,
+                                                             int64_t n, uint64_t V,
+                                                             KeyT* __restrict__ ids) {
+  for (int64_t i = blockIdx.x * int64_t(kFillThreads) + threadIdx.x; i < n;
+       i += int64_t(gridDim.x) * kFillThreads)
+    ids[i] = static_cast<KeyT>(__umul64hi(r[i], V));
+}
+
+int sample_run(const uint64_t* r, int64_t n, int64_t V, void* ids, int idtype, hipStream_t st) {
+  if (n == 0) return LM_OK;
+  int64_t blocks = (n + kFillThreads - 1) / kFillThreads;
+  if (blocks > 65536) blocks = 65536;
+  if (idtype == LM_I64)
+    k_sample_ids<int64_t><<<static_cast<uint32_t>(blocks), kFillThreads, 0, st>>>(
+        r, n, static_cast<uint64_t>(V), static_cast<int64_t*>(ids));
+  else
+    k_sample_ids<int32_t><<<static_cast<uint32_t>(blocks), kFillThreads, 0, st>>>(
+        r, n, static_cast<uint64_t>(V), static_cast<int32_t*>(ids));
+  return launch_status(hipGetLastError());
+}
+
+}  // namespace lmz

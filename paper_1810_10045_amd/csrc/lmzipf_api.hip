@@ -36,6 +36,8 @@ int apply_run_f16(float* table, int64_t V, int64_t D, int64_t ld_table, const vo
                   float eps, float weight_decay, int64_t step, float* m, float* v,
                   int32_t* dev_err, hipStream_t st);
 
+int sample_run(const uint64_t* r, int64_t n, int64_t V, void* ids, int idtype, hipStream_t st);
+
 int launch_status(hipError_t e) { return e == hipSuccess ? LM_OK : LM_E_HIP; }
 
 static bool finite_nonzero(float x) { return x == x && x != 0.f && x - x == 0.f; }
@@ -67,7 +69,7 @@ const char* lm_status_string(int status) {
   }
 }
 
-int lm_abi_version(void) { return 101; }
+int lm_abi_version(void) { return 102; }
 
 int lm_workspace_clear(void* ws, size_t bytes, void* stream) {
   if (bytes == 0) return LM_OK;
@@ -212,6 +214,15 @@ int lm_sparse_apply_f16(float* table, int64_t V, int64_t D, int64_t ld_table, co
   return apply_run_f16(table, V, D, ld_table, rows, idtype, n_rows, rows_cap, vals, ld_vals,
                        inv_scale, opt, lr, beta1, beta2, eps, weight_decay, step, m, v, dev_err,
                        static_cast<hipStream_t>(stream));
+}
+
+int lm_sample_ids(const uint64_t* r, int64_t n, int64_t V, void* ids, int32_t idtype,
+                  void* stream) {
+  if (!valid_idtype(idtype)) return LM_E_UNSUPPORTED;
+  if (n < 0 || V < 1) return LM_E_INVAL;
+  if (idtype == LM_I32 && V > (int64_t(1) << 31)) return LM_E_INVAL;
+  if (n > 0 && (!r || !ids)) return LM_E_INVAL;
+  return sample_run(r, n, V, ids, idtype, static_cast<hipStream_t>(stream));
 }
 
 }  // extern "C"

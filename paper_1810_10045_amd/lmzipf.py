@@ -31,7 +31,7 @@ MAX_K = 1 << 30
 EXPORTS = ("lm_status_string", "lm_abi_version", "lm_workspace_clear",
            "lm_unique_workspace_bytes", "lm_unique", "lm_segsum_workspace_bytes",
            "lm_segsum", "lm_map_ids", "lm_fill_values", "lm_sparse_apply",
-           "lm_fill_values_f16", "lm_sparse_apply_f16")
+           "lm_fill_values_f16", "lm_sparse_apply_f16", "lm_sample_ids")
 
 
 class LmError(RuntimeError):
@@ -68,8 +68,10 @@ def _load():
                                      F, P, P]
     L.lm_sparse_apply_f16.argtypes = [P, I64_, I64_, I64_, P, I32_, P, I64_, P, I64_, F, I32_,
                                       F, F, F, F, F, I64_, P, P, P, P]
+    L.lm_sample_ids.argtypes = [P, I64_, I64_, P, I32_, P]
     for f in ("lm_abi_version", "lm_workspace_clear", "lm_unique", "lm_segsum", "lm_map_ids",
-              "lm_fill_values", "lm_sparse_apply", "lm_fill_values_f16", "lm_sparse_apply_f16"):
+              "lm_fill_values", "lm_sparse_apply", "lm_fill_values_f16", "lm_sparse_apply_f16",
+              "lm_sample_ids"):
         getattr(L, f).restype = ctypes.c_int
     return L
 
@@ -356,3 +358,19 @@ def sparse_apply_f16(table: torch.Tensor, rows: torch.Tensor, n_rows: torch.Tens
                                    weight_decay, step, _ptr(m), _ptr(v), _ptr(dev_err),
                                    _stream(stream)), "lm_sparse_apply_f16")
     return table
+
+
+def sample_ids(r: torch.Tensor, V: int, out: Optional[torch.Tensor] = None,
+               id_dtype=torch.int32, stream=None) -> torch.Tensor:
+    """lm_sample_ids: Sec. III-B candidate sampler, ids = floor(r * V / 2^64)
+    of caller-drawn 64-bit random words (``r`` int64 or uint64 bits)."""
+    _dev(r, "r")
+    if r.dtype not in (torch.int64, torch.uint64):
+        raise LmError("random words must be 64-bit")
+    if out is None:
+        out = torch.empty(r.numel(), dtype=id_dtype, device=r.device)
+    if out.numel() < r.numel():
+        raise LmError("ids shorter than r")
+    _call(_lib.lm_sample_ids(_ptr(r), r.numel(), V, _ptr(out), _idtype(out), _stream(stream)),
+          "lm_sample_ids")
+    return out

@@ -155,13 +155,15 @@ class Workload:
     shards: int = 1
     perm_seed: int = 0       # > 0: ranks spread over the ids by a fixed permutation
     scale: float = 1.0       # compression scale F of a binary16 payload (Sec. III-C)
+    samples: int = 0         # > 0: sampled-softmax candidates per GPU (Sec. III-B)
+    seed_rule: str = ""      # how many sampler seeds the shards (GPUs) use
     lr: float = 0.0
     table_std: float = 0.02
     adam: tuple = field(default=(0.9, 0.999, 1e-8))
 
     @property
     def tokens(self) -> int:
-        return self.K * self.shards
+        return (self.K + self.samples) * self.shards
 
     def batch(self, b: int) -> "Workload":
         """The b-th independent batch of this workload (b = 0 is the
@@ -187,8 +189,24 @@ class Workload:
     def shard_ids(self, g: int) -> np.ndarray:
         return self._draw(1000 * self.number + 100 + g)
 
+    def sampler_words(self, seed_of_gpu) -> np.ndarray:
+        """The sampled-softmax random words, shards x samples uint64: shard g
+        takes the raw 64-bit outputs of PCG64(SeedSequence([1000n+6, j])),
+        j = seed_of_gpu[g], so shards that share a seed share their words."""
+        out = np.empty((self.shards, self.samples), np.uint64)
+        streams = {}
+        for g, j in enumerate(seed_of_gpu):
+            if j not in streams:
+                bg = np.random.PCG64(np.random.SeedSequence([1000 * self.number + 6, int(j)]))
+                streams[j] = bg.random_raw(self.samples).astype(np.uint64)
+            out[g] = streams[j]
+        return out.reshape(-1)
+
     def grads_f32(self) -> np.ndarray:
-        """fp32 gradients (before any bf16 rounding), K*shards x D."""
+        """fp32 gradients (before any bf16 rounding), one row per token (for a
+        sampled-softmax workload: the shards' sampled rows, then their words)."""
+        if self.samples:
+            return normal_rows(self.tokens, self.D, 1000 * self.number + 2)
         if self.shards == 1:
             return normal_rows(self.K, self.D, 1000 * self.number + 2)
         return stacked_normal_rows(self.K, self.D,
@@ -233,3 +251,15 @@ WORKLOADS = {
                                    grad_dtype="f32", id_dtype="i32", step="sgd", number=2,
                                    lr=0.1, perm_seed=77),
 }
+
+# The output embedding under sampled softmax (Sec. III-B), at the word-LM
+# shape of Sec. IV-B on 64 GPUs: each GPU samples 1024 candidates uniformly
+# from the 800K vocabulary and adds the 32 x 20 = 640 words of its batch;
+# Unique + Seg-Sum run over the 64 x 1664 gathered rows (D = 512, the
+# projection width) and SGD updates the output embedding. One workload per
+# seeding rule: all GPUs different, G^0.64, log2 G, ln G, log10 G, one seed.
+for _rule in ("G", "pow0.64", "log2", "ln", "log10", "one"):
+    _name = "sampled_softmax_64x1024_" + _rule
+    WORKLOADS[_name] = Workload(_name, K=640, V=800_000, s=1.0, D=512, grad_dtype="f32",
+                                id_dtype="i32", step="softmax_sgd", number=6, shards=64,
+                                samples=1024, seed_rule=_rule, lr=0.1)

@@ -43,7 +43,7 @@ def test_binding_names_match_the_header():
     for n in declared_functions():
         assert f'"{n}"' in src, n
     for n in ("unique", "segsum", "map_ids", "fill_values", "sparse_apply", "fill_values_f16",
-              "sparse_apply_f16"):
+              "sparse_apply_f16", "sample_ids"):
         assert re.search(rf"^def {n}\(", src, re.M), n
 
 
@@ -51,7 +51,7 @@ def test_status_strings(lib):
     lib.lm_status_string.restype = ctypes.c_char_p
     for code in (0, 1, 3, 4, 5, 99):
         assert lib.lm_status_string(code)
-    assert lib.lm_abi_version() == 101
+    assert lib.lm_abi_version() == 102
 
 
 def test_workspace_queries(lib):
@@ -118,6 +118,11 @@ def test_argument_errors_return_before_any_launch(lib):
                                    0.999, 1e-8, 0.0, 1, None, None, _v(), None) == 5
     assert lib.lm_sparse_apply_f16(_v(), 10, 8, 8, _v(), 0, _v(), 5, _v(), 8, 1 / 256, 1, 0.1, 0.9,
                                    0.999, 1e-8, 0.0, 1, None, None, _v(), None) == 1
+    lib.lm_sample_ids.argtypes = [P, I64, I64, P, I32, P]
+    assert lib.lm_sample_ids(_v(), 10, 0, _v(), 0, None) == 1          # V < 1
+    assert lib.lm_sample_ids(_v(), 10, 1 << 32, _v(), 0, None) == 1    # int32 ids, V > 2^31
+    assert lib.lm_sample_ids(None, 10, 100, _v(), 0, None) == 1
+    assert lib.lm_sample_ids(_v(), 10, 100, _v(), 4, None) == 5
     lib.lm_map_ids.argtypes = [P, P, I64, P, P, I64, I32, P, P, P]
     assert lib.lm_map_ids(_v(), _v(), 4, _v(), _v(), 4, 3, _v(), _v(), None) == 5
     assert lib.lm_map_ids(None, _v(), 4, _v(), _v(), 4, 0, _v(), _v(), None) == 1

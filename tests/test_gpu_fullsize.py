@@ -231,3 +231,37 @@ def test_full_vocab2m_adam_i64(lz):
     assert int(torch.count_nonzero(st["m"][others])) == 0
     assert int(torch.count_nonzero(st["v"][others])) == 0
     _release(pipe)
+
+
+@pytest.mark.parametrize("rule", ["G", "pow0.64", "one"])
+def test_full_sampled_softmax(lz, rule):
+    """The output embedding under sampled softmax (Sec. III-B) for 64 GPUs on
+    one GPU: each samples 1024 candidates from 800K words with its group's
+    seed and adds its 640 batch words; the GPU's sampled ids equal the
+    oracle's sampler on the same random words, then Unique, every Seg-Sum
+    row (D = 512) and the SGD update are checked as for the word step."""
+    from paper_1810_10045_amd import seeding
+    w = synth.WORKLOADS["sampled_softmax_64x1024_" + rule]
+    words = w.sampler_words(seeding.seed_of_gpus(w.shards, rule))
+    ids = np.concatenate([oracle.sample_ids(words, w.V).astype(np.int32), w.ids()])
+    g, table0 = w.grads(), w.table()
+    import bench
+    dev = torch.device("cuda:0")
+    _say(f"[fullsize] {w.name}: {w.tokens} rows, {seeding.num_seeds(w.shards, rule)} seeds")
+    pipe = bench.Pipeline(w, [bench.Batch(w, torch, dev, ids=ids, grads=g, words=words)], torch,
+                          lz, dev, table=table0)
+    pipe.step(0)
+    torch.cuda.synchronize()
+    lz.check(pipe.dev_err)
+    assert np.array_equal(pipe.batches[0].ids.cpu().numpy(), ids), "sampled ids"
+    o = H.assert_unique_matches(pipe.ures, ids, w.V, oracle, w.name)
+    U = len(o[0])
+    S = oracle.segsum(g, o[3], U)
+    sq = H.sum_of_squares(g, o[3], U, oracle)
+    assert H.row_rel_err(pipe.out[:U].cpu().numpy(), S, sq) <= H.TOL_F32
+    lr = _f32(w.lr)
+    ref = oracle.sgd(table0[o[0]], S, lr)
+    table = pipe.state["table"]
+    rows_t = torch.from_numpy(o[0]).to(table.device)
+    H.assert_sgd_rows(table[rows_t].cpu().numpy(), ref, S, lr, H.row_delta(S, H.TOL_F32, sq))
+    _release(pipe)

@@ -428,3 +428,17 @@ def test_apply_adam(lz, step, wd):
 
 def test_apply_sgd_odd_width(lz):
     _apply_case(lz, "sgd", np.int32, 900, 2000, 13, 131)
+
+
+# ---------------------------------------------------------------------------
+# Candidate sampler (Sec. III-B)
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("V,dt", [(800_000, np.int32), (1, np.int32), (97, np.int32),
+                                  (1 << 31, np.int32), ((1 << 40) + 3, np.int64)])
+def test_sample_ids(lz, V, dt):
+    r = np.random.Generator(np.random.PCG64(401)).bit_generator.random_raw(70_001).astype(np.uint64)
+    r[:4] = [0, 2**64 - 1, 2**63, 1]
+    out = lz.sample_ids(_t(r.view(np.int64)), V, id_dtype=torch.int32 if dt == np.int32 else torch.int64)
+    torch.cuda.synchronize()
+    assert np.array_equal(out.cpu().numpy().astype(np.int64), oracle.sample_ids(r, V))
