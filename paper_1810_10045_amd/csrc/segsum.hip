@@ -53,6 +53,15 @@ namespace lmz {
 #ifndef LMZ_SEG_RF2
 #define LMZ_SEG_RF2 8                // rows per gather batch with <= 2 vectors per lane
 #endif
+#ifndef LMZ_SEG_LONG_R
+#define LMZ_SEG_LONG_R 512           // from this chunk length on, the *_LONG batches
+#endif
+#ifndef LMZ_SEG_RF4_LONG
+#define LMZ_SEG_RF4_LONG 8           // long chunks walk long enough to keep more rows in flight
+#endif
+#ifndef LMZ_SEG_RF2_LONG
+#define LMZ_SEG_RF2_LONG 16
+#endif
 #ifndef LMZ_SEG_NV_MAX
 #define LMZ_SEG_NV_MAX 4             // 16-byte vectors per lane per row (fp32)
 #endif
@@ -485,16 +494,29 @@ constexpr int t_for() {
   return t < 1 ? 1 : (t > 64 ? 64 : t);
 }
 
-template <typename GT, int VEC, int NV, int RF>
+// Rows per gather batch: more for long chunks (R >= LMZ_SEG_LONG_R), whose
+// walks are long enough to use the extra rows in flight.
+template <int NV, int R>
+constexpr int rf_for() {
+  return NV >= 4 ? (R >= LMZ_SEG_LONG_R ? LMZ_SEG_RF4_LONG : LMZ_SEG_RF4)
+                 : (R >= LMZ_SEG_LONG_R ? LMZ_SEG_RF2_LONG : LMZ_SEG_RF2);
+}
+
+template <typename GT, int VEC, int NV, int R>
+static void launch_one(const SegArgs& a, dim3 grid, hipStream_t st) {
+  k_segsum<GT, VEC, NV, rf_for<NV, R>(), R, t_for<R>()><<<grid, kSegThreads, 0, st>>>(a);
+}
+
+template <typename GT, int VEC, int NV>
 static hipError_t launch_r(const SegArgs& a, hipStream_t st) {
   constexpr int CT = NV * kWave * VEC;
   dim3 grid((a.nchunks + kSegWaves - 1) / kSegWaves, (a.D + CT - 1) / CT);
   switch (a.R) {
-    case 32: k_segsum<GT, VEC, NV, RF, 32, t_for<32>()><<<grid, kSegThreads, 0, st>>>(a); break;
-    case 64: k_segsum<GT, VEC, NV, RF, 64, t_for<64>()><<<grid, kSegThreads, 0, st>>>(a); break;
-    case 128: k_segsum<GT, VEC, NV, RF, 128, t_for<128>()><<<grid, kSegThreads, 0, st>>>(a); break;
-    case 256: k_segsum<GT, VEC, NV, RF, 256, t_for<256>()><<<grid, kSegThreads, 0, st>>>(a); break;
-    default: k_segsum<GT, VEC, NV, RF, 512, t_for<512>()><<<grid, kSegThreads, 0, st>>>(a); break;
+    case 32: launch_one<GT, VEC, NV, 32>(a, grid, st); break;
+    case 64: launch_one<GT, VEC, NV, 64>(a, grid, st); break;
+    case 128: launch_one<GT, VEC, NV, 128>(a, grid, st); break;
+    case 256: launch_one<GT, VEC, NV, 256>(a, grid, st); break;
+    default: launch_one<GT, VEC, NV, 512>(a, grid, st); break;
   }
   return hipGetLastError();
 }
@@ -504,10 +526,10 @@ static hipError_t dispatch_nv(const SegArgs& a, int nv_max, hipStream_t st) {
   const int per = kWave * VEC;
   int nv = (a.D + per - 1) / per;
   if (nv > nv_max) nv = nv_max;
-  if (nv <= 1) return launch_r<GT, VEC, 1, LMZ_SEG_RF2>(a, st);
-  if (nv == 2) return launch_r<GT, VEC, 2, LMZ_SEG_RF2>(a, st);
-  if constexpr (sizeof(GT) == 4 || VEC == 1) return launch_r<GT, VEC, 4, LMZ_SEG_RF4>(a, st);
-  return launch_r<GT, VEC, 2, LMZ_SEG_RF2>(a, st);
+  if (nv <= 1) return launch_r<GT, VEC, 1>(a, st);
+  if (nv == 2) return launch_r<GT, VEC, 2>(a, st);
+  if constexpr (sizeof(GT) == 4 || VEC == 1) return launch_r<GT, VEC, 4>(a, st);
+  return launch_r<GT, VEC, 2>(a, st);
 }
 
 static bool al16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
