@@ -12,20 +12,23 @@
 //   law fall in the sorted order (equal-length chunks left the waves of the
 //   tail, one write per row, twice as long as those of the heads). A wave
 //   finds its bounds with a 32-ary search of offsets, two targets at once.
-//   The segment (type) of a position is inverse[perm[i]], so a wave learns
-//   every segment boundary of its chunk from two gathers and a ballot,
-//   without searching. A segment shorter than T rows belongs entirely to the
+//   The search ends at the segments holding the two bounds, which tells the
+//   wave where the first and last segment of its chunk begin and end. The
+//   segment (type) of a position is inverse[perm[i]], so a wave learns
+//   every other segment boundary of its chunk from two gathers and a
+//   ballot, without searching. A segment shorter than T rows belongs entirely to the
 //   chunk holding its first position, even where it runs past the chunk
 //   end; a longer one is cut at chunk boundaries and every chunk sums its
 //   piece into a partial row:
 //     part_start[c]  the piece of a long segment that starts in chunk c and
 //                    continues past it (desc[c] names that segment),
-//     part_cont[c]   the piece of a long segment that started before chunk c
-//                    (cont_seg[c] names that segment).
-//   k_segsum_fix then sums, for each desc[c] >= 0, part_start[c] and the
-//   part_cont rows of the chunks after c that name the same segment, in
-//   order: one wave per column tile for a segment of at most 16 pieces,
-//   all waves of a workgroup (fixed stride split of the pieces, fixed-order
+//     part_cont[c]   the piece of a long segment that started before chunk c.
+//   The chunk that starts such a segment also records in npieces[c] how many
+//   chunks after c it reaches (the chunk of its last position, from the same
+//   cost formula), so that k_segsum_fix finds every piece from one load. It
+//   sums part_start[c] and part_cont[c + 1 .. c + npieces[c]] in order: one
+//   wave per column tile for a segment of fewer than 16 further pieces, all
+//   waves of a workgroup (fixed stride split of the pieces, fixed-order
 //   combine in LDS) for a head.
 // A chunk holds at most R positions (N is sized for U = min(K, u_cap)) and
 // reads at most R + T - 1 rows.
@@ -87,14 +90,14 @@ struct SegArgs {
   float* part_cont;
   float* part_start;
   int32_t* desc;
-  int32_t* cont_seg;
+  int32_t* npieces;
   int R, nchunks, rw, ww;  // cost of a position / of a segment end
   int32_t* dev_err;
 };
 
 struct SegLayout {
   int R, max_chunks;
-  size_t cont, start, desc, cont_seg, total;
+  size_t cont, start, desc, npieces, total;
 };
 
 static inline size_t a256(size_t x) { return (x + 255) & ~size_t(255); }
@@ -121,7 +124,7 @@ static SegLayout seg_layout(int64_t K, int64_t D) {
   L.cont = off;     off += a256(n * D * 4);
   L.start = off;    off += a256(n * D * 4);
   L.desc = off;     off += a256(n * 4);
-  L.cont_seg = off; off += a256(n * 4);
+  L.npieces = off;  off += a256(n * 4);
   L.total = off;
   return L;
 }
@@ -141,10 +144,14 @@ constexpr int windows_for() { return (R + T) / 64 + 1; }
 // half-wave for the largest u < U with f(u) = rw * offsets[u] + ww * u <= t
 // (f(0) = 0), then b = offsets[u] + min(ceil((t - f(u)) / rw), len(u));
 // b = K once t >= rw * K + ww * U. Every value the search keeps is
-// wave-uniform.
+// wave-uniform. Besides b it returns that u and offsets[u], offsets[u + 1]:
+// b lies strictly inside segment u exactly when offsets[u] < b < offsets[u + 1].
+struct Bound {
+  int b, u, o0, o1;
+};
 __device__ __forceinline__ void chunk_bounds(const int32_t* __restrict__ offsets, int U, int rw,
-                                             int ww, int K, int64_t tA, int64_t tB, int& bA,
-                                             int& bB) {
+                                             int ww, int K, int64_t tA, int64_t tB, Bound& A,
+                                             Bound& B) {
   const int lane = lane_id();
   const bool hi = lane >= 32;
   const int hl = lane & 31;
@@ -173,8 +180,8 @@ __device__ __forceinline__ void chunk_bounds(const int32_t* __restrict__ offsets
   const int64_t into = (t - (int64_t(rw) * o0 + int64_t(ww) * u) + rw - 1) / rw;
   int b = int64_t(o0) + into < int64_t(o1) ? static_cast<int>(int64_t(o0) + into) : o1;
   if (t >= int64_t(rw) * K + int64_t(ww) * U) b = K;
-  bA = first_lane(b);
-  bB = read_lane(b, 32);
+  A = Bound{first_lane(b), first_lane(u), first_lane(o0), first_lane(o1)};
+  B = Bound{read_lane(b, 32), read_lane(u, 32), read_lane(o0, 32), read_lane(o1, 32)};
 }
 
 template <typename GT, int VEC, int NV, int RF, int R, int T>
@@ -198,7 +205,7 @@ __global__ __launch_bounds__(kSegThreads) void k_segsum(SegArgs a) {
   if (U < 1) {  // K > 0 always has a type: only a bad count gets here
     if (ct == 0 && lane == 0) {
       a.desc[c] = -1;
-      a.cont_seg[c] = -1;
+      a.npieces[c] = 0;
       if (c == 0) raise_err(a.dev_err, LM_DEVERR_CAPACITY);
     }
     return;
@@ -206,29 +213,67 @@ __global__ __launch_bounds__(kSegThreads) void k_segsum(SegArgs a) {
   const int Ub = U < a.u_cap ? U : static_cast<int>(a.u_cap);
   const int64_t cost = int64_t(a.rw) * K + int64_t(a.ww) * Ub;
   const int64_t Q = (cost + a.nchunks - 1) / a.nchunks;
-  int p0, p1;
-  chunk_bounds(a.offsets, U, a.rw, a.ww, K, int64_t(c) * Q, int64_t(c + 1) * Q, p0, p1);
-  if (c == a.nchunks - 1) p1 = K;
+  Bound A, B;
+  chunk_bounds(a.offsets, U, a.rw, a.ww, K, int64_t(c) * Q, int64_t(c + 1) * Q, A, B);
+  const int p0 = A.b;
+  int p1 = B.b;
+  bool cut_after = c < a.nchunks - 1;  // p1 is a cut of the cost, not the end of the positions
+  if (!cut_after) p1 = K;
   if (p1 - p0 > R) {  // only inconsistent offsets: never walk past the windows
     if (lane == 0) raise_err(a.dev_err, LM_DEVERR_CAPACITY);
     p1 = p0 + R;
+    cut_after = false;
   }
   if (p1 <= p0) {  // an empty chunk (a segment end cost more than Q)
     if (ct == 0 && lane == 0) {
       a.desc[c] = -1;
-      a.cont_seg[c] = -1;
+      a.npieces[c] = 0;
     }
     return;
   }
 
-  // 1. Gather the permutation and the segment of every position in the
-  //    windows (sentinels: -2 before position 0, -1 from position K on).
-  int pw[NW], sw[NW];
+  // 1. The first and the last segment of the chunk, from the search: the
+  //    first started before the chunk when p0 lies strictly inside it, the
+  //    last runs on after the chunk when p1 does.
+  const bool started_before = p0 > A.o0 && p0 < A.o1;
+  const int s_f = A.u, len_f = A.o1 - A.o0;
+  const bool cont_after = cut_after && p1 > B.o0 && p1 < B.o1;
+  const int s_l = B.u, len_l = B.o1 - B.o0;
+  const bool long_f = started_before && len_f >= T;
+  const bool long_l = cont_after && len_l >= T;
+  if (ct == 0 && lane == 0) {
+    // A long segment that starts in this chunk ends in the chunk of its last
+    // position, whose cost is rw * (offsets[s_l + 1] - 1) + ww * s_l.
+    const bool starts_long = long_l && !(started_before && s_l == s_f);
+    int np = 0;
+    if (starts_long) {
+      int64_t ce = (int64_t(a.rw) * (B.o1 - 1) + int64_t(a.ww) * s_l) / Q;
+      if (ce > a.nchunks - 1) ce = a.nchunks - 1;
+      np = static_cast<int>(ce - c);
+    }
+    a.desc[c] = starts_long && np >= 1 ? s_l : -1;
+    a.npieces[c] = np;
+  }
+  // Rows this chunk sums: skip a short segment owned by the previous chunk,
+  // run a short last segment to its end, stop a long one at p1.
+  const int q = started_before && !long_f ? A.o1 : p0;
+  int q_end = cont_after && !long_l ? B.o1 : p1;
+  const int walk_max = p0 - 1 + NW * kWave - 1;  // last position whose end bit is known
   bool bad = false;
+  if (q_end > walk_max) {
+    bad = true;  // only inconsistent offsets get here: never walk past the windows
+    q_end = walk_max;
+  }
+
+  // 2. Gather the permutation and the segment of every position in the
+  //    windows (sentinels: -2 before position 0, -1 from position K on).
+  //    The loads are unconditional, at clamped positions: a load under a
+  //    lane condition makes the compiler wait for every load before it.
+  int pw[NW], sw[NW];
 #pragma unroll
   for (int w = 0; w < NW; ++w) {
     const int pos = p0 - 1 + w * kWave + lane;
-    pw[w] = (pos >= 0 && pos < K) ? a.perm[pos] : 0;
+    pw[w] = a.perm[pos < 0 ? 0 : (pos < K ? pos : K - 1)];
   }
 #pragma unroll
   for (int w = 0; w < NW; ++w) {
@@ -237,7 +282,8 @@ __global__ __launch_bounds__(kSegThreads) void k_segsum(SegArgs a) {
     const bool kin = static_cast<uint32_t>(pw[w]) < static_cast<uint32_t>(K);
     bad |= ok && !kin;
     if (!kin) pw[w] = 0;
-    sw[w] = ok ? a.inverse[pw[w]] : (pos < 0 ? -2 : -1);
+    const int sv = a.inverse[pw[w]];
+    sw[w] = ok ? sv : (pos < 0 ? -2 : -1);
   }
   // ends[w] bit j: position p0-1+64w+j is the last of its segment.
   uint64_t ends[NW];
@@ -247,57 +293,6 @@ __global__ __launch_bounds__(kSegThreads) void k_segsum(SegArgs a) {
     if (lane == kWave - 1) nxt = w + 1 < NW ? read_lane(sw[w + 1 < NW ? w + 1 : w], 0) : -3;
     ends[w] = ballot(sw[w] != nxt);
   }
-  // 2. First and last segment of the chunk and, where needed, their lengths.
-  const int s_f = read_lane(sw[0], 1);                     // segment of p0
-  const bool started_before = read_lane(sw[0], 0) == s_f;  // p0 - 1 in the same segment
-  const int il = p1 - p0;                                  // window index of p1 - 1
-  int s_l = 0;
-  bool cont_after = false;                                 // p1 in the segment of p1 - 1
-#pragma unroll
-  for (int w = 0; w < NW; ++w) {
-    if (il / kWave == w) s_l = read_lane(sw[w], il % kWave);
-  }
-#pragma unroll
-  for (int w = 0; w < NW; ++w) {
-    if ((il + 1) / kWave == w) cont_after = read_lane(sw[w], (il + 1) % kWave) == s_l;
-  }
-  const bool sf_ok = s_f >= 0 && s_f < U, sl_ok = s_l >= 0 && s_l < U;
-  bad |= !sf_ok || !sl_ok;
-  const int len_f = first_lane(sf_ok && started_before ? a.offsets[s_f + 1] - a.offsets[s_f] : 0);
-  const int b_l = first_lane(sl_ok && cont_after ? a.offsets[s_l + 1] : p1);
-  const int len_l = first_lane(sl_ok && cont_after ? b_l - a.offsets[s_l] : 0);
-  const bool long_f = started_before && len_f >= T;
-  const bool long_l = cont_after && len_l >= T;
-  if (ct == 0 && lane == 0) {
-    a.desc[c] = (long_l && !(started_before && s_l == s_f)) ? s_l : -1;
-    a.cont_seg[c] = long_f ? s_f : -1;
-  }
-
-  // Rows this chunk sums: skip a short segment owned by the previous chunk,
-  // run a short last segment to its end, stop a long one at p1.
-  int q = p0;
-  if (started_before && !long_f) {
-    int first_end = K;  // first end bit at or after p0
-#pragma unroll
-    for (int w = NW - 1; w >= 0; --w) {
-      uint64_t m = ends[w];
-      if (w == 0) m &= ~uint64_t(1);
-      if (m) first_end = p0 - 1 + w * kWave + __builtin_ctzll(m);
-    }
-    q = first_end + 1;
-  }
-  int q_end = cont_after && !long_l ? b_l : p1;
-  const int walk_max = p0 - 1 + NW * kWave - 1;  // last position whose end bit is known
-  if (q_end > walk_max) {
-    bad = true;  // only inconsistent offsets get here: never walk past the windows
-    q_end = walk_max;
-  }
-  if (ballot(bad) && lane == 0) raise_err(a.dev_err, LM_DEVERR_CAPACITY);
-  // Every lane holds the same walk bounds: tell the compiler, so the row
-  // loop below is scalar control flow and the gathers of a batch stay in
-  // flight together.
-  q = first_lane(q);
-  q_end = first_lane(q_end);
 
   // 3. Walk rows q .. q_end - 1, window by window. Lanes past the last column
   //    load a valid vector of the same row (col_ld) and never store it, so
@@ -336,6 +331,9 @@ __global__ __launch_bounds__(kSegThreads) void k_segsum(SegArgs a) {
 #pragma unroll
         for (int v = 0; v < NV; ++v) buf[r][v] = RV::load(row + col_ld[v]);
       }
+      // All RF rows in flight before the first add: keep the scheduler from
+      // interleaving the adds of early rows with the loads of later ones.
+      __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int r = 0; r < RF; ++r) {
         if (r < n) {
@@ -364,30 +362,39 @@ __global__ __launch_bounds__(kSegThreads) void k_segsum(SegArgs a) {
       }
     }
   }
+  // Report a segment map that disagrees with offsets at the chunk start.
+  const int seg_before = read_lane(sw[0], 0), seg_p0 = read_lane(sw[0], 1);
+  if (started_before) bad |= seg_before != s_f || seg_p0 != s_f;
+  else bad |= seg_before == seg_p0 || seg_p0 != (p0 == A.o1 ? A.u + 1 : A.u);
+  if (ballot(bad) && lane == 0) raise_err(a.dev_err, LM_DEVERR_CAPACITY);
 }
 
 // Sum the pieces of every long segment that spans chunks (piece 0 is
 // part_start[c], piece t >= 1 is part_cont[c + t], added in order of t).
 // Grid: one workgroup of kFixWaves waves per kFixChunks chunks and per
-// column tile of 64 * VEC columns. Few chunks start such a segment, so a workgroup reads
-// the desc entries of its chunks with one coalesced load and a ballot, and
-// only waves with work touch the partial rows (launching a wave per chunk
-// cost more than the sums). The partial rows were just written, so the sums
-// are bound by load latency: a wave keeps RF pieces in flight at once. A
-// segment of at most RF pieces is summed by one wave in one round; a longer
-// one (a head of the Zipf law) by all kFixWaves waves, wave v adding pieces
-// v, v + kFixWaves, ... in order, their partial rows then added in wave
-// order through LDS.
+// column tile of 64 * VEC columns. Few chunks start such a segment, so a
+// workgroup reads the desc and npieces entries of its chunks with one
+// coalesced load and a ballot, and only waves with work touch the partial
+// rows (launching a wave per chunk cost more than the sums). The partial
+// rows were just written, so the sums are bound by load latency: every wave
+// issues all its piece loads before it waits for any. A segment of fewer
+// than RF further pieces is summed by one wave; a longer one (a head of the
+// Zipf law) by all kFixWaves waves, wave v adding pieces v, v + kFixWaves,
+// ... in order, their partial rows then added in wave order through LDS.
+// Long segments start at least RF chunks apart, so with kFixChunks <= RF a
+// workgroup holds at most one head, and with kFixChunks <= kFixWaves each
+// wave at most one shorter segment.
 #ifndef LMZ_SEG_FIX_WAVES
 #define LMZ_SEG_FIX_WAVES 8          // waves of a fix-up workgroup
 #endif
 #ifndef LMZ_SEG_FIX_CHUNKS
-#define LMZ_SEG_FIX_CHUNKS 8         // chunks a fix-up workgroup looks after (<= 64)
+#define LMZ_SEG_FIX_CHUNKS 8         // chunks a fix-up workgroup looks after
 #endif
 constexpr int kFixWaves = LMZ_SEG_FIX_WAVES;
 constexpr int kFixThreads = kFixWaves * kWave;
 constexpr int kFixChunks = LMZ_SEG_FIX_CHUNKS;
-static_assert(kFixChunks <= kWave, "one desc entry per lane");
+static_assert(kFixChunks <= kFixWaves && kFixChunks <= LMZ_SEG_FIX_RF,
+              "at most one short segment per wave and one head per workgroup");
 
 template <int VEC, int RF>
 __global__ __launch_bounds__(kFixThreads) void k_segsum_fix(SegArgs a) {
@@ -401,90 +408,87 @@ __global__ __launch_bounds__(kFixThreads) void k_segsum_fix(SegArgs a) {
   const int col = blockIdx.y * kCols + lane * VEC;
   const int col_ld = col < D ? col : D - VEC;  // past the end: a valid, unstored vector
 
-  // Chunks c0 + i that start a long segment, as a mask over i (the same in
-  // every wave).
+  // Chunks c0 + i that start a long segment (the same masks in every wave).
   const int ci = c0 + lane;
-  int sd = (lane < kFixChunks && ci < a.nchunks) ? a.desc[ci] : -1;
-  const bool has = sd >= 0 && sd < U && sd < a.u_cap;
+  const bool mine = lane < kFixChunks && ci < a.nchunks;
+  const int sd = mine ? a.desc[ci] : -1;
+  const int np = mine ? a.npieces[ci] : 0;
+  const bool has = sd >= 0 && sd < U && sd < a.u_cap && np >= 1 && np <= a.nchunks - 1 - ci;
   const uint64_t todo = ballot(has);
+  if (!todo) return;
+  const uint64_t heads = ballot(has && np >= RF);
+  const uint64_t shorts = todo & ~heads;
   auto piece = [&](int cs, int t) {
     return (t == 0 ? a.part_start + static_cast<int64_t>(cs) * D
                    : a.part_cont + static_cast<int64_t>(cs + t) * D) + col_ld;
   };
-  auto pieces_after = [&](int cs, int s) {  // chunks after cs that hold a piece of s
-    int P = 0;
-    while (true) {
-      const int cc = cs + 1 + P + lane;
-      const bool same = cc < a.nchunks && a.cont_seg[cc] == s;
-      const uint64_t m = ballot(same);
-      const int run = ~m ? __builtin_ctzll(~m) : kWave;
-      P += run;
-      if (run < kWave) break;
-    }
-    return P;
-  };
 
-  // Pass 1: segments of at most RF pieces, the j-th of the mask by wave
-  // j % kFixWaves.
-  uint64_t m = todo;
-  for (int j = 0; m; ++j, m &= m - 1) {
-    if (j % kFixWaves != wave) continue;
-    const int i = __builtin_ctzll(m);
-    const int cs = c0 + i;
-    const int s = read_lane(sd, i);
-    const int P = pieces_after(cs, s);
-    if (P >= RF) continue;
-    float buf[RF][VEC];
+  // This wave's short segment: the wave-th of the mask.
+  uint64_t m = shorts;
+  for (int j = 0; j < wave && m; ++j) m &= m - 1;
+  const int is = m ? __builtin_ctzll(m) : -1;
+  const int ss = is >= 0 ? read_lane(sd, is) : -1, sP = is >= 0 ? read_lane(np, is) : 0;
+  // The head, if any.
+  const int ih = heads ? __builtin_ctzll(heads) : -1;
+  const int hs = ih >= 0 ? read_lane(sd, ih) : -1, hP = ih >= 0 ? read_lane(np, ih) : 0;
+
+  float sbuf[RF][VEC], hbuf[RF][VEC];
+  if (is >= 0) {
 #pragma unroll
-    for (int r = 0; r < RF; ++r) load_vec<VEC>(piece(cs, r <= P ? r : 0), buf[r]);
+    for (int r = 0; r < RF; ++r) load_vec<VEC>(piece(c0 + is, r <= sP ? r : 0), sbuf[r]);
+  }
+  if (ih >= 0) {
+#pragma unroll
+    for (int r = 0; r < RF; ++r) {
+      const int t = wave + r * kFixWaves;
+      load_vec<VEC>(piece(c0 + ih, t <= hP ? t : wave), hbuf[r]);
+    }
+  }
+  if (is >= 0) {
     float acc[VEC];
 #pragma unroll
-    for (int e = 0; e < VEC; ++e) acc[e] = buf[0][e];
+    for (int e = 0; e < VEC; ++e) acc[e] = sbuf[0][e];
 #pragma unroll
     for (int r = 1; r < RF; ++r)
-      if (r <= P)
+      if (r <= sP)
 #pragma unroll
-        for (int e = 0; e < VEC; ++e) acc[e] += buf[r][e];
-    if (col < D) store_vec<VEC>(a.out + static_cast<int64_t>(s) * a.ld_out + col, acc);
+        for (int e = 0; e < VEC; ++e) acc[e] += sbuf[r][e];
+    if (col < D) store_vec<VEC>(a.out + static_cast<int64_t>(ss) * a.ld_out + col, acc);
   }
-
-  // Pass 2: segments of more pieces, one after the other, all waves.
-  for (m = todo; m; m &= m - 1) {
-    const int i = __builtin_ctzll(m);
-    const int cs = c0 + i;
-    const int sb = read_lane(sd, i);
-    const int PB = pieces_after(cs, sb);
-    if (PB < RF) continue;  // the same in every thread
-    float acc[VEC];
+  if (ih < 0) return;  // the same in every wave: no barrier below is skipped by only some
+  float acc[VEC];
 #pragma unroll
-    for (int e = 0; e < VEC; ++e) acc[e] = 0.f;
-    for (int t0 = wave; t0 <= PB; t0 += kFixWaves * RF) {
-      float buf[RF][VEC];
+  for (int e = 0; e < VEC; ++e) acc[e] = 0.f;
 #pragma unroll
-      for (int r = 0; r < RF; ++r) {
-        const int t = t0 + r * kFixWaves;
-        load_vec<VEC>(piece(cs, t <= PB ? t : t0), buf[r]);
-      }
+  for (int r = 0; r < RF; ++r)
+    if (wave + r * kFixWaves <= hP)
 #pragma unroll
-      for (int r = 0; r < RF; ++r)
-        if (t0 + r * kFixWaves <= PB)
+      for (int e = 0; e < VEC; ++e) acc[e] += hbuf[r][e];
+  // Heads longer than kFixWaves * RF pieces: further rounds.
+  for (int t0 = wave + kFixWaves * RF; t0 <= hP; t0 += kFixWaves * RF) {
 #pragma unroll
-          for (int e = 0; e < VEC; ++e) acc[e] += buf[r][e];
+    for (int r = 0; r < RF; ++r) {
+      const int t = t0 + r * kFixWaves;
+      load_vec<VEC>(piece(c0 + ih, t <= hP ? t : t0), hbuf[r]);
     }
 #pragma unroll
-    for (int e = 0; e < VEC; ++e) s_part[wave][lane * VEC + e] = acc[e];
-    __syncthreads();
-    // Thread x adds column x of the tile over the waves in order.
-    for (int x = threadIdx.x; x < kCols; x += kFixThreads) {
-      const int cx = blockIdx.y * kCols + x;
-      if (cx < D) {
-        float sum = 0.f;
+    for (int r = 0; r < RF; ++r)
+      if (t0 + r * kFixWaves <= hP)
 #pragma unroll
-        for (int w = 0; w < kFixWaves; ++w) sum += s_part[w][x];
-        a.out[static_cast<int64_t>(sb) * a.ld_out + cx] = sum;
-      }
+        for (int e = 0; e < VEC; ++e) acc[e] += hbuf[r][e];
+  }
+#pragma unroll
+  for (int e = 0; e < VEC; ++e) s_part[wave][lane * VEC + e] = acc[e];
+  __syncthreads();
+  // Thread x adds column x of the tile over the waves in order.
+  for (int x = threadIdx.x; x < kCols; x += kFixThreads) {
+    const int cx = blockIdx.y * kCols + x;
+    if (cx < D) {
+      float sum = 0.f;
+#pragma unroll
+      for (int w = 0; w < kFixWaves; ++w) sum += s_part[w][x];
+      a.out[static_cast<int64_t>(hs) * a.ld_out + cx] = sum;
     }
-    __syncthreads();
   }
 }
 
@@ -557,7 +561,7 @@ int segsum_run(const void* grad, int gtype, int64_t K, int64_t D, int64_t ld_gra
   a.part_cont = reinterpret_cast<float*>(w + L.cont);
   a.part_start = reinterpret_cast<float*>(w + L.start);
   a.desc = reinterpret_cast<int32_t*>(w + L.desc);
-  a.cont_seg = reinterpret_cast<int32_t*>(w + L.cont_seg);
+  a.npieces = reinterpret_cast<int32_t*>(w + L.npieces);
   a.R = L.R;
   a.rw = read_cost(gtype);
   a.ww = kWriteCost;

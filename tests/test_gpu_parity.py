@@ -213,6 +213,30 @@ def test_segsum_permuted_ids(lz, K, V, s, D, gdt, seed):
     test_segsum_random(lz, K, V, s, D, gdt, seed, perm_seed=seed + 500)
 
 
+@pytest.mark.parametrize("gdt", ["bf16", "f32"])
+def test_segsum_chunks_inside_short_segments(lz, gdt):
+    """One head of 30,000 tokens and 600 types of 15 (just under the
+    long-segment threshold of 16 at this K): with so few types for the
+    capacity, a bf16 chunk holds about 13.6 positions, and some chunks lie
+    wholly inside a short segment owned by an earlier chunk."""
+    base = np.concatenate([np.full(30_000, 0)] + [np.full(15, 1000 * t) for t in range(1, 601)])
+    ids = np.random.Generator(np.random.PCG64(81)).permutation(base).astype(np.int32)
+    K, V, D = len(ids), 800_000, 64
+    _say(f"segsum short segments K={K} {gdt}")
+    g32 = synth.normal_rows(K, D, 82)
+    grad = synth.bf16_bits(g32) if gdt == "bf16" else g32
+    tgrad = _t(g32).to(torch.bfloat16) if gdt == "bf16" else _t(g32)
+    res = lz.unique(_t(ids), V)
+    out = lz.segsum(tgrad, res.perm, res.inverse, res.offsets, res.num_unique, dev_err=res.dev_err)
+    torch.cuda.synchronize()
+    lz.check(res.dev_err)
+    o = H.assert_unique_matches(res, ids, V, oracle)
+    U = len(o[0])
+    ref = oracle.segsum(grad, o[3], U)
+    err = H.row_rel_err(out[:U].double().cpu().numpy(), ref, H.sum_of_squares(grad, o[3], U, oracle))
+    assert err <= (H.TOL_BF16 if gdt == "bf16" else H.TOL_F32)
+
+
 def test_segsum_deterministic(lz):
     a = _segsum_case(lz, 60_000, 500, 1.2, 1024, "f32", 51)[3].clone()
     b = _segsum_case(lz, 60_000, 500, 1.2, 1024, "f32", 51)[3]
