@@ -43,6 +43,9 @@ constexpr int kHistThreads = 1024;
 #ifndef LMZ_UNIQUE_DIGIT_BITS_LARGE
 #define LMZ_UNIQUE_DIGIT_BITS_LARGE 10 // widest digit with 1024-thread tiles
 #endif
+#ifndef LMZ_UNIQUE_LOOKBACK_W
+#define LMZ_UNIQUE_LOOKBACK_W 4        // predecessor tiles a look-back round reads
+#endif
 constexpr int kSmallDigitBits = LMZ_UNIQUE_DIGIT_BITS;
 constexpr int kLargeDigitBits = LMZ_UNIQUE_DIGIT_BITS_LARGE;
 constexpr int kMaxPasses = 8;              // ceil(64 / 8)
@@ -182,7 +185,7 @@ __global__ __launch_bounds__(NT) void k_onesweep(
   constexpr int kRadix = 1 << RB;
   constexpr int DPT = kRadix >= NT ? kRadix / NT : 1;
   constexpr int kDigitThreads = kRadix / DPT;        // threads that own digits
-  constexpr int W = 16;                              // predecessors per look-back round
+  constexpr int W = LMZ_UNIQUE_LOOKBACK_W;           // predecessors per look-back round
   __shared__ KeyT s_keys[kTile];
   __shared__ int32_t s_vals[kTile];
   __shared__ uint16_t s_cnt[kWaves][kRadix];         // per-wave digit counts, then offsets
