@@ -49,7 +49,23 @@ constexpr int kHistThreads = 1024;
 constexpr int kSmallDigitBits = LMZ_UNIQUE_DIGIT_BITS;
 constexpr int kLargeDigitBits = LMZ_UNIQUE_DIGIT_BITS_LARGE;
 constexpr int kMaxPasses = 8;              // ceil(64 / 8)
-constexpr int kItems = 4;                  // keys per thread in a tile
+// Keys per thread of a sort or dedup tile, by input size: bigger tiles mean
+// fewer tiles for the look-back to pass, smaller ones spread a small input
+// over more CUs. Measured best: with 256-thread tiles, 2 keys up to 16K ids
+// and 4 above; with 1024-thread tiles, 2 up to 512K, 4 up to 1.5M, 8 above.
+#ifndef LMZ_UNIQUE_SMALL_ITEMS2_MAX_K
+#define LMZ_UNIQUE_SMALL_ITEMS2_MAX_K (1 << 14)
+#endif
+#ifndef LMZ_UNIQUE_LARGE_ITEMS2_MAX_K
+#define LMZ_UNIQUE_LARGE_ITEMS2_MAX_K (1 << 19)
+#endif
+#ifndef LMZ_UNIQUE_LARGE_ITEMS4_MAX_K
+#define LMZ_UNIQUE_LARGE_ITEMS4_MAX_K (3 << 19)
+#endif
+static inline int items_for(int64_t K, int nt) {
+  if (nt == 256) return K <= LMZ_UNIQUE_SMALL_ITEMS2_MAX_K ? 2 : 4;
+  return K <= LMZ_UNIQUE_LARGE_ITEMS2_MAX_K ? 2 : (K <= LMZ_UNIQUE_LARGE_ITEMS4_MAX_K ? 4 : 8);
+}
 constexpr int kHistItems = 16;             // keys per thread per histogram round
 constexpr int kHistKeysPerBlock = 1 << 12;
 constexpr int kMaxHistBlocks = 64;
@@ -62,7 +78,7 @@ constexpr uint64_t kD31 = (1ull << 31) - 1;
 
 struct UniqueLayout {
   size_t bhist, tickets, status, dstatus, keys0, keys1, vals0, vals1, total;
-  int passes, bits, tiles, hist_blocks, nt;
+  int passes, bits, tiles, hist_blocks, nt, items;
   int rstride;  // digit slots per pass in the histogram rows and status arrays
   int shift[kMaxPasses], nbits[kMaxPasses];
 };
@@ -96,7 +112,8 @@ static UniqueLayout unique_layout(int64_t K, int idtype, int64_t V) {
     L.nbits[p] = nb;
     sh += nb;
   }
-  const int64_t tile_keys = int64_t(L.nt) * kItems;
+  L.items = items_for(K, L.nt);
+  const int64_t tile_keys = int64_t(L.nt) * L.items;
   L.tiles = static_cast<int>((K + tile_keys - 1) / tile_keys);
   const int64_t hb = (K + kHistKeysPerBlock - 1) / kHistKeysPerBlock;
   L.hist_blocks = static_cast<int>(hb < 1 ? 1 : (hb > kMaxHistBlocks ? kMaxHistBlocks : hb));
@@ -115,6 +132,9 @@ static UniqueLayout unique_layout(int64_t K, int idtype, int64_t V) {
   L.total = off;
   return L;
 }
+
+template <int N>
+using I = std::integral_constant<int, N>;
 
 struct PassBits {
   int shift[kMaxPasses], nbits[kMaxPasses];
@@ -174,13 +194,14 @@ __global__ __launch_bounds__(kHistThreads) void k_hist(
 // nbits <= RB. Thread t answers for digits t*DPT .. t*DPT+DPT-1 (DPT = 2 for
 // 11-bit digits; for 8-bit digits threads 0..255 answer for one each).
 // ---------------------------------------------------------------------------
-template <typename KeyT, int RB, int NT>
+template <typename KeyT, int RB, int NT, int ITEMS>
 __global__ __launch_bounds__(NT) void k_onesweep(
     const KeyT* __restrict__ keys_in, const int32_t* __restrict__ vals_in,
     KeyT* __restrict__ keys_out, int32_t* __restrict__ vals_out, int K, int shift, int nbits,
     const uint32_t* __restrict__ bhist, int hist_blocks, int hist_stride,
     uint32_t* __restrict__ status, uint32_t* __restrict__ ticket, int32_t* __restrict__ dev_err) {
   constexpr int kWaves = NT / kWave;
+  constexpr int kItems = ITEMS;
   constexpr int kTile = NT * kItems;
   constexpr int kRadix = 1 << RB;
   constexpr int DPT = kRadix >= NT ? kRadix / NT : 1;
@@ -393,13 +414,14 @@ __global__ __launch_bounds__(NT) void k_onesweep(
 // k_dedup: thread t of tile `tile` owns the 4 sorted positions
 // base + 4t .. base + 4t + 3.
 // ---------------------------------------------------------------------------
-template <typename KeyT, int NT>
+template <typename KeyT, int NT, int ITEMS>
 __global__ __launch_bounds__(NT) void k_dedup(
     const KeyT* __restrict__ skeys, const int32_t* __restrict__ perm, int K, int cap,
     KeyT* __restrict__ uniq, int32_t* __restrict__ counts, int32_t* __restrict__ offsets,
     int32_t* __restrict__ inverse, int64_t* __restrict__ num_unique,
     uint64_t* __restrict__ status, uint32_t* __restrict__ ticket, int32_t* __restrict__ dev_err) {
   constexpr int kWaves = NT / kWave;
+  constexpr int kItems = ITEMS;
   constexpr int kTile = NT * kItems;
   __shared__ uint32_t s_scan[kWaves];
   __shared__ int s_maxs[kWaves];
@@ -544,12 +566,12 @@ size_t unique_workspace_bytes(int64_t K, int idtype, int64_t V) {
   return unique_layout(K, idtype, V).total;
 }
 
-template <typename KeyT, int RB, int NT>
+template <typename KeyT, int RB, int NT, int ITEMS>
 static hipError_t launch_pass(const UniqueLayout& L, int p, const KeyT* kin, const int32_t* vin,
                               KeyT* kout, int32_t* vout, int K, uint32_t* bhist,
                               uint32_t* status, uint32_t* tickets, int32_t* dev_err,
                               hipStream_t st) {
-  k_onesweep<KeyT, RB, NT><<<L.tiles, NT, 0, st>>>(
+  k_onesweep<KeyT, RB, NT, ITEMS><<<L.tiles, NT, 0, st>>>(
       kin, vin, kout, vout, K, L.shift[p], L.nbits[p], bhist + size_t(p) * L.rstride,
       L.hist_blocks, L.passes * L.rstride, status + size_t(p) * L.tiles * L.rstride, tickets + p,
       dev_err);
@@ -591,29 +613,42 @@ static int run_unique(const KeyT* ids, int K, int64_t V, KeyT* uniq, int32_t* co
     int32_t* vout = p == L.passes - 1 ? perm : vb[p & 1];
     // The narrowest compiled digit that holds this pass's bits.
     const bool narrow = L.nbits[p] <= kSmallDigitBits;
+    auto pass = [&](auto rb, auto nt, auto items) {
+      return launch_pass<KeyT, decltype(rb)::value, decltype(nt)::value, decltype(items)::value>(
+          L, p, kin, vin, kout, vout, K, bhist, status, tickets, dev_err, st);
+    };
+    auto by_items = [&](auto rb, auto nt) {
+      if constexpr (decltype(nt)::value == 256)
+        return L.items == 2 ? pass(rb, nt, I<2>{}) : pass(rb, nt, I<4>{});
+      else
+        return L.items == 2 ? pass(rb, nt, I<2>{})
+                            : (L.items == 4 ? pass(rb, nt, I<4>{}) : pass(rb, nt, I<8>{}));
+    };
     hipError_t e;
     if (L.nt == 256)
-      e = narrow ? launch_pass<KeyT, kSmallDigitBits, 256>(L, p, kin, vin, kout, vout, K, bhist,
-                                                            status, tickets, dev_err, st)
-                 : launch_pass<KeyT, kLargeDigitBits, 256>(L, p, kin, vin, kout, vout, K, bhist,
-                                                            status, tickets, dev_err, st);
+      e = narrow ? by_items(I<kSmallDigitBits>{}, I<256>{}) : by_items(I<kLargeDigitBits>{}, I<256>{});
     else
-      e = narrow ? launch_pass<KeyT, kSmallDigitBits, 1024>(L, p, kin, vin, kout, vout, K, bhist,
-                                                             status, tickets, dev_err, st)
-                 : launch_pass<KeyT, kLargeDigitBits, 1024>(L, p, kin, vin, kout, vout, K, bhist,
-                                                             status, tickets, dev_err, st);
+      e = narrow ? by_items(I<kSmallDigitBits>{}, I<1024>{})
+                 : by_items(I<kLargeDigitBits>{}, I<1024>{});
     if (e != hipSuccess) return launch_status(e);
     kin = kout;
     vin = vout;
   }
   const int cap = static_cast<int>(K < V ? K : V);
-  if (L.nt == 256)
-    k_dedup<KeyT, 256><<<L.tiles, 256, 0, st>>>(kin, perm, K, cap, uniq, counts, offsets, inverse,
-                                                num_unique, dstatus, tickets + kMaxPasses, dev_err);
-  else
-    k_dedup<KeyT, 1024><<<L.tiles, 1024, 0, st>>>(kin, perm, K, cap, uniq, counts, offsets,
+  auto dedup = [&](auto nt, auto items) {
+    constexpr int NT = decltype(nt)::value, IT = decltype(items)::value;
+    k_dedup<KeyT, NT, IT><<<L.tiles, NT, 0, st>>>(kin, perm, K, cap, uniq, counts, offsets,
                                                   inverse, num_unique, dstatus,
                                                   tickets + kMaxPasses, dev_err);
+  };
+  if (L.nt == 256) {
+    if (L.items == 2) dedup(I<256>{}, I<2>{});
+    else dedup(I<256>{}, I<4>{});
+  } else {
+    if (L.items == 2) dedup(I<1024>{}, I<2>{});
+    else if (L.items == 4) dedup(I<1024>{}, I<4>{});
+    else dedup(I<1024>{}, I<8>{});
+  }
   return launch_status(hipGetLastError());
 }
 

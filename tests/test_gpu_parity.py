@@ -81,6 +81,10 @@ UNIQUE_CASES = [
     # 9-bit and an 8-bit pass), and the last K that still takes small tiles
     (150_001, 2**40, 0.9, np.int64, 18), (140_000, 1 << 20, 1.0, np.int32, 19),
     (131_073, 1 << 17, 1.0, np.int32, 20), (131_072, 800_000, 1.0, np.int32, 21),
+    # the larger tile shapes (4 keys per thread above 512K ids, 8 above 1.5M)
+    # with ragged last tiles
+    (700_001, 800_000, 1.0, np.int32, 22), (1_600_003, 800_000, 1.0, np.int32, 23),
+    (1_700_001, 2**40, 0.9, np.int64, 24),
     # heads on the first item of a thread, tails several threads later (the
     # case a compiler miscompile of the dedup scan once got wrong)
     (4096, 50, 1.0, np.int32, 3), (5000, 30, 1.0, np.int32, 8),
