@@ -72,7 +72,13 @@ namespace lmz {
 #define LMZ_SEG_FIX_RF 16            // partial rows per wave in flight in the fix-up
 #endif
 
-constexpr int kSegThreads = 256;
+#ifndef LMZ_SEG_WG_THREADS
+#define LMZ_SEG_WG_THREADS 64        // threads of a main-walk workgroup (one chunk per wave)
+#endif
+#ifndef LMZ_SEG_LDS_PAD
+#define LMZ_SEG_LDS_PAD 0            // LDS bytes reserved per workgroup (caps waves per CU)
+#endif
+constexpr int kSegThreads = LMZ_SEG_WG_THREADS;
 constexpr int kSegWaves = kSegThreads / kWave;
 constexpr int kMinR = 32, kMaxR = 512;
 
@@ -508,7 +514,7 @@ constexpr int rf_for() {
 
 template <typename GT, int VEC, int NV, int R>
 static void launch_one(const SegArgs& a, dim3 grid, hipStream_t st) {
-  k_segsum<GT, VEC, NV, rf_for<NV, R>(), R, t_for<R>()><<<grid, kSegThreads, 0, st>>>(a);
+  k_segsum<GT, VEC, NV, rf_for<NV, R>(), R, t_for<R>()><<<grid, kSegThreads, LMZ_SEG_LDS_PAD, st>>>(a);
 }
 
 template <typename GT, int VEC, int NV>
