@@ -241,6 +241,63 @@ def test_segsum_chunks_inside_short_segments(lz, gdt):
     assert err <= (H.TOL_BF16 if gdt == "bf16" else H.TOL_F32)
 
 
+def _piece_counts(ids, V, rw):
+    """Host restatement of the walk's cost partition (a position costs rw,
+    a segment end 16; R the power of two near K/1024 in 32..512, T = R/4):
+    for every segment of at least T rows that spans chunks, the number of
+    chunks after its first that it reaches, and its first chunk."""
+    K = len(ids)
+    _, c = np.unique(ids, return_counts=True)
+    U = len(c)
+    off = np.concatenate([[0], np.cumsum(c)])
+    R = 32
+    while R < (K + 1023) // 1024 and R < 512:
+        R *= 2
+    T, ww = R // 4, 16
+    n = -(-(rw * K + ww * min(K, V)) // (rw * R))
+    Q = -(-(rw * K + ww * U) // n)
+    f = rw * off[:-1] + ww * np.arange(U)
+    cs, ce = f // Q, np.minimum((f + rw * (c - 1)) // Q, n - 1)
+    lg = (c >= T) & (ce > cs)
+    return (ce - cs)[lg], cs[lg]
+
+
+@pytest.mark.parametrize("gdt", ["f32", "bf16"])
+def test_segsum_fixup_piece_counts(lz, gdt):
+    """Long segments of graded lengths: 1, 15 and 16 further pieces (the
+    last count summed by one wave and the first summed by a workgroup), a
+    head of more than 128 (several rounds per wave), and 8-chunk fix-up
+    groups that start both a head and a shorter long segment."""
+    rng = np.random.Generator(np.random.PCG64(3))
+    sc, lens = 45, []
+    for k in range(1, 22):
+        lens += [1] * int(rng.integers(3, 40)) + [16 + sc * k + int(rng.integers(0, sc))]
+    for _ in range(12):
+        lens += [1] * int(rng.integers(3, 40)) + [int(rng.integers(sc + 20, 2 * sc)),
+                                                 int(rng.integers(17 * sc, 20 * sc))]
+    lens += [1] * 20 + [135 * sc]
+    lens += [1] * (60_000 - sum(lens))
+    ids = rng.permutation(np.repeat(np.arange(len(lens)) * 7 + 3, lens)).astype(np.int32)
+    K, V, D = len(ids), 800_000, 96
+    P, cs = _piece_counts(ids, V, 4 if gdt == "bf16" else 8)
+    grp = cs // 8
+    assert {1, 15, 16} <= set(P.tolist()) and P.max() > 128
+    assert any((P[grp == g] >= 16).any() and (P[grp == g] < 16).any() for g in set(grp.tolist()))
+    _say(f"segsum fix-up piece counts K={K} {gdt}: {len(P)} long segments, max {P.max()} pieces")
+    g32 = synth.normal_rows(K, D, 91)
+    grad = synth.bf16_bits(g32) if gdt == "bf16" else g32
+    tgrad = _t(g32).to(torch.bfloat16) if gdt == "bf16" else _t(g32)
+    res = lz.unique(_t(ids), V)
+    out = lz.segsum(tgrad, res.perm, res.inverse, res.offsets, res.num_unique, dev_err=res.dev_err)
+    torch.cuda.synchronize()
+    lz.check(res.dev_err)
+    o = H.assert_unique_matches(res, ids, V, oracle)
+    U = len(o[0])
+    ref = oracle.segsum(grad, o[3], U)
+    err = H.row_rel_err(out[:U].double().cpu().numpy(), ref, H.sum_of_squares(grad, o[3], U, oracle))
+    assert err <= (H.TOL_BF16 if gdt == "bf16" else H.TOL_F32)
+
+
 def test_segsum_deterministic(lz):
     a = _segsum_case(lz, 60_000, 500, 1.2, 1024, "f32", 51)[3].clone()
     b = _segsum_case(lz, 60_000, 500, 1.2, 1024, "f32", 51)[3]
