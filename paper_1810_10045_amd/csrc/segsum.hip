@@ -7,19 +7,19 @@
 //   read (rw) and a segment end one row write (ww, weighted for writes
 //   costing more than reads of the same size), so the cost before position p
 //   of segment u is rw * p + ww * u; chunk c starts where that reaches c * Q,
-//   Q = ceil((rw * K + ww * U) / N). Reads and writes
-//   thus balance across waves wherever the heads and the tail of the Zipf
-//   law fall in the sorted order (equal-length chunks left the waves of the
-//   tail, one write per row, twice as long as those of the heads). A wave
-//   finds its bounds with a 32-ary search of offsets, two targets at once.
-//   The search ends at the segments holding the two bounds, which tells the
-//   wave where the first and last segment of its chunk begin and end. The
-//   segment (type) of a position is inverse[perm[i]], so a wave learns
-//   every other segment boundary of its chunk from two gathers and a
-//   ballot, without searching. A segment shorter than T rows belongs entirely to the
-//   chunk holding its first position, even where it runs past the chunk
-//   end; a longer one is cut at chunk boundaries and every chunk sums its
-//   piece into a partial row:
+//   Q = ceil((rw * K + ww * U) / N). Reads and writes thus balance across
+//   waves wherever the heads and the tail of the Zipf law fall in the sorted
+//   order (equal-length chunks left the waves of the tail, one write per row,
+//   twice as long as those of the heads). A wave finds its bounds with a
+//   32-ary search of offsets, two targets at once. The search ends at the
+//   segments holding the two bounds, which tells the wave where the first
+//   and last segment of its chunk begin and end. The segment (type) of a
+//   position is inverse[perm[i]], so a wave learns every other segment
+//   boundary of its chunk from two gathers and a ballot, without searching.
+//   A segment shorter than T rows belongs entirely to the chunk holding its
+//   first position, even where it runs past the chunk end; a longer one is
+//   cut at chunk boundaries and every chunk sums its piece into a partial
+//   row:
 //     part_start[c]  the piece of a long segment that starts in chunk c and
 //                    continues past it (desc[c] names that segment),
 //     part_cont[c]   the piece of a long segment that started before chunk c.
