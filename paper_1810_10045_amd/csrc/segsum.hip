@@ -36,6 +36,8 @@
 // Each wave gathers whole 16-byte column vectors of RF rows at a time
 // (RF x NV x 1 KiB in flight), adds them in fp32 registers and writes a row
 // as soon as its segment ends; grad is streamed with non-temporal loads.
+#include <atomic>
+
 #include "common.hpp"
 
 namespace lmz {
@@ -75,6 +77,9 @@ namespace lmz {
 #ifndef LMZ_SEG_WG_THREADS
 #define LMZ_SEG_WG_THREADS 64        // threads of a main-walk workgroup (one chunk per wave)
 #endif
+#ifndef LMZ_SEG_FUSED
+#define LMZ_SEG_FUSED 1              // fix-up workgroups in the walk's launch (one column tile)
+#endif
 #ifndef LMZ_SEG_LDS_PAD
 #define LMZ_SEG_LDS_PAD 0            // LDS bytes reserved per workgroup (caps waves per CU)
 #endif
@@ -97,13 +102,16 @@ struct SegArgs {
   float* part_start;
   int32_t* desc;
   int32_t* npieces;
+  uint64_t* flags;   // fused launch: flags[c] == epoch once chunk c's descriptor and
+  uint64_t epoch;    // partial rows are visible to every workgroup
+  int main_blocks, fix_tiles, fused;
   int R, nchunks, rw, ww;  // cost of a position / of a segment end
   int32_t* dev_err;
 };
 
 struct SegLayout {
   int R, max_chunks;
-  size_t cont, start, desc, npieces, total;
+  size_t cont, start, desc, npieces, flags, total;
 };
 
 static inline size_t a256(size_t x) { return (x + 255) & ~size_t(255); }
@@ -131,6 +139,7 @@ static SegLayout seg_layout(int64_t K, int64_t D) {
   L.start = off;    off += a256(n * D * 4);
   L.desc = off;     off += a256(n * 4);
   L.npieces = off;  off += a256(n * 4);
+  L.flags = off;    off += a256(n * 8);
   L.total = off;
   return L;
 }
@@ -190,8 +199,168 @@ __device__ __forceinline__ void chunk_bounds(const int32_t* __restrict__ offsets
   B = Bound{read_lane(b, 32), read_lane(u, 32), read_lane(o0, 32), read_lane(o1, 32)};
 }
 
-template <typename GT, int VEC, int NV, int RF, int R, int T>
-__global__ __launch_bounds__(kSegThreads) void k_segsum(SegArgs a) {
+// ---------------------------------------------------------------------------
+// Fused launch: fix-up workgroups after the walk's in the same grid.
+// Workgroups are dispatched in the order of their index (per XCD), so every
+// walk workgroup holds a slot or has finished before a fix-up workgroup
+// starts; walk workgroups never wait, so a fix-up's wait for their flags
+// always ends (bounded all the same: LM_DEVERR_SPIN). Partial rows and
+// descriptors go out as agent-scope stores (coherent across the XCDs'
+// L2s), the walk waits for them before it sets its flag to the call's
+// epoch, and the fix-up reads them with agent-scope loads once the flag
+// holds that epoch: no workspace contents need clearing between calls.
+// ---------------------------------------------------------------------------
+constexpr int kFusedThreads = 256;
+constexpr int kFusedWaves = kFusedThreads / kWave;
+#ifndef LMZ_SEG_FUSED_SPAN
+#define LMZ_SEG_FUSED_SPAN 4         // chunks a fused fix-up workgroup looks after (<= 64)
+#endif
+#ifndef LMZ_SEG_FUSED_RF
+#define LMZ_SEG_FUSED_RF 8           // pieces per wave per round in the fused fix-up
+#endif
+#ifndef LMZ_SEG_FUSED_SLEEP
+#define LMZ_SEG_FUSED_SLEEP 8        // s_sleep argument (x 64 cycles) between flag polls
+#endif
+constexpr int kFusedSpan = LMZ_SEG_FUSED_SPAN;
+constexpr int kFusedCols = kWave * 4;  // columns of a fused fix-up tile
+static_assert(kFusedSpan <= kWave, "one descriptor per lane");
+
+template <int VEC>
+__device__ __forceinline__ void store_vec_agent(float* p, const float* v) {
+  static_assert(VEC % 2 == 0, "pairs of fp32 values");
+#pragma unroll
+  for (int i = 0; i < VEC; i += 2)
+    st_agent(reinterpret_cast<uint64_t*>(p + i),
+             uint64_t(__float_as_uint(v[i])) | (uint64_t(__float_as_uint(v[i + 1])) << 32));
+}
+
+__device__ __forceinline__ void load4_agent(const float* p, float* v) {
+  const uint64_t x = ld_agent(reinterpret_cast<const uint64_t*>(p));
+  const uint64_t y = ld_agent(reinterpret_cast<const uint64_t*>(p) + 1);
+  v[0] = __uint_as_float(static_cast<uint32_t>(x));
+  v[1] = __uint_as_float(static_cast<uint32_t>(x >> 32));
+  v[2] = __uint_as_float(static_cast<uint32_t>(y));
+  v[3] = __uint_as_float(static_cast<uint32_t>(y >> 32));
+}
+
+// Every lane of the wave calls this; the lanes with need wait until
+// flags[idx] holds the epoch. False if the wait gave up.
+__device__ __forceinline__ bool wait_flags(const SegArgs& a, int idx, bool need) {
+  for (uint32_t spin = 0;; ++spin) {
+    const bool ok = !need || ld_agent(a.flags + idx) == a.epoch;
+    if (!ballot(!ok)) return true;
+    if (spin >= kSpinLimit) {
+      if (lane_id() == 0) raise_err(a.dev_err, LM_DEVERR_SPIN);
+      return false;
+    }
+    __builtin_amdgcn_s_sleep(LMZ_SEG_FUSED_SLEEP);
+  }
+}
+
+// Fix-up workgroup f: chunks [c0, c0 + kFusedSpan) of span f / fix_tiles,
+// columns of tile f % fix_tiles. It waits for the span's descriptors, then
+// sums each long segment that starts there as k_segsum_fix does (one wave
+// for fewer than 16 further pieces, all waves and an LDS combine for a
+// head), waiting for each piece's flag before loading it.
+__device__ __forceinline__ void fused_fix(const SegArgs& a) {
+  constexpr int RF = LMZ_SEG_FUSED_RF;
+  constexpr int kShortMax = 16;  // further pieces below this: one wave
+  __shared__ float s_part[kFusedWaves][kFusedCols];
+  const int lane = lane_id();
+  const int wave = first_lane(static_cast<int>(threadIdx.x >> 6));
+  const int f = static_cast<int>(blockIdx.x) - a.main_blocks;
+  const int c0 = (f / a.fix_tiles) * kFusedSpan;
+  const int nc = a.nchunks - c0 < kFusedSpan ? a.nchunks - c0 : kFusedSpan;
+  const int D = a.D;
+  const int col = (f % a.fix_tiles) * kFusedCols + lane * 4;
+  const int col_ld = col < D ? col : D - 4;  // past the end: a valid, unstored vector
+  const int U = first_lane(static_cast<int>(*a.num_unique));
+
+  // Wave 0 waits for the span and reads its descriptors once; every wave
+  // takes them from LDS, so all agree on the heads (and on the barriers).
+  __shared__ int s_desc[kWave], s_np[kWave];
+  const bool mine = lane < nc;
+  const int ci = c0 + (mine ? lane : 0);
+  if (wave == 0) {
+    wait_flags(a, ci, mine);
+    s_desc[lane] = mine ? ld_agent(a.desc + ci) : -1;
+    s_np[lane] = mine ? ld_agent(a.npieces + ci) : 0;
+  }
+  __syncthreads();
+  const int sd = s_desc[lane], np = s_np[lane];
+  const bool has = sd >= 0 && sd < U && sd < a.u_cap && np >= 1 && np <= a.nchunks - 1 - ci;
+  const uint64_t todo = ballot(has);
+  const uint64_t heads = ballot(has && np >= kShortMax);
+  auto piece = [&](int cs, int t) {
+    return (t == 0 ? a.part_start + static_cast<int64_t>(cs) * D
+                   : a.part_cont + static_cast<int64_t>(cs + t) * D) + col_ld;
+  };
+
+  // Shorter long segments: the j-th to wave j % kFusedWaves.
+  int j = 0;
+  for (uint64_t m = todo & ~heads; m; m &= m - 1, ++j) {
+    if (j % kFusedWaves != wave) continue;
+    const int i = __builtin_ctzll(m);
+    const int cs = c0 + i, s = read_lane(sd, i), P = read_lane(np, i);
+    wait_flags(a, cs + (lane <= P ? lane : 0), lane <= P);
+    float acc[4] = {0.f, 0.f, 0.f, 0.f};
+    for (int t0 = 0; t0 <= P; t0 += RF) {
+      float buf[RF][4];
+#pragma unroll
+      for (int r = 0; r < RF; ++r) load4_agent(piece(cs, t0 + r <= P ? t0 + r : 0), buf[r]);
+#pragma unroll
+      for (int r = 0; r < RF; ++r)
+        if (t0 + r <= P)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) acc[e] += buf[r][e];
+    }
+    if (col < D) store_vec<4>(a.out + static_cast<int64_t>(s) * a.ld_out + col, acc);
+  }
+
+  // Heads, one after the other, all waves: wave w adds pieces w, w + W, ...
+  for (uint64_t m = heads; m; m &= m - 1) {
+    const int i = __builtin_ctzll(m);
+    const int cs = c0 + i, s = read_lane(sd, i), P = read_lane(np, i);
+    float acc[4] = {0.f, 0.f, 0.f, 0.f};
+    for (int t0 = wave; t0 <= P; t0 += kFusedWaves * RF) {
+      const int tl = t0 + (lane < RF ? lane : 0) * kFusedWaves;  // lane r: piece t0 + r * W
+      wait_flags(a, cs + (tl <= P ? tl : 0), lane < RF && tl <= P);
+      float buf[RF][4];
+#pragma unroll
+      for (int r = 0; r < RF; ++r) {
+        const int t = t0 + r * kFusedWaves;
+        load4_agent(piece(cs, t <= P ? t : t0), buf[r]);
+      }
+#pragma unroll
+      for (int r = 0; r < RF; ++r)
+        if (t0 + r * kFusedWaves <= P)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) acc[e] += buf[r][e];
+    }
+#pragma unroll
+    for (int e = 0; e < 4; ++e) s_part[wave][lane * 4 + e] = acc[e];
+    __syncthreads();
+    for (int x = threadIdx.x; x < kFusedCols; x += kFusedThreads) {
+      const int cx = (f % a.fix_tiles) * kFusedCols + x;
+      if (cx < D) {
+        float sum = 0.f;
+#pragma unroll
+        for (int w = 0; w < kFusedWaves; ++w) sum += s_part[w][x];
+        a.out[static_cast<int64_t>(s) * a.ld_out + cx] = sum;
+      }
+    }
+    __syncthreads();
+  }
+}
+
+template <typename GT, int VEC, int NV, int RF, int R, int T, int NTHR, bool FUSED>
+__global__ __launch_bounds__(NTHR) void k_segsum(SegArgs a) {
+  if constexpr (FUSED) {
+    if (static_cast<int>(blockIdx.x) >= a.main_blocks) {
+      fused_fix(a);
+      return;
+    }
+  }
   using RV = RowVec<GT, VEC>;
   using raw_t = typename RV::raw_t;
   constexpr int kColsPerVec = kWave * VEC;
@@ -199,8 +368,17 @@ __global__ __launch_bounds__(kSegThreads) void k_segsum(SegArgs a) {
   constexpr int NW = windows_for<R, T>();
 
   const int lane = lane_id();
-  const int c = first_lane(blockIdx.x * kSegWaves + (threadIdx.x >> 6));  // one chunk per wave
+  const int c = first_lane(blockIdx.x * (NTHR / kWave) + (threadIdx.x >> 6));  // one chunk per wave
   if (c >= a.nchunks) return;
+  // Fused launch: once this chunk's descriptor and partial rows are visible
+  // at agent scope (written with agent-scope stores, then waited for),
+  // flags[c] says so to the fix-up workgroups.
+  auto publish = [&]() {
+    if constexpr (FUSED) {
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+      if (lane_id() == 0) st_agent(a.flags + c, a.epoch);
+    }
+  };
   const int ct = blockIdx.y;
   const int K = a.K, D = a.D;
 
@@ -210,10 +388,11 @@ __global__ __launch_bounds__(kSegThreads) void k_segsum(SegArgs a) {
   const int U = first_lane(static_cast<int>(U64 < K ? U64 : K));
   if (U < 1) {  // K > 0 always has a type: only a bad count gets here
     if (ct == 0 && lane == 0) {
-      a.desc[c] = -1;
-      a.npieces[c] = 0;
+      st_agent(a.desc + c, -1);
+      st_agent(a.npieces + c, 0);
       if (c == 0) raise_err(a.dev_err, LM_DEVERR_CAPACITY);
     }
+    publish();
     return;
   }
   const int Ub = U < a.u_cap ? U : static_cast<int>(a.u_cap);
@@ -232,9 +411,10 @@ __global__ __launch_bounds__(kSegThreads) void k_segsum(SegArgs a) {
   }
   if (p1 <= p0) {  // an empty chunk (a segment end cost more than Q)
     if (ct == 0 && lane == 0) {
-      a.desc[c] = -1;
-      a.npieces[c] = 0;
+      st_agent(a.desc + c, -1);
+      st_agent(a.npieces + c, 0);
     }
+    publish();
     return;
   }
 
@@ -257,8 +437,8 @@ __global__ __launch_bounds__(kSegThreads) void k_segsum(SegArgs a) {
       if (ce > a.nchunks - 1) ce = a.nchunks - 1;
       np = static_cast<int>(ce - c);
     }
-    a.desc[c] = starts_long && np >= 1 ? s_l : -1;
-    a.npieces[c] = np;
+    st_agent(a.desc + c, starts_long && np >= 1 ? s_l : -1);
+    st_agent(a.npieces + c, np);
   }
   // Rows this chunk sums: skip a short segment owned by the previous chunk,
   // run a short last segment to its end, stop a long one at p1.
@@ -351,13 +531,25 @@ __global__ __launch_bounds__(kSegThreads) void k_segsum(SegArgs a) {
             // is_end false here means a long last segment stopped at p1.
             const int s = read_lane(sw[w], j);
             float* dst;
+            bool part = true;
             if (s == s_f && started_before) dst = a.part_cont + static_cast<int64_t>(c) * D;
             else if (!is_end) dst = a.part_start + static_cast<int64_t>(c) * D;
-            else dst = (s >= 0 && s < a.u_cap) ? a.out + static_cast<int64_t>(s) * a.ld_out : nullptr;
+            else {
+              part = false;
+              dst = (s >= 0 && s < a.u_cap) ? a.out + static_cast<int64_t>(s) * a.ld_out : nullptr;
+            }
             if (dst) {
 #pragma unroll
-              for (int v = 0; v < NV; ++v)
-                if (col_ok[v]) store_vec<VEC>(dst + col0 + v * kColsPerVec, acc[v]);
+              for (int v = 0; v < NV; ++v) {
+                if (!col_ok[v]) continue;
+                float* d = dst + col0 + v * kColsPerVec;
+                if constexpr (FUSED) {
+                  if (part) store_vec_agent<VEC>(d, acc[v]);
+                  else store_vec<VEC>(d, acc[v]);
+                } else {
+                  store_vec<VEC>(d, acc[v]);
+                }
+              }
             }
 #pragma unroll
             for (int v = 0; v < NV; ++v)
@@ -373,6 +565,7 @@ __global__ __launch_bounds__(kSegThreads) void k_segsum(SegArgs a) {
   if (started_before) bad |= seg_before != s_f || seg_p0 != s_f;
   else bad |= seg_before == seg_p0 || seg_p0 != (p0 == A.o1 ? A.u + 1 : A.u);
   if (ballot(bad) && lane == 0) raise_err(a.dev_err, LM_DEVERR_CAPACITY);
+  publish();
 }
 
 // Sum the pieces of every long segment that spans chunks (piece 0 is
@@ -514,7 +707,16 @@ constexpr int rf_for() {
 
 template <typename GT, int VEC, int NV, int R>
 static void launch_one(const SegArgs& a, dim3 grid, hipStream_t st) {
-  k_segsum<GT, VEC, NV, rf_for<NV, R>(), R, t_for<R>()><<<grid, kSegThreads, LMZ_SEG_LDS_PAD, st>>>(a);
+  constexpr int RF = rf_for<NV, R>(), T = t_for<R>();
+  if constexpr (VEC >= 2) {
+    if (a.fused) {
+      const int fix_blocks = (a.nchunks + kFusedSpan - 1) / kFusedSpan * a.fix_tiles;
+      k_segsum<GT, VEC, NV, RF, R, T, kFusedThreads, true>
+          <<<dim3(a.main_blocks + fix_blocks), kFusedThreads, 0, st>>>(a);
+      return;
+    }
+  }
+  k_segsum<GT, VEC, NV, RF, R, T, kSegThreads, false><<<grid, kSegThreads, LMZ_SEG_LDS_PAD, st>>>(a);
 }
 
 template <typename GT, int VEC, int NV>
@@ -575,16 +777,26 @@ int segsum_run(const void* grad, int gtype, int64_t K, int64_t D, int64_t ld_gra
   a.dev_err = dev_err;
 
   const bool out_vec = al16(out) && ld_out % 4 == 0 && D % 4 == 0;
+  const bool vec = gtype == LM_F32 ? out_vec && al16(grad) && ld_grad % 4 == 0
+                                   : out_vec && al16(grad) && ld_grad % 8 == 0 && D % 8 == 0;
+  // One launch for the walk and the fix-up where the walk has one column
+  // tile (vector path, D <= 1024).
+  a.fused = LMZ_SEG_FUSED != 0 && vec && D <= 1024 && (LMZ_SEG_NV_MAX >= 4 || gtype != LM_F32);
+  if (a.fused) {
+    static std::atomic<uint64_t> epoch{0x9e3779b97f4a7c15ull};
+    a.flags = reinterpret_cast<uint64_t*>(w + L.flags);
+    a.epoch = epoch.fetch_add(1, std::memory_order_relaxed) + 1;
+    a.main_blocks = (a.nchunks + kFusedWaves - 1) / kFusedWaves;
+    a.fix_tiles = static_cast<int>((D + kFusedCols - 1) / kFusedCols);
+  }
   hipError_t e;
-  if (gtype == LM_F32) {
-    const bool vec = out_vec && al16(grad) && ld_grad % 4 == 0;
+  if (gtype == LM_F32)
     e = vec ? dispatch_nv<float, 4>(a, LMZ_SEG_NV_MAX, st) : dispatch_nv<float, 1>(a, 4, st);
-  } else {
-    const bool vec = out_vec && al16(grad) && ld_grad % 8 == 0 && D % 8 == 0;
+  else
     e = vec ? dispatch_nv<bf16_t, 8>(a, LMZ_SEG_NV_MAX < 2 ? LMZ_SEG_NV_MAX : 2, st)
             : dispatch_nv<bf16_t, 1>(a, 4, st);
-  }
   if (e != hipSuccess) return launch_status(e);
+  if (a.fused) return LM_OK;
   const uint32_t fix_blocks = static_cast<uint32_t>((a.nchunks + kFixChunks - 1) / kFixChunks);
   if (D % 4 == 0)
     k_segsum_fix<4, LMZ_SEG_FIX_RF><<<dim3(fix_blocks, (D + 255) / 256), kFixThreads, 0, st>>>(a);

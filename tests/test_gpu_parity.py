@@ -298,6 +298,27 @@ def test_segsum_fixup_piece_counts(lz, gdt):
     assert err <= (H.TOL_BF16 if gdt == "bf16" else H.TOL_F32)
 
 
+def test_segsum_workspace_reuse(lz):
+    """One workspace through calls of different shapes: each layout puts the
+    per-chunk flags of the one-launch path where another call left partial
+    rows or flags, and a call must never take an earlier call's flag for its
+    own. Each result is checked against the oracle."""
+    ws = lz.Workspace(DEV)
+    cases = [(65_536, 800_000, 1.0, 1024, "f32", 101), (20_000, 300, 1.2, 96, "f32", 102),
+             (70_000, 800_000, 1.0, 1024, "bf16", 103), (65_536, 800_000, 1.0, 1024, "f32", 104),
+             (9000, 500, 1.0, 100, "bf16", 105), (65_536, 800_000, 1.0, 1024, "f32", 101)]
+    for K, V, s, D, gdt, seed in cases:
+        _say(f"segsum workspace reuse K={K} D={D} {gdt}")
+        ids, grad, res, out = _segsum_case(lz, K, V, s, D, gdt, seed, ws=ws)
+        torch.cuda.synchronize()
+        lz.check(res.dev_err)
+        o = H.assert_unique_matches(res, ids, V, oracle)
+        U = len(o[0])
+        ref = oracle.segsum(grad, o[3], U)
+        err = H.row_rel_err(out[:U].double().cpu().numpy(), ref, H.sum_of_squares(grad, o[3], U, oracle))
+        assert err <= (H.TOL_BF16 if gdt == "bf16" else H.TOL_F32)
+
+
 def test_segsum_deterministic(lz):
     a = _segsum_case(lz, 60_000, 500, 1.2, 1024, "f32", 51)[3].clone()
     b = _segsum_case(lz, 60_000, 500, 1.2, 1024, "f32", 51)[3]
