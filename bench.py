@@ -35,6 +35,7 @@ TRAFFIC_FILE = os.path.join(ROOT, "profiles", "segsum_traffic_{workload}.md")
 SEGSUM_SRCS = [os.path.join(ROOT, "paper_1810_10045_amd", "csrc", f)
                for f in ("segsum.hip", "common.hpp")]
 COPY_BYTES = 1 << 30  # the plain copy that scales the HBM byte counters
+SEGSUM_KERNELS = "lm_segsum (k_segsum: walk and fix-up workgroups in one launch)"
 
 
 def log(msg):
@@ -365,7 +366,8 @@ def main():
                    "resident_batches": nbatch, "types_per_batch": r["U"]},
         "stages_ms": {"unique": r["stage_ms"][0], "segsum": r["stage_ms"][1],
                       w.step: r["stage_ms"][2]},
-        "roofline": {"bound": "hbm", "kernel": "lm_segsum (k_segsum + k_segsum_fix)",
+        "roofline": {"bound": "hbm", "kernel": SEGSUM_KERNELS if w.D <= 1024 else
+                     "lm_segsum (k_segsum, then k_segsum_fix)",
                      "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBPS,
                      "bytes_per_launch": r["seg_bytes"], "avg_launch_ms": r["seg_ms"],
