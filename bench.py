@@ -21,6 +21,7 @@ import hashlib
 import json
 import math
 import os
+import re
 import sys
 import time
 
@@ -43,10 +44,17 @@ def log(msg):
 
 
 def segsum_source_hash() -> str:
+    """Hash of the Seg-Sum sources' code: comments, blank lines and trailing
+    blanks left out, so that only a change of what is compiled voids the
+    recorded counters."""
     h = hashlib.sha256()
     for path in SEGSUM_SRCS:
-        with open(path, "rb") as f:
-            h.update(f.read())
+        with open(path) as f:
+            text = re.sub(r"/\*.*?\*/", "", f.read(), flags=re.S)
+        for line in text.splitlines():
+            line = re.sub(r"//.*$", "", line).rstrip()
+            if line:
+                h.update(line.encode() + b"\n")
     return h.hexdigest()[:16]
 
 

@@ -29,7 +29,9 @@
 //   sums part_start[c] and part_cont[c + 1 .. c + npieces[c]] in order: one
 //   wave per column tile for a segment of fewer than 16 further pieces, all
 //   waves of a workgroup (fixed stride split of the pieces, fixed-order
-//   combine in LDS) for a head.
+//   combine in LDS) for a head. Where the walk has one column tile, the same
+//   fix-up runs as workgroups of the walk's own launch, each waiting for the
+//   flags of the chunks it reads (the fused launch below).
 // A chunk holds at most R positions (N is sized for U = min(K, u_cap)) and
 // reads at most R + T - 1 rows.
 //
