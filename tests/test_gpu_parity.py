@@ -366,6 +366,14 @@ def test_segsum_strided_and_capacity(lz):
     lz.segsum(tw[:, :D], res.perm, res.inverse, res.offsets, res.num_unique, u_cap=10, out=small, dev_err=err)
     torch.cuda.synchronize()
     assert int(err.item()) & lz.DEVERR_CAPACITY
+    # the same on the vector path (walk and fix-up in one launch): the
+    # capacity error, and no fix-up wait that gave up
+    g64 = _t(synth.normal_rows(K, 64, 73))
+    err2 = torch.zeros(1, dtype=torch.int32, device=DEV)
+    small2 = torch.full((10, 64), 7.0, device=DEV)
+    lz.segsum(g64, res.perm, res.inverse, res.offsets, res.num_unique, u_cap=10, out=small2, dev_err=err2)
+    torch.cuda.synchronize()
+    assert int(err2.item()) == lz.DEVERR_CAPACITY
 
 
 # ---------------------------------------------------------------------------
