@@ -784,6 +784,16 @@ int segsum_run(const void* grad, int gtype, int64_t K, int64_t D, int64_t ld_gra
   // One launch for the walk and the fix-up where the walk has one column
   // tile (vector path, D <= 1024).
   a.fused = LMZ_SEG_FUSED != 0 && vec && D <= 1024 && (LMZ_SEG_NV_MAX >= 4 || gtype != LM_F32);
+  // A captured launch would replay with this call's epoch every time, and a
+  // replay could take the previous replay's flags for its own: under stream
+  // capture the fix-up is a second launch, which keeps no state across calls.
+  if (a.fused) {
+    hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
+    if (hipStreamIsCapturing(st, &cap) != hipSuccess || cap != hipStreamCaptureStatusNone) {
+      (void)hipGetLastError();
+      a.fused = 0;
+    }
+  }
   if (a.fused) {
     static std::atomic<uint64_t> epoch{0x9e3779b97f4a7c15ull};
     a.flags = reinterpret_cast<uint64_t*>(w + L.flags);

@@ -1,0 +1,77 @@
+"""lm_segsum captured in a HIP graph and replayed on changing inputs, with
+eager calls on the same workspace in between: every replay is checked
+against the oracle. (Under capture lm_segsum takes its two-launch form: the
+one-launch form tells its calls apart by a per-call value that a replay
+would repeat.)"""
+import os
+import sys
+
+import numpy as np
+import pytest
+
+sys.path.insert(0, os.path.dirname(os.path.abspath(__file__)))
+import gpu_helpers as H  # noqa: E402
+import oracle  # noqa: E402
+from paper_1810_10045_amd import synth  # noqa: E402
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+DEV = "cuda"
+
+
+@pytest.fixture(scope="module")
+def lz():
+    from paper_1810_10045_amd import lmzipf
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    return lmzipf
+
+
+def _check(out, ids, grad, V):
+    o = oracle.unique(ids, V)
+    U = len(o[0])
+    ref = oracle.segsum(grad, o[3], U)
+    err = H.row_rel_err(out[:U].double().cpu().numpy(), ref, H.sum_of_squares(grad, o[3], U, oracle))
+    assert err <= H.TOL_F32, err
+
+
+def test_segsum_graph_replays(lz):
+    K, V, D = 65_536, 800_000, 1024
+    ws = lz.Workspace(DEV)
+    ids = synth.zipf_ids(K, V, 1.0, 201, np.int32)
+    g32 = synth.normal_rows(K, D, 202)
+    res = lz.unique(torch.from_numpy(ids).to(DEV), V, ws=ws)
+    grad = torch.from_numpy(g32).to(DEV)
+    out = torch.empty((res.offsets.numel() - 1, D), dtype=torch.float32, device=DEV)
+    err = torch.zeros(1, dtype=torch.int32, device=DEV)
+    lz.segsum(grad, res.perm, res.inverse, res.offsets, res.num_unique, out=out, dev_err=err, ws=ws)
+    torch.cuda.synchronize()
+    lz.check(err)
+    _check(out, ids, g32, V)
+
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph, stream=side):
+        lz.segsum(grad, res.perm, res.inverse, res.offsets, res.num_unique, out=out, dev_err=err, ws=ws)
+    torch.cuda.synchronize()
+
+    other_ids = synth.zipf_ids(K, V, 1.0, 299, np.int32)
+    other_grad = torch.from_numpy(synth.normal_rows(K, D, 298)).to(DEV)
+    for i, seed in enumerate((203, 205, 207, 209, 211)):
+        print(f"graph replay with inputs of seed {seed}", flush=True)
+        ids = synth.zipf_ids(K, V, 1.0, seed, np.int32)
+        g32 = synth.normal_rows(K, D, seed + 1)
+        lz.unique(torch.from_numpy(ids).to(DEV), V, out=res, ws=ws)  # the graph's input buffers
+        grad.copy_(torch.from_numpy(g32))
+        out.fill_(float("nan"))
+        if i % 2:
+            # eager Seg-Sum on the same workspace between two replays (the
+            # others follow each other with only new inputs in between)
+            r2 = lz.unique(torch.from_numpy(other_ids).to(DEV), V, ws=ws)
+            lz.segsum(other_grad, r2.perm, r2.inverse, r2.offsets, r2.num_unique, dev_err=err, ws=ws)
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        lz.check(err)
+        _check(out, ids, g32, V)
