@@ -22,8 +22,8 @@
  * - Every pointer named as a device buffer is device memory (hipMalloc or a
  *   torch CUDA tensor); host pointers are never accepted for those.
  * - The caller owns every buffer. The library allocates nothing, keeps no
- *   pointer past the call, and holds no global state; all work is enqueued
- *   on `stream` (a hipStream_t; NULL is the default stream) and the call
+ *   pointer past the call, and holds no global state but one per-process
+ *   call counter (lm_segsum); all work is enqueued on `stream` (a hipStream_t; NULL is the default stream) and the call
  *   returns without synchronising.
  * - Counts that the GPU computes (num_unique, n_src, ...) stay on the device.
  *   Grids are sized from the host-side capacities (K, u_cap, ...), and the
@@ -148,6 +148,13 @@ int lm_unique(const void* ids, int32_t idtype, int64_t K, int64_t V,
  * dev_err    device int32, zeroed by the caller.
  * ws         device workspace of lm_segsum_workspace_bytes(K, D) bytes,
  *            256-byte aligned; no initial contents are required.
+ *
+ * With D <= 1024 on the 16-byte vector path, the segments that span the
+ * walk's chunks are summed by workgroups of the same launch, which wait for
+ * per-chunk flags tagged with a per-call value from a process-wide counter
+ * (bounded waits; LM_DEVERR_SPIN if one gave up, which a correct call never
+ * does). Otherwise, and always while `stream` is being captured into a
+ * graph (a replay would repeat the tag), they are summed by a second launch.
  * ------------------------------------------------------------------------ */
 size_t lm_segsum_workspace_bytes(int64_t K, int64_t D);
 int lm_segsum(const void* grad, int32_t gtype, int64_t K, int64_t D,
