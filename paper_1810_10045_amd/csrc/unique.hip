@@ -67,8 +67,25 @@ static inline int items_for(int64_t K, int nt) {
   return K <= LMZ_UNIQUE_LARGE_ITEMS2_MAX_K ? 2 : (K <= LMZ_UNIQUE_LARGE_ITEMS4_MAX_K ? 4 : 8);
 }
 constexpr int kHistItems = 16;             // keys per thread per histogram round
-constexpr int kHistKeysPerBlock = 1 << 12;
-constexpr int kMaxHistBlocks = 64;
+// Histogram workgroups: about K / 2048 of them, 8 to 32, up to 2^18 ids
+// (measured best: 8 at 8K ids, 32 at 64K and 262K), 64 above (larger
+// blocks serialise on LDS atomics at the Zipf heads).
+#ifndef LMZ_UNIQUE_HIST_RULE
+#define LMZ_UNIQUE_HIST_RULE 1
+#endif
+#ifndef LMZ_UNIQUE_HIST_KEYS
+#define LMZ_UNIQUE_HIST_KEYS 4096      // ids per histogram workgroup without the rule
+#endif
+constexpr int kHistKeysPerBlock = LMZ_UNIQUE_HIST_KEYS;
+static inline int hist_blocks_for(int64_t K) {
+  if (LMZ_UNIQUE_HIST_RULE) {
+    if (K > (int64_t(1) << 18)) return 64;
+    const int64_t b = K / 2048;
+    return static_cast<int>(b < 8 ? 8 : (b > 32 ? 32 : b));
+  }
+  const int64_t hb = (K + kHistKeysPerBlock - 1) / kHistKeysPerBlock;
+  return static_cast<int>(hb < 1 ? 1 : (hb > 64 ? 64 : hb));
+}
 
 // Status words of the sort look-back: 2-bit flag | 30-bit count.
 constexpr uint32_t kFlagAgg = 1u << 30, kFlagPrefix = 2u << 30, kValMask = (1u << 30) - 1;
@@ -115,8 +132,7 @@ static UniqueLayout unique_layout(int64_t K, int idtype, int64_t V) {
   L.items = items_for(K, L.nt);
   const int64_t tile_keys = int64_t(L.nt) * L.items;
   L.tiles = static_cast<int>((K + tile_keys - 1) / tile_keys);
-  const int64_t hb = (K + kHistKeysPerBlock - 1) / kHistKeysPerBlock;
-  L.hist_blocks = static_cast<int>(hb < 1 ? 1 : (hb > kMaxHistBlocks ? kMaxHistBlocks : hb));
+  L.hist_blocks = hist_blocks_for(K);
   size_t off = 0;
   L.rstride = 1 << kSmallDigitBits;
   for (int p = 0; p < L.passes; ++p)
@@ -240,18 +256,20 @@ __global__ __launch_bounds__(NT) void k_onesweep(
 #pragma unroll
   for (int i = 0; i < DPT; ++i) dig_total[i] = 0;
   if (owner) {
-    // 16 rows in flight per round: one round for up to 64K keys.
-    for (int b = 0; b < hist_blocks; b += 16) {
-      uint32_t h[16][DPT];
+    // Rows in flight per round: 16 with 256-thread tiles (at most 32 rows),
+    // 32 with 1024-thread tiles (32 or 64 rows).
+    constexpr int kHistRows = NT == 256 ? 16 : 32;
+    for (int b = 0; b < hist_blocks; b += kHistRows) {
+      uint32_t h[kHistRows][DPT];
 #pragma unroll
-      for (int r = 0; r < 16; ++r)
+      for (int r = 0; r < kHistRows; ++r)
 #pragma unroll
         for (int i = 0; i < DPT; ++i) {
           const int br = b + r < hist_blocks ? b + r : b;  // repeat a valid row, unused
           h[r][i] = bhist[size_t(br) * hist_stride + tid * DPT + i];
         }
 #pragma unroll
-      for (int r = 0; r < 16; ++r)
+      for (int r = 0; r < kHistRows; ++r)
 #pragma unroll
         for (int i = 0; i < DPT; ++i) dig_total[i] += b + r < hist_blocks ? h[r][i] : 0u;
     }
