@@ -5,8 +5,10 @@ Tensors are torch CUDA tensors (PyTorch supplies device memory and the
 current stream); nothing here computes on the host. If the library has not
 been built, importing this module raises — there is no fallback path.
 
-Entry points have the C names without the ``lm_`` prefix:
-``unique``, ``segsum``, ``map_ids``, ``fill_values``, ``sparse_apply``.
+Entry points have the C names without the ``lm_`` prefix: ``unique``,
+``segsum``, ``map_ids``, ``fill_values``, ``sparse_apply``, the binary16
+payload forms ``fill_values_f16`` and ``sparse_apply_f16``, and
+``sample_ids``.
 """
 from __future__ import annotations
 
