@@ -7,14 +7,11 @@
 //   k_hist      digit histograms of every radix pass in one read of the ids,
 //               one row per workgroup (4096 ids each, at most 64 rows); also
 //               clears this call's tile tickets and look-back status words.
-//   k_onesweep  one LSD radix pass over a digit of up to 8 bits (the
-//               ceil(log2 V) key bits are split evenly over the fewest
-//               passes; 8-bit digits measured faster per key bit than 10- or
-//               11-bit ones, whose counters and look-back cost twice as
-//               much per pass). A workgroup of NT threads (256 for inputs
-//               of up to LMZ_UNIQUE_SMALL_TILE_MAX_K keys, so that they
-//               spread over more CUs, else 1024) ranks a tile of 4 * NT
-//               keys (4 per thread) with
+//   k_onesweep  one LSD radix pass over a digit (the ceil(log2 V) key bits
+//               are split evenly over the fewest passes). A workgroup of NT
+//               threads (256 for inputs of up to LMZ_UNIQUE_SMALL_TILE_MAX_K
+//               keys, so that they spread over more CUs, else 1024) ranks a
+//               tile of ITEMS * NT keys with
 //               wave64 ballot matching, publishes its per-digit counts,
 //               learns the counts of the tiles before it through a decoupled
 //               look-back, reorders the tile in LDS and writes it out in
@@ -35,7 +32,7 @@ namespace lmz {
 
 constexpr int kHistThreads = 1024;
 #ifndef LMZ_UNIQUE_SMALL_TILE_MAX_K
-#define LMZ_UNIQUE_SMALL_TILE_MAX_K (1 << 17)  // up to this K, 256-thread tiles
+#define LMZ_UNIQUE_SMALL_TILE_MAX_K (1 << 14)  // up to this K, 256-thread tiles
 #endif
 #ifndef LMZ_UNIQUE_DIGIT_BITS
 #define LMZ_UNIQUE_DIGIT_BITS 8        // widest digit with 256-thread tiles
@@ -52,7 +49,8 @@ constexpr int kMaxPasses = 8;              // ceil(64 / 8)
 // Keys per thread of a sort or dedup tile, by input size: bigger tiles mean
 // fewer tiles for the look-back to pass, smaller ones spread a small input
 // over more CUs. Measured best: with 256-thread tiles, 2 keys up to 16K ids
-// and 4 above; with 1024-thread tiles, 2 up to 512K, 4 up to 1.5M, 8 above.
+// (4 above, where 256-thread tiles are no longer the default); with
+// 1024-thread tiles, 2 up to 512K, 4 up to 1.5M, 8 above.
 #ifndef LMZ_UNIQUE_SMALL_ITEMS2_MAX_K
 #define LMZ_UNIQUE_SMALL_ITEMS2_MAX_K (1 << 14)
 #endif
@@ -112,10 +110,12 @@ static UniqueLayout unique_layout(int64_t K, int idtype, int64_t V) {
   UniqueLayout L{};
   const size_t ks = idtype == LM_I64 ? 8 : 4;
   L.bits = key_bits_for(V);
-  // Workgroups of 256 threads (tiles of 1024 keys) spread a small input over
-  // more CUs; large inputs take 1024-thread tiles, which keep the look-back
-  // status arrays (one word per digit and tile) 4x smaller and can afford
-  // wider digits where that saves a pass.
+  // Workgroups of 256 threads take 8-bit digits; 1024-thread workgroups take
+  // digits of up to 10 bits where that saves a pass (20-bit keys: two passes
+  // instead of three), with fewer tiles for the look-back to pass. Measured
+  // per call: 256-thread tiles are faster up to 16K ids (4K ids at V = 800K:
+  // 26 against 29 us), 1024-thread tiles above (64K ids: 37 against 43 us;
+  // 131K ids: 43 against 51 us).
   L.nt = K <= LMZ_UNIQUE_SMALL_TILE_MAX_K ? 256 : 1024;
   const int narrow = kSmallDigitBits < kLargeDigitBits ? kSmallDigitBits : kLargeDigitBits;
   const int widest = L.nt == 256 ? kSmallDigitBits : kLargeDigitBits;

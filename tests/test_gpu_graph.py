@@ -1,8 +1,9 @@
-"""lm_segsum captured in a HIP graph and replayed on changing inputs, with
-eager calls on the same workspace in between: every replay is checked
-against the oracle. (Under capture lm_segsum takes its two-launch form: the
-one-launch form tells its calls apart by a per-call value that a replay
-would repeat.)"""
+"""lm_unique and lm_segsum captured in HIP graphs and replayed on changing
+inputs, with eager calls on the same workspace in between: every replay is
+checked against the oracle. (Under capture lm_segsum takes its two-launch
+form: the one-launch form tells its calls apart by a per-call value that a
+replay would repeat. lm_unique's first kernel clears the tile tickets and
+status words that its later kernels use, inside the graph as well.)"""
 import os
 import sys
 
@@ -75,3 +76,38 @@ def test_segsum_graph_replays(lz):
         torch.cuda.synchronize()
         lz.check(err)
         _check(out, ids, g32, V)
+
+
+def test_unique_graph_replays(lz):
+    K, V = 65_536, 800_000
+    ws = lz.Workspace(DEV)
+    ids_dev = torch.from_numpy(synth.zipf_ids(K, V, 1.0, 301, np.int32)).to(DEV)
+    res = lz.unique(ids_dev, V, ws=ws)
+    torch.cuda.synchronize()
+    lz.check(res.dev_err)
+
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph, stream=side):
+        lz.unique(ids_dev, V, out=res, ws=ws)
+    torch.cuda.synchronize()
+
+    other = torch.from_numpy(synth.zipf_ids(K // 2 + 7, V, 1.0, 399, np.int32)).to(DEV)
+    for i, seed in enumerate((303, 305, 307, 309)):
+        print(f"unique graph replay with ids of seed {seed}", flush=True)
+        ids = synth.zipf_ids(K, V, 1.0, seed, np.int32)
+        ids_dev.copy_(torch.from_numpy(ids))
+        res.perm.fill_(-1)
+        res.inverse.fill_(-1)
+        if i % 2:
+            # an eager call on the same workspace between replays
+            r2 = lz.unique(other, V, ws=ws)
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        lz.check(res.dev_err)
+        H.assert_unique_matches(res, ids, V, oracle, f"replay {i}")
+        if i % 2:
+            lz.check(r2.dev_err)
+            H.assert_unique_matches(r2, other.cpu().numpy(), V, oracle, f"eager {i}")

@@ -76,11 +76,13 @@ UNIQUE_CASES = [
     (262_144 + 77, 2_000_000, 0.9, np.int64, 13), (50_000, 2**31 - 1, 0.8, np.int32, 14),
     (30_001, 2**40, 0.9, np.int64, 15), (12_345, 256, 0.5, np.int32, 16),
     (20_000, 257, 1.0, np.int64, 17),
-    # 1024-thread tiles from 2^17 + 1 keys: 10-bit digits where they save a
+    # 1024-thread tiles from 2^14 + 1 keys: 10-bit digits where they save a
     # pass (40-bit int64 keys: 4 passes of 10; 20 bits: 2 of 10; 17 bits: a
     # 9-bit and an 8-bit pass), and the last K that still takes small tiles
     (150_001, 2**40, 0.9, np.int64, 18), (140_000, 1 << 20, 1.0, np.int32, 19),
     (131_073, 1 << 17, 1.0, np.int32, 20), (131_072, 800_000, 1.0, np.int32, 21),
+    (16_385, 1 << 17, 1.0, np.int32, 25), (16_384, 800_000, 1.0, np.int32, 26),
+    (16_385, 2**40, 0.9, np.int64, 27), (16_383, 2**40, 0.9, np.int64, 28),
     # the larger tile shapes (4 keys per thread above 512K ids, 8 above 1.5M)
     # with ragged last tiles
     (700_001, 800_000, 1.0, np.int32, 22), (1_600_003, 800_000, 1.0, np.int32, 23),
