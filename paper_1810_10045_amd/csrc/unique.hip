@@ -2,7 +2,9 @@
 // ascending order, with counts, CSR offsets, the token->type map and the
 // stable sort permutation.
 //
-// Pipeline (all on one stream, no host sync; the only atomics are the tile
+// Inputs of up to LMZ_UNIQUE_BLOCK_MAX_K ids take one workgroup that holds
+// every key in LDS (k_unique_block, below). Larger inputs take a pipeline of
+// kernels (all on one stream, no host sync; the only atomics are the tile
 // tickets):
 //   k_hist      digit histograms of every radix pass in one read of the ids,
 //               one row per workgroup (4096 ids each, at most 64 rows); also
@@ -39,6 +41,10 @@ constexpr int kHistThreads = 1024;
 #endif
 #ifndef LMZ_UNIQUE_DIGIT_BITS_LARGE
 #define LMZ_UNIQUE_DIGIT_BITS_LARGE 10 // widest digit with 1024-thread tiles
+#endif
+constexpr int kBlockThreadsHost = 1024;  // threads of k_unique_block
+#ifndef LMZ_UNIQUE_BLOCK_MAX_K
+#define LMZ_UNIQUE_BLOCK_MAX_K 8192    // up to this K, one workgroup does it all
 #endif
 #ifndef LMZ_UNIQUE_LOOKBACK_W
 #define LMZ_UNIQUE_LOOKBACK_W 4        // predecessor tiles a look-back round reads
@@ -94,6 +100,7 @@ constexpr uint64_t kD31 = (1ull << 31) - 1;
 struct UniqueLayout {
   size_t bhist, tickets, status, dstatus, keys0, keys1, vals0, vals1, total;
   int passes, bits, tiles, hist_blocks, nt, items;
+  int block_items;  // > 0: one workgroup (k_unique_block) with this many keys per thread
   int rstride;  // digit slots per pass in the histogram rows and status arrays
   int shift[kMaxPasses], nbits[kMaxPasses];
 };
@@ -117,8 +124,15 @@ static UniqueLayout unique_layout(int64_t K, int idtype, int64_t V) {
   // 26 against 29 us), 1024-thread tiles above (64K ids: 37 against 43 us;
   // 131K ids: 43 against 51 us).
   L.nt = K <= LMZ_UNIQUE_SMALL_TILE_MAX_K ? 256 : 1024;
+  // One workgroup holds up to 1024 * 8 keys (8 per thread keep the ranking
+  // and dedup state in registers).
+  L.block_items = 0;
+  if (K <= LMZ_UNIQUE_BLOCK_MAX_K && K <= 8 * kBlockThreadsHost) {
+    L.block_items = 1;
+    while (int64_t(L.block_items) * 1024 < K) L.block_items *= 2;
+  }
   const int narrow = kSmallDigitBits < kLargeDigitBits ? kSmallDigitBits : kLargeDigitBits;
-  const int widest = L.nt == 256 ? kSmallDigitBits : kLargeDigitBits;
+  const int widest = L.nt == 256 || L.block_items ? kSmallDigitBits : kLargeDigitBits;
   const int p_narrow = (L.bits + narrow - 1) / narrow, p_wide = (L.bits + widest - 1) / widest;
   L.passes = L.bits == 0 ? 1 : (p_wide < p_narrow ? p_wide : p_narrow);
   // Split the key bits evenly: the low passes take the extra bit.
@@ -570,6 +584,190 @@ __global__ __launch_bounds__(NT) void k_dedup(
   if (ballot(over) && lane_id() == 0) raise_err(dev_err, LM_DEVERR_CAPACITY);
 }
 
+// ---------------------------------------------------------------------------
+// k_unique_block: the whole of Unique in one workgroup of 1024 threads, for
+// inputs of up to 1024 * ITEMS keys. The keys stay in LDS through every
+// radix pass (8-bit digits, ranked by wave64 ballot matching as in
+// k_onesweep, with digit offsets from a block scan instead of a look-back)
+// and through the dedup (run heads by ballot, a scan of the head counts
+// over the 16 waves), so the call is one launch with no waits between
+// workgroups: a small batch is bound by latency, not by bytes. The inverse
+// map, the type ids and the offsets are staged in LDS and written out
+// coalesced: one CU issuing a scattered 4-byte store per token took longer
+// than all the passes.
+// ---------------------------------------------------------------------------
+constexpr int kBlockThreads = kBlockThreadsHost;
+constexpr int kBlockWaves = kBlockThreads / kWave;
+
+template <typename KeyT, int ITEMS>
+__global__ __launch_bounds__(kBlockThreads) void k_unique_block(
+    const KeyT* __restrict__ ids, int K, uint64_t V, int passes, PassBits pb, int cap,
+    KeyT* __restrict__ uniq, int32_t* __restrict__ counts, int32_t* __restrict__ offsets,
+    int32_t* __restrict__ inverse, int32_t* __restrict__ perm, int64_t* __restrict__ num_unique,
+    int32_t* __restrict__ dev_err) {
+  constexpr int RB = kSmallDigitBits, kRadix = 1 << RB;
+  constexpr int kN = kBlockThreads * ITEMS;
+  __shared__ KeyT s_keys[kN];
+  __shared__ int32_t s_vals[kN + 1];                // + 1: the end offset of the last type
+  __shared__ uint16_t s_cnt[kBlockWaves][kRadix];  // per-wave digit counts, then offsets
+  __shared__ uint32_t s_start[kRadix];             // first sorted position of each digit
+  __shared__ uint32_t s_scan[kBlockWaves];
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = first_lane(tid >> 6);
+
+  // Item i of a lane is position wave * 64 * ITEMS + i * 64 + lane: (wave, i,
+  // lane) order is position order, which keeps every pass stable.
+  KeyT key[ITEMS];
+  int32_t val[ITEMS];
+  bool bad = false;
+#pragma unroll
+  for (int i = 0; i < ITEMS; ++i) {
+    const int pos = wave * (ITEMS * kWave) + i * kWave + lane;
+    key[i] = pos < K ? ids[pos] : KeyT(0);
+    val[i] = pos;
+    bad |= pos < K && key_bits(key[i]) >= V;
+  }
+  if (ballot(bad) && lane == 0) raise_err(dev_err, LM_DEVERR_ID_RANGE);
+
+  for (int p = 0; p < passes; ++p) {
+    const int shift = pb.shift[p], nbits = pb.nbits[p];
+    const uint32_t mask = nbits > 0 ? (1u << nbits) - 1 : 0u;
+    for (int j = tid; j < kBlockWaves * kRadix / 2; j += kBlockThreads)
+      reinterpret_cast<uint32_t*>(&s_cnt[0][0])[j] = 0;
+    __syncthreads();
+    uint32_t dig[ITEMS], rank[ITEMS];
+#pragma unroll
+    for (int i = 0; i < ITEMS; ++i) {
+      const int pos = wave * (ITEMS * kWave) + i * kWave + lane;
+      dig[i] = pos < K ? digit_of(key[i], shift, mask) : kRadix;
+    }
+    // Rank every key among the equal-digit keys before it in its wave.
+#pragma unroll
+    for (int i = 0; i < ITEMS; ++i) {
+      const bool ok = dig[i] < kRadix;
+      uint64_t peers = ballot(ok);
+#pragma unroll
+      for (int b = 0; b < RB; ++b) {
+        if (b < nbits) {
+          const bool bit = (dig[i] >> b) & 1u;
+          const uint64_t bb = ballot(bit);
+          peers &= bit ? bb : ~bb;
+        }
+      }
+      uint32_t prior = 0;
+      if (ok) prior = s_cnt[wave][dig[i]];
+      const uint32_t below = popc_below(peers);
+      rank[i] = prior + below;
+      if (ok && below == 0) s_cnt[wave][dig[i]] = static_cast<uint16_t>(prior + __popcll(peers));
+    }
+    __syncthreads();
+    // Thread d < kRadix: per-wave offsets within digit d and its total; a
+    // block scan of the totals gives each digit's first sorted position.
+    uint32_t tot = 0;
+    if (tid < kRadix) {
+#pragma unroll
+      for (int w = 0; w < kBlockWaves; ++w) {
+        const uint32_t c = s_cnt[w][tid];
+        s_cnt[w][tid] = static_cast<uint16_t>(tot);
+        tot += c;
+      }
+    }
+    uint32_t all;
+    const uint32_t start = block_excl_sum<kBlockWaves, uint32_t>(tot, s_scan, all);
+    if (tid < kRadix) s_start[tid] = start;
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < ITEMS; ++i) {
+      if (dig[i] < kRadix) {
+        const int dst = static_cast<int>(s_start[dig[i]] + s_cnt[wave][dig[i]] + rank[i]);
+        s_keys[dst] = key[i];
+        s_vals[dst] = val[i];
+      }
+    }
+    __syncthreads();
+    if (p + 1 < passes) {
+#pragma unroll
+      for (int i = 0; i < ITEMS; ++i) {
+        const int pos = wave * (ITEMS * kWave) + i * kWave + lane;
+        key[i] = s_keys[pos];
+        val[i] = s_vals[pos];
+      }
+      __syncthreads();  // every read done before the next pass overwrites
+    }
+  }
+
+  // Dedup, in the same (wave, i, lane) order: position pos is a run head when
+  // its key differs from the one before. The perm goes out as it is read.
+  KeyT k[ITEMS];
+  int32_t src[ITEMS];
+  uint64_t hm[ITEMS];
+  uint32_t wave_heads = 0;
+#pragma unroll
+  for (int i = 0; i < ITEMS; ++i) {
+    const int pos = wave * (ITEMS * kWave) + i * kWave + lane;
+    const bool ok = pos < K;
+    k[i] = ok ? s_keys[pos] : KeyT(0);
+    src[i] = ok ? s_vals[pos] : 0;
+    const KeyT before = ok && pos > 0 ? s_keys[pos - 1] : KeyT(0);
+    hm[i] = ballot(ok && (pos == 0 || k[i] != before));
+    wave_heads += static_cast<uint32_t>(__popcll(hm[i]));
+    if (ok) perm[pos] = src[i];
+  }
+  if (lane == 0) s_scan[wave] = wave_heads;
+  __syncthreads();  // also: every read of s_keys / s_vals is done
+  uint32_t heads_before = 0, U = 0;
+#pragma unroll
+  for (int w = 0; w < kBlockWaves; ++w) {
+    const uint32_t x = s_scan[w];
+    heads_before += w < wave ? x : 0u;
+    U += x;
+  }
+  // Types can only outnumber cap = min(K, V) when ids lie outside [0, V)
+  // (LM_DEVERR_ID_RANGE is raised then): every write stays in the buffers.
+  const int Uc = static_cast<int>(U) < cap ? static_cast<int>(U) : cap;
+  // seg[i]: the type of position pos (heads up to and including it, minus 1).
+  int seg[ITEMS];
+  uint32_t run = heads_before;
+#pragma unroll
+  for (int i = 0; i < ITEMS; ++i) {
+    const bool head = (hm[i] >> lane) & 1u;
+    seg[i] = static_cast<int>(run + popc_below(hm[i]) + (head ? 1u : 0u)) - 1;
+    run += static_cast<uint32_t>(__popcll(hm[i]));
+  }
+  // Stage the inverse map (by token) and the type ids in LDS, then write
+  // both out coalesced.
+#pragma unroll
+  for (int i = 0; i < ITEMS; ++i) {
+    const int pos = wave * (ITEMS * kWave) + i * kWave + lane;
+    if (pos < K) {
+      s_vals[src[i]] = seg[i];
+      if (((hm[i] >> lane) & 1u) && seg[i] < Uc) s_keys[seg[i]] = k[i];
+    }
+  }
+  __syncthreads();
+  for (int j = tid; j < K; j += kBlockThreads) inverse[j] = s_vals[j];
+  for (int j = tid; j < Uc; j += kBlockThreads) uniq[j] = s_keys[j];
+  __syncthreads();
+  // Stage the first position of every type, then write offsets and counts.
+#pragma unroll
+  for (int i = 0; i < ITEMS; ++i) {
+    const int pos = wave * (ITEMS * kWave) + i * kWave + lane;
+    if (pos < K && ((hm[i] >> lane) & 1u) && seg[i] <= Uc) s_vals[seg[i]] = pos;
+  }
+  if (tid == 0 && static_cast<int>(U) == Uc) s_vals[Uc] = K;
+  __syncthreads();
+  for (int j = tid; j < Uc; j += kBlockThreads) {
+    const int o = s_vals[j];
+    offsets[j] = o;
+    counts[j] = s_vals[j + 1] - o;
+  }
+  if (tid == 0) {
+    offsets[Uc] = K;
+    *num_unique = Uc;
+    if (static_cast<int>(U) > cap) raise_err(dev_err, LM_DEVERR_CAPACITY);
+  }
+}
+
 __global__ void k_unique_empty(int64_t* num_unique, int32_t* offsets) {
   if (threadIdx.x == 0) {
     *num_unique = 0;
@@ -604,6 +802,26 @@ static int run_unique(const KeyT* ids, int K, int64_t V, KeyT* uniq, int32_t* co
     k_unique_empty<<<1, 64, 0, st>>>(num_unique, offsets);
     return launch_status(hipGetLastError());
   }
+  PassBits pb{};
+  for (int p = 0; p < L.passes; ++p) {
+    pb.shift[p] = L.shift[p];
+    pb.nbits[p] = L.nbits[p];
+  }
+  const int cap = static_cast<int>(K < V ? K : V);
+  if (L.block_items > 0) {
+    auto block = [&](auto items) {
+      k_unique_block<KeyT, decltype(items)::value><<<1, kBlockThreads, 0, st>>>(
+          ids, K, static_cast<uint64_t>(V), L.passes, pb, cap, uniq, counts, offsets, inverse,
+          perm, num_unique, dev_err);
+    };
+    switch (L.block_items) {
+      case 1: block(I<1>{}); break;
+      case 2: block(I<2>{}); break;
+      case 4: block(I<4>{}); break;
+      default: block(I<8>{}); break;
+    }
+    return launch_status(hipGetLastError());
+  }
   uint32_t* bhist = reinterpret_cast<uint32_t*>(ws + L.bhist);
   uint32_t* tickets = reinterpret_cast<uint32_t*>(ws + L.tickets);
   uint32_t* status = reinterpret_cast<uint32_t*>(ws + L.status);
@@ -611,11 +829,6 @@ static int run_unique(const KeyT* ids, int K, int64_t V, KeyT* uniq, int32_t* co
   KeyT* kb[2] = {reinterpret_cast<KeyT*>(ws + L.keys0), reinterpret_cast<KeyT*>(ws + L.keys1)};
   int32_t* vb[2] = {reinterpret_cast<int32_t*>(ws + L.vals0), reinterpret_cast<int32_t*>(ws + L.vals1)};
 
-  PassBits pb{};
-  for (int p = 0; p < L.passes; ++p) {
-    pb.shift[p] = L.shift[p];
-    pb.nbits[p] = L.nbits[p];
-  }
   // tickets .. end of dstatus is contiguous: k_hist clears it.
   const int64_t clear_words = static_cast<int64_t>((L.keys0 - L.tickets) / 4);
   const size_t hist_lds = size_t(L.passes) * L.rstride * 4;
@@ -652,7 +865,6 @@ static int run_unique(const KeyT* ids, int K, int64_t V, KeyT* uniq, int32_t* co
     kin = kout;
     vin = vout;
   }
-  const int cap = static_cast<int>(K < V ? K : V);
   auto dedup = [&](auto nt, auto items) {
     constexpr int NT = decltype(nt)::value, IT = decltype(items)::value;
     k_dedup<KeyT, NT, IT><<<L.tiles, NT, 0, st>>>(kin, perm, K, cap, uniq, counts, offsets,

@@ -90,6 +90,12 @@ UNIQUE_CASES = [
     # heads on the first item of a thread, tails several threads later (the
     # case a compiler miscompile of the dedup scan once got wrong)
     (4096, 50, 1.0, np.int32, 3), (5000, 30, 1.0, np.int32, 8),
+    # the one-workgroup path: every keys-per-thread shape, its last K and the
+    # first K past it, all-distinct types filling the block, 64-bit keys
+    (1024, 1 << 20, 0.0, np.int32, 29), (1025, 100_000, 1.0, np.int32, 30),
+    (2049, 100_000, 1.0, np.int32, 31), (8192, 100_000, 1.0, np.int32, 32),
+    (8193, 100_000, 1.0, np.int32, 33), (8192, 2**40, 0.9, np.int64, 34),
+    (3000, 2**40, 0.0, np.int64, 35), (8192, 3, 1.0, np.int32, 36),
 ]
 
 
@@ -108,8 +114,9 @@ def test_unique_random(lz, K, V, s, dt, seed):
     H.assert_unique_matches(res, ids, V, oracle, f"K={K} V={V}")
 
 
-def test_unique_all_same_and_all_distinct(lz):
-    K = 9000
+@pytest.mark.parametrize("K", [9000, 8192, 1024])
+def test_unique_all_same_and_all_distinct(lz, K):
+    # 8192 and 1024: a full one-workgroup tile, every id its own type
     same = np.full(K, 4242, np.int32)
     res = lz.unique(_t(same), 5000)
     perm_ids = np.random.Generator(np.random.PCG64(5)).permutation(K).astype(np.int32)
