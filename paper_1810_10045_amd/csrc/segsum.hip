@@ -4,8 +4,8 @@
 // Work partition (no float atomics, run-to-run bit-identical):
 //   The K sorted positions are cut into N chunks of equal cost, one chunk per
 //   wave and per column tile of up to 1024 columns. A position costs one row
-//   read (rw) and a segment end one row write (ww, weighted for writes
-//   costing more than reads of the same size), so the cost before position p
+//   read (rw) and a segment end one row write (ww, weighted per gradient
+//   dtype by measurement), so the cost before position p
 //   of segment u is rw * p + ww * u; chunk c starts where that reaches c * Q,
 //   Q = ceil((rw * K + ww * U) / N). Reads and writes thus balance across
 //   waves wherever the heads and the tail of the Zipf law fall in the sorted
@@ -48,8 +48,11 @@ namespace lmz {
 #ifndef LMZ_SEG_TARGET_CHUNKS
 #define LMZ_SEG_TARGET_CHUNKS 1024   // R = the power of two near K / this (32..512)
 #endif
-#ifndef LMZ_SEG_WRITE_X2
-#define LMZ_SEG_WRITE_X2 4           // cost of a row written / a row read, times 2
+#ifndef LMZ_SEG_WRITE_X2_F32
+#define LMZ_SEG_WRITE_X2_F32 2       // fp32 rows: cost of a row written / a row read, times 2
+#endif
+#ifndef LMZ_SEG_WRITE_X2_BF16
+#define LMZ_SEG_WRITE_X2_BF16 4      // bf16 rows: the same ratio, times 2
 #endif
 #ifndef LMZ_SEG_TDIV
 #define LMZ_SEG_TDIV 4               // long-segment threshold T = R / this (1..64)
@@ -119,13 +122,22 @@ struct SegLayout {
 static inline size_t a256(size_t x) { return (x + 255) & ~size_t(255); }
 
 // Costs: a sorted position (a row read) costs rw = 2 * sizeof(grad) per
-// column, a segment end (a row written) ww = 4 * LMZ_SEG_WRITE_X2. A call
-// has at most rw * K + ww * min(K, u_cap) of it, at most rw * R per chunk.
+// column, a segment end (a row written, always fp32) ww = 4 * X2, where X2 / 2
+// is the cost of a written row relative to a read row. Measured on MI355X:
+// with fp32 rows a written row is best weighted by its bytes (X2 = 2: 1-5%
+// faster Seg-Sum than X2 = 4 on the fp32 workloads), with bf16 rows at twice
+// the bytes of a read row (X2 = 4: 3% faster than X2 = 2 on the bf16 merge).
+// A call has at most rw * K + ww * min(K, u_cap) of it, at most rw * R per
+// chunk.
 static inline int read_cost(int gtype) { return gtype == LM_BF16 ? 4 : 8; }
-constexpr int kWriteCost = 4 * LMZ_SEG_WRITE_X2;
-static inline int64_t chunks_for(int64_t K, int R, int rw, int64_t u_cap) {
+static inline int write_cost(int gtype) {
+  return 4 * (gtype == LM_BF16 ? LMZ_SEG_WRITE_X2_BF16 : LMZ_SEG_WRITE_X2_F32);
+}
+constexpr int kMaxWriteCost =
+    4 * (LMZ_SEG_WRITE_X2_BF16 > LMZ_SEG_WRITE_X2_F32 ? LMZ_SEG_WRITE_X2_BF16 : LMZ_SEG_WRITE_X2_F32);
+static inline int64_t chunks_for(int64_t K, int R, int rw, int ww, int64_t u_cap) {
   const int64_t ub = u_cap < K ? u_cap : K;
-  return (int64_t(rw) * K + int64_t(kWriteCost) * ub + int64_t(rw) * R - 1) / (int64_t(rw) * R);
+  return (int64_t(rw) * K + int64_t(ww) * ub + int64_t(rw) * R - 1) / (int64_t(rw) * R);
 }
 
 static SegLayout seg_layout(int64_t K, int64_t D) {
@@ -134,7 +146,7 @@ static SegLayout seg_layout(int64_t K, int64_t D) {
   int R = kMinR;
   while (R < want && R < kMaxR) R *= 2;
   L.R = R;
-  L.max_chunks = static_cast<int>(chunks_for(K, R, 4, K));  // any dtype and capacity
+  L.max_chunks = static_cast<int>(chunks_for(K, R, 4, kMaxWriteCost, K));  // any dtype and capacity
   const size_t n = size_t(L.max_chunks);
   size_t off = 0;
   L.cont = off;     off += a256(n * D * 4);
@@ -774,8 +786,8 @@ int segsum_run(const void* grad, int gtype, int64_t K, int64_t D, int64_t ld_gra
   a.npieces = reinterpret_cast<int32_t*>(w + L.npieces);
   a.R = L.R;
   a.rw = read_cost(gtype);
-  a.ww = kWriteCost;
-  a.nchunks = static_cast<int>(chunks_for(K, L.R, a.rw, u_cap));
+  a.ww = write_cost(gtype);
+  a.nchunks = static_cast<int>(chunks_for(K, L.R, a.rw, a.ww, u_cap));
   a.dev_err = dev_err;
 
   const bool out_vec = al16(out) && ld_out % 4 == 0 && D % 4 == 0;

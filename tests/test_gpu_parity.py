@@ -250,9 +250,9 @@ def test_segsum_chunks_inside_short_segments(lz, gdt):
     assert err <= (H.TOL_BF16 if gdt == "bf16" else H.TOL_F32)
 
 
-def _piece_counts(ids, V, rw):
+def _piece_counts(ids, V, rw, ww):
     """Host restatement of the walk's cost partition (a position costs rw,
-    a segment end 16; R the power of two near K/1024 in 32..512, T = R/4):
+    a segment end ww; R the power of two near K/1024 in 32..512, T = R/4):
     for every segment of at least T rows that spans chunks, the number of
     chunks after its first that it reaches, and its first chunk."""
     K = len(ids)
@@ -262,7 +262,7 @@ def _piece_counts(ids, V, rw):
     R = 32
     while R < (K + 1023) // 1024 and R < 512:
         R *= 2
-    T, ww = R // 4, 16
+    T = R // 4
     n = -(-(rw * K + ww * min(K, V)) // (rw * R))
     Q = -(-(rw * K + ww * U) // n)
     f = rw * off[:-1] + ww * np.arange(U)
@@ -284,11 +284,13 @@ def test_segsum_fixup_piece_counts(lz, gdt):
     for _ in range(12):
         lens += [1] * int(rng.integers(3, 40)) + [int(rng.integers(sc + 20, 2 * sc)),
                                                  int(rng.integers(17 * sc, 20 * sc))]
-    lens += [1] * 20 + [135 * sc]
+    lens += [1] * 20 + [160 * sc]
     lens += [1] * (60_000 - sum(lens))
     ids = rng.permutation(np.repeat(np.arange(len(lens)) * 7 + 3, lens)).astype(np.int32)
     K, V, D = len(ids), 800_000, 96
-    P, cs = _piece_counts(ids, V, 4 if gdt == "bf16" else 8)
+    # (rw, ww): a read row costs 2 * sizeof(grad), a written fp32 row 8 (its
+    # bytes) with fp32 rows and 16 with bf16 rows
+    P, cs = _piece_counts(ids, V, *((4, 16) if gdt == "bf16" else (8, 8)))
     grp = cs // 8
     assert {1, 15, 16} <= set(P.tolist()) and P.max() > 128
     assert any((P[grp == g] >= 16).any() and (P[grp == g] < 16).any() for g in set(grp.tolist()))
