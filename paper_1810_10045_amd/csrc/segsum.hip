@@ -46,7 +46,7 @@ namespace lmz {
 
 // Tuning knobs (overridable at build time).
 #ifndef LMZ_SEG_TARGET_CHUNKS
-#define LMZ_SEG_TARGET_CHUNKS 1024   // R = the power of two near K / this (32..512)
+#define LMZ_SEG_TARGET_CHUNKS 1024   // R = the power of two near K / this (16..512)
 #endif
 #ifndef LMZ_SEG_WRITE_X2_F32
 #define LMZ_SEG_WRITE_X2_F32 2       // fp32 rows: cost of a row written / a row read, times 2
@@ -90,7 +90,7 @@ namespace lmz {
 #endif
 constexpr int kSegThreads = LMZ_SEG_WG_THREADS;
 constexpr int kSegWaves = kSegThreads / kWave;
-constexpr int kMinR = 32, kMaxR = 512;
+constexpr int kMinR = 16, kMaxR = 512;
 
 struct SegArgs {
   const void* grad;
@@ -738,6 +738,7 @@ static hipError_t launch_r(const SegArgs& a, hipStream_t st) {
   constexpr int CT = NV * kWave * VEC;
   dim3 grid((a.nchunks + kSegWaves - 1) / kSegWaves, (a.D + CT - 1) / CT);
   switch (a.R) {
+    case 16: launch_one<GT, VEC, NV, 16>(a, grid, st); break;
     case 32: launch_one<GT, VEC, NV, 32>(a, grid, st); break;
     case 64: launch_one<GT, VEC, NV, 64>(a, grid, st); break;
     case 128: launch_one<GT, VEC, NV, 128>(a, grid, st); break;

@@ -252,14 +252,14 @@ def test_segsum_chunks_inside_short_segments(lz, gdt):
 
 def _piece_counts(ids, V, rw, ww):
     """Host restatement of the walk's cost partition (a position costs rw,
-    a segment end ww; R the power of two near K/1024 in 32..512, T = R/4):
+    a segment end ww; R the power of two near K/1024 in 16..512, T = R/4):
     for every segment of at least T rows that spans chunks, the number of
     chunks after its first that it reaches, and its first chunk."""
     K = len(ids)
     _, c = np.unique(ids, return_counts=True)
     U = len(c)
     off = np.concatenate([[0], np.cumsum(c)])
-    R = 32
+    R = 16
     while R < (K + 1023) // 1024 and R < 512:
         R *= 2
     T = R // 4
