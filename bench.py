@@ -331,8 +331,9 @@ def main():
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one GPU: the multi-GPU collectives of the method are not part "
-              "of this build (run with --gpus 1)", file=sys.stderr)
+        print("bench.py measures one GPU: the library does not implement the multi-GPU "
+              "collectives of the method (the all-gather of the ids and the all-reduce of the "
+              "reduced rows); run with --gpus 1", file=sys.stderr)
         sys.exit(2)
 
     import torch

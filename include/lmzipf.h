@@ -55,7 +55,7 @@ enum {
   LM_E_INVAL = 1,       /* a NULL, negative or inconsistent argument */
   LM_E_WORKSPACE = 3,   /* ws_bytes below the size the *_workspace_bytes query returns */
   LM_E_HIP = 4,         /* a HIP launch or runtime call failed */
-  LM_E_UNSUPPORTED = 5  /* an enum value or a size this build does not handle */
+  LM_E_UNSUPPORTED = 5  /* an enum value or a size the library does not handle */
 };
 
 /* Bits OR-ed into *dev_err by the kernels. */
