@@ -469,15 +469,23 @@ __global__ __launch_bounds__(NTHR) void k_segsum(SegArgs a) {
   //    windows (sentinels: -2 before position 0, -1 from position K on).
   //    The loads are unconditional, at clamped positions: a load under a
   //    lane condition makes the compiler wait for every load before it.
+  //    The windows cover the longest chunk; the walk reads rows q ..
+  //    q_end - 1, and the end bit of row q_end - 1 needs the segment of
+  //    position q_end, so past q_end every lane repeats it (one line, a
+  //    cache hit) instead of fetching positions no row uses.
   int pw[NW], sw[NW];
+  auto win_pos = [&](int w) {
+    const int p = p0 - 1 + w * kWave + lane;
+    return p < q_end ? p : q_end;
+  };
 #pragma unroll
   for (int w = 0; w < NW; ++w) {
-    const int pos = p0 - 1 + w * kWave + lane;
+    const int pos = win_pos(w);
     pw[w] = a.perm[pos < 0 ? 0 : (pos < K ? pos : K - 1)];
   }
 #pragma unroll
   for (int w = 0; w < NW; ++w) {
-    const int pos = p0 - 1 + w * kWave + lane;
+    const int pos = win_pos(w);
     const bool ok = pos >= 0 && pos < K;
     const bool kin = static_cast<uint32_t>(pw[w]) < static_cast<uint32_t>(K);
     bad |= ok && !kin;
