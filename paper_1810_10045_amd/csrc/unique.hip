@@ -101,6 +101,7 @@ struct UniqueLayout {
   size_t bhist, tickets, status, dstatus, keys0, keys1, vals0, vals1, total;
   int passes, bits, tiles, hist_blocks, nt, items;
   int block_items;  // > 0: one workgroup (k_unique_block) with this many keys per thread
+  int block_rb;     // its digit width (8, 9 or 10): the widest digit of its passes
   int rstride;  // digit slots per pass in the histogram rows and status arrays
   int shift[kMaxPasses], nbits[kMaxPasses];
 };
@@ -132,7 +133,13 @@ static UniqueLayout unique_layout(int64_t K, int idtype, int64_t V) {
     while (int64_t(L.block_items) * 1024 < K) L.block_items *= 2;
   }
   const int narrow = kSmallDigitBits < kLargeDigitBits ? kSmallDigitBits : kLargeDigitBits;
-  const int widest = L.nt == 256 || L.block_items ? kSmallDigitBits : kLargeDigitBits;
+  // The one workgroup takes digits of up to 10 bits (a thread per digit):
+  // the fewest passes, with the narrowest digits that reach them (17-bit
+  // keys: 9 + 8 bits). Measured at 8,192 ids: 21.2 against 24.1 us for three
+  // 8-bit passes at 17-bit keys, 24.2 against 25.8 us at 20-bit keys; where
+  // wider digits save no pass (15 and 31 bits) 8-bit ones stay faster.
+  const int widest = L.block_items ? kLargeDigitBits
+                                    : (L.nt == 256 ? kSmallDigitBits : kLargeDigitBits);
   const int p_narrow = (L.bits + narrow - 1) / narrow, p_wide = (L.bits + widest - 1) / widest;
   L.passes = L.bits == 0 ? 1 : (p_wide < p_narrow ? p_wide : p_narrow);
   // Split the key bits evenly: the low passes take the extra bit.
@@ -143,6 +150,9 @@ static UniqueLayout unique_layout(int64_t K, int idtype, int64_t V) {
     L.nbits[p] = nb;
     sh += nb;
   }
+  L.block_rb = kSmallDigitBits;
+  for (int p = 0; p < L.passes; ++p)
+    if (L.block_items && L.nbits[p] > L.block_rb) L.block_rb = L.nbits[p];
   L.items = items_for(K, L.nt);
   const int64_t tile_keys = int64_t(L.nt) * L.items;
   L.tiles = static_cast<int>((K + tile_keys - 1) / tile_keys);
@@ -587,7 +597,7 @@ __global__ __launch_bounds__(NT) void k_dedup(
 // ---------------------------------------------------------------------------
 // k_unique_block: the whole of Unique in one workgroup of 1024 threads, for
 // inputs of up to 1024 * ITEMS keys. The keys stay in LDS through every
-// radix pass (8-bit digits, ranked by wave64 ballot matching as in
+// radix pass (RB-bit digits, RB = 8..10, ranked by wave64 ballot matching as in
 // k_onesweep, with digit offsets from a block scan instead of a look-back)
 // and through the dedup (run heads by ballot, a scan of the head counts
 // over the 16 waves), so the call is one launch with no waits between
@@ -599,13 +609,14 @@ __global__ __launch_bounds__(NT) void k_dedup(
 constexpr int kBlockThreads = kBlockThreadsHost;
 constexpr int kBlockWaves = kBlockThreads / kWave;
 
-template <typename KeyT, int ITEMS>
+template <typename KeyT, int ITEMS, int RB>
 __global__ __launch_bounds__(kBlockThreads) void k_unique_block(
     const KeyT* __restrict__ ids, int K, uint64_t V, int passes, PassBits pb, int cap,
     KeyT* __restrict__ uniq, int32_t* __restrict__ counts, int32_t* __restrict__ offsets,
     int32_t* __restrict__ inverse, int32_t* __restrict__ perm, int64_t* __restrict__ num_unique,
     int32_t* __restrict__ dev_err) {
-  constexpr int RB = kSmallDigitBits, kRadix = 1 << RB;
+  constexpr int kRadix = 1 << RB;
+  static_assert(kRadix <= kBlockThreads, "one thread per digit");
   constexpr int kN = kBlockThreads * ITEMS;
   __shared__ KeyT s_keys[kN];
   __shared__ int32_t s_vals[kN + 1];                // + 1: the end offset of the last type
@@ -809,10 +820,15 @@ static int run_unique(const KeyT* ids, int K, int64_t V, KeyT* uniq, int32_t* co
   }
   const int cap = static_cast<int>(K < V ? K : V);
   if (L.block_items > 0) {
+    auto launch = [&](auto items, auto rb) {
+      k_unique_block<KeyT, decltype(items)::value, decltype(rb)::value>
+          <<<1, kBlockThreads, 0, st>>>(ids, K, static_cast<uint64_t>(V), L.passes, pb, cap, uniq,
+                                        counts, offsets, inverse, perm, num_unique, dev_err);
+    };
     auto block = [&](auto items) {
-      k_unique_block<KeyT, decltype(items)::value><<<1, kBlockThreads, 0, st>>>(
-          ids, K, static_cast<uint64_t>(V), L.passes, pb, cap, uniq, counts, offsets, inverse,
-          perm, num_unique, dev_err);
+      if (L.block_rb <= 8) launch(items, I<8>{});
+      else if (L.block_rb == 9) launch(items, I<9>{});
+      else launch(items, I<10>{});
     };
     switch (L.block_items) {
       case 1: block(I<1>{}); break;

@@ -96,6 +96,11 @@ UNIQUE_CASES = [
     (2049, 100_000, 1.0, np.int32, 31), (8192, 100_000, 1.0, np.int32, 32),
     (8193, 100_000, 1.0, np.int32, 33), (8192, 2**40, 0.9, np.int64, 34),
     (3000, 2**40, 0.0, np.int64, 35), (8192, 3, 1.0, np.int32, 36),
+    # its digit widths: 8 bits over 2 and 4 passes (15- and 31-bit keys),
+    # 9 bits (17-bit keys above, and 62-bit keys in 7 passes), 10 bits
+    # (20- and 40-bit keys above)
+    (7000, 20_000, 1.2, np.int32, 37), (8000, 2**31 - 1, 0.0, np.int32, 38),
+    (5000, 2**62, 0.8, np.int64, 39),
 ]
 
 
