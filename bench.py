@@ -64,6 +64,20 @@ def segsum_bytes(K, D, U, grad_bytes):
     return K * D * grad_bytes + U * D * 4 + K * 4 + (U + 1) * 4
 
 
+def unique_bytes(K, U, id_bytes):
+    """Algorithmic bytes of one Unique: read the ids, write the inverse map
+    and the permutation, write the type ids, counts and offsets."""
+    return K * id_bytes + K * 4 + K * 4 + U * (id_bytes + 8)
+
+
+# Algorithmic bytes of the stage after Seg-Sum, per type row of D fp32: the
+# apply reads the reduced row and reads and writes the table row (Adam also
+# m and v); SCATTER reads the reduced row and writes the table row. The
+# merge's EXPAND stage also runs shard 0's own Unique and Seg-Sum, so it has
+# no single byte count here.
+AFTER_ROWS = {"sgd": 3, "softmax_sgd": 3, "adam": 7, "scatter": 2}
+
+
 class HipEvents:
     """Timing events created with hipEventDisableSystemFence, recorded on the
     stream the kernels run on (torch's current stream). Torch's own events
@@ -245,10 +259,16 @@ def run_gpu(w, steps, warmup, nbatch, torch, lz):
                    for i in range(steps)])
     ev.close()
     gb = 2 if w.grad_dtype == "bf16" else 4
-    seg_bytes = np.mean([segsum_bytes(K, D, U_of[i % nbatch], gb) for i in range(steps)])
+    ib = 8 if w.id_dtype == "i64" else 4
+    Us = [U_of[i % nbatch] for i in range(steps)]
+    seg_bytes = np.mean([segsum_bytes(K, D, U, gb) for U in Us])
     seg_ms = float(st[:, 1].mean())
+    uniq_bytes = float(np.mean([unique_bytes(K, U, ib) for U in Us]))
+    rows = AFTER_ROWS.get(w.step)
+    after_bytes = float(np.mean([rows * U * D * 4 for U in Us])) if rows else None
     return dict(total_ms=total_ms, stage_ms=st.mean(axis=0).tolist(), seg_ms=seg_ms,
-                seg_bytes=float(seg_bytes), U=U_of)
+                seg_bytes=float(seg_bytes), uniq_bytes=uniq_bytes, after_bytes=after_bytes,
+                U=U_of)
 
 
 def run_cpu_baseline(w, budget_s):
@@ -375,6 +395,11 @@ def main():
                    "resident_batches": nbatch, "types_per_batch": r["U"]},
         "stages_ms": {"unique": r["stage_ms"][0], "segsum": r["stage_ms"][1],
                       w.step: r["stage_ms"][2]},
+        # algorithmic bytes of each stage / its event-measured time (GB/s)
+        "stages_gbps": {"unique": r["uniq_bytes"] / (r["stage_ms"][0] / 1e3) / 1e9,
+                        "segsum": achieved,
+                        w.step: (r["after_bytes"] / (r["stage_ms"][2] / 1e3) / 1e9
+                                 if r["after_bytes"] else None)},
         "roofline": {"bound": "hbm", "kernel": SEGSUM_KERNELS if w.D <= 1024 else
                      "lm_segsum (k_segsum, then k_segsum_fix)",
                      "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
