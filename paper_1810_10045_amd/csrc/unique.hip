@@ -453,10 +453,37 @@ __global__ __launch_bounds__(NT) void k_onesweep(
 }
 
 // ---------------------------------------------------------------------------
-// k_dedup: thread t of tile `tile` owns the 4 sorted positions
-// base + 4t .. base + 4t + 3.
+// A thread's run of N consecutive elements from p (aligned to the run's
+// bytes) in 16- or 8-byte loads: the scalar form spread each load
+// instruction of a wave over 64 runs, one line each, and the compiler cannot
+// widen it without knowing the alignment.
 // ---------------------------------------------------------------------------
-template <typename KeyT, int NT, int ITEMS>
+template <typename T, int N>
+__device__ __forceinline__ void load_run(const T* __restrict__ p, T (&out)[N]) {
+  constexpr int kBytes = N * static_cast<int>(sizeof(T));
+  if constexpr (kBytes % 16 == 0) {
+    constexpr int kPer = 16 / sizeof(T);
+#pragma unroll
+    for (int c = 0; c < N / kPer; ++c) {
+      const u32x4 v = *reinterpret_cast<const u32x4*>(p + c * kPer);
+      const uint32_t w[4] = {v[0], v[1], v[2], v[3]};
+      __builtin_memcpy(&out[c * kPer], w, 16);
+    }
+  } else if constexpr (kBytes == 8) {
+    const uint64_t v = *reinterpret_cast<const uint64_t*>(p);
+    __builtin_memcpy(&out[0], &v, 8);
+  } else {
+#pragma unroll
+    for (int i = 0; i < N; ++i) out[i] = p[i];
+  }
+}
+
+// ---------------------------------------------------------------------------
+// k_dedup: thread t of tile `tile` owns the ITEMS sorted positions
+// base + ITEMS*t .. base + ITEMS*t + ITEMS - 1 (runs read in 16-byte loads;
+// the permutation too when the caller's buffer is 16-byte aligned).
+// ---------------------------------------------------------------------------
+template <typename KeyT, int NT, int ITEMS, bool PERM_RUNS>
 __global__ __launch_bounds__(NT) void k_dedup(
     const KeyT* __restrict__ skeys, const int32_t* __restrict__ perm, int K, int cap,
     KeyT* __restrict__ uniq, int32_t* __restrict__ counts, int32_t* __restrict__ offsets,
@@ -478,11 +505,21 @@ __global__ __launch_bounds__(NT) void k_dedup(
   int32_t src[kItems];
   auto fetch = [&](int64_t base) {
     const int64_t p0 = base + int64_t(tid) * kItems;
+    if (p0 + kItems <= K) {  // a whole run: the workspace keys are 256-byte aligned
+      load_run<KeyT, kItems>(skeys + p0, k);
+      if constexpr (PERM_RUNS) {
+        load_run<int32_t, kItems>(perm + p0, src);
+      } else {
 #pragma unroll
-    for (int i = 0; i < kItems; ++i) {
-      const bool ok = p0 + i < K;
-      k[i] = ok ? skeys[p0 + i] : KeyT(0);
-      src[i] = ok ? perm[p0 + i] : 0;
+        for (int i = 0; i < kItems; ++i) src[i] = perm[p0 + i];
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < kItems; ++i) {
+        const bool ok = p0 + i < K;
+        k[i] = ok ? skeys[p0 + i] : KeyT(0);
+        src[i] = ok ? perm[p0 + i] : 0;
+      }
     }
     kprev = p0 > 0 && p0 - 1 < K ? skeys[p0 - 1] : KeyT(0);
     knext = p0 + kItems < K ? skeys[p0 + kItems] : KeyT(0);
@@ -881,11 +918,17 @@ static int run_unique(const KeyT* ids, int K, int64_t V, KeyT* uniq, int32_t* co
     kin = kout;
     vin = vout;
   }
+  const bool perm_runs = (reinterpret_cast<uintptr_t>(perm) & 15) == 0;
   auto dedup = [&](auto nt, auto items) {
     constexpr int NT = decltype(nt)::value, IT = decltype(items)::value;
-    k_dedup<KeyT, NT, IT><<<L.tiles, NT, 0, st>>>(kin, perm, K, cap, uniq, counts, offsets,
-                                                  inverse, num_unique, dstatus,
-                                                  tickets + kMaxPasses, dev_err);
+    if (perm_runs)
+      k_dedup<KeyT, NT, IT, true><<<L.tiles, NT, 0, st>>>(kin, perm, K, cap, uniq, counts,
+                                                          offsets, inverse, num_unique, dstatus,
+                                                          tickets + kMaxPasses, dev_err);
+    else
+      k_dedup<KeyT, NT, IT, false><<<L.tiles, NT, 0, st>>>(kin, perm, K, cap, uniq, counts,
+                                                           offsets, inverse, num_unique, dstatus,
+                                                           tickets + kMaxPasses, dev_err);
   };
   if (L.nt == 256) {
     if (L.items == 2) dedup(I<256>{}, I<2>{});
