@@ -151,6 +151,31 @@ def test_unique_out_of_range_sets_error(lz):
     assert int(res.dev_err.item()) & lz.DEVERR_ID_RANGE
 
 
+@pytest.mark.parametrize("K,V,dt", [(70_000, 800_000, np.int32), (9000, 100_000, np.int64),
+                                     (5000, 100_000, np.int32)])
+def test_unique_outputs_not_16_byte_aligned(lz, K, V, dt):
+    """Output buffers that start one element into their allocation (4- or
+    8-byte aligned, not 16): the dedup then reads the permutation with
+    scalar loads, and every output lands where the caller asked."""
+    ids = synth.zipf_ids(K, V, 1.0, 61, dt)
+    tdt = torch.int64 if dt == np.int64 else torch.int32
+    cap = min(K, V)
+
+    def shifted(n, dtype):
+        return torch.full((n + 1,), -7, dtype=dtype, device=DEV)[1:]
+
+    out = lz.UniqueResult(shifted(cap, tdt), shifted(cap, torch.int32), shifted(cap + 1, torch.int32),
+                          shifted(K, torch.int32), shifted(K, torch.int32),
+                          torch.zeros(1, dtype=torch.int64, device=DEV),
+                          torch.zeros(1, dtype=torch.int32, device=DEV))
+    assert out.perm.data_ptr() % 16 != 0
+    _say(f"unique unaligned outputs K={K} V={V} dtype={dt.__name__}")
+    res = lz.unique(_t(ids), V, out=out)
+    torch.cuda.synchronize()
+    lz.check(res.dev_err)
+    H.assert_unique_matches(res, ids, V, oracle, f"unaligned K={K}")
+
+
 def test_unique_workspace_reuse_and_determinism(lz):
     """Back-to-back calls on one workspace, with different sizes and a
     workspace full of garbage, stay exact."""
