@@ -37,6 +37,7 @@ int apply_run_f16(float* table, int64_t V, int64_t D, int64_t ld_table, const vo
                   int32_t* dev_err, hipStream_t st);
 
 int sample_run(const uint64_t* r, int64_t n, int64_t V, void* ids, int idtype, hipStream_t st);
+void segsum_force_wait_failure(bool enable, uint32_t limit);
 
 int launch_status(hipError_t e) { return e == hipSuccess ? LM_OK : LM_E_HIP; }
 
@@ -69,7 +70,7 @@ const char* lm_status_string(int status) {
   }
 }
 
-int lm_abi_version(void) { return 102; }
+int lm_abi_version(void) { return 103; }
 
 int lm_workspace_clear(void* ws, size_t bytes, void* stream) {
   if (bytes == 0) return LM_OK;
@@ -101,6 +102,11 @@ int lm_unique(const void* ids, int32_t idtype, int64_t K, int64_t V, void* uniq,
   if (ws_bytes < unique_workspace_bytes(K, idtype, V)) return LM_E_WORKSPACE;
   return unique_run(ids, idtype, K, V, uniq, counts, offsets, inverse, perm, num_unique, dev_err,
                     ws, ws_bytes, static_cast<hipStream_t>(stream));
+}
+
+int lm_test_force_wait_failure(int32_t enable, uint32_t spin_limit) {
+  segsum_force_wait_failure(enable != 0, spin_limit);
+  return LM_OK;
 }
 
 size_t lm_segsum_workspace_bytes(int64_t K, int64_t D) {

@@ -109,6 +109,9 @@ struct SegArgs {
   int32_t* npieces;
   uint64_t* flags;   // fused launch: flags[c] == epoch once chunk c's descriptor and
   uint64_t epoch;    // partial rows are visible to every workgroup
+  uint64_t wait_epoch;  // the value the fix-up waits for: epoch (or, with the
+                        // failure-path test hook, one no walk writes)
+  uint32_t spin_limit;  // polls of a flag before the wait gives up
   int main_blocks, fix_tiles, fused;
   int R, nchunks, rw, ww;  // cost of a position / of a segment end
   int32_t* dev_err;
@@ -261,9 +264,9 @@ __device__ __forceinline__ void load4_agent(const float* p, float* v) {
 // flags[idx] holds the epoch. False if the wait gave up.
 __device__ __forceinline__ bool wait_flags(const SegArgs& a, int idx, bool need) {
   for (uint32_t spin = 0;; ++spin) {
-    const bool ok = !need || ld_agent(a.flags + idx) == a.epoch;
+    const bool ok = !need || ld_agent(a.flags + idx) == a.wait_epoch;
     if (!ballot(!ok)) return true;
-    if (spin >= kSpinLimit) {
+    if (spin >= a.spin_limit) {
       if (lane_id() == 0) raise_err(a.dev_err, LM_DEVERR_SPIN);
       return false;
     }
@@ -769,6 +772,18 @@ static hipError_t dispatch_nv(const SegArgs& a, int nv_max, hipStream_t st) {
 
 static bool al16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
 
+// Test hook for the failure path of the one-launch form: while set, the
+// fix-up workgroups wait for a flag value that no walk writes, so every such
+// wait gives up after `limit` polls and raises LM_DEVERR_SPIN; the launch
+// still drains and stays inside its buffers. Off by default.
+static std::atomic<bool> g_force_wait_failure{false};
+static std::atomic<uint32_t> g_forced_spin_limit{kSpinLimit};
+
+void segsum_force_wait_failure(bool enable, uint32_t limit) {
+  g_forced_spin_limit.store(limit < 1 ? 1u : limit, std::memory_order_relaxed);
+  g_force_wait_failure.store(enable, std::memory_order_relaxed);
+}
+
 int segsum_run(const void* grad, int gtype, int64_t K, int64_t D, int64_t ld_grad,
                const int32_t* perm, const int32_t* inverse, const int32_t* offsets,
                const int64_t* num_unique, int64_t u_cap, float* out, int64_t ld_out,
@@ -778,6 +793,7 @@ int segsum_run(const void* grad, int gtype, int64_t K, int64_t D, int64_t ld_gra
   if (K == 0 || D == 0 || u_cap == 0) return LM_OK;
   char* w = static_cast<char*>(ws);
   SegArgs a{};
+  a.spin_limit = kSpinLimit;
   a.grad = grad;
   a.ld_grad = ld_grad;
   a.K = static_cast<int>(K);
@@ -819,6 +835,9 @@ int segsum_run(const void* grad, int gtype, int64_t K, int64_t D, int64_t ld_gra
     static std::atomic<uint64_t> epoch{0x9e3779b97f4a7c15ull};
     a.flags = reinterpret_cast<uint64_t*>(w + L.flags);
     a.epoch = epoch.fetch_add(1, std::memory_order_relaxed) + 1;
+    const bool fail = g_force_wait_failure.load(std::memory_order_relaxed);
+    a.wait_epoch = fail ? a.epoch ^ (uint64_t(1) << 63) : a.epoch;
+    a.spin_limit = fail ? g_forced_spin_limit.load(std::memory_order_relaxed) : kSpinLimit;
     a.main_blocks = (a.nchunks + kFusedWaves - 1) / kFusedWaves;
     a.fix_tiles = static_cast<int>((D + kFusedCols - 1) / kFusedCols);
   }

@@ -71,9 +71,10 @@ def _load():
     L.lm_sparse_apply_f16.argtypes = [P, I64_, I64_, I64_, P, I32_, P, I64_, P, I64_, F, I32_,
                                       F, F, F, F, F, I64_, P, P, P, P]
     L.lm_sample_ids.argtypes = [P, I64_, I64_, P, I32_, P]
+    L.lm_test_force_wait_failure.argtypes = [I32_, ctypes.c_uint32]
     for f in ("lm_abi_version", "lm_workspace_clear", "lm_unique", "lm_segsum", "lm_map_ids",
               "lm_fill_values", "lm_sparse_apply", "lm_fill_values_f16", "lm_sparse_apply_f16",
-              "lm_sample_ids"):
+              "lm_sample_ids", "lm_test_force_wait_failure"):
         getattr(L, f).restype = ctypes.c_int
     return L
 
@@ -360,6 +361,13 @@ def sparse_apply_f16(table: torch.Tensor, rows: torch.Tensor, n_rows: torch.Tens
                                    weight_decay, step, _ptr(m), _ptr(v), _ptr(dev_err),
                                    _stream(stream)), "lm_sparse_apply_f16")
     return table
+
+
+def force_wait_failure(enable: bool, spin_limit: int = 64):
+    """lm_test_force_wait_failure: test hook for the failure path of the
+    one-launch Seg-Sum's bounded waits (see include/lmzipf.h)."""
+    _call(_lib.lm_test_force_wait_failure(1 if enable else 0, int(spin_limit)),
+          "lm_test_force_wait_failure")
 
 
 def sample_ids(r: torch.Tensor, V: int, out: Optional[torch.Tensor] = None,

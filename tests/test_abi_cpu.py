@@ -51,7 +51,7 @@ def test_status_strings(lib):
     lib.lm_status_string.restype = ctypes.c_char_p
     for code in (0, 1, 3, 4, 5, 99):
         assert lib.lm_status_string(code)
-    assert lib.lm_abi_version() == 102
+    assert lib.lm_abi_version() == 103
 
 
 def test_workspace_queries(lib):

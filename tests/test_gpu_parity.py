@@ -360,6 +360,40 @@ def test_segsum_workspace_reuse(lz):
         assert err <= (H.TOL_BF16 if gdt == "bf16" else H.TOL_F32)
 
 
+def test_segsum_wait_failure_is_reported(lz):
+    """The failure path of the one-launch form's bounded waits, forced from
+    the host: with the test hook set, the fix-up workgroups wait for a flag
+    value no walk writes, give up after 64 polls and raise LM_DEVERR_SPIN,
+    and the launch still finishes. With the hook cleared, the next call on
+    the same workspace is exact again."""
+    K, V, D = 65_536, 800_000, 1024
+    ids = synth.zipf_ids(K, V, 1.0, 71, np.int32)
+    g32 = synth.normal_rows(K, D, 72)
+    ws = lz.Workspace(DEV)
+    res = lz.unique(_t(ids), V, ws=ws)
+    grad = _t(g32)
+    torch.cuda.synchronize()
+    lz.check(res.dev_err)
+    _say("segsum with forced wait failures")
+    lz.force_wait_failure(True, 64)
+    try:
+        err = torch.zeros(1, dtype=torch.int32, device=DEV)
+        lz.segsum(grad, res.perm, res.inverse, res.offsets, res.num_unique, dev_err=err, ws=ws)
+        torch.cuda.synchronize()
+    finally:
+        lz.force_wait_failure(False)
+    assert int(err.item()) & lz.DEVERR_SPIN
+    err2 = torch.zeros(1, dtype=torch.int32, device=DEV)
+    out = lz.segsum(grad, res.perm, res.inverse, res.offsets, res.num_unique, dev_err=err2, ws=ws)
+    torch.cuda.synchronize()
+    lz.check(err2)
+    o = oracle.unique(ids, V)
+    U = len(o[0])
+    ref = oracle.segsum(g32, o[3], U)
+    rel = H.row_rel_err(out[:U].double().cpu().numpy(), ref, H.sum_of_squares(g32, o[3], U, oracle))
+    assert rel <= H.TOL_F32
+
+
 def test_segsum_deterministic(lz):
     a = _segsum_case(lz, 60_000, 500, 1.2, 1024, "f32", 51)[3].clone()
     b = _segsum_case(lz, 60_000, 500, 1.2, 1024, "f32", 51)[3]
