@@ -158,13 +158,15 @@ int lm_unique(const void* ids, int32_t idtype, int64_t K, int64_t V,
  * ------------------------------------------------------------------------ */
 size_t lm_segsum_workspace_bytes(int64_t K, int64_t D);
 
-/* Test hook for the failure path of the bounded waits above (not for use
- * in training). While enable is nonzero, the fix-up workgroups of the
- * one-launch form wait for a flag value that the walk never writes, so each
- * such wait gives up after spin_limit polls (at least 1) and sets
- * LM_DEVERR_SPIN; the launch still finishes and writes only inside its
- * buffers, but the sums of segments that span chunks are unspecified.
- * Process-wide; off by default. Returns LM_OK. */
+/* Test hook for the failure path of the bounded waits between workgroups
+ * (not for use in training). While enable is nonzero, the fix-up
+ * workgroups of lm_segsum's one-launch form wait for a flag value that the
+ * walk never writes, and the look-backs of lm_unique's multi-workgroup
+ * kernels (inputs above 8,192 ids) read every predecessor as not ready:
+ * each such wait gives up after spin_limit polls (at least 1) and sets
+ * LM_DEVERR_SPIN. The launches still finish and write only inside their
+ * buffers; their results are then unspecified. Process-wide; off by
+ * default. Returns LM_OK. */
 int lm_test_force_wait_failure(int32_t enable, uint32_t spin_limit);
 int lm_segsum(const void* grad, int32_t gtype, int64_t K, int64_t D,
               int64_t ld_grad, const int32_t* perm, const int32_t* inverse,

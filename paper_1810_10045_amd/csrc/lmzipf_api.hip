@@ -38,6 +38,7 @@ int apply_run_f16(float* table, int64_t V, int64_t D, int64_t ld_table, const vo
 
 int sample_run(const uint64_t* r, int64_t n, int64_t V, void* ids, int idtype, hipStream_t st);
 void segsum_force_wait_failure(bool enable, uint32_t limit);
+void unique_force_wait_failure(bool enable, uint32_t limit);
 
 int launch_status(hipError_t e) { return e == hipSuccess ? LM_OK : LM_E_HIP; }
 
@@ -106,6 +107,7 @@ int lm_unique(const void* ids, int32_t idtype, int64_t K, int64_t V, void* uniq,
 
 int lm_test_force_wait_failure(int32_t enable, uint32_t spin_limit) {
   segsum_force_wait_failure(enable != 0, spin_limit);
+  unique_force_wait_failure(enable != 0, spin_limit);
   return LM_OK;
 }
 

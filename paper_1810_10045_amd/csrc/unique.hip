@@ -28,6 +28,8 @@
 // tile's inputs are fetched for tile = blockIdx.x while the ticket is in
 // flight (workgroups are dispatched in order, so the guess almost always
 // holds) and fetched again when it does not.
+#include <atomic>
+
 #include "common.hpp"
 
 namespace lmz {
@@ -176,6 +178,26 @@ static UniqueLayout unique_layout(int64_t K, int idtype, int64_t V) {
 template <int N>
 using I = std::integral_constant<int, N>;
 
+// The look-backs' bounded waits: polls before giving up (LM_DEVERR_SPIN),
+// and the test hook for that path (every predecessor read as not ready).
+struct WaitCfg {
+  uint32_t spin_limit;
+  int force_fail;
+};
+static std::atomic<bool> g_force_wait_failure{false};
+static std::atomic<uint32_t> g_forced_spin_limit{kSpinLimit};
+
+void unique_force_wait_failure(bool enable, uint32_t limit) {
+  g_forced_spin_limit.store(limit < 1 ? 1u : limit, std::memory_order_relaxed);
+  g_force_wait_failure.store(enable, std::memory_order_relaxed);
+}
+
+static WaitCfg wait_cfg() {
+  const bool fail = g_force_wait_failure.load(std::memory_order_relaxed);
+  return WaitCfg{fail ? g_forced_spin_limit.load(std::memory_order_relaxed) : kSpinLimit,
+                 fail ? 1 : 0};
+}
+
 struct PassBits {
   int shift[kMaxPasses], nbits[kMaxPasses];
 };
@@ -239,7 +261,8 @@ __global__ __launch_bounds__(NT) void k_onesweep(
     const KeyT* __restrict__ keys_in, const int32_t* __restrict__ vals_in,
     KeyT* __restrict__ keys_out, int32_t* __restrict__ vals_out, int K, int shift, int nbits,
     const uint32_t* __restrict__ bhist, int hist_blocks, int hist_stride,
-    uint32_t* __restrict__ status, uint32_t* __restrict__ ticket, int32_t* __restrict__ dev_err) {
+    uint32_t* __restrict__ status, uint32_t* __restrict__ ticket, int32_t* __restrict__ dev_err,
+    WaitCfg wc) {
   constexpr int kWaves = NT / kWave;
   constexpr int kItems = ITEMS;
   constexpr int kTile = NT * kItems;
@@ -388,7 +411,7 @@ __global__ __launch_bounds__(NT) void k_onesweep(
 #pragma unroll
         for (int r = 0; r < W; ++r) {
           if (!stop) {
-            const uint32_t f = s[i][r] & ~kValMask;
+            const uint32_t f = wc.force_fail ? 0u : s[i][r] & ~kValMask;
             if (f == 0) {
               stop = true;
               stalled = true;
@@ -404,7 +427,7 @@ __global__ __launch_bounds__(NT) void k_onesweep(
       }
       if (all_done) break;
       if (stalled) {
-        if (++spins > kSpinLimit) { raise_err(dev_err, LM_DEVERR_SPIN); break; }
+        if (++spins > wc.spin_limit) { raise_err(dev_err, LM_DEVERR_SPIN); break; }
         __builtin_amdgcn_s_sleep(1);
       }
     }
@@ -488,7 +511,8 @@ __global__ __launch_bounds__(NT) void k_dedup(
     const KeyT* __restrict__ skeys, const int32_t* __restrict__ perm, int K, int cap,
     KeyT* __restrict__ uniq, int32_t* __restrict__ counts, int32_t* __restrict__ offsets,
     int32_t* __restrict__ inverse, int64_t* __restrict__ num_unique,
-    uint64_t* __restrict__ status, uint32_t* __restrict__ ticket, int32_t* __restrict__ dev_err) {
+    uint64_t* __restrict__ status, uint32_t* __restrict__ ticket, int32_t* __restrict__ dev_err,
+    WaitCfg wc) {
   constexpr int kWaves = NT / kWave;
   constexpr int kItems = ITEMS;
   constexpr int kTile = NT * kItems;
@@ -567,7 +591,7 @@ __global__ __launch_bounds__(NT) void k_dedup(
       while (true) {
         const int pos = j - lane;
         const uint64_t s = pos >= 0 ? ld_agent(status + pos) : kDFlagPrefix;
-        const uint64_t f = s & kDFlags;
+        const uint64_t f = wc.force_fail ? 0 : s & kDFlags;
         const uint64_t notready = ballot(f == 0);
         const uint64_t prefix = ballot(f == kDFlagPrefix);
         const int first_nr = notready ? __builtin_ctzll(notready) : kWave;
@@ -586,7 +610,7 @@ __global__ __launch_bounds__(NT) void k_dedup(
         if (done) break;
         j -= take;
         if (take == 0) {
-          if (++spins > kSpinLimit) { raise_err(dev_err, LM_DEVERR_SPIN); break; }
+          if (++spins > wc.spin_limit) { raise_err(dev_err, LM_DEVERR_SPIN); break; }
           __builtin_amdgcn_s_sleep(1);
         }
       }
@@ -838,7 +862,7 @@ static hipError_t launch_pass(const UniqueLayout& L, int p, const KeyT* kin, con
   k_onesweep<KeyT, RB, NT, ITEMS><<<L.tiles, NT, 0, st>>>(
       kin, vin, kout, vout, K, L.shift[p], L.nbits[p], bhist + size_t(p) * L.rstride,
       L.hist_blocks, L.passes * L.rstride, status + size_t(p) * L.tiles * L.rstride, tickets + p,
-      dev_err);
+      dev_err, wait_cfg());
   return hipGetLastError();
 }
 
@@ -924,11 +948,13 @@ static int run_unique(const KeyT* ids, int K, int64_t V, KeyT* uniq, int32_t* co
     if (perm_runs)
       k_dedup<KeyT, NT, IT, true><<<L.tiles, NT, 0, st>>>(kin, perm, K, cap, uniq, counts,
                                                           offsets, inverse, num_unique, dstatus,
-                                                          tickets + kMaxPasses, dev_err);
+                                                          tickets + kMaxPasses, dev_err,
+                                                          wait_cfg());
     else
       k_dedup<KeyT, NT, IT, false><<<L.tiles, NT, 0, st>>>(kin, perm, K, cap, uniq, counts,
                                                            offsets, inverse, num_unique, dstatus,
-                                                           tickets + kMaxPasses, dev_err);
+                                                           tickets + kMaxPasses, dev_err,
+                                                           wait_cfg());
   };
   if (L.nt == 256) {
     if (L.items == 2) dedup(I<256>{}, I<2>{});

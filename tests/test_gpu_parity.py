@@ -176,6 +176,29 @@ def test_unique_outputs_not_16_byte_aligned(lz, K, V, dt):
     H.assert_unique_matches(res, ids, V, oracle, f"unaligned K={K}")
 
 
+def test_unique_wait_failure_is_reported(lz):
+    """The failure path of the look-backs of the multi-workgroup Unique,
+    forced from the host: with the test hook set, every predecessor reads as
+    not ready, each look-back gives up after 64 polls with LM_DEVERR_SPIN,
+    and the kernels still finish inside their buffers. With the hook
+    cleared, the next call on the same workspace is exact again."""
+    K, V = 70_000, 800_000
+    ids = synth.zipf_ids(K, V, 1.0, 73, np.int32)
+    ws = lz.Workspace(DEV)
+    _say("unique with forced look-back failures")
+    lz.force_wait_failure(True, 64)
+    try:
+        bad = lz.unique(_t(ids), V, ws=ws)
+        torch.cuda.synchronize()
+    finally:
+        lz.force_wait_failure(False)
+    assert int(bad.dev_err.item()) & lz.DEVERR_SPIN
+    res = lz.unique(_t(ids), V, ws=ws)
+    torch.cuda.synchronize()
+    lz.check(res.dev_err)
+    H.assert_unique_matches(res, ids, V, oracle, "after the forced failures")
+
+
 def test_unique_workspace_reuse_and_determinism(lz):
     """Back-to-back calls on one workspace, with different sizes and a
     workspace full of garbage, stay exact."""
