@@ -300,7 +300,21 @@ def run_cpu_baseline(w, budget_s):
         toks += len(ids)
     return dict(value=toks / t_used, unit="tokens/s", cores=1, kind="oracle",
                 sample=f"{done} whole {w.name} batch(es) of {len(ids)} tokens, "
-                       f"unique+segsum+{w.step}, fp64, 1 thread, {t_used:.1f}s")
+                       f"unique+segsum+{w.step}, fp64, 1 thread of {cpu_model()}, {t_used:.1f}s")
+
+
+def cpu_model() -> str:
+    """The host CPU's model name (and how many cores the host has)."""
+    name = "unknown CPU"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    name = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return f"{name} ({os.cpu_count()} cores)"
 
 
 def load_traffic(workload):
