@@ -48,6 +48,18 @@ constexpr int kBlockThreadsHost = 1024;  // threads of k_unique_block
 #ifndef LMZ_UNIQUE_BLOCK_MAX_K
 #define LMZ_UNIQUE_BLOCK_MAX_K 8192    // up to this K, one workgroup does it all
 #endif
+#ifndef LMZ_UNIQUE_GATHER
+#define LMZ_UNIQUE_GATHER 1            // tile-local passes joined by gathers (see k_sort_local)
+#endif
+#ifndef LMZ_UNIQUE_GATHER_MAX_TILES
+#define LMZ_UNIQUE_GATHER_MAX_TILES 64 // a wave holds one digit's runs of every tile
+#endif
+#ifndef LMZ_UNIQUE_GATHER_MIN_TILES
+#define LMZ_UNIQUE_GATHER_MIN_TILES 16 // fewer tiles: the look-back passes are faster
+#endif
+#ifndef LMZ_UNIQUE_GATHER_DIGIT_BITS
+#define LMZ_UNIQUE_GATHER_DIGIT_BITS 9 // widest digit of the tile-local passes
+#endif
 #ifndef LMZ_UNIQUE_LOOKBACK_W
 #define LMZ_UNIQUE_LOOKBACK_W 4        // predecessor tiles a look-back round reads
 #endif
@@ -104,6 +116,8 @@ struct UniqueLayout {
   int passes, bits, tiles, hist_blocks, nt, items;
   int block_items;  // > 0: one workgroup (k_unique_block) with this many keys per thread
   int block_rb;     // its digit width (8, 9 or 10): the widest digit of its passes
+  int gather;       // 1: tile-local passes (k_sort_local) and a gathering dedup; the
+                    // histogram region then holds the runs of each pass and tile
   int rstride;  // digit slots per pass in the histogram rows and status arrays
   int shift[kMaxPasses], nbits[kMaxPasses];
 };
@@ -134,6 +148,11 @@ static UniqueLayout unique_layout(int64_t K, int idtype, int64_t V) {
     L.block_items = 1;
     while (int64_t(L.block_items) * 1024 < K) L.block_items *= 2;
   }
+  L.items = items_for(K, L.nt);
+  const int64_t tile_keys = int64_t(L.nt) * L.items;
+  L.tiles = static_cast<int>((K + tile_keys - 1) / tile_keys);
+  L.gather = LMZ_UNIQUE_GATHER && !L.block_items && L.nt == 1024 && L.items == 2 &&
+             L.tiles <= LMZ_UNIQUE_GATHER_MAX_TILES && L.tiles >= LMZ_UNIQUE_GATHER_MIN_TILES;
   const int narrow = kSmallDigitBits < kLargeDigitBits ? kSmallDigitBits : kLargeDigitBits;
   // The one workgroup takes digits of up to 10 bits (a thread per digit):
   // the fewest passes, with the narrowest digits that reach them (17-bit
@@ -141,7 +160,8 @@ static UniqueLayout unique_layout(int64_t K, int idtype, int64_t V) {
   // 8-bit passes at 17-bit keys, 24.2 against 25.8 us at 20-bit keys; where
   // wider digits save no pass (15 and 31 bits) 8-bit ones stay faster.
   const int widest = L.block_items ? kLargeDigitBits
-                                    : (L.nt == 256 ? kSmallDigitBits : kLargeDigitBits);
+                     : L.gather  ? LMZ_UNIQUE_GATHER_DIGIT_BITS
+                                 : (L.nt == 256 ? kSmallDigitBits : kLargeDigitBits);
   const int p_narrow = (L.bits + narrow - 1) / narrow, p_wide = (L.bits + widest - 1) / widest;
   L.passes = L.bits == 0 ? 1 : (p_wide < p_narrow ? p_wide : p_narrow);
   // Split the key bits evenly: the low passes take the extra bit.
@@ -155,17 +175,16 @@ static UniqueLayout unique_layout(int64_t K, int idtype, int64_t V) {
   L.block_rb = kSmallDigitBits;
   for (int p = 0; p < L.passes; ++p)
     if (L.block_items && L.nbits[p] > L.block_rb) L.block_rb = L.nbits[p];
-  L.items = items_for(K, L.nt);
-  const int64_t tile_keys = int64_t(L.nt) * L.items;
-  L.tiles = static_cast<int>((K + tile_keys - 1) / tile_keys);
   L.hist_blocks = hist_blocks_for(K);
+  if (L.gather) L.hist_blocks = L.tiles;  // one row of runs per pass and tile
   size_t off = 0;
   L.rstride = 1 << kSmallDigitBits;
   for (int p = 0; p < L.passes; ++p)
     if (L.nbits[p] > kSmallDigitBits) L.rstride = 1 << kLargeDigitBits;
   L.bhist = off;   off += align256(size_t(L.hist_blocks) * L.passes * L.rstride * 4);
   L.tickets = off; off += 256;
-  L.status = off;  off += align256(size_t(L.passes) * L.tiles * L.rstride * 4);
+  L.status = off;  // the look-backs' words (none when the passes gather)
+  if (!L.gather) off += align256(size_t(L.passes) * L.tiles * L.rstride * 4);
   L.dstatus = off; off += align256(size_t(L.tiles) * 8);
   L.keys0 = off;   off += align256(size_t(K) * ks);
   L.keys1 = off;   off += align256(size_t(K) * ks);
@@ -476,6 +495,268 @@ __global__ __launch_bounds__(NT) void k_onesweep(
 }
 
 // ---------------------------------------------------------------------------
+// Tile-local passes. Where an input takes at most 64 tiles, each radix pass
+// sorts its tile by the pass's digit in LDS and writes it back over the
+// tile's own range, publishing for every digit d one word,
+// (start of d within the tile) << 16 | (keys of d in the tile). The pass's
+// global (stable) order is then implied: the keys of digit d from tile t
+// begin at D(d) + the counts of d in the tiles before t, where D(d) counts
+// the keys of smaller digits. The next pass, and the dedup after the last,
+// gather the range of that order they own from the tiles' runs. No pass waits
+// on another workgroup and no histogram kernel runs first: each workgroup
+// adds up the counts of every tile (one column of words per digit) instead.
+// ---------------------------------------------------------------------------
+constexpr uint32_t kRunCountMask = 0xFFFFu;
+
+// Keys of digit d over every tile of the previous pass (0 for d >= R).
+__device__ __forceinline__ uint32_t run_total(const uint32_t* __restrict__ runs, int tiles,
+                                              int rstride, int d, int R) {
+  uint32_t tot = 0;
+  if (d < R) {
+    constexpr int kRows = 32;  // loads in flight per round
+    for (int t0 = 0; t0 < tiles; t0 += kRows) {
+      uint32_t w[kRows];
+#pragma unroll
+      for (int r = 0; r < kRows; ++r) {
+        const int t = t0 + r < tiles ? t0 + r : t0;  // repeat a valid row, unused
+        w[r] = runs[size_t(t) * rstride + d];
+      }
+#pragma unroll
+      for (int r = 0; r < kRows; ++r) tot += t0 + r < tiles ? (w[r] & kRunCountMask) : 0u;
+    }
+  }
+  return tot;
+}
+
+// Marks where each (digit, tile) run starts among the positions gs .. gs+m-1
+// of the previous pass's order: s_mark[e] = e at the first position e of a
+// run within the range (the caller set -1 everywhere before), s_src[e] = the
+// index that position is read from. Thread d holds digit d's total `tot`
+// and its start D(d). A wave takes one digit at a time, lane t the run of
+// tile t (tiles <= 64), and a wave prefix sum places the runs.
+template <int NT>
+__device__ __forceinline__ void mark_runs(const uint32_t* __restrict__ runs, int tiles,
+                                          int rstride, int tile_keys, int d, uint32_t tot,
+                                          uint32_t start, int64_t gs, int m, int* s_mark,
+                                          int* s_src, int* s_dig, uint32_t* s_dstart,
+                                          uint32_t* s_scan) {
+  constexpr int kWaves = NT / kWave;
+  const int lane = threadIdx.x & 63;
+  const int wave = first_lane(static_cast<int>(threadIdx.x) >> 6);
+  const bool ov = tot > 0 && int64_t(start) < gs + m && int64_t(start) + tot > gs;
+  uint32_t nd;
+  const uint32_t q = block_excl_sum<kWaves, uint32_t>(ov ? 1u : 0u, s_scan, nd);
+  if (ov) {
+    s_dig[q] = d;
+    s_dstart[q] = start;
+  }
+  __syncthreads();
+  auto place = [&](uint32_t w, uint32_t dstart) {
+    const uint32_t c = w & kRunCountMask;
+    const int64_t g = int64_t(dstart) + (wave_incl_sum(c) - c);
+    const int64_t lo = g > gs ? g : gs;
+    const int64_t hi = g + c < gs + m ? g + c : gs + m;
+    if (lo < hi) {
+      const int e = static_cast<int>(lo - gs);
+      s_mark[e] = e;
+      s_src[e] = lane * tile_keys + static_cast<int>(w >> 16) + static_cast<int>(lo - g);
+    }
+  };
+  // Two digits per round: their loads fly together.
+  for (int q0 = wave; q0 < static_cast<int>(nd); q0 += 2 * kWaves) {
+    const int q1 = q0 + kWaves;
+    const bool two = q1 < static_cast<int>(nd);
+    const int d0 = s_dig[q0], d1 = two ? s_dig[q1] : d0;
+    const uint32_t w0 = lane < tiles ? runs[size_t(lane) * rstride + d0] : 0u;
+    const uint32_t w1 = two && lane < tiles ? runs[size_t(lane) * rstride + d1] : 0u;
+    place(w0, s_dstart[q0]);
+    if (two) place(w1, s_dstart[q1]);
+  }
+  __syncthreads();
+}
+
+// s_mark[e] = the start of the run that holds position e (the last mark at
+// or before e), for e < m; thread t takes positions t*CH .. t*CH + CH - 1.
+template <int NT, int CH>
+__device__ __forceinline__ void spread_marks(int* s_mark, int m, int* s_maxs) {
+  constexpr int kWaves = NT / kWave;
+  const int e0 = static_cast<int>(threadIdx.x) * CH;
+  int v[CH];
+  int run = -1;
+#pragma unroll
+  for (int c = 0; c < CH; ++c) {
+    v[c] = e0 + c < m ? s_mark[e0 + c] : -1;
+    run = v[c] > run ? v[c] : run;
+  }
+  int total;
+  int before = block_excl_max<kWaves>(run, s_maxs, total);
+#pragma unroll
+  for (int c = 0; c < CH; ++c) {
+    before = v[c] > before ? v[c] : before;
+    if (e0 + c < m) s_mark[e0 + c] = before;
+  }
+  __syncthreads();
+}
+
+// The index position e of the range is read from. Counts that do not add up
+// (never for counts a pass published) set `bad` and give index 0.
+__device__ __forceinline__ int run_src(const int* s_mark, const int* s_src, int e, int K,
+                                       bool& bad) {
+  const int h = s_mark[e];
+  const int src = h >= 0 ? s_src[h] + (e - h) : -1;
+  const bool ok = static_cast<uint32_t>(src) < static_cast<uint32_t>(K);
+  bad |= !ok;
+  return ok ? src : 0;
+}
+
+// ---------------------------------------------------------------------------
+// k_sort_local: one stable radix pass over the digit (key >> shift) &
+// (2^nbits - 1), nbits <= RB, within tile blockIdx.x. The first pass
+// (GATHER = false) reads the ids, checks their range and clears the dedup's
+// ticket and look-back words; later passes gather their tile's positions of
+// the previous pass's order. Ranking as in k_onesweep (ballot matching, per-
+// wave counters), then the tile is reordered in LDS and written back over
+// the tile's range, and each digit's run word is published.
+// ---------------------------------------------------------------------------
+template <typename KeyT, int RB, int NT, int ITEMS, bool GATHER>
+__global__ __launch_bounds__(NT) void k_sort_local(
+    const KeyT* __restrict__ keys_in, const int32_t* __restrict__ vals_in, int K, uint64_t V,
+    int shift, int nbits, const uint32_t* __restrict__ prev_runs, int prev_nbits,
+    KeyT* __restrict__ keys_out, int32_t* __restrict__ vals_out, uint32_t* __restrict__ runs,
+    int rstride, uint32_t* __restrict__ clear, int64_t clear_words,
+    int32_t* __restrict__ dev_err) {
+  constexpr int kWaves = NT / kWave;
+  constexpr int kItems = ITEMS;
+  constexpr int kTile = NT * kItems;
+  constexpr int kRadix = 1 << RB;
+  static_assert(kRadix <= NT, "a thread per digit");
+  static_assert(kTile <= int(kRunCountMask), "run starts and counts fit 16 bits");
+  constexpr int kG = GATHER ? 1 : 0;
+  __shared__ KeyT s_keys[kTile];
+  __shared__ int32_t s_vals[kTile];
+  __shared__ uint16_t s_cnt[kWaves][kRadix];  // per-wave digit counts, then offsets
+  __shared__ int32_t s_local[kRadix];         // tile-local start of each digit
+  __shared__ uint32_t s_scan[kWaves];
+  __shared__ int s_maxs[kWaves];
+  __shared__ int s_mark[kG * kTile + 1];
+  __shared__ int s_src[kG * kTile + 1];
+  __shared__ int s_dig[kG * NT + 1];
+  __shared__ uint32_t s_dstart[kG * NT + 1];
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = first_lane(tid >> 6);
+  const int tile = blockIdx.x;
+  const int64_t base = int64_t(tile) * kTile;
+  const int n = static_cast<int>(K - base < kTile ? K - base : kTile);
+  const uint32_t mask = nbits > 0 ? (1u << nbits) - 1 : 0u;
+  for (int i = tid; i < kWaves * kRadix / 2; i += NT)
+    reinterpret_cast<uint32_t*>(&s_cnt[0][0])[i] = 0;
+
+  // Item i of a lane is tile position wave*64*ITEMS + i*64 + lane: (wave, i,
+  // lane) order is position order.
+  KeyT key[kItems];
+  int32_t val[kItems];
+  if constexpr (!GATHER) {
+    for (int64_t i = int64_t(blockIdx.x) * NT + tid; i < clear_words; i += int64_t(gridDim.x) * NT)
+      clear[i] = 0;
+    bool bad = false;
+#pragma unroll
+    for (int i = 0; i < kItems; ++i) {
+      const int64_t pos = base + int64_t(wave) * (kItems * kWave) + i * kWave + lane;
+      const bool ok = pos < K;
+      key[i] = ok ? keys_in[pos] : KeyT(0);
+      val[i] = static_cast<int32_t>(pos);
+      bad |= ok && key_bits(key[i]) >= V;
+    }
+    if (ballot(bad) && lane == 0) raise_err(dev_err, LM_DEVERR_ID_RANGE);
+  } else {
+    for (int e = tid; e < n; e += NT) s_mark[e] = -1;
+    const uint32_t tot = run_total(prev_runs, gridDim.x, rstride, tid, 1 << prev_nbits);
+    uint32_t all;
+    const uint32_t start = block_excl_sum<kWaves, uint32_t>(tot, s_scan, all);
+    mark_runs<NT>(prev_runs, gridDim.x, rstride, kTile, tid, tot, start, base, n, s_mark, s_src,
+                  s_dig, s_dstart, s_scan);
+    spread_marks<NT, kItems>(s_mark, n, s_maxs);
+    bool bad = false;
+#pragma unroll
+    for (int i = 0; i < kItems; ++i) {
+      const int e = wave * (kItems * kWave) + i * kWave + lane;
+      key[i] = KeyT(0);
+      val[i] = 0;
+      if (e < n) {
+        const int src = run_src(s_mark, s_src, e, K, bad);
+        key[i] = keys_in[src];
+        val[i] = vals_in[src];
+      }
+    }
+    if (ballot(bad) && lane == 0) raise_err(dev_err, LM_DEVERR_CAPACITY);
+  }
+  __syncthreads();
+
+  uint32_t dig[kItems];
+#pragma unroll
+  for (int i = 0; i < kItems; ++i) {
+    const int e = wave * (kItems * kWave) + i * kWave + lane;
+    dig[i] = e < n ? digit_of(key[i], shift, mask) : kRadix;
+  }
+  uint32_t rank[kItems];
+#pragma unroll
+  for (int i = 0; i < kItems; ++i) {
+    const bool ok = dig[i] < kRadix;
+    uint64_t peers = ballot(ok);
+#pragma unroll
+    for (int b = 0; b < RB; ++b) {
+      if (b < nbits) {
+        const bool bit = (dig[i] >> b) & 1u;
+        const uint64_t bb = ballot(bit);
+        peers &= bit ? bb : ~bb;
+      }
+    }
+    uint32_t prior = 0;
+    if (ok) prior = s_cnt[wave][dig[i]];
+    const uint32_t below = popc_below(peers);
+    rank[i] = prior + below;
+    if (ok && below == 0) s_cnt[wave][dig[i]] = static_cast<uint16_t>(prior + __popcll(peers));
+  }
+  __syncthreads();
+
+  // Per-wave exclusive offsets of digit tid, its tile count and start.
+  uint32_t tot = 0;
+  if (tid < kRadix) {
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) {
+      const uint32_t c = s_cnt[w][tid];
+      s_cnt[w][tid] = static_cast<uint16_t>(tot);
+      tot += c;
+    }
+  }
+  uint32_t tile_sum;
+  const uint32_t local = block_excl_sum<kWaves, uint32_t>(tot, s_scan, tile_sum);
+  if (tid < kRadix) {
+    s_local[tid] = static_cast<int32_t>(local);
+    runs[size_t(tile) * rstride + tid] = (local << 16) | tot;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int i = 0; i < kItems; ++i) {
+    if (dig[i] < kRadix) {
+      const int lp = s_local[dig[i]] + static_cast<int>(s_cnt[wave][dig[i]]) + static_cast<int>(rank[i]);
+      s_keys[lp] = key[i];
+      s_vals[lp] = val[i];
+    }
+  }
+  __syncthreads();
+#pragma unroll
+  for (int i = 0; i < kItems; ++i) {
+    const int jj = tid + i * NT;
+    if (jj < n) {
+      keys_out[base + jj] = s_keys[jj];
+      vals_out[base + jj] = s_vals[jj];
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
 // A thread's run of N consecutive elements from p (aligned to the run's
 // bytes) in 16- or 8-byte loads: the scalar form spread each load
 // instruction of a wave over 64 runs, one line each, and the compiler cannot
@@ -504,29 +785,71 @@ __device__ __forceinline__ void load_run(const T* __restrict__ p, T (&out)[N]) {
 // ---------------------------------------------------------------------------
 // k_dedup: thread t of tile `tile` owns the ITEMS sorted positions
 // base + ITEMS*t .. base + ITEMS*t + ITEMS - 1 (runs read in 16-byte loads;
-// the permutation too when the caller's buffer is 16-byte aligned).
+// the permutation too when the caller's buffer is 16-byte aligned). With
+// GATHER, skeys and perm hold the last tile-local pass (k_sort_local), whose
+// runs words are `runs`: the tile gathers its positions (and the one on
+// either side) from them and writes the permutation to perm_out.
 // ---------------------------------------------------------------------------
-template <typename KeyT, int NT, int ITEMS, bool PERM_RUNS>
+template <typename KeyT, int NT, int ITEMS, bool PERM_RUNS, bool GATHER>
 __global__ __launch_bounds__(NT) void k_dedup(
     const KeyT* __restrict__ skeys, const int32_t* __restrict__ perm, int K, int cap,
     KeyT* __restrict__ uniq, int32_t* __restrict__ counts, int32_t* __restrict__ offsets,
     int32_t* __restrict__ inverse, int64_t* __restrict__ num_unique,
     uint64_t* __restrict__ status, uint32_t* __restrict__ ticket, int32_t* __restrict__ dev_err,
-    WaitCfg wc) {
+    WaitCfg wc, const uint32_t* __restrict__ runs, int runs_nbits, int rstride,
+    int32_t* __restrict__ perm_out) {
   constexpr int kWaves = NT / kWave;
   constexpr int kItems = ITEMS;
   constexpr int kTile = NT * kItems;
+  constexpr int kG = GATHER ? 1 : 0;
   __shared__ uint32_t s_scan[kWaves];
   __shared__ int s_maxs[kWaves];
   __shared__ uint32_t s_tile;
   __shared__ uint32_t s_excl_heads;
   __shared__ int s_excl_last;
+  __shared__ int s_mark[kG * (kTile + 2) + 1];
+  __shared__ int s_src[kG * (kTile + 2) + 1];
+  __shared__ int s_dig[kG * NT + 1];
+  __shared__ uint32_t s_dstart[kG * NT + 1];
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = first_lane(tid >> 6);
   if (tid == 0) s_tile = add_agent(ticket, 1u);
   KeyT k[kItems], kprev, knext;
   int32_t src[kItems];
+  int tile;
+  if constexpr (GATHER) {
+    // Positions base-1 .. base+kTile of the last pass's order (within [0, K)).
+    for (int e = tid; e < kTile + 2; e += NT) s_mark[e] = -1;
+    const uint32_t tot = run_total(runs, gridDim.x, rstride, tid, 1 << runs_nbits);
+    uint32_t all;
+    const uint32_t start = block_excl_sum<kWaves, uint32_t>(tot, s_scan, all);
+    tile = first_lane(static_cast<int>(s_tile));
+    const int64_t base = int64_t(tile) * kTile;
+    const int64_t gs = base > 0 ? base - 1 : 0;
+    const int64_t ge = base + kTile + 1 < K ? base + kTile + 1 : K;
+    const int m = static_cast<int>(ge - gs);
+    mark_runs<NT>(runs, gridDim.x, rstride, kTile, tid, tot, start, gs, m, s_mark, s_src, s_dig,
+                  s_dstart, s_scan);
+    spread_marks<NT, kItems + 1>(s_mark, m, s_maxs);
+    const int64_t p0 = base + int64_t(tid) * kItems;
+    bool bad = false;
+#pragma unroll
+    for (int i = 0; i < kItems; ++i) {
+      k[i] = KeyT(0);
+      src[i] = 0;
+      if (p0 + i < K) {
+        const int j = run_src(s_mark, s_src, static_cast<int>(p0 + i - gs), K, bad);
+        k[i] = skeys[j];
+        src[i] = perm[j];
+      }
+    }
+    kprev = KeyT(0);
+    knext = KeyT(0);
+    if (p0 > 0 && p0 - 1 < K) kprev = skeys[run_src(s_mark, s_src, static_cast<int>(p0 - 1 - gs), K, bad)];
+    if (p0 + kItems < K) knext = skeys[run_src(s_mark, s_src, static_cast<int>(p0 + kItems - gs), K, bad)];
+    if (ballot(bad) && lane == 0) raise_err(dev_err, LM_DEVERR_CAPACITY);
+  } else {
   auto fetch = [&](int64_t base) {
     const int64_t p0 = base + int64_t(tid) * kItems;
     if (p0 + kItems <= K) {  // a whole run: the workspace keys are 256-byte aligned
@@ -550,9 +873,10 @@ __global__ __launch_bounds__(NT) void k_dedup(
   };
   fetch(int64_t(blockIdx.x) * kTile);
   __syncthreads();
-  const int tile = first_lane(static_cast<int>(s_tile));
+  tile = first_lane(static_cast<int>(s_tile));
+  if (tile != static_cast<int>(blockIdx.x)) fetch(int64_t(tile) * kTile);
+  }
   const int64_t base = int64_t(tile) * kTile;
-  if (tile != static_cast<int>(blockIdx.x)) fetch(base);
   const int64_t p0 = base + int64_t(tid) * kItems;
 
   // Run heads and tails as bit masks (bit i: item i), evaluated without
@@ -646,6 +970,7 @@ __global__ __launch_bounds__(NT) void k_dedup(
       if (((tmask >> i) & 1u) && in_cap) counts[seg] = static_cast<int32_t>(p + 1 - hp);
       if (static_cast<uint32_t>(src[i]) < static_cast<uint32_t>(K)) inverse[src[i]] = seg;
       else over = true;
+      if constexpr (GATHER) perm_out[p] = src[i];
       if (p == K - 1) {
         *num_unique = seg + 1 < cap ? seg + 1 : cap;
         offsets[seg + 1 < cap ? seg + 1 : cap] = K;
@@ -906,8 +1231,41 @@ static int run_unique(const KeyT* ids, int K, int64_t V, KeyT* uniq, int32_t* co
   KeyT* kb[2] = {reinterpret_cast<KeyT*>(ws + L.keys0), reinterpret_cast<KeyT*>(ws + L.keys1)};
   int32_t* vb[2] = {reinterpret_cast<int32_t*>(ws + L.vals0), reinterpret_cast<int32_t*>(ws + L.vals1)};
 
-  // tickets .. end of dstatus is contiguous: k_hist clears it.
+  // tickets .. end of dstatus is contiguous: k_hist (or the first
+  // tile-local pass) clears it.
   const int64_t clear_words = static_cast<int64_t>((L.keys0 - L.tickets) / 4);
+  if (L.gather) {
+    // Tile-local passes (1024 threads, 2 keys each); the runs words of pass
+    // p and tile t sit in the histogram region at row p * tiles + t.
+    for (int p = 0; p < L.passes; ++p) {
+      const KeyT* kin = p == 0 ? ids : kb[(p - 1) & 1];
+      const int32_t* vin = p == 0 ? nullptr : vb[(p - 1) & 1];
+      const uint32_t* prev = p == 0 ? nullptr : bhist + size_t(p - 1) * L.tiles * L.rstride;
+      const int prev_nbits = p == 0 ? 0 : L.nbits[p - 1];
+      uint32_t* runs = bhist + size_t(p) * L.tiles * L.rstride;
+      auto pass = [&](auto rb, auto gather) {
+        k_sort_local<KeyT, decltype(rb)::value, 1024, 2, decltype(gather)::value>
+            <<<L.tiles, 1024, 0, st>>>(kin, vin, K, static_cast<uint64_t>(V), L.shift[p],
+                                       L.nbits[p], prev, prev_nbits, kb[p & 1], vb[p & 1], runs,
+                                       L.rstride, tickets, clear_words, dev_err);
+      };
+      const bool narrow = L.nbits[p] <= kSmallDigitBits;
+      if (p == 0) {
+        if (narrow) pass(I<kSmallDigitBits>{}, std::false_type{});
+        else pass(I<kLargeDigitBits>{}, std::false_type{});
+      } else {
+        if (narrow) pass(I<kSmallDigitBits>{}, std::true_type{});
+        else pass(I<kLargeDigitBits>{}, std::true_type{});
+      }
+      if (hipError_t e = hipGetLastError(); e != hipSuccess) return launch_status(e);
+    }
+    const int q = L.passes - 1;
+    k_dedup<KeyT, 1024, 2, false, true><<<L.tiles, 1024, 0, st>>>(
+        kb[q & 1], vb[q & 1], K, cap, uniq, counts, offsets, inverse, num_unique, dstatus,
+        tickets + kMaxPasses, dev_err, wait_cfg(), bhist + size_t(q) * L.tiles * L.rstride,
+        L.nbits[q], L.rstride, perm);
+    return launch_status(hipGetLastError());
+  }
   const size_t hist_lds = size_t(L.passes) * L.rstride * 4;
   k_hist<KeyT><<<L.hist_blocks, kHistThreads, hist_lds, st>>>(
       ids, K, static_cast<uint64_t>(V), L.passes, L.rstride, pb, bhist, tickets, clear_words,
@@ -946,15 +1304,13 @@ static int run_unique(const KeyT* ids, int K, int64_t V, KeyT* uniq, int32_t* co
   auto dedup = [&](auto nt, auto items) {
     constexpr int NT = decltype(nt)::value, IT = decltype(items)::value;
     if (perm_runs)
-      k_dedup<KeyT, NT, IT, true><<<L.tiles, NT, 0, st>>>(kin, perm, K, cap, uniq, counts,
-                                                          offsets, inverse, num_unique, dstatus,
-                                                          tickets + kMaxPasses, dev_err,
-                                                          wait_cfg());
+      k_dedup<KeyT, NT, IT, true, false><<<L.tiles, NT, 0, st>>>(
+          kin, perm, K, cap, uniq, counts, offsets, inverse, num_unique, dstatus,
+          tickets + kMaxPasses, dev_err, wait_cfg(), nullptr, 0, 0, nullptr);
     else
-      k_dedup<KeyT, NT, IT, false><<<L.tiles, NT, 0, st>>>(kin, perm, K, cap, uniq, counts,
-                                                           offsets, inverse, num_unique, dstatus,
-                                                           tickets + kMaxPasses, dev_err,
-                                                           wait_cfg());
+      k_dedup<KeyT, NT, IT, false, false><<<L.tiles, NT, 0, st>>>(
+          kin, perm, K, cap, uniq, counts, offsets, inverse, num_unique, dstatus,
+          tickets + kMaxPasses, dev_err, wait_cfg(), nullptr, 0, 0, nullptr);
   };
   if (L.nt == 256) {
     if (L.items == 2) dedup(I<256>{}, I<2>{});

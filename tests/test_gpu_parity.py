@@ -101,6 +101,14 @@ UNIQUE_CASES = [
     # (20- and 40-bit keys above)
     (7000, 20_000, 1.2, np.int32, 37), (8000, 2**31 - 1, 0.0, np.int32, 38),
     (5000, 2**62, 0.8, np.int64, 39),
+    # tile-local passes joined by gathers (1024-thread tiles, 16 to 64 of
+    # them; the cases above from 30,721 to 131,072 ids take them too): the
+    # last K before them and the first, one pass over 0 key bits, one 9-bit
+    # pass, two 9-bit passes, three 7-bit passes, 64 tiles of 40-bit keys
+    (30_720, 800_000, 1.0, np.int32, 43), (30_721, 800_000, 1.0, np.int32, 44),
+    (40_000, 1, 1.0, np.int32, 40), (40_000, 300, 1.0, np.int32, 45),
+    (65_536, 1 << 18, 1.0, np.int64, 46), (70_001, 1 << 21, 1.0, np.int32, 41),
+    (131_072, 2**40, 0.9, np.int64, 42),
 ]
 
 
@@ -119,7 +127,7 @@ def test_unique_random(lz, K, V, s, dt, seed):
     H.assert_unique_matches(res, ids, V, oracle, f"K={K} V={V}")
 
 
-@pytest.mark.parametrize("K", [9000, 8192, 1024])
+@pytest.mark.parametrize("K", [70_000, 9000, 8192, 1024])
 def test_unique_all_same_and_all_distinct(lz, K):
     # 8192 and 1024: a full one-workgroup tile, every id its own type
     same = np.full(K, 4242, np.int32)
@@ -149,6 +157,22 @@ def test_unique_out_of_range_sets_error(lz):
     res = lz.unique(_t(ids), 10)
     torch.cuda.synchronize()
     assert int(res.dev_err.item()) & lz.DEVERR_ID_RANGE
+
+
+@pytest.mark.parametrize("K", [12_000, 70_000, 300_000])
+def test_unique_out_of_range_sets_error_multi_tile(lz, K):
+    # 256-thread tiles, tile-local passes, 1024-thread look-back passes: one
+    # id past V in the last tile, one negative id in the first
+    ids = synth.zipf_ids(K, 1000, 1.0, 62, np.int32)
+    ids[K - 1] = 1000
+    res = lz.unique(_t(ids), 1000)
+    ids2 = ids.copy()
+    ids2[K - 1] = 7
+    ids2[3] = -1
+    res2 = lz.unique(_t(ids2), 1000)
+    torch.cuda.synchronize()
+    assert int(res.dev_err.item()) & lz.DEVERR_ID_RANGE
+    assert int(res2.dev_err.item()) & lz.DEVERR_ID_RANGE
 
 
 @pytest.mark.parametrize("K,V,dt", [(70_000, 800_000, np.int32), (9000, 100_000, np.int64),
