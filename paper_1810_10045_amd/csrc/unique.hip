@@ -55,7 +55,7 @@ constexpr int kBlockThreadsHost = 1024;  // threads of k_unique_block
 #define LMZ_UNIQUE_GATHER_MAX_TILES 64 // a wave holds one digit's runs of every tile
 #endif
 #ifndef LMZ_UNIQUE_GATHER_MIN_TILES
-#define LMZ_UNIQUE_GATHER_MIN_TILES 16 // fewer tiles: the look-back passes are faster
+#define LMZ_UNIQUE_GATHER_MIN_TILES 12 // fewer tiles: the look-back passes are faster
 #endif
 #ifndef LMZ_UNIQUE_GATHER_DIGIT_BITS
 #define LMZ_UNIQUE_GATHER_DIGIT_BITS 9 // widest digit of the tile-local passes
@@ -151,6 +151,12 @@ static UniqueLayout unique_layout(int64_t K, int idtype, int64_t V) {
   L.items = items_for(K, L.nt);
   const int64_t tile_keys = int64_t(L.nt) * L.items;
   L.tiles = static_cast<int>((K + tile_keys - 1) / tile_keys);
+  // Tile-local passes joined by gathers (k_sort_local) from 12 to 64 tiles,
+  // with digits of at most 9 bits: a gather adds up every tile's count of
+  // each digit, which 10-bit digits made the larger cost. Measured per call
+  // (us, look-back passes / gathers): 65,536 ids at V = 800K 37.1 / 32.0
+  // (10-bit digits: 38.1), 131,072 ids 43.0 / 33.7, 24,576 ids 32.6 / 31.5;
+  // at 9 tiles (16,385 ids, V = 262,144) 31.9 / 36.2.
   L.gather = LMZ_UNIQUE_GATHER && !L.block_items && L.nt == 1024 && L.items == 2 &&
              L.tiles <= LMZ_UNIQUE_GATHER_MAX_TILES && L.tiles >= LMZ_UNIQUE_GATHER_MIN_TILES;
   const int narrow = kSmallDigitBits < kLargeDigitBits ? kSmallDigitBits : kLargeDigitBits;
@@ -508,49 +514,63 @@ __global__ __launch_bounds__(NT) void k_onesweep(
 // ---------------------------------------------------------------------------
 constexpr uint32_t kRunCountMask = 0xFFFFu;
 
-// Keys of digit d over every tile of the previous pass (0 for d >= R).
+// Keys of digit d over every tile of the previous pass, for thread d < R (0
+// for the others); R is a power of two. The threads split the rows: thread
+// tid adds up rows g, g + G, ... of digit tid % R (g = tid / R, G = the
+// number of such groups, at most 16), and thread d then adds the G sums.
+template <int NT>
 __device__ __forceinline__ uint32_t run_total(const uint32_t* __restrict__ runs, int tiles,
-                                              int rstride, int d, int R) {
-  uint32_t tot = 0;
-  if (d < R) {
-    constexpr int kRows = 32;  // loads in flight per round
-    for (int t0 = 0; t0 < tiles; t0 += kRows) {
-      uint32_t w[kRows];
+                                              int rstride, int R, uint32_t* s_part) {
+  const int tid = threadIdx.x;
+  const int G = NT / R < 16 ? NT / R : 16;
+  const int d = tid & (R - 1), g = tid / R;
+  uint32_t part = 0;
+  if (g < G) {
+    constexpr int kU = 8;  // loads in flight per round
+    for (int t0 = g; t0 < tiles; t0 += kU * G) {
+      uint32_t w[kU];
 #pragma unroll
-      for (int r = 0; r < kRows; ++r) {
-        const int t = t0 + r < tiles ? t0 + r : t0;  // repeat a valid row, unused
-        w[r] = runs[size_t(t) * rstride + d];
+      for (int u = 0; u < kU; ++u) {
+        const int t = t0 + u * G < tiles ? t0 + u * G : t0;  // repeat a valid row, unused
+        w[u] = runs[size_t(t) * rstride + d];
       }
 #pragma unroll
-      for (int r = 0; r < kRows; ++r) tot += t0 + r < tiles ? (w[r] & kRunCountMask) : 0u;
+      for (int u = 0; u < kU; ++u) part += t0 + u * G < tiles ? (w[u] & kRunCountMask) : 0u;
     }
+    s_part[g * R + d] = part;
   }
+  __syncthreads();
+  uint32_t tot = 0;
+  if (tid < R)
+    for (int j = 0; j < G; ++j) tot += s_part[j * R + tid];
   return tot;
 }
 
 // Marks where each (digit, tile) run starts among the positions gs .. gs+m-1
-// of the previous pass's order: s_mark[e] = e at the first position e of a
-// run within the range (the caller set -1 everywhere before), s_src[e] = the
-// index that position is read from. Thread d holds digit d's total `tot`
-// and its start D(d). A wave takes one digit at a time, lane t the run of
-// tile t (tiles <= 64), and a wave prefix sum places the runs.
+// (m >= 1) of the previous pass's order: s_mark[e] = e at the first position
+// e of a run within the range (the caller set -1 everywhere before), s_src[e]
+// = the index that position is read from. Thread d < R holds digit d's total
+// `tot` and its start D(d); the caller set s_lohi to {0, -1} before a barrier.
+// The digits that reach into the range form one interval, from the digit
+// holding position gs to the one holding gs+m-1. A wave takes one digit of it
+// at a time, lane t the run of tile t (tiles <= 64), and a wave prefix sum
+// places the runs.
 template <int NT>
 __device__ __forceinline__ void mark_runs(const uint32_t* __restrict__ runs, int tiles,
-                                          int rstride, int tile_keys, int d, uint32_t tot,
+                                          int rstride, int tile_keys, int R, uint32_t tot,
                                           uint32_t start, int64_t gs, int m, int* s_mark,
-                                          int* s_src, int* s_dig, uint32_t* s_dstart,
-                                          uint32_t* s_scan) {
+                                          int* s_src, uint32_t* s_dstart, int* s_lohi) {
   constexpr int kWaves = NT / kWave;
-  const int lane = threadIdx.x & 63;
-  const int wave = first_lane(static_cast<int>(threadIdx.x) >> 6);
-  const bool ov = tot > 0 && int64_t(start) < gs + m && int64_t(start) + tot > gs;
-  uint32_t nd;
-  const uint32_t q = block_excl_sum<kWaves, uint32_t>(ov ? 1u : 0u, s_scan, nd);
-  if (ov) {
-    s_dig[q] = d;
-    s_dstart[q] = start;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = first_lane(tid >> 6);
+  if (tid < R) {
+    s_dstart[tid] = start;
+    if (tot > 0 && int64_t(start) <= gs && int64_t(start) + tot > gs) s_lohi[0] = tid;
+    if (tot > 0 && int64_t(start) < gs + m && int64_t(start) + tot >= gs + m) s_lohi[1] = tid;
   }
   __syncthreads();
+  const int dlo = first_lane(s_lohi[0]);
+  const int dhi = first_lane(s_lohi[1] < R ? s_lohi[1] : R - 1);
   auto place = [&](uint32_t w, uint32_t dstart) {
     const uint32_t c = w & kRunCountMask;
     const int64_t g = int64_t(dstart) + (wave_incl_sum(c) - c);
@@ -563,14 +583,13 @@ __device__ __forceinline__ void mark_runs(const uint32_t* __restrict__ runs, int
     }
   };
   // Two digits per round: their loads fly together.
-  for (int q0 = wave; q0 < static_cast<int>(nd); q0 += 2 * kWaves) {
-    const int q1 = q0 + kWaves;
-    const bool two = q1 < static_cast<int>(nd);
-    const int d0 = s_dig[q0], d1 = two ? s_dig[q1] : d0;
+  for (int d0 = dlo + wave; d0 <= dhi; d0 += 2 * kWaves) {
+    const int d1 = d0 + kWaves;
+    const bool two = d1 <= dhi;
     const uint32_t w0 = lane < tiles ? runs[size_t(lane) * rstride + d0] : 0u;
     const uint32_t w1 = two && lane < tiles ? runs[size_t(lane) * rstride + d1] : 0u;
-    place(w0, s_dstart[q0]);
-    if (two) place(w1, s_dstart[q1]);
+    place(w0, s_dstart[d0]);
+    if (two) place(w1, s_dstart[d1]);
   }
   __syncthreads();
 }
@@ -640,8 +659,8 @@ __global__ __launch_bounds__(NT) void k_sort_local(
   __shared__ int s_maxs[kWaves];
   __shared__ int s_mark[kG * kTile + 1];
   __shared__ int s_src[kG * kTile + 1];
-  __shared__ int s_dig[kG * NT + 1];
-  __shared__ uint32_t s_dstart[kG * NT + 1];
+  __shared__ uint32_t s_dstart[kG * NT + 1];  // also the partial totals
+  __shared__ int s_lohi[2];
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = first_lane(tid >> 6);
@@ -671,11 +690,13 @@ __global__ __launch_bounds__(NT) void k_sort_local(
     if (ballot(bad) && lane == 0) raise_err(dev_err, LM_DEVERR_ID_RANGE);
   } else {
     for (int e = tid; e < n; e += NT) s_mark[e] = -1;
-    const uint32_t tot = run_total(prev_runs, gridDim.x, rstride, tid, 1 << prev_nbits);
+    if (tid == 0) { s_lohi[0] = 0; s_lohi[1] = -1; }
+    const int R = 1 << prev_nbits;
+    const uint32_t tot = run_total<NT>(prev_runs, gridDim.x, rstride, R, s_dstart);
     uint32_t all;
     const uint32_t start = block_excl_sum<kWaves, uint32_t>(tot, s_scan, all);
-    mark_runs<NT>(prev_runs, gridDim.x, rstride, kTile, tid, tot, start, base, n, s_mark, s_src,
-                  s_dig, s_dstart, s_scan);
+    mark_runs<NT>(prev_runs, gridDim.x, rstride, kTile, R, tot, start, base, n, s_mark, s_src,
+                  s_dstart, s_lohi);
     spread_marks<NT, kItems>(s_mark, n, s_maxs);
     bool bad = false;
 #pragma unroll
@@ -809,8 +830,8 @@ __global__ __launch_bounds__(NT) void k_dedup(
   __shared__ int s_excl_last;
   __shared__ int s_mark[kG * (kTile + 2) + 1];
   __shared__ int s_src[kG * (kTile + 2) + 1];
-  __shared__ int s_dig[kG * NT + 1];
-  __shared__ uint32_t s_dstart[kG * NT + 1];
+  __shared__ uint32_t s_dstart[kG * NT + 1];  // also the partial totals
+  __shared__ int s_lohi[2];
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = first_lane(tid >> 6);
@@ -821,7 +842,9 @@ __global__ __launch_bounds__(NT) void k_dedup(
   if constexpr (GATHER) {
     // Positions base-1 .. base+kTile of the last pass's order (within [0, K)).
     for (int e = tid; e < kTile + 2; e += NT) s_mark[e] = -1;
-    const uint32_t tot = run_total(runs, gridDim.x, rstride, tid, 1 << runs_nbits);
+    if (tid == 0) { s_lohi[0] = 0; s_lohi[1] = -1; }
+    const int R = 1 << runs_nbits;
+    const uint32_t tot = run_total<NT>(runs, gridDim.x, rstride, R, s_dstart);
     uint32_t all;
     const uint32_t start = block_excl_sum<kWaves, uint32_t>(tot, s_scan, all);
     tile = first_lane(static_cast<int>(s_tile));
@@ -829,8 +852,8 @@ __global__ __launch_bounds__(NT) void k_dedup(
     const int64_t gs = base > 0 ? base - 1 : 0;
     const int64_t ge = base + kTile + 1 < K ? base + kTile + 1 : K;
     const int m = static_cast<int>(ge - gs);
-    mark_runs<NT>(runs, gridDim.x, rstride, kTile, tid, tot, start, gs, m, s_mark, s_src, s_dig,
-                  s_dstart, s_scan);
+    mark_runs<NT>(runs, gridDim.x, rstride, kTile, R, tot, start, gs, m, s_mark, s_src, s_dstart,
+                  s_lohi);
     spread_marks<NT, kItems + 1>(s_mark, m, s_maxs);
     const int64_t p0 = base + int64_t(tid) * kItems;
     bool bad = false;

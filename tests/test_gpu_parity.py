@@ -101,11 +101,11 @@ UNIQUE_CASES = [
     # (20- and 40-bit keys above)
     (7000, 20_000, 1.2, np.int32, 37), (8000, 2**31 - 1, 0.0, np.int32, 38),
     (5000, 2**62, 0.8, np.int64, 39),
-    # tile-local passes joined by gathers (1024-thread tiles, 16 to 64 of
-    # them; the cases above from 30,721 to 131,072 ids take them too): the
+    # tile-local passes joined by gathers (1024-thread tiles, 12 to 64 of
+    # them; the cases above from 22,529 to 131,072 ids take them too): the
     # last K before them and the first, one pass over 0 key bits, one 9-bit
     # pass, two 9-bit passes, three 7-bit passes, 64 tiles of 40-bit keys
-    (30_720, 800_000, 1.0, np.int32, 43), (30_721, 800_000, 1.0, np.int32, 44),
+    (22_528, 800_000, 1.0, np.int32, 43), (22_529, 800_000, 1.0, np.int32, 44),
     (40_000, 1, 1.0, np.int32, 40), (40_000, 300, 1.0, np.int32, 45),
     (65_536, 1 << 18, 1.0, np.int64, 46), (70_001, 1 << 21, 1.0, np.int32, 41),
     (131_072, 2**40, 0.9, np.int64, 42),
