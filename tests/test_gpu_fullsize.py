@@ -265,3 +265,36 @@ def test_full_sampled_softmax(lz, rule):
     rows_t = torch.from_numpy(o[0]).to(table.device)
     H.assert_sgd_rows(table[rows_t].cpu().numpy(), ref, S, lr, H.row_delta(S, H.TOL_F32, sq))
     _release(pipe)
+
+
+def test_overlapped_schedule_matches_serial(lz):
+    """bench.py's overlapped schedule (the Unique calls on a second stream,
+    up to three steps ahead, with four sets of their outputs) leaves the
+    same SGD table, bit for bit, as the serial steps: every Seg-Sum reads
+    the Unique of its own batch and no Unique overwrites a set still in
+    use. Seven steps wrap around the four sets."""
+    import bench
+    w = synth.WORKLOADS["word_step_64k"]
+    dev = torch.device("cuda:0")
+    nb, steps = 3, 7
+    _say(f"[fullsize] overlapped vs serial: {w.name}, {nb} batches, {steps} steps")
+    batches = [bench.Batch(w.batch(b), torch, dev) for b in range(nb)]
+    table0 = w.table()
+    serial = bench.Pipeline(w, batches, torch, lz, dev, table=table0)
+    for i in range(steps):
+        serial.step(i)
+    torch.cuda.synchronize()
+    serial.check()
+    want = serial.state["table"]
+    pipe = bench.Pipeline(w, batches, torch, lz, dev, table=table0)
+    pipe.enable_overlap()
+    main, side = torch.cuda.current_stream(), torch.cuda.Stream(device=dev)
+    sync = bench.HipEvents(2 * steps + 2, timing=False)
+    pipe.run_overlapped(0, steps, torch, main, side, sync)
+    torch.cuda.synchronize()
+    sync.close()
+    pipe.check()
+    assert torch.equal(pipe.state["table"], want)
+    assert not torch.equal(want, torch.from_numpy(table0).to(dev)), "the steps changed the table"
+    del serial, pipe, want, batches
+    torch.cuda.empty_cache()
