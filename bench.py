@@ -202,8 +202,8 @@ class Pipeline:
         dev = self.ures.uniq.device
         idt = self.ures.uniq.dtype
         self.ws_u = lz.Workspace(dev)
-        self.ws_u.get(max(lz._lib.lm_unique_workspace_bytes(w.tokens, lz._idtype(self.ures.uniq), w.V),
-                          lz._lib.lm_unique_workspace_bytes(w.K, lz._idtype(self.ures.uniq), w.V)))
+        self.ws_u.get(max(lz.unique_workspace_bytes(w.tokens, w.V, idt),
+                          lz.unique_workspace_bytes(w.K, w.V, idt)))
         u0 = self.state.get("u0")
         self.sets = [(self.ures, u0)] + [
             (lz.unique_buffers(w.tokens, w.V, idt, dev),

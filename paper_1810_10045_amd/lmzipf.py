@@ -8,7 +8,8 @@ been built, importing this module raises — there is no fallback path.
 Entry points have the C names without the ``lm_`` prefix: ``unique``,
 ``segsum``, ``map_ids``, ``fill_values``, ``sparse_apply``, the binary16
 payload forms ``fill_values_f16`` and ``sparse_apply_f16``, and
-``sample_ids``.
+``sample_ids``; ``unique_workspace_bytes`` is the workspace query that
+``unique`` makes itself, for callers that size a workspace up front.
 """
 from __future__ import annotations
 
@@ -187,6 +188,13 @@ def unique_buffers(K: int, V: int, id_dtype, device) -> UniqueResult:
         torch.empty(cap + 1, dtype=torch.int32, **z), torch.empty(max(K, 1), dtype=torch.int32, **z),
         torch.empty(max(K, 1), dtype=torch.int32, **z), torch.zeros(1, dtype=torch.int64, **z),
         torch.zeros(1, dtype=torch.int32, **z))
+
+
+def unique_workspace_bytes(K: int, V: int, id_dtype=torch.int32) -> int:
+    """lm_unique_workspace_bytes: the workspace one lm_unique call of K ids
+    of dtype id_dtype over [0, V) needs (0: the sizes are rejected)."""
+    idt = I64 if id_dtype == torch.int64 else I32
+    return int(_lib.lm_unique_workspace_bytes(K, idt, V))
 
 
 def unique(ids: torch.Tensor, V: int, out: Optional[UniqueResult] = None,
