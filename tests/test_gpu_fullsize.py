@@ -267,25 +267,46 @@ def test_full_sampled_softmax(lz, rule):
     _release(pipe)
 
 
-def test_overlapped_schedule_matches_serial(lz):
+def _overlap_case(name):
+    w = synth.WORKLOADS[name if name in synth.WORKLOADS else "merge_64x32k_bf16"]
+    if name == "merge_8x32k_bf16":
+        import dataclasses
+        w = dataclasses.replace(w, name=name, shards=8)
+    return w
+
+
+def _final_state(pipe, ures):
+    """What the steps leave behind: the table for SGD, else the EXPAND
+    destination rows of the last step's merged types (rows past them are
+    never written)."""
+    if "table" in pipe.state:
+        return pipe.state["table"]
+    U = int(ures.num_unique.item())
+    return pipe.state["M"][:U]
+
+
+@pytest.mark.parametrize("name", ["word_step_64k", "sampled_softmax_64x1024_G", "merge_8x32k_bf16"])
+def test_overlapped_schedule_matches_serial(lz, name):
     """bench.py's overlapped schedule (the Unique calls on a second stream,
     up to three steps ahead, with four sets of their outputs) leaves the
-    same SGD table, bit for bit, as the serial steps: every Seg-Sum reads
-    the Unique of its own batch and no Unique overwrites a set still in
-    use. Seven steps wrap around the four sets."""
+    same result, bit for bit, as the serial steps: every Seg-Sum reads the
+    Unique of its own batch and no Unique overwrites a set still in use.
+    Seven steps wrap around the four sets. The sampled-softmax case also
+    draws its candidate ids on the second stream; the merge runs two Unique
+    calls per step (the merged list and shard 0's own)."""
     import bench
-    w = synth.WORKLOADS["word_step_64k"]
+    w = _overlap_case(name)
     dev = torch.device("cuda:0")
     nb, steps = 3, 7
     _say(f"[fullsize] overlapped vs serial: {w.name}, {nb} batches, {steps} steps")
     batches = [bench.Batch(w.batch(b), torch, dev) for b in range(nb)]
-    table0 = w.table()
+    table0 = w.table() if w.step in ("sgd", "softmax_sgd") else None
     serial = bench.Pipeline(w, batches, torch, lz, dev, table=table0)
     for i in range(steps):
         serial.step(i)
     torch.cuda.synchronize()
     serial.check()
-    want = serial.state["table"]
+    want = _final_state(serial, serial.ures)
     pipe = bench.Pipeline(w, batches, torch, lz, dev, table=table0)
     pipe.enable_overlap()
     main, side = torch.cuda.current_stream(), torch.cuda.Stream(device=dev)
@@ -294,7 +315,12 @@ def test_overlapped_schedule_matches_serial(lz):
     torch.cuda.synchronize()
     sync.close()
     pipe.check()
-    assert torch.equal(pipe.state["table"], want)
-    assert not torch.equal(want, torch.from_numpy(table0).to(dev)), "the steps changed the table"
-    del serial, pipe, want, batches
+    last = pipe.sets[(steps - 1) % len(pipe.sets)][0]
+    got = _final_state(pipe, last)
+    U = int(serial.ures.num_unique.item())
+    assert int(last.num_unique.item()) == U and torch.equal(last.uniq[:U], serial.ures.uniq[:U])
+    assert got.shape == want.shape and torch.equal(got, want)
+    if table0 is not None:
+        assert not torch.equal(want, torch.from_numpy(table0).to(dev)), "the steps changed the table"
+    del serial, pipe, want, got, batches
     torch.cuda.empty_cache()
