@@ -66,6 +66,7 @@ constexpr int kBlockThreadsHost = 1024;  // threads of k_unique_block
 constexpr int kSmallDigitBits = LMZ_UNIQUE_DIGIT_BITS;
 constexpr int kLargeDigitBits = LMZ_UNIQUE_DIGIT_BITS_LARGE;
 constexpr int kMaxPasses = 8;              // ceil(64 / 8)
+constexpr int kGatherSmallTileKeys = 1024;  // keys per 256-thread tile-local workgroup
 // Keys per thread of a sort or dedup tile, by input size: bigger tiles mean
 // fewer tiles for the look-back to pass, smaller ones spread a small input
 // over more CUs. Measured best: with 256-thread tiles, 2 keys up to 16K ids
@@ -159,6 +160,21 @@ static UniqueLayout unique_layout(int64_t K, int idtype, int64_t V) {
   // at 9 tiles (16,385 ids, V = 262,144) 31.9 / 36.2.
   L.gather = LMZ_UNIQUE_GATHER && !L.block_items && L.nt == 1024 && L.items == 2 &&
              L.tiles <= LMZ_UNIQUE_GATHER_MAX_TILES && L.tiles >= LMZ_UNIQUE_GATHER_MIN_TILES;
+  // Where tiles of 1024 keys still number at most 64 (up to 65,536 ids),
+  // 256-thread workgroups take them, with digits of at most 8 bits so that
+  // every gathering workgroup has a thread per digit of the pass before.
+  // Four-wave workgroups fit beside the one-wave Seg-Sum and update
+  // workgroups of an earlier step when Unique runs on a stream of its own:
+  // measured at 65,536 ids over 800K words, 34 -> 36 us per call alone, and
+  // the overlapped word step 143.6 -> 129.6 us.
+  if (L.gather) {
+    const int64_t small_tiles = (K + kGatherSmallTileKeys - 1) / kGatherSmallTileKeys;
+    if (small_tiles <= LMZ_UNIQUE_GATHER_MAX_TILES) {
+      L.nt = 256;
+      L.items = kGatherSmallTileKeys / 256;
+      L.tiles = static_cast<int>(small_tiles);
+    }
+  }
   const int narrow = kSmallDigitBits < kLargeDigitBits ? kSmallDigitBits : kLargeDigitBits;
   // The one workgroup takes digits of up to 10 bits (a thread per digit):
   // the fewest passes, with the narrowest digits that reach them (17-bit
@@ -166,7 +182,7 @@ static UniqueLayout unique_layout(int64_t K, int idtype, int64_t V) {
   // 8-bit passes at 17-bit keys, 24.2 against 25.8 us at 20-bit keys; where
   // wider digits save no pass (15 and 31 bits) 8-bit ones stay faster.
   const int widest = L.block_items ? kLargeDigitBits
-                     : L.gather  ? LMZ_UNIQUE_GATHER_DIGIT_BITS
+                     : L.gather  ? (L.nt == 256 ? kSmallDigitBits : LMZ_UNIQUE_GATHER_DIGIT_BITS)
                                  : (L.nt == 256 ? kSmallDigitBits : kLargeDigitBits);
   const int p_narrow = (L.bits + narrow - 1) / narrow, p_wide = (L.bits + widest - 1) / widest;
   L.passes = L.bits == 0 ? 1 : (p_wide < p_narrow ? p_wide : p_narrow);
@@ -1258,36 +1274,48 @@ static int run_unique(const KeyT* ids, int K, int64_t V, KeyT* uniq, int32_t* co
   // tile-local pass) clears it.
   const int64_t clear_words = static_cast<int64_t>((L.keys0 - L.tickets) / 4);
   if (L.gather) {
-    // Tile-local passes (1024 threads, 2 keys each); the runs words of pass
-    // p and tile t sit in the histogram region at row p * tiles + t.
-    for (int p = 0; p < L.passes; ++p) {
-      const KeyT* kin = p == 0 ? ids : kb[(p - 1) & 1];
-      const int32_t* vin = p == 0 ? nullptr : vb[(p - 1) & 1];
-      const uint32_t* prev = p == 0 ? nullptr : bhist + size_t(p - 1) * L.tiles * L.rstride;
-      const int prev_nbits = p == 0 ? 0 : L.nbits[p - 1];
-      uint32_t* runs = bhist + size_t(p) * L.tiles * L.rstride;
-      auto pass = [&](auto rb, auto gather) {
-        k_sort_local<KeyT, decltype(rb)::value, 1024, 2, decltype(gather)::value>
-            <<<L.tiles, 1024, 0, st>>>(kin, vin, K, static_cast<uint64_t>(V), L.shift[p],
-                                       L.nbits[p], prev, prev_nbits, kb[p & 1], vb[p & 1], runs,
-                                       L.rstride, tickets, clear_words, dev_err);
-      };
-      const bool narrow = L.nbits[p] <= kSmallDigitBits;
-      if (p == 0) {
-        if (narrow) pass(I<kSmallDigitBits>{}, std::false_type{});
-        else pass(I<kLargeDigitBits>{}, std::false_type{});
-      } else {
-        if (narrow) pass(I<kSmallDigitBits>{}, std::true_type{});
-        else pass(I<kLargeDigitBits>{}, std::true_type{});
+    // Tile-local passes (1024 threads and 2 keys each, or 256 threads and 4
+    // keys each with digits of at most 8 bits); the runs words of pass p and
+    // tile t sit in the histogram region at row p * tiles + t.
+    auto passes = [&](auto nt) -> hipError_t {
+      constexpr int kNT = decltype(nt)::value;
+      constexpr int kIT = kNT == 256 ? kGatherSmallTileKeys / 256 : 2;
+      for (int p = 0; p < L.passes; ++p) {
+        const KeyT* kin = p == 0 ? ids : kb[(p - 1) & 1];
+        const int32_t* vin = p == 0 ? nullptr : vb[(p - 1) & 1];
+        const uint32_t* prev = p == 0 ? nullptr : bhist + size_t(p - 1) * L.tiles * L.rstride;
+        const int prev_nbits = p == 0 ? 0 : L.nbits[p - 1];
+        uint32_t* runs = bhist + size_t(p) * L.tiles * L.rstride;
+        auto pass = [&](auto rb, auto gather) {
+          k_sort_local<KeyT, decltype(rb)::value, kNT, kIT, decltype(gather)::value>
+              <<<L.tiles, kNT, 0, st>>>(kin, vin, K, static_cast<uint64_t>(V), L.shift[p],
+                                        L.nbits[p], prev, prev_nbits, kb[p & 1], vb[p & 1], runs,
+                                        L.rstride, tickets, clear_words, dev_err);
+        };
+        const bool narrow = L.nbits[p] <= kSmallDigitBits;
+        if constexpr (kNT == 1024) {
+          if (p == 0) {
+            if (narrow) pass(I<kSmallDigitBits>{}, std::false_type{});
+            else pass(I<kLargeDigitBits>{}, std::false_type{});
+          } else {
+            if (narrow) pass(I<kSmallDigitBits>{}, std::true_type{});
+            else pass(I<kLargeDigitBits>{}, std::true_type{});
+          }
+        } else {
+          if (!narrow) return hipErrorInvalidValue;  // the layout keeps digits to 8 bits here
+          if (p == 0) pass(I<kSmallDigitBits>{}, std::false_type{});
+          else pass(I<kSmallDigitBits>{}, std::true_type{});
+        }
+        if (hipError_t e = hipGetLastError(); e != hipSuccess) return e;
       }
-      if (hipError_t e = hipGetLastError(); e != hipSuccess) return launch_status(e);
-    }
-    const int q = L.passes - 1;
-    k_dedup<KeyT, 1024, 2, false, true><<<L.tiles, 1024, 0, st>>>(
-        kb[q & 1], vb[q & 1], K, cap, uniq, counts, offsets, inverse, num_unique, dstatus,
-        tickets + kMaxPasses, dev_err, wait_cfg(), bhist + size_t(q) * L.tiles * L.rstride,
-        L.nbits[q], L.rstride, perm);
-    return launch_status(hipGetLastError());
+      const int q = L.passes - 1;
+      k_dedup<KeyT, kNT, kIT, false, true><<<L.tiles, kNT, 0, st>>>(
+          kb[q & 1], vb[q & 1], K, cap, uniq, counts, offsets, inverse, num_unique, dstatus,
+          tickets + kMaxPasses, dev_err, wait_cfg(), bhist + size_t(q) * L.tiles * L.rstride,
+          L.nbits[q], L.rstride, perm);
+      return hipGetLastError();
+    };
+    return launch_status(L.nt == 256 ? passes(I<256>{}) : passes(I<1024>{}));
   }
   const size_t hist_lds = size_t(L.passes) * L.rstride * 4;
   k_hist<KeyT><<<L.hist_blocks, kHistThreads, hist_lds, st>>>(
