@@ -12,6 +12,9 @@ Parity status per routine (what pins it lives in ``tests/test_oracle_pins.py``):
   segsum          pinned (worked examples, fp64 numpy accumulation, dense
                   scatter, column sums, special cases)
   segsum_select   pinned (equal to segsum rows)
+  segsum_cols,
+  segsum_threads  pinned (equal to segsum bit for bit, any column split;
+                  numpy add.at on a column range)
   dense_scatter   pinned (numpy ``add.at``)
   map, expand,
   scatter         pinned (worked two-GPU example, numpy, invariants)
@@ -53,6 +56,7 @@ def _declare(L):
     I = ctypes.c_int64
     L.orc_unique.argtypes = [P, I, I, P, P, P, P, P, P]
     L.orc_segsum.argtypes = [P, ctypes.c_int, I, I, I, P, I, P]
+    L.orc_segsum_cols.argtypes = [P, ctypes.c_int, I, I, I, P, I, I, I, P]
     L.orc_segsum_select.argtypes = [P, ctypes.c_int, I, I, I, P, P, I, P]
     L.orc_dense_scatter.argtypes = [P, ctypes.c_int, I, I, I, P, I, P]
     L.orc_map.argtypes = [P, I, P, I, P]
@@ -65,7 +69,7 @@ def _declare(L):
     L.orc_compress.argtypes = [P, I, I, ctypes.c_float, P]
     L.orc_decompress.argtypes = [P, I, I, ctypes.c_float, P]
     L.orc_sample_ids.argtypes = [P, I, I, P]
-    for f in ("orc_unique", "orc_segsum", "orc_segsum_select",
+    for f in ("orc_unique", "orc_segsum", "orc_segsum_cols", "orc_segsum_select",
               "orc_dense_scatter", "orc_map", "orc_expand", "orc_scatter",
               "orc_sgd", "orc_adam", "orc_f16_from_f32", "orc_f32_from_f16",
               "orc_compress", "orc_decompress", "orc_sample_ids"):
@@ -156,6 +160,46 @@ def segsum(grad, inverse, U: int) -> np.ndarray:
     return out
 
 
+def segsum_cols(grad, inverse, U: int, d0: int, d1: int, out=None) -> np.ndarray:
+    """Step 2 over the columns [d0, d1) of a U x D fp64 matrix ``out`` (a new
+    NaN-filled one when None); the other columns are left as they are."""
+    g, code, D = _grad(grad)
+    inv = np.ascontiguousarray(inverse, dtype=np.int32)
+    if out is None:
+        out = np.full((U, D), np.nan)
+    if out.shape != (U, D) or out.dtype != np.float64 or not out.flags.c_contiguous:
+        raise OracleError("segsum_cols: out must be a C-contiguous U x D float64 matrix")
+    _check(lib().orc_segsum_cols(_p(g), code, g.shape[0], D, D, _p(inv), U, d0, d1, _p(out)),
+           "segsum_cols")
+    return out
+
+
+def column_ranges(D: int, parts: int):
+    """[d0, d1) ranges that split D columns into ``parts`` near-equal pieces
+    (empty pieces dropped)."""
+    parts = max(1, min(parts, max(D, 1)))
+    edges = [D * i // parts for i in range(parts + 1)]
+    return [(edges[i], edges[i + 1]) for i in range(parts) if edges[i + 1] > edges[i]]
+
+
+def segsum_threads(grad, inverse, U: int, threads: int) -> np.ndarray:
+    """Step 2 with the D columns split over ``threads`` threads, each running
+    orc_segsum_cols on its own range (the all-core CPU baseline). The ctypes
+    calls release the GIL, so the threads run in parallel; no two write the
+    same element, and each column is summed in the same token order as
+    segsum, so the result equals it bit for bit."""
+    from concurrent.futures import ThreadPoolExecutor
+    g, code, D = _grad(grad)
+    inv = np.ascontiguousarray(inverse, dtype=np.int32)
+    out = np.full((U, D), np.nan)
+    ranges = column_ranges(D, threads)
+    if len(ranges) <= 1:
+        return segsum_cols(g, inv, U, 0, D, out)
+    with ThreadPoolExecutor(len(ranges)) as ex:
+        list(ex.map(lambda r: segsum_cols(g, inv, U, r[0], r[1], out), ranges))
+    return out
+
+
 def segsum_select(grad, J, sel) -> np.ndarray:
     """Step 2 evaluated only for the word ids in ``sel`` (strictly ascending)."""
     g, code, D = _grad(grad)
@@ -236,6 +280,68 @@ def adam(p, m, v, g, lr, beta1, beta2, eps, weight_decay, step):
     _check(lib().orc_adam(_p(p), _p(m), _p(v), _p(g), n, D, lr, beta1, beta2,
                           eps, weight_decay, step), "adam")
     return p, m, v
+
+
+def _row_parts(n: int, threads: int):
+    parts = max(1, min(threads, max(n, 1)))
+    edges = [n * i // parts for i in range(parts + 1)]
+    return [(edges[i], edges[i + 1]) for i in range(parts) if edges[i + 1] > edges[i]]
+
+
+def _run_parts(fn, parts):
+    from concurrent.futures import ThreadPoolExecutor
+    if len(parts) <= 1:
+        for r in parts:
+            fn(r)
+        return
+    with ThreadPoolExecutor(len(parts)) as ex:
+        list(ex.map(fn, parts))
+
+
+def sgd_threads(p, g, lr: float, threads: int) -> np.ndarray:
+    """sgd with the rows split over ``threads`` threads (each row is updated
+    on its own, so the result equals sgd exactly)."""
+    p = np.array(p, dtype=np.float64, copy=True, order="C")
+    g = np.ascontiguousarray(g, dtype=np.float64)
+    n, D = p.shape
+
+    def part(r):
+        _check(lib().orc_sgd(_p(p[r[0]:r[1]]), _p(g[r[0]:r[1]]), r[1] - r[0], D, lr), "sgd")
+    _run_parts(part, _row_parts(n, threads))
+    return p
+
+
+def adam_threads(p, m, v, g, lr, beta1, beta2, eps, weight_decay, step, threads: int):
+    """adam with the rows split over ``threads`` threads (equal to adam)."""
+    p = np.array(p, dtype=np.float64, copy=True, order="C")
+    m = np.array(m, dtype=np.float64, copy=True, order="C")
+    v = np.array(v, dtype=np.float64, copy=True, order="C")
+    g = np.ascontiguousarray(g, dtype=np.float64)
+    n, D = p.shape
+
+    def part(r):
+        a, b = r
+        _check(lib().orc_adam(_p(p[a:b]), _p(m[a:b]), _p(v[a:b]), _p(g[a:b]), b - a, D, lr,
+                              beta1, beta2, eps, weight_decay, step), "adam")
+    _run_parts(part, _row_parts(n, threads))
+    return p, m, v
+
+
+def scatter_threads(src, src_ids, dst, threads: int) -> np.ndarray:
+    """SCATTER of src rows into a copy of the dense table ``dst`` (row = id),
+    the source rows split over ``threads`` threads; the ids are distinct, so
+    no two threads write the same row (equal to scatter with dst_ids None)."""
+    src = np.ascontiguousarray(src, dtype=np.float64)
+    src_ids = _ids(src_ids)
+    out = np.array(dst, dtype=np.float64, copy=True, order="C")
+    D = src.shape[1]
+
+    def part(r):
+        a, b = r
+        _check(lib().orc_scatter(_p(src[a:b]), b - a, D, _p(src_ids[a:b]), None, 0, _p(out),
+                                 out.shape[0], 0), "scatter")
+    _run_parts(part, _row_parts(src_ids.size, threads))
+    return out
 
 
 def f16_from_f32(x) -> np.ndarray:

@@ -12,6 +12,8 @@
  * uniqueness method (Sec. III-A) with no blocking, fusion or reordering:
  *   orc_unique          steps 1 and 4   (types of a token list, total order)
  *   orc_segsum          step 2          (local reduction of gradient rows)
+ *   orc_segsum_cols     step 2, over a range of columns (one thread's share
+ *                                        in the all-core CPU baseline)
  *   orc_segsum_select   step 2, evaluated for a chosen set of word ids only
  *   orc_dense_scatter   Sec. II-A       (the baseline reverse map: every
  *                                        gradient row accumulated into its
@@ -119,6 +121,29 @@ int orc_segsum(const void* grad, int gtype, int64_t K, int64_t D, int64_t ld,
     int64_t u = inverse[k];
     if (u < 0 || u >= U) return ORC_RANGE;
     for (int64_t d = 0; d < D; ++d) out[u * D + d] += grad_at(grad, gtype, ld, k, d);
+  }
+  return ORC_OK;
+}
+
+/*
+ * Step 2 over the columns [d0, d1) only: the same sums as orc_segsum, in
+ * the same token order, for those columns of out (U x D fp64, row stride D);
+ * the other columns are left as they are. Columns of the reduction are
+ * independent, so calls on disjoint column ranges share no writes: the
+ * all-core CPU baseline runs one such call per thread.
+ */
+int orc_segsum_cols(const void* grad, int gtype, int64_t K, int64_t D, int64_t ld,
+                    const int32_t* inverse, int64_t U, int64_t d0, int64_t d1,
+                    double* out) {
+  if (K < 0 || D < 0 || U < 0 || ld < D || d0 < 0 || d1 < d0 || d1 > D ||
+      (gtype != ORC_F32 && gtype != ORC_BF16))
+    return ORC_BADARG;
+  for (int64_t u = 0; u < U; ++u)
+    for (int64_t d = d0; d < d1; ++d) out[u * D + d] = 0.0;
+  for (int64_t k = 0; k < K; ++k) {
+    int64_t u = inverse[k];
+    if (u < 0 || u >= U) return ORC_RANGE;
+    for (int64_t d = d0; d < d1; ++d) out[u * D + d] += grad_at(grad, gtype, ld, k, d);
   }
   return ORC_OK;
 }

@@ -203,6 +203,40 @@ def check_segsum_special_cases():
     assert oracle.segsum(np.zeros((0, D), np.float32), u0[3], 0).shape == (0, D)
 
 
+def check_segsum_columns():
+    """The all-core form of step 2: every column range equals numpy's fp64
+    add.at on those columns and leaves the other columns untouched, and any
+    split of the columns over threads gives the one-thread result bit for
+    bit (each column is summed in the same token order). The row-split
+    updates equal their one-thread forms."""
+    for K, V, D, s, seed in ((3000, 500, 7, 1.0, 51), (5000, 20_000, 256, 1.2, 52),
+                             (700, 40, 1, 1.0, 53)):
+        J = synth.zipf_ids(K, V, s, seed, np.int64)
+        G = synth.normal_rows(K, D, seed + 100)
+        uniq, counts, offsets, inverse, perm = oracle.unique(J, V)
+        U = len(uniq)
+        for grad, vals in ((G, G), (synth.bf16_bits(G), synth.bf16_to_f32(synth.bf16_bits(G)))):
+            one = oracle.segsum(grad, inverse, U)
+            for threads in (1, 2, 3, 8):
+                assert np.array_equal(oracle.segsum_threads(grad, inverse, U, threads), one)
+            d0, d1 = D // 3, D - D // 4
+            part = oracle.segsum_cols(grad, inverse, U, d0, d1)
+            want = np.zeros((U, d1 - d0), np.float64)
+            np.add.at(want, inverse, vals[:, d0:d1].astype(np.float64))
+            assert np.array_equal(part[:, d0:d1], want)
+            assert np.isnan(part[:, :d0]).all() and np.isnan(part[:, d1:]).all()
+        table = synth.normal_rows(V, D, seed + 200, 0.02).astype(np.float64)
+        g = oracle.segsum(G, inverse, U)
+        assert np.array_equal(oracle.sgd_threads(table[uniq], g, 0.1, 3),
+                              oracle.sgd(table[uniq], g, 0.1))
+        m0 = np.full((U, D), 0.01)
+        a = oracle.adam_threads(table[uniq], m0, m0, g, 1e-3, 0.9, 0.999, 1e-8, 0.0, 3, 5)
+        b = oracle.adam(table[uniq], m0, m0, g, 1e-3, 0.9, 0.999, 1e-8, 0.0, 3)
+        assert all(np.array_equal(x, y) for x, y in zip(a, b))
+        assert np.array_equal(oracle.scatter_threads(g, uniq, table, 4),
+                              oracle.scatter(g, uniq, table))
+
+
 def check_segsum_select():
     K, D, V = 2000, 11, 97
     G = synth.normal_rows(K, D, 41)
@@ -439,7 +473,7 @@ ALL_CHECKS = [
     check_to_be_or_not_to_be, check_numpy_unique, check_brute_force_unique,
     check_unique_invariants, check_unique_rejects_out_of_range,
     check_fig2_i_want_a_pen_and_a, check_segsum_numpy, check_segsum_special_cases,
-    check_segsum_select, check_fig3_two_gpus, check_shards_merge, check_map_and_fill,
+    check_segsum_columns, check_segsum_select, check_fig3_two_gpus, check_shards_merge, check_map_and_fill,
     check_sgd, check_adam_closed_forms, check_f16_conversion, check_compression,
     check_sample_ids,
 ]

@@ -51,6 +51,12 @@ MUTANTS = [
     ("adam_v_uncorrected", "double vhat = v[i] / c2;", "double vhat = v[i];"),
     ("adam_eps_inside_sqrt", "(sqrt(vhat) + eps)", "sqrt(vhat + eps)"),
     ("adam_decay_dropped", "+ wd * p[i]);", ");"),
+    ("segsum_cols_shifted_column",
+     "for (int64_t d = d0; d < d1; ++d) out[u * D + d] += grad_at(grad, gtype, ld, k, d);",
+     "for (int64_t d = d0; d < d1; ++d) out[u * D + d] += grad_at(grad, gtype, ld, k, d - d0);"),
+    ("segsum_cols_clears_every_column",
+     "for (int64_t d = d0; d < d1; ++d) out[u * D + d] = 0.0;",
+     "for (int64_t d = 0; d < D; ++d) out[u * D + d] = 0.0;"),
     ("select_skips_first_token", "for (int64_t k = 0; k < K; ++k) {\n    int64_t lo = 0, hi = nsel;",
      "for (int64_t k = 1; k < K; ++k) {\n    int64_t lo = 0, hi = nsel;"),
 ]
