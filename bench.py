@@ -4,10 +4,11 @@ One step = one pass of the whole path over one batch of synthetic tokens
 already resident in HBM:
     Unique (lm_unique) -> Seg-Sum (lm_segsum) -> Fill-Values / update
 (SGD or Adam via lm_sparse_apply, SCATTER into a dense table or EXPAND into
-the merged type list via lm_fill_values, by workload). The default workload
-is the per-GPU word-LM step: K = 65,536 Zipf(1.0) token ids over an 800K
-vocabulary, 1024-wide fp32 gradients, SGD (lr 0.1) into an 800K x 1024 fp32
-table. Steps cycle through several independently seeded batches so that the
+the merged type list via lm_fill_values, by workload). The headline workload
+is the largest one with fp32 gradients: K = 1,048,576 Zipf(1.2) token ids
+over a 20K character vocabulary, 2048-wide fp32 gradients (8 GiB per batch),
+SCATTER of the U reduced rows into the dense 20K x 2048 table. Steps cycle
+through resident batches (at least 2 GiB of gradients in all) so that the
 gradient rows are not served from the 256 MB Infinity Cache.
 
 The headline runs the Unique calls on a second stream, up to three steps
@@ -16,8 +17,11 @@ trainer has before the gradients exist); every step still does all of its
 work. The serial schedule (one stream) is timed too and printed beside it.
 
 Prints one JSON line: tokens/s, ms per step, the Seg-Sum roofline (algorithmic
-bytes per launch / average launch time from HIP events on the launch stream)
-and the CPU oracle timed on a bounded sample of the same workload.
+bytes per lm_segsum call / its average duration from HIP events on the launch
+stream, all of the call's kernels), the CPU oracle timed on whole copies of
+the same batch (one thread, and every core of the process), the check of the
+timed kernels' outputs against the oracle's, and the same figures for each of
+the five workloads (`workloads`), measured in the same run.
 """
 from __future__ import annotations
 
@@ -329,15 +333,39 @@ def run_overlap_pass(pipe, steps, warmup, torch, main, side):
     return ms
 
 
-def run_gpu(w, steps, warmup, nbatch, torch, lz):
+class HostInputs:
+    """Batch 0 of a workload on the host: the arrays copied to the GPU and
+    handed to the CPU oracle, so both sides see the very same values."""
+
+    def __init__(self, w):
+        self.words = None
+        if w.samples:
+            from paper_1810_10045_amd import seeding
+            self.words = w.sampler_words(seeding.seed_of_gpus(w.shards, w.seed_rule))
+        self.true_ids = w.ids()
+        self.grads = w.grads()      # storage dtype (bf16 as uint16 bits)
+        self.table = w.table() if w.step in ("sgd", "adam", "softmax_sgd") else None
+
+    def oracle_ids(self, w, oracle):
+        if self.words is None:
+            return self.true_ids
+        return np.concatenate([oracle.sample_ids(self.words, w.V), self.true_ids])
+
+
+def run_gpu(w, steps, warmup, nbatch, torch, lz, host):
+    """The three timed passes of one workload (serial; serial with an event
+    around each entry point; overlapped), then one more step over batch 0
+    whose Unique and Seg-Sum outputs are returned for the oracle check."""
     dev = torch.device("cuda:0")
     log(f"workload {w.name}: K={w.tokens} V={w.V} D={w.D} s={w.s} {w.grad_dtype}/{w.id_dtype} "
         f"step={w.step}, {nbatch} resident batches")
     t0 = time.time()
-    batches = [Batch(w.batch(b), torch, dev) for b in range(nbatch)]
+    batches = [Batch(w, torch, dev, ids=None if w.samples else host.true_ids, grads=host.grads,
+                     words=host.words)]
+    batches += [Batch(w.batch(b), torch, dev) for b in range(1, nbatch)]
     log(f"inputs generated and copied in {time.time() - t0:.1f}s")
     K, D = w.tokens, w.D
-    pipe = Pipeline(w, batches, torch, lz, dev)
+    pipe = Pipeline(w, batches, torch, lz, dev, table=host.table)
     ures, dev_err, step = pipe.ures, pipe.dev_err, pipe.step
     stream = torch.cuda.current_stream()
 
@@ -381,6 +409,17 @@ def run_gpu(w, steps, warmup, nbatch, torch, lz):
     pipe.enable_overlap()
     overlap_ms = run_overlap_pass(pipe, steps, warmup, torch, stream,
                                   torch.cuda.Stream(device=dev))
+    # One more serial step over batch 0: the outputs the oracle checks.
+    step(0)
+    torch.cuda.synchronize()
+    lz.check(dev_err)
+    U0 = int(ures.num_unique.item())
+    outputs = dict(U=U0, uniq=ures.uniq[:U0].cpu().numpy().astype(np.int64),
+                   counts=ures.counts[:U0].cpu().numpy(), offsets=ures.offsets[:U0 + 1].cpu().numpy(),
+                   inverse=ures.inverse[:K].cpu().numpy(), perm=ures.perm[:K].cpu().numpy(),
+                   out=pipe.out[:U0].cpu().numpy())
+    del pipe, batches
+    torch.cuda.empty_cache()
     gb = 2 if w.grad_dtype == "bf16" else 4
     ib = 8 if w.id_dtype == "i64" else 4
     Us = [U_of[i % nbatch] for i in range(steps)]
@@ -391,39 +430,101 @@ def run_gpu(w, steps, warmup, nbatch, torch, lz):
     after_bytes = float(np.mean([rows * U * D * 4 for U in Us])) if rows else None
     return dict(total_ms=total_ms, overlap_ms=overlap_ms, stage_ms=st.mean(axis=0).tolist(), seg_ms=seg_ms,
                 seg_bytes=float(seg_bytes), uniq_bytes=uniq_bytes, after_bytes=after_bytes,
-                U=U_of)
+                U=U_of, outputs=outputs)
 
 
-def run_cpu_baseline(w, budget_s):
-    """The CPU oracle as it stands, single-threaded, on whole batches of the
-    same workload until about budget_s seconds of work are done."""
+def host_threads() -> int:
+    """Threads of the all-core oracle leg: the cores this process may run on,
+    at most 16 (a one-GPU share of the host)."""
+    try:
+        n = len(os.sched_getaffinity(0))
+    except AttributeError:
+        n = os.cpu_count() or 1
+    return max(1, min(16, n))
+
+
+def oracle_pass(w, oracle, ids, host, threads):
+    """One whole step of the oracle over batch 0: unique, then segsum and the
+    stage after it, on one thread (threads = 1) or with the columns of the
+    reduction and the rows of the update split over `threads` threads (the
+    unique stays on one thread). Returns the unique outputs and the sums."""
+    grads = host.grads
+    uniq, counts, offsets, inverse, perm = oracle.unique(ids, w.V)
+    U = len(uniq)
+    if threads == 1:
+        red = oracle.segsum(grads, inverse, U)
+    else:
+        red = oracle.segsum_threads(grads, inverse, U, threads)
+    if w.step in ("sgd", "softmax_sgd"):
+        p = host.table[uniq]
+        (oracle.sgd(p, red, w.lr) if threads == 1 else oracle.sgd_threads(p, red, w.lr, threads))
+    elif w.step == "adam":
+        p, z = host.table[uniq], np.zeros((U, w.D))
+        if threads == 1:
+            oracle.adam(p, z, z, red, w.lr, *w.adam, 0.0, 1)
+        else:
+            oracle.adam_threads(p, z, z, red, w.lr, *w.adam, 0.0, 1, threads)
+    elif w.step == "scatter":
+        dense = np.zeros((w.V, w.D))
+        (oracle.scatter(red, uniq, dense) if threads == 1
+         else oracle.scatter_threads(red, uniq, dense, threads))
+    return (uniq, counts, offsets, inverse, perm), red
+
+
+def run_cpu_baseline(w, host, budget_s):
+    """The CPU oracle as it stands on whole copies of batch 0, until about
+    budget_s seconds of work are done (at least one pass), in two legs: one
+    thread, and every core of the process (the reduction's columns and the
+    update's rows split over the threads). Returns both legs and the first
+    pass's outputs."""
     import oracle
-    wl = w
-    ids = wl.ids()
-    if w.samples:
-        from paper_1810_10045_amd import seeding
-        words = w.sampler_words(seeding.seed_of_gpus(w.shards, w.seed_rule))
-        ids = np.concatenate([oracle.sample_ids(words, w.V), ids])
-    grads = wl.grads() if wl.grad_dtype == "bf16" else wl.grads_f32()
-    table = wl.table() if w.step in ("sgd", "adam", "softmax_sgd") else None
-    done, t_used, toks = 0, 0.0, 0
-    while t_used < budget_s and done < 1000:
-        t0 = time.perf_counter()
-        uniq, counts, offsets, inverse, perm = oracle.unique(ids, w.V)
-        red = oracle.segsum(grads, inverse, len(uniq))
-        if w.step in ("sgd", "softmax_sgd"):
-            oracle.sgd(table[uniq], red, w.lr)
-        elif w.step == "adam":
-            z = np.zeros((len(uniq), w.D))
-            oracle.adam(table[uniq], z, z, red, w.lr, *w.adam, 0.0, 1)
-        elif w.step == "scatter":
-            oracle.scatter(red, uniq, np.zeros((w.V, w.D)))
-        t_used += time.perf_counter() - t0
-        done += 1
-        toks += len(ids)
-    return dict(value=toks / t_used, unit="tokens/s", cores=1, kind="oracle",
-                sample=f"{done} whole {w.name} batch(es) of {len(ids)} tokens, "
-                       f"unique+segsum+{w.step}, fp64, 1 thread of {cpu_model()}, {t_used:.1f}s")
+    ids = host.oracle_ids(w, oracle)
+    legs, first = {}, None
+    for threads in (1, host_threads()):
+        done, t_used = 0, 0.0
+        while t_used < budget_s and done < 1000:
+            t0 = time.perf_counter()
+            res = oracle_pass(w, oracle, ids, host, threads)
+            t_used += time.perf_counter() - t0
+            done += 1
+            if first is None:
+                first = res
+            del res
+        what = ("1 thread" if threads == 1 else
+                f"{threads} threads (unique on one; the reduction's columns and the update's rows "
+                f"split over the threads)")
+        legs[threads] = dict(value=done * len(ids) / t_used, unit="tokens/s", cores=threads,
+                             kind="oracle",
+                             sample=f"{done} whole {w.name} batch(es) of {len(ids)} tokens, "
+                                    f"unique+segsum+{w.step}, fp64, {what} of {cpu_model()}, "
+                                    f"{t_used:.1f}s")
+    return legs, first, ids
+
+
+def check_outputs(w, gpu, ora):
+    """The timed kernels' outputs for batch 0 against the oracle's: every
+    integer output of Unique bit for bit, and every Seg-Sum row within the
+    per-row normwise tolerance of its gradient dtype (with count-1 rows
+    exact)."""
+    (uniq, counts, offsets, inverse, perm), red = ora
+    ok_int = (gpu["U"] == len(uniq) and np.array_equal(gpu["uniq"], uniq)
+              and np.array_equal(gpu["counts"], counts) and np.array_equal(gpu["offsets"], offsets)
+              and np.array_equal(gpu["inverse"], inverse) and np.array_equal(gpu["perm"], perm))
+    err, ones_exact = None, False
+    if ok_int:
+        got = gpu["out"].astype(np.float64)
+        scale = np.abs(red).max(axis=1)
+        diff = np.abs(got - red).max(axis=1)
+        nz = scale > 0
+        err = float((diff[nz] / scale[nz]).max()) if nz.any() else 0.0
+        if not np.all(diff[~nz] == 0):
+            err = float("inf")
+        single = counts == 1
+        ones_exact = bool(np.array_equal(got[single], red[single]))
+    tol = 2e-3 if w.grad_dtype == "bf16" else 1e-5
+    ok = bool(ok_int and err is not None and err <= tol and ones_exact)
+    return {"ok": ok, "unique_bit_exact": bool(ok_int), "segsum_rows": int(len(red)),
+            "segsum_max_row_rel_err": err, "tolerance": tol, "count1_rows_exact": ones_exact}
 
 
 def cpu_model() -> str:
@@ -441,9 +542,10 @@ def cpu_model() -> str:
 
 
 def load_traffic(workload):
-    """HBM bytes per Seg-Sum launch from the committed rocprofv3 counter
-    summary (FETCH_SIZE + WRITE_SIZE, scaled by a plain copy), only while the
-    Seg-Sum sources are unchanged since the counters were taken."""
+    """HBM bytes per lm_segsum call (all its kernels) from the committed
+    rocprofv3 counter summary (FETCH_SIZE + WRITE_SIZE, scaled by a plain
+    copy), only while the Seg-Sum sources are unchanged since the counters
+    were taken."""
     path = TRAFFIC_FILE.format(workload=workload)
     if not os.path.exists(path):
         return None
@@ -474,15 +576,88 @@ def copy_calibration(torch, reps=3):
     torch.cuda.empty_cache()
 
 
+def segsum_kernels(w):
+    """The kernels of one lm_segsum call at this workload's shape."""
+    return SEGSUM_KERNELS if w.D <= 1024 else "lm_segsum (k_segsum walk, then k_segsum_fix)"
+
+
+def measure(w, args, torch, lz, cpu_budget):
+    """Everything the bench reports for one workload."""
+    gb = 2 if w.grad_dtype == "bf16" else 4
+    nbatch = args.batches or max(1, min(8, math.ceil((2 << 30) / (w.tokens * w.D * gb))))
+    t0 = time.time()
+    host = HostInputs(w)
+    log(f"{w.name}: batch 0 generated on the host in {time.time() - t0:.1f}s")
+    r = run_gpu(w, args.steps, args.warmup, nbatch, torch, lz, host)
+    ms = r["overlap_ms"] / args.steps
+    serial_ms = r["total_ms"] / args.steps
+    achieved = r["seg_bytes"] / (r["seg_ms"] / 1e3) / 1e9
+    res = dict(w=w, nbatch=nbatch, r=r, ms=ms, serial_ms=serial_ms, achieved=achieved,
+               value=w.tokens / (ms / 1e3), traffic=load_traffic(w.name), cpu=None, check=None)
+    if not args.no_cpu:
+        t0 = time.time()
+        legs, ora, _ = run_cpu_baseline(w, host, cpu_budget)
+        res["cpu"] = legs
+        res["check"] = check_outputs(w, r["outputs"], ora)
+        log(f"{w.name}: oracle legs and check in {time.time() - t0:.1f}s: "
+            f"{legs[1]['value']:.3g} / {legs[max(legs)]['value']:.3g} tokens/s; "
+            f"check {res['check']}")
+        del ora
+    del host, r["outputs"]
+    return res
+
+
+def cpu_baseline_entry(res):
+    """The cpu_baseline object: the all-core leg, with the one-thread leg and
+    the GPU/CPU ratios beside it."""
+    legs = res["cpu"]
+    if not legs:
+        return None
+    allc = legs[max(legs)]
+    one = legs[1]
+    return {**allc, "one_thread": one,
+            "gpu_over_cpu": {"all_cores": res["value"] / allc["value"],
+                             "one_thread": res["value"] / one["value"]}}
+
+
+def workload_summary(res):
+    """One workload's figures for the per-workload table of the line."""
+    w, r = res["w"], res["r"]
+    legs = res["cpu"] or {}
+    return {
+        "tokens": w.tokens, "V": w.V, "D": w.D, "zipf_s": w.s, "ids": w.id_dtype,
+        "grad": w.grad_dtype, "after_segsum": w.step, "resident_batches": res["nbatch"],
+        "types_batch0": r["U"][0],
+        "value": res["value"], "ms_per_step": res["ms"],
+        "serial_value": w.tokens / (res["serial_ms"] / 1e3), "serial_ms_per_step": res["serial_ms"],
+        "stages_ms": {"unique": r["stage_ms"][0], "segsum": r["stage_ms"][1],
+                      w.step: r["stage_ms"][2]},
+        "segsum": {"kernels": segsum_kernels(w), "achieved_gbps": res["achieved"],
+                   "frac": res["achieved"] / HBM_PEAK_GBPS, "bytes_per_launch": r["seg_bytes"],
+                   "avg_launch_ms": r["seg_ms"], "traffic": res["traffic"]},
+        "cpu_tokens_per_s": {str(k): v["value"] for k, v in legs.items()},
+        "gpu_over_cpu_all_cores": (res["value"] / legs[max(legs)]["value"]) if legs else None,
+        "oracle_check": res["check"],
+    }
+
+
+FIVE = ("word_tiny_8k", "word_step_64k", "merge_64x32k_bf16", "char_heavy_1m", "vocab2m_adam_i64")
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
-    ap.add_argument("--workload", default="word_step_64k")
+    ap.add_argument("--workload", default="char_heavy_1m",
+                    help="the headline workload (default: char_heavy_1m, the largest fp32 one)")
+    ap.add_argument("--workloads", default=",".join(FIVE),
+                    help="workloads measured after the headline for the per-workload table "
+                         "(comma-separated; 'none' for the headline alone)")
     ap.add_argument("--batches", type=int, default=0, help="resident batches (0: auto)")
-    ap.add_argument("--cpu-seconds", type=float, default=10.0)
-    ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle leg")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0,
+                    help="oracle time per leg for the headline (other workloads: at most 3 s)")
+    ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle legs and check")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="first run plain 1 GiB copies (scale for HBM byte counters)")
     args = ap.parse_args()
@@ -500,27 +675,24 @@ def main():
     if args.copy_calibration:
         copy_calibration(torch)
     w = synth.WORKLOADS[args.workload]
-    gb = 2 if w.grad_dtype == "bf16" else 4
-    batch_bytes = w.tokens * w.D * gb
-    nbatch = args.batches or max(1, min(8, math.ceil((2 << 30) / batch_bytes)))
-    r = run_gpu(w, args.steps, args.warmup, nbatch, torch, lz)
-    ms = r["overlap_ms"] / args.steps
-    tokens_per_s = w.tokens / (ms / 1e3)
-    serial_ms = r["total_ms"] / args.steps
-    achieved = r["seg_bytes"] / (r["seg_ms"] / 1e3) / 1e9
-    rank = int(os.environ.get("RANK", "0"))
-    cpu = None
-    if not args.no_cpu and rank == 0:
-        cpu = run_cpu_baseline(w, args.cpu_seconds)
-    traffic = load_traffic(w.name)
+    head = measure(w, args, torch, lz, args.cpu_seconds)
+    others = [] if args.workloads == "none" else [n for n in args.workloads.split(",") if n]
+    table = {}
+    for name in others:
+        if name == w.name:
+            table[name] = workload_summary(head)
+            continue
+        table[name] = workload_summary(measure(synth.WORKLOADS[name], args, torch, lz,
+                                               min(args.cpu_seconds, 3.0)))
+    r = head["r"]
     line = {
         "metric": METRIC,
-        "value": tokens_per_s,
+        "value": head["value"],
         "unit": "tokens/s",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": ms,
+        "ms_per_step": head["ms"],
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -530,26 +702,31 @@ def main():
                    "ids": w.id_dtype, "grad": w.grad_dtype, "after_segsum": w.step,
                    **({"gpus_simulated": w.shards, "samples_per_gpu": w.samples,
                        "seed_rule": w.seed_rule} if w.samples else {}),
-                   "resident_batches": nbatch, "types_per_batch": r["U"]},
+                   "resident_batches": head["nbatch"], "types_per_batch": r["U"]},
         "stages_ms": {"unique": r["stage_ms"][0], "segsum": r["stage_ms"][1],
                       w.step: r["stage_ms"][2]},
         # algorithmic bytes of each stage / its event-measured time (GB/s)
         "stages_gbps": {"unique": r["uniq_bytes"] / (r["stage_ms"][0] / 1e3) / 1e9,
-                        "segsum": achieved,
+                        "segsum": head["achieved"],
                         w.step: (r["after_bytes"] / (r["stage_ms"][2] / 1e3) / 1e9
                                  if r["after_bytes"] else None)},
-        "roofline": {"bound": "hbm", "kernel": SEGSUM_KERNELS if w.D <= 1024 else
-                     "lm_segsum (k_segsum, then k_segsum_fix)",
-                     "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-                     "frac": achieved / HBM_PEAK_GBPS,
+        "roofline": {"bound": "hbm", "kernel": segsum_kernels(w),
+                     "achieved": head["achieved"], "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                     "frac": head["achieved"] / HBM_PEAK_GBPS,
                      "bytes_per_launch": r["seg_bytes"], "avg_launch_ms": r["seg_ms"],
-                     "traffic": traffic},
-        "cpu_baseline": cpu,
+                     "traffic": head["traffic"]},
+        "cpu_baseline": cpu_baseline_entry(head),
+        "oracle_check": head["check"],
         "schedule": "unique on a second stream, up to 3 steps ahead (4 sets of its outputs)",
-        "serial": {"value": w.tokens / (serial_ms / 1e3), "ms_per_step": serial_ms,
+        "serial": {"value": w.tokens / (head["serial_ms"] / 1e3), "ms_per_step": head["serial_ms"],
                    "schedule": "one stream, the steps one after another"},
+        "workloads": table,
     }
     print(json.dumps(line), flush=True)
+    checks = [head["check"]] + [t["oracle_check"] for t in table.values()]
+    if any(c is not None and not c["ok"] for c in checks):
+        log("the GPU outputs differ from the oracle's (oracle_check): see the line")
+        sys.exit(1)
 
 
 if __name__ == "__main__":

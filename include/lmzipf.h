@@ -21,10 +21,11 @@
  * ---------------------------------------
  * - Every pointer named as a device buffer is device memory (hipMalloc or a
  *   torch CUDA tensor); host pointers are never accepted for those.
- * - The caller owns every buffer. The library allocates nothing, keeps no
- *   pointer past the call, and holds no global state but one per-process
- *   call counter (lm_segsum); all work is enqueued on `stream` (a hipStream_t; NULL is the default stream) and the call
- *   returns without synchronising.
+ * - The caller owns every buffer. The library allocates nothing and keeps
+ *   no pointer past the call. Its only global state is a per-process call
+ *   counter (lm_segsum's flag tags) and the lm_segsum_set_two_launches
+ *   setting. All work is enqueued on `stream` (a hipStream_t; NULL is the
+ *   default stream) and the call returns without synchronising.
  * - Counts that the GPU computes (num_unique, n_src, ...) stay on the device.
  *   Grids are sized from the host-side capacities (K, u_cap, ...), and the
  *   kernels stop at the device-side count, so no call syncs the host.
@@ -153,26 +154,30 @@ int lm_unique(const void* ids, int32_t idtype, int64_t K, int64_t V,
  * walk's chunks are summed by workgroups of the same launch, which wait for
  * per-chunk flags tagged with a per-call value from a process-wide counter
  * (bounded waits; LM_DEVERR_SPIN if one gave up, which a correct call never
- * does). Otherwise, and always while `stream` is being captured into a
- * graph (a replay would repeat the tag), they are summed by a second launch.
+ * does). Otherwise, always while `stream` is being captured into a graph (a
+ * replay would repeat the tag), and while lm_segsum_set_two_launches is on,
+ * they are summed by a second launch.
  * ------------------------------------------------------------------------ */
 size_t lm_segsum_workspace_bytes(int64_t K, int64_t D);
 
-/* Test hook for the failure path of the bounded waits between workgroups
- * (not for use in training). While enable is nonzero, the fix-up
- * workgroups of lm_segsum's one-launch form wait for a flag value that the
- * walk never writes, and the look-backs of lm_unique's multi-workgroup
- * kernels (inputs above 8,192 ids) read every predecessor as not ready:
- * each such wait gives up after spin_limit polls (at least 1) and sets
- * LM_DEVERR_SPIN. The launches still finish and write only inside their
- * buffers; their results are then unspecified. Process-wide; off by
- * default. Returns LM_OK. */
-int lm_test_force_wait_failure(int32_t enable, uint32_t spin_limit);
 int lm_segsum(const void* grad, int32_t gtype, int64_t K, int64_t D,
               int64_t ld_grad, const int32_t* perm, const int32_t* inverse,
               const int32_t* offsets, const int64_t* num_unique, int64_t u_cap,
               float* out, int64_t ld_out, int32_t* dev_err, void* ws,
               size_t ws_bytes, void* stream);
+
+/* The one-launch form of lm_segsum relies on the hardware starting the
+ * walk's workgroups before the fix-up workgroups that wait on them (they come
+ * first in the grid). lm_segsum_set_two_launches(1) makes every later call
+ * in the process use the two-launch form instead (the walk, then a separate
+ * fix-up kernel: no workgroup ever waits on another), the fallback should a
+ * device break that order; 0 restores the default. The environment variable
+ * LMZIPF_SEGSUM_TWO_LAUNCHES=1, read at the first lm_segsum call, sets it
+ * too. Results agree with the one-launch form within the Seg-Sum tolerance
+ * (the heads' partial rows are added in a different grouping) and are
+ * bit-identical from run to run. Process-wide; returns the previous
+ * setting (0 or 1). */
+int lm_segsum_set_two_launches(int32_t enable);
 
 /* ------------------------------------------------------------------------
  * Map — Sec. III-A step 4: the local-to-global map J^ -> I^. Both id lists

@@ -38,6 +38,7 @@ int apply_run_f16(float* table, int64_t V, int64_t D, int64_t ld_table, const vo
 
 int sample_run(const uint64_t* r, int64_t n, int64_t V, void* ids, int idtype, hipStream_t st);
 void segsum_force_wait_failure(bool enable, uint32_t limit);
+int segsum_set_two_launches(bool enable);
 void unique_force_wait_failure(bool enable, uint32_t limit);
 
 int launch_status(hipError_t e) { return e == hipSuccess ? LM_OK : LM_E_HIP; }
@@ -71,7 +72,7 @@ const char* lm_status_string(int status) {
   }
 }
 
-int lm_abi_version(void) { return 103; }
+int lm_abi_version(void) { return 104; }
 
 int lm_workspace_clear(void* ws, size_t bytes, void* stream) {
   if (bytes == 0) return LM_OK;
@@ -104,6 +105,8 @@ int lm_unique(const void* ids, int32_t idtype, int64_t K, int64_t V, void* uniq,
   return unique_run(ids, idtype, K, V, uniq, counts, offsets, inverse, perm, num_unique, dev_err,
                     ws, ws_bytes, static_cast<hipStream_t>(stream));
 }
+
+int lm_segsum_set_two_launches(int32_t enable) { return segsum_set_two_launches(enable != 0); }
 
 int lm_test_force_wait_failure(int32_t enable, uint32_t spin_limit) {
   segsum_force_wait_failure(enable != 0, spin_limit);

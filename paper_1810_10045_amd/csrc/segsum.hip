@@ -39,6 +39,7 @@
 // (RF x NV x 1 KiB in flight), adds them in fp32 registers and writes a row
 // as soon as its segment ends; grad is streamed with non-temporal loads.
 #include <atomic>
+#include <cstdlib>
 
 #include "common.hpp"
 
@@ -784,6 +785,28 @@ void segsum_force_wait_failure(bool enable, uint32_t limit) {
   g_force_wait_failure.store(enable, std::memory_order_relaxed);
 }
 
+// The host switch to the two-launch form (lm_segsum_set_two_launches):
+// -1 until the first call reads LMZIPF_SEGSUM_TWO_LAUNCHES, then 0 or 1.
+static std::atomic<int> g_two_launches{-1};
+
+static bool two_launches() {
+  int v = g_two_launches.load(std::memory_order_relaxed);
+  if (v < 0) {
+    const char* e = std::getenv("LMZIPF_SEGSUM_TWO_LAUNCHES");
+    const int from_env = (e && e[0] == '1') ? 1 : 0;
+    int expected = -1;
+    g_two_launches.compare_exchange_strong(expected, from_env, std::memory_order_relaxed);
+    v = g_two_launches.load(std::memory_order_relaxed);
+  }
+  return v == 1;
+}
+
+int segsum_set_two_launches(bool enable) {
+  const int prev = two_launches() ? 1 : 0;
+  g_two_launches.store(enable ? 1 : 0, std::memory_order_relaxed);
+  return prev;
+}
+
 int segsum_run(const void* grad, int gtype, int64_t K, int64_t D, int64_t ld_grad,
                const int32_t* perm, const int32_t* inverse, const int32_t* offsets,
                const int64_t* num_unique, int64_t u_cap, float* out, int64_t ld_out,
@@ -820,7 +843,8 @@ int segsum_run(const void* grad, int gtype, int64_t K, int64_t D, int64_t ld_gra
                                    : out_vec && al16(grad) && ld_grad % 8 == 0 && D % 8 == 0;
   // One launch for the walk and the fix-up where the walk has one column
   // tile (vector path, D <= 1024).
-  a.fused = LMZ_SEG_FUSED != 0 && vec && D <= 1024 && (LMZ_SEG_NV_MAX >= 4 || gtype != LM_F32);
+  a.fused = LMZ_SEG_FUSED != 0 && vec && D <= 1024 && (LMZ_SEG_NV_MAX >= 4 || gtype != LM_F32) &&
+            !two_launches();
   // A captured launch would replay with this call's epoch every time, and a
   // replay could take the previous replay's flags for its own: under stream
   // capture the fix-up is a second launch, which keeps no state across calls.

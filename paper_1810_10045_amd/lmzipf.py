@@ -72,10 +72,11 @@ def _load():
     L.lm_sparse_apply_f16.argtypes = [P, I64_, I64_, I64_, P, I32_, P, I64_, P, I64_, F, I32_,
                                       F, F, F, F, F, I64_, P, P, P, P]
     L.lm_sample_ids.argtypes = [P, I64_, I64_, P, I32_, P]
+    L.lm_segsum_set_two_launches.argtypes = [I32_]
     L.lm_test_force_wait_failure.argtypes = [I32_, ctypes.c_uint32]
     for f in ("lm_abi_version", "lm_workspace_clear", "lm_unique", "lm_segsum", "lm_map_ids",
               "lm_fill_values", "lm_sparse_apply", "lm_fill_values_f16", "lm_sparse_apply_f16",
-              "lm_sample_ids", "lm_test_force_wait_failure"):
+              "lm_sample_ids", "lm_segsum_set_two_launches", "lm_test_force_wait_failure"):
         getattr(L, f).restype = ctypes.c_int
     return L
 
@@ -369,6 +370,13 @@ def sparse_apply_f16(table: torch.Tensor, rows: torch.Tensor, n_rows: torch.Tens
                                    weight_decay, step, _ptr(m), _ptr(v), _ptr(dev_err),
                                    _stream(stream)), "lm_sparse_apply_f16")
     return table
+
+
+def segsum_two_launches(enable: bool) -> bool:
+    """lm_segsum_set_two_launches: every later lm_segsum call in the process
+    takes the two-launch form (walk, then a separate fix-up kernel) while
+    enabled. Returns the previous setting."""
+    return bool(_lib.lm_segsum_set_two_launches(1 if enable else 0))
 
 
 def force_wait_failure(enable: bool, spin_limit: int = 64):

@@ -8,12 +8,12 @@ import re
 import pytest
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
-HEADER = os.path.join(ROOT, "include", "lmzipf.h")
+HEADERS = [os.path.join(ROOT, "include", h) for h in ("lmzipf.h", "lmzipf_test.h")]
 LIB = os.path.join(ROOT, "paper_1810_10045_amd", "liblmzipf.so")
 
 
 def declared_functions():
-    text = open(HEADER).read()
+    text = "".join(open(h).read() for h in HEADERS)
     text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
     return sorted(set(re.findall(r"\b(lm_[a-z_]+)\s*\(", text)))
 
@@ -26,6 +26,17 @@ def lib():
     return ctypes.CDLL(LIB)
 
 
+def test_include_holds_only_these_headers():
+    """Every header under include/ is one the symbol checks read."""
+    found = sorted(f for f in os.listdir(os.path.join(ROOT, "include")) if f.endswith(".h"))
+    assert found == sorted(os.path.basename(h) for h in HEADERS)
+
+
+def test_test_hook_is_not_in_the_training_header():
+    text = open(HEADERS[0]).read()
+    assert "lm_test_" not in text
+
+
 def test_header_declares_the_boundary():
     names = declared_functions()
     for n in ("lm_unique", "lm_segsum", "lm_fill_values", "lm_sparse_apply", "lm_map_ids",
@@ -35,7 +46,7 @@ def test_header_declares_the_boundary():
 
 def test_library_exports_every_declared_symbol(lib):
     for n in declared_functions():
-        assert hasattr(lib, n), f"{n} declared in include/lmzipf.h but not exported"
+        assert hasattr(lib, n), f"{n} declared in include/ but not exported"
 
 
 def test_binding_names_match_the_header():
@@ -51,7 +62,7 @@ def test_status_strings(lib):
     lib.lm_status_string.restype = ctypes.c_char_p
     for code in (0, 1, 3, 4, 5, 99):
         assert lib.lm_status_string(code)
-    assert lib.lm_abi_version() == 103
+    assert lib.lm_abi_version() == 104
 
 
 def test_workspace_queries(lib):

@@ -2,16 +2,17 @@
 very launches that bench.py times (its Batch and Pipeline, batch 0).
 
 * Unique: every integer output bit-exact against the oracle, whole input.
-* Seg-Sum: per-row tolerance against the oracle's fp64 sums, on every row
-  where the oracle finishes in seconds; on the merge (2M tokens) and the 2M
-  vocabulary a sample of rows (the heaviest types, which span the most
-  chunks and go through the fix-up, plus seeded random types and the first
-  and last), each evaluated by oracle.segsum_select over the tokens of the
-  sampled types only.
+* Seg-Sum: every row against the oracle's fp64 sums (the oracle's column
+  split over the host's cores for the largest inputs), within the contract
+  for the gradient dtype and within the fp32 accumulation bound for bf16
+  inputs too; rows of types with one token must be exact copies.
+* Map J^ -> I^ at the merge's real shape (shard 0's types into the merged
+  list), bit-exact.
 * What follows Seg-Sum, end to end from the oracle's own sums: SCATTER into a
   dense table (against the dense per-token scatter-add for the 100K x 512
-  case), SGD, the first lazy-Adam step (moments too), EXPAND of shard 0 into
-  the merged type list; rows the step must not touch are compared exactly.
+  case), SGD, the first lazy-Adam step (moments too, every touched row),
+  EXPAND of shard 0 into the merged type list; rows the step must not touch
+  are compared exactly.
 """
 import os
 import sys
@@ -28,7 +29,9 @@ pytestmark = pytest.mark.gpu
 
 torch = pytest.importorskip("torch")
 
-N_HEADS, N_RANDOM = 16, 240
+# Host threads for the oracle's column-split Seg-Sum (at most the 16 cores a
+# one-GPU share of the host has).
+THREADS = max(1, min(16, len(os.sched_getaffinity(0))))
 
 
 @pytest.fixture(scope="module")
@@ -64,29 +67,6 @@ def _release(pipe):
     torch.cuda.empty_cache()
 
 
-def _as_f32(g):
-    return synth.bf16_to_f32(g) if g.dtype == np.uint16 else g
-
-
-def _sample_types(counts, seed):
-    """Row positions: the N_HEADS heaviest types, N_RANDOM seeded random
-    ones, the first and the last (ascending, distinct)."""
-    U = len(counts)
-    heads = np.argsort(-counts, kind="stable")[:N_HEADS]
-    rnd = np.random.default_rng(seed).choice(U, min(U, N_RANDOM), replace=False)
-    return np.unique(np.concatenate([heads, rnd, [0, U - 1]]))
-
-
-def _sampled_sums(ids, grads, sel_ids):
-    """Oracle Seg-Sum rows (and sums of squares) of the word ids sel_ids,
-    from only the tokens that carry them (the others add nothing)."""
-    keep = np.isin(ids, sel_ids)
-    sub_ids, sub_g = ids[keep], grads[keep]
-    S = oracle.segsum_select(sub_g, sub_ids, sel_ids)
-    sq = oracle.segsum_select(np.square(_as_f32(sub_g)), sub_ids, sel_ids)
-    return S, sq
-
-
 def test_full_word_tiny_8k(lz):
     """8,192 tokens over 100K words, D = 512: Seg-Sum on every row and the
     dense V x 512 table filled by SCATTER against the per-token scatter-add."""
@@ -97,7 +77,9 @@ def test_full_word_tiny_8k(lz):
     U = len(o[0])
     S = oracle.segsum(g, o[3], U)
     sq = H.sum_of_squares(g, o[3], U, oracle)
-    assert H.row_rel_err(pipe.out[:U].cpu().numpy(), S, sq) <= H.TOL_F32
+    got = pipe.out[:U].cpu().numpy()
+    H.check_rows(got, S, sq)
+    H.assert_single_rows_exact(got, S, o[1])
     dense = oracle.dense_scatter(g, ids, w.V)
     T = pipe.state["table"].cpu().numpy()
     others = np.ones(w.V, bool)
@@ -119,7 +101,9 @@ def test_full_word_step_64k(lz, name):
     U = len(o[0])
     S = oracle.segsum(g, o[3], U)
     sq = H.sum_of_squares(g, o[3], U, oracle)
-    assert H.row_rel_err(pipe.out[:U].cpu().numpy(), S, sq) <= H.TOL_F32
+    got = pipe.out[:U].cpu().numpy()
+    H.check_rows(got, S, sq)
+    H.assert_single_rows_exact(got, S, o[1])
     lr = _f32(w.lr)
     ref = oracle.sgd(table0[o[0]], S, lr)
     table = pipe.state["table"]
@@ -136,36 +120,47 @@ def test_full_word_step_64k(lz, name):
 @pytest.mark.parametrize("name", ["merge_64x32k_bf16", "merge_64x32k_f16"])
 def test_full_merge_64x32k_bf16(lz, name):
     """64 concatenated shards of 32,768 tokens (2,097,152), bf16 gradients:
-    Unique of the concatenation and of shard 0, sampled Seg-Sum rows of the
-    concatenation, every Seg-Sum row of shard 0 and its EXPAND into the
-    merged type list, as fp32 or as the binary16 payload of Sec. III-C
-    (F = 64)."""
+    Unique of the concatenation and of shard 0, every Seg-Sum row of the
+    concatenation (326K types) and of shard 0, the map of shard 0's types
+    into the merged list (lm_map_ids) and the EXPAND of shard 0's rows into
+    it, as fp32 or as the binary16 payload of Sec. III-C (F = 64). With
+    1024 columns a row's largest |sum| always exceeds the rms of its
+    summands, so the rows are scaled by their largest entry alone."""
     w = synth.WORKLOADS[name]
     ids, g = w.ids(), w.grads()
     pipe = _run(lz, w, ids, g)
     o = H.assert_unique_matches(pipe.ures, ids, w.V, oracle, w.name)
     UG = len(o[0])
-    pos = _sample_types(o[1], 31)
-    S, sq = _sampled_sums(ids, g, o[0][pos])
-    got = pipe.out[torch.from_numpy(pos).to(pipe.out.device)].cpu().numpy()
-    assert H.row_rel_err(got, S, sq) <= H.TOL_BF16
-    # shard 0: steps 1-2 on its own tokens, step 5 into the merged rows
+    S = oracle.segsum_threads(g, o[3], UG, THREADS)
+    got = pipe.out[:UG].cpu().numpy()
+    H.check_rows(got, S, None, w.grad_dtype, "merged rows")
+    H.assert_single_rows_exact(got, S, o[1], "merged rows")
+    del S, got
+    # shard 0: steps 1-2 on its own tokens, step 4's map, step 5 into the
+    # merged rows
     ids0, g0 = ids[:w.K], g[:w.K]
     u0 = pipe.state["u0"]
     o0 = H.assert_unique_matches(u0, ids0, w.V, oracle, w.name + " shard 0")
     U0 = len(o0[0])
     S0 = oracle.segsum(g0, o0[3], U0)
     sq0 = H.sum_of_squares(g0, o0[3], U0, oracle)
-    assert H.row_rel_err(pipe.state["out0"][:U0].cpu().numpy(), S0, sq0) <= H.TOL_BF16
+    got0 = pipe.state["out0"][:U0].cpu().numpy()
+    H.check_rows(got0, S0, sq0, w.grad_dtype, "shard 0 rows")
+    H.assert_single_rows_exact(got0, S0, o0[1], "shard 0 rows")
     mp, missing = oracle.map_ids(o0[0], o[0])
     assert not missing
+    gmap = lz.map_ids(u0.uniq, u0.num_unique, pipe.ures.uniq, pipe.ures.num_unique,
+                      dev_err=pipe.dev_err)
+    torch.cuda.synchronize()
+    lz.check(pipe.dev_err)
+    assert np.array_equal(gmap[:U0].cpu().numpy(), mp), "lm_map_ids at the merge's shape"
     want = oracle.expand(S0, o0[0], o[0])
     others = np.ones(UG, bool)
     others[mp] = False
     if w.step == "expand":
         M = pipe.state["M"][:UG].cpu().numpy()
         assert not M[others].any() and not want[others].any(), "EXPAND must zero the other rows"
-        assert H.row_rel_err(M[mp], want[mp], sq0) <= H.TOL_BF16
+        H.check_rows(M[mp], want[mp], sq0, w.grad_dtype, "EXPAND rows")
     else:
         # The payload codes from the GPU's fp32 sums against the oracle's
         # compression of its fp64 sums: a code may sit one binary16 step away.
@@ -174,7 +169,7 @@ def test_full_merge_64x32k_bf16(lz, name):
         assert not got[others].any(), "EXPAND must zero the other rows"
         dg = oracle.decompress(got[mp], 1.0 / F)
         dr = oracle.decompress(oracle.compress(want[mp], F), 1.0 / F)
-        delta = H.row_delta(S0, H.TOL_BF16, sq0)
+        delta = H.row_delta(S0, H.TOL_F32, sq0)
         bound = delta[:, None] + 2.0 ** -10 * np.abs(dr) + 2.0 ** -24 / F
         assert np.all(np.abs(dg - dr) <= bound)
     _release(pipe)
@@ -190,8 +185,10 @@ def test_full_char_heavy_1m(lz):
     pipe = _run(lz, w, ids, g)
     o = H.assert_unique_matches(pipe.ures, ids, w.V, oracle, w.name)
     U = len(o[0])
-    S = oracle.segsum(g, o[3], U)
-    assert H.row_rel_err(pipe.out[:U].cpu().numpy(), S) <= H.TOL_F32
+    S = oracle.segsum_threads(g, o[3], U, THREADS)
+    got = pipe.out[:U].cpu().numpy()
+    H.check_rows(got, S)
+    H.assert_single_rows_exact(got, S, o[1])
     T = pipe.state["table"].cpu().numpy()
     others = np.ones(w.V, bool)
     others[o[0]] = False
@@ -201,30 +198,34 @@ def test_full_char_heavy_1m(lz):
 
 
 def test_full_vocab2m_adam_i64(lz):
-    """262,144 int64 ids over a 2M vocabulary (Zipf 0.9), D = 1024: sampled
-    Seg-Sum rows, then the first lazy-Adam step (beta1 0.9, beta2 0.999,
-    eps 1e-8, lr 1e-3, zero moments) on the touched rows of the 2M x 1024
+    """262,144 int64 ids over a 2M vocabulary (Zipf 0.9), D = 1024: every
+    Seg-Sum row, then the first lazy-Adam step (beta1 0.9, beta2 0.999,
+    eps 1e-8, lr 1e-3, zero moments) on every touched row of the 2M x 1024
     param, m and v tables; every untouched row is compared exactly."""
     w = synth.WORKLOADS["vocab2m_adam_i64"]
     ids, g, table0 = w.ids(), w.grads(), w.table()
     pipe = _run(lz, w, ids, g, table0)
     o = H.assert_unique_matches(pipe.ures, ids, w.V, oracle, w.name)
-    pos = _sample_types(o[1], 51)
-    sel = o[0][pos]
-    S, sq = _sampled_sums(ids, g, sel)
-    dev = pipe.out.device
-    got = pipe.out[torch.from_numpy(pos).to(dev)].cpu().numpy()
-    assert H.row_rel_err(got, S, sq) <= H.TOL_F32
+    U = len(o[0])
+    S = oracle.segsum_threads(g, o[3], U, THREADS)
+    got = pipe.out[:U].cpu().numpy()
+    H.check_rows(got, S)
+    H.assert_single_rows_exact(got, S, o[1])
+    del got
+    sel = o[0]
     lr, (b1, b2, eps) = _f32(w.lr), (_f32(x) for x in w.adam)
     z = np.zeros_like(S)
-    rp, rm, rv = oracle.adam(table0[sel], z, z, S, lr, b1, b2, eps, 0.0, 1)
+    rp, rm, rv = oracle.adam_threads(table0[sel], z, z, S, lr, b1, b2, eps, 0.0, 1, THREADS)
+    del z
+    dev = pipe.out.device
     sel_t = torch.from_numpy(sel).to(dev)
     st = pipe.state
     H.assert_adam_first_step(st["table"][sel_t].cpu().numpy(), st["m"][sel_t].cpu().numpy(),
                              st["v"][sel_t].cpu().numpy(), rp, rm, rv, S, lr, b1, b2, eps,
-                             H.row_delta(S, H.TOL_F32, sq))
+                             H.row_delta(S, H.TOL_F32))
+    del rp, rm, rv
     others = torch.ones(w.V, dtype=torch.bool, device=dev)
-    others[torch.from_numpy(o[0]).to(dev)] = False
+    others[sel_t] = False
     t0 = torch.from_numpy(table0).to(dev)
     assert torch.equal(st["table"][others], t0[others]), "untouched rows must be bit-unchanged"
     del t0
@@ -233,21 +234,36 @@ def test_full_vocab2m_adam_i64(lz):
     _release(pipe)
 
 
-@pytest.mark.parametrize("rule", ["G", "pow0.64", "one"])
+# Sec. III-B at G = 64 GPUs, restated here rather than taken from the
+# package: the number of sampler seeds of each rule (ceil of the rule's
+# value, at least one), and GPU g of G using seed j when g lies in
+# [ceil(j G / n), ceil((j + 1) G / n)) -- n contiguous groups of equal size
+# to within one.
+SEEDS_AT_64 = {"G": 64, "pow0.64": 15, "log2": 6, "ln": 5, "log10": 2, "one": 1}
+
+
+def _seed_table(G, n):
+    bounds = [-(-j * G // n) for j in range(n + 1)]
+    return [j for j in range(n) for _ in range(bounds[j], bounds[j + 1])]
+
+
+@pytest.mark.parametrize("rule", list(SEEDS_AT_64))
 def test_full_sampled_softmax(lz, rule):
     """The output embedding under sampled softmax (Sec. III-B) for 64 GPUs on
     one GPU: each samples 1024 candidates from 800K words with its group's
     seed and adds its 640 batch words; the GPU's sampled ids equal the
     oracle's sampler on the same random words, then Unique, every Seg-Sum
-    row (D = 512) and the SGD update are checked as for the word step."""
-    from paper_1810_10045_amd import seeding
+    row (D = 512) and the SGD update are checked as for the word step. The
+    seed of each GPU comes from the table above, for every rule."""
     w = synth.WORKLOADS["sampled_softmax_64x1024_" + rule]
-    words = w.sampler_words(seeding.seed_of_gpus(w.shards, rule))
+    seeds = _seed_table(w.shards, SEEDS_AT_64[rule])
+    assert len(seeds) == w.shards and len(set(seeds)) == SEEDS_AT_64[rule]
+    words = w.sampler_words(seeds)
     ids = np.concatenate([oracle.sample_ids(words, w.V).astype(np.int32), w.ids()])
     g, table0 = w.grads(), w.table()
     import bench
     dev = torch.device("cuda:0")
-    _say(f"[fullsize] {w.name}: {w.tokens} rows, {seeding.num_seeds(w.shards, rule)} seeds")
+    _say(f"[fullsize] {w.name}: {w.tokens} rows, {SEEDS_AT_64[rule]} seeds")
     pipe = bench.Pipeline(w, [bench.Batch(w, torch, dev, ids=ids, grads=g, words=words)], torch,
                           lz, dev, table=table0)
     pipe.step(0)
@@ -258,7 +274,9 @@ def test_full_sampled_softmax(lz, rule):
     U = len(o[0])
     S = oracle.segsum(g, o[3], U)
     sq = H.sum_of_squares(g, o[3], U, oracle)
-    assert H.row_rel_err(pipe.out[:U].cpu().numpy(), S, sq) <= H.TOL_F32
+    got = pipe.out[:U].cpu().numpy()
+    H.check_rows(got, S, sq)
+    H.assert_single_rows_exact(got, S, o[1])
     lr = _f32(w.lr)
     ref = oracle.sgd(table0[o[0]], S, lr)
     table = pipe.state["table"]

@@ -101,13 +101,22 @@ UNIQUE_CASES = [
     # (20- and 40-bit keys above)
     (7000, 20_000, 1.2, np.int32, 37), (8000, 2**31 - 1, 0.0, np.int32, 38),
     (5000, 2**62, 0.8, np.int64, 39),
-    # tile-local passes joined by gathers (1024-thread tiles, 12 to 64 of
-    # them; the cases above from 22,529 to 131,072 ids take them too): the
-    # last K before them and the first, one pass over 0 key bits, one 9-bit
-    # pass, two 9-bit passes, three 7-bit passes, 64 tiles of 40-bit keys
+    # tile-local passes joined by gathers, 12 to 64 tiles (the cases above
+    # from 22,529 to 131,072 ids take them too). Up to 65,536 ids: tiles of
+    # 1,024 keys on 256 threads, digits of at most 8 bits; the last K before
+    # them (11 tiles of 2,048: look-back passes, two 10-bit digits) and the
+    # first (23 tiles, 7 + 7 + 6 bits), one pass over 0 key bits, 9-bit keys
+    # as 5 + 4 bits, 18-bit int64 keys as 6 + 6 + 6 bits.
     (22_528, 800_000, 1.0, np.int32, 43), (22_529, 800_000, 1.0, np.int32, 44),
     (40_000, 1, 1.0, np.int32, 40), (40_000, 300, 1.0, np.int32, 45),
-    (65_536, 1 << 18, 1.0, np.int64, 46), (70_001, 1 << 21, 1.0, np.int32, 41),
+    (65_536, 1 << 18, 1.0, np.int64, 46),
+    # From 65,537 to 131,072 ids: tiles of 2,048 keys on 1024 threads, digits
+    # of up to 9 bits: 21-bit keys as 7 + 7 + 7 bits; one 9-bit pass; 17-bit
+    # keys as 9 + 8 bits; two 9-bit passes (int32 and int64); three 9-bit
+    # passes over 27-bit int64 keys; 64 tiles of 40-bit keys in 8-bit passes.
+    (70_001, 1 << 21, 1.0, np.int32, 41), (70_001, 512, 1.0, np.int32, 47),
+    (100_000, 1 << 17, 1.0, np.int32, 48), (100_000, 1 << 18, 1.0, np.int32, 49),
+    (100_000, 1 << 18, 1.0, np.int64, 50), (131_072, 1 << 27, 0.9, np.int64, 51),
     (131_072, 2**40, 0.9, np.int64, 42),
 ]
 
@@ -281,12 +290,8 @@ def test_segsum_random(lz, K, V, s, D, gdt, seed, perm_seed=0):
     U = len(o[0])
     ref = oracle.segsum(grad, o[3], U)
     got = out[:U].double().cpu().numpy()
-    err = H.row_rel_err(got, ref, H.sum_of_squares(grad, o[3], U, oracle))
-    tol = H.TOL_BF16 if gdt == "bf16" else H.TOL_F32
-    _say(f"  U={U} max row-relative error {err:.3e} (tol {tol})")
-    assert err <= tol
-    ones = o[1] == 1
-    assert np.array_equal(got[ones], ref[ones]), "count-1 rows must be exact copies"
+    H.check_rows(got, ref, H.sum_of_squares(grad, o[3], U, oracle), gdt)
+    H.assert_single_rows_exact(got, ref, o[1])
 
 
 PERM_CASES = [
@@ -323,8 +328,7 @@ def test_segsum_chunks_inside_short_segments(lz, gdt):
     o = H.assert_unique_matches(res, ids, V, oracle)
     U = len(o[0])
     ref = oracle.segsum(grad, o[3], U)
-    err = H.row_rel_err(out[:U].double().cpu().numpy(), ref, H.sum_of_squares(grad, o[3], U, oracle))
-    assert err <= (H.TOL_BF16 if gdt == "bf16" else H.TOL_F32)
+    H.check_rows(out[:U].double().cpu().numpy(), ref, H.sum_of_squares(grad, o[3], U, oracle), gdt)
 
 
 def _piece_counts(ids, V, rw, ww):
@@ -382,8 +386,7 @@ def test_segsum_fixup_piece_counts(lz, gdt):
     o = H.assert_unique_matches(res, ids, V, oracle)
     U = len(o[0])
     ref = oracle.segsum(grad, o[3], U)
-    err = H.row_rel_err(out[:U].double().cpu().numpy(), ref, H.sum_of_squares(grad, o[3], U, oracle))
-    assert err <= (H.TOL_BF16 if gdt == "bf16" else H.TOL_F32)
+    H.check_rows(out[:U].double().cpu().numpy(), ref, H.sum_of_squares(grad, o[3], U, oracle), gdt)
 
 
 def test_segsum_workspace_reuse(lz):
@@ -403,8 +406,8 @@ def test_segsum_workspace_reuse(lz):
         o = H.assert_unique_matches(res, ids, V, oracle)
         U = len(o[0])
         ref = oracle.segsum(grad, o[3], U)
-        err = H.row_rel_err(out[:U].double().cpu().numpy(), ref, H.sum_of_squares(grad, o[3], U, oracle))
-        assert err <= (H.TOL_BF16 if gdt == "bf16" else H.TOL_F32)
+        H.check_rows(out[:U].double().cpu().numpy(), ref, H.sum_of_squares(grad, o[3], U, oracle),
+                     gdt)
 
 
 def test_segsum_wait_failure_is_reported(lz):
@@ -442,10 +445,40 @@ def test_segsum_wait_failure_is_reported(lz):
 
 
 def test_segsum_deterministic(lz):
-    a = _segsum_case(lz, 60_000, 500, 1.2, 1024, "f32", 51)[3].clone()
-    b = _segsum_case(lz, 60_000, 500, 1.2, 1024, "f32", 51)[3]
+    _, _, ra, a = _segsum_case(lz, 60_000, 500, 1.2, 1024, "f32", 51)
+    _, _, rb, b = _segsum_case(lz, 60_000, 500, 1.2, 1024, "f32", 51)
     torch.cuda.synchronize()
-    assert torch.equal(a, b)
+    U = int(ra.num_unique.item())
+    assert U == int(rb.num_unique.item())
+    assert torch.equal(a[:U], b[:U])  # rows past U are never written
+
+
+@pytest.mark.parametrize("K,V,s,D,gdt,seed", [(65_536, 800_000, 1.0, 1024, "f32", 121),
+                                               (60_000, 500, 1.2, 1024, "f32", 122),
+                                               (70_000, 800_000, 1.0, 1024, "bf16", 123)])
+def test_segsum_two_launch_switch(lz, K, V, s, D, gdt, seed):
+    """lm_segsum_set_two_launches: shapes that take the one-launch form by
+    default run as the walk plus a separate fix-up kernel while the switch
+    is on. Both forms are checked against the oracle; the two-launch form is
+    bit-identical from run to run; switching back restores the default."""
+    _say(f"segsum two-launch switch K={K} D={D} {gdt}")
+    assert lz.segsum_two_launches(True) is False, "the switch is off by default"
+    try:
+        ids, grad, res, two = _segsum_case(lz, K, V, s, D, gdt, seed)
+        again = _segsum_case(lz, K, V, s, D, gdt, seed)[3]
+        torch.cuda.synchronize()
+        lz.check(res.dev_err)
+    finally:
+        assert lz.segsum_two_launches(False) is True
+    one = _segsum_case(lz, K, V, s, D, gdt, seed)[3]
+    torch.cuda.synchronize()
+    o = H.assert_unique_matches(res, ids, V, oracle)
+    U = len(o[0])
+    ref = oracle.segsum(grad, o[3], U)
+    sq = H.sum_of_squares(grad, o[3], U, oracle)
+    assert torch.equal(two[:U], again[:U]), "two-launch form not deterministic"
+    H.check_rows(two[:U].double().cpu().numpy(), ref, sq, gdt, "two launches")
+    H.check_rows(one[:U].double().cpu().numpy(), ref, sq, gdt, "one launch")
 
 
 def test_segsum_special_rows(lz):
