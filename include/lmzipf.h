@@ -129,6 +129,24 @@ int lm_unique(const void* ids, int32_t idtype, int64_t K, int64_t V,
               int32_t* perm, int64_t* num_unique, int32_t* dev_err,
               void* ws, size_t ws_bytes, void* stream);
 
+/* lm_unique_noalloc — for callers that cannot allocate device memory
+ * (code under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc): lm_unique with the same arguments, outputs and errors, but
+ * with its workspace in a 12 MiB device array of the library instead of a
+ * caller's buffer. The call allocates nothing (no hipMalloc, no allocating
+ * library routine). Each GPU the library runs on holds its own array from
+ * module load until the process ends; its address is looked up on the first
+ * call on a device (the current device, which must be the stream's).
+ * K > LM_UNIQUE_NOALLOC_MAX_K returns LM_E_UNSUPPORTED before anything is
+ * enqueued. The array needs no initial contents (the call's first kernel
+ * clears what it uses), but every call on one GPU shares it: calls that
+ * overlap on one GPU (other streams, other host threads) race, so order
+ * them on one stream or use lm_unique with a workspace each. */
+#define LM_UNIQUE_NOALLOC_MAX_K ((int64_t)262144)
+int lm_unique_noalloc(const void* ids, int32_t idtype, int64_t K, int64_t V,
+                      void* uniq, int32_t* counts, int32_t* offsets, int32_t* inverse,
+                      int32_t* perm, int64_t* num_unique, int32_t* dev_err, void* stream);
+
 /* ------------------------------------------------------------------------
  * Seg-Sum — Sec. III-A step 2 (and Sec. II-A: several rows of Delta map to
  * one row of E, so the reverse map is an accumulation):

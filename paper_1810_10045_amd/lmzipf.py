@@ -60,6 +60,7 @@ def _load():
     L.lm_unique_workspace_bytes.argtypes = [I64_, I32_, I64_]
     L.lm_unique_workspace_bytes.restype = SZ
     L.lm_unique.argtypes = [P, I32_, I64_, I64_, P, P, P, P, P, P, P, P, SZ, P]
+    L.lm_unique_noalloc.argtypes = [P, I32_, I64_, I64_, P, P, P, P, P, P, P, P]
     L.lm_segsum_workspace_bytes.argtypes = [I64_, I64_]
     L.lm_segsum_workspace_bytes.restype = SZ
     L.lm_segsum.argtypes = [P, I32_, I64_, I64_, I64_, P, P, P, P, I64_, P, I64_, P, P, SZ, P]
@@ -74,7 +75,8 @@ def _load():
     L.lm_sample_ids.argtypes = [P, I64_, I64_, P, I32_, P]
     L.lm_segsum_set_two_launches.argtypes = [I32_]
     L.lm_test_force_wait_failure.argtypes = [I32_, ctypes.c_uint32]
-    for f in ("lm_abi_version", "lm_workspace_clear", "lm_unique", "lm_segsum", "lm_map_ids",
+    for f in ("lm_abi_version", "lm_workspace_clear", "lm_unique", "lm_unique_noalloc",
+              "lm_segsum", "lm_map_ids",
               "lm_fill_values", "lm_sparse_apply", "lm_fill_values_f16", "lm_sparse_apply_f16",
               "lm_sample_ids", "lm_segsum_set_two_launches", "lm_test_force_wait_failure"):
         getattr(L, f).restype = ctypes.c_int
@@ -191,6 +193,20 @@ def unique_buffers(K: int, V: int, id_dtype, device) -> UniqueResult:
         torch.zeros(1, dtype=torch.int32, **z))
 
 
+def _check_unique_out(out: UniqueResult, ids: torch.Tensor, V: int):
+    """The output buffers must hold what the kernels write: min(K, V) types,
+    one offset more, K inverse and perm entries, on the ids' device."""
+    K = ids.numel()
+    cap = min(K, V)
+    need = ((out.uniq, cap, ids.dtype), (out.counts, cap, torch.int32),
+            (out.offsets, cap + 1, torch.int32), (out.inverse, K, torch.int32),
+            (out.perm, K, torch.int32), (out.num_unique, 1, torch.int64),
+            (out.dev_err, 1, torch.int32))
+    for t, n, dt in need:
+        if t.device != ids.device or t.dtype != dt or not t.is_contiguous() or t.numel() < n:
+            raise LmError(f"unique output buffer: need {n} contiguous {dt} on {ids.device}")
+
+
 def unique_workspace_bytes(K: int, V: int, id_dtype=torch.int32) -> int:
     """lm_unique_workspace_bytes: the workspace one lm_unique call of K ids
     of dtype id_dtype over [0, V) needs (0: the sizes are rejected)."""
@@ -208,6 +224,7 @@ def unique(ids: torch.Tensor, V: int, out: Optional[UniqueResult] = None,
     ids = ids.contiguous()
     if out is None:
         out = unique_buffers(K, V, ids.dtype, ids.device)
+    _check_unique_out(out, ids, V)
     ws = ws or default_workspace(ids.device)
     need = _lib.lm_unique_workspace_bytes(K, idt, V)
     if need == 0 and K > 0:
@@ -216,6 +233,26 @@ def unique(ids: torch.Tensor, V: int, out: Optional[UniqueResult] = None,
     _call(_lib.lm_unique(_ptr(ids), idt, K, V, _ptr(out.uniq), _ptr(out.counts), _ptr(out.offsets),
                          _ptr(out.inverse), _ptr(out.perm), _ptr(out.num_unique), _ptr(out.dev_err),
                          _ptr(buf), buf.numel(), _stream(stream)), "lm_unique")
+    return out
+
+
+UNIQUE_NOALLOC_MAX_K = 262144  # LM_UNIQUE_NOALLOC_MAX_K
+
+
+def unique_noalloc(ids: torch.Tensor, V: int, out: UniqueResult, stream=None) -> UniqueResult:
+    """lm_unique_noalloc: lm_unique with the library's own device workspace,
+    for callers that cannot allocate. The outputs must be given (allocating
+    them is the caller's business); at most UNIQUE_NOALLOC_MAX_K ids. Calls
+    that overlap on one GPU share the workspace and race."""
+    _dev(ids, "ids")
+    if not ids.is_contiguous():
+        raise LmError("ids must be contiguous (a copy would allocate)")
+    K = ids.numel()
+    _check_unique_out(out, ids, V)
+    _call(_lib.lm_unique_noalloc(_ptr(ids), _idtype(ids), K, V, _ptr(out.uniq), _ptr(out.counts),
+                                 _ptr(out.offsets), _ptr(out.inverse), _ptr(out.perm),
+                                 _ptr(out.num_unique), _ptr(out.dev_err), _stream(stream)),
+          "lm_unique_noalloc")
     return out
 
 
