@@ -115,6 +115,7 @@ struct SegArgs {
   uint32_t spin_limit;  // polls of a flag before the wait gives up
   int main_blocks, fix_tiles, fused;
   int R, nchunks, rw, ww;  // cost of a position / of a segment end
+  int max_chunks;          // chunks the workspace holds
   int32_t* dev_err;
 };
 
@@ -731,37 +732,102 @@ constexpr int rf_for() {
                  : (R >= LMZ_SEG_LONG_R ? LMZ_SEG_RF2_LONG : LMZ_SEG_RF2);
 }
 
+// Multiprocessors of the current device (queried once per device).
+static int device_cus() {
+  static std::atomic<int> cus[64];
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) {
+    (void)hipGetLastError();
+    return 0;
+  }
+  int n = cus[dev].load(std::memory_order_relaxed);
+  if (n <= 0) {
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) {
+      (void)hipGetLastError();
+      return 0;
+    }
+    cus[dev].store(n, std::memory_order_relaxed);
+  }
+  return n;
+}
+
+// Workgroups of kernel k that fit on one multiprocessor at once (the
+// occupancy the compiled kernel allows), cached by the caller.
+template <typename Kern>
+static int blocks_per_cu(Kern k, int threads, size_t lds, std::atomic<int>& cache) {
+  int b = cache.load(std::memory_order_relaxed);
+  if (b < 0) {
+    b = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&b, k, threads, lds) != hipSuccess) {
+      (void)hipGetLastError();
+      b = 0;
+    }
+    cache.store(b, std::memory_order_relaxed);
+  }
+  return b;
+}
+
+// Whole rounds of waves. The walk's waves (chunks x column tiles) of equal
+// cost run in rounds of as many waves as fit on the device at once. Where
+// they take more than one round, a last round of a few waves runs nearly
+// alone, far below the memory system's rate: the chunk count grows (so the
+// chunks shrink) until the last round is full, at most to the workspace's
+// capacity (a chunk count above the minimum only shortens chunks). Measured
+// at K = 1,048,576, D = 2048 fp32 (two column tiles, room for 2,048 waves):
+// 2,088 chunks (4,176 waves) 1,591 us, 3,072 chunks 1,488 us. Applied to
+// the two-launch form only: in the one-launch form (one column tile) it
+// changed nothing measurable where the last round was half full or more
+// (the bf16 merge: 10,347 waves on room for 4,096), and more chunks than
+// one round made the 2M vocabulary 2% slower; inputs of less than one round
+// are left as they are.
+static int whole_rounds(int nchunks, int tiles, int64_t waves_per_round, int max_chunks) {
+  if (waves_per_round <= 0 || tiles <= 0) return nchunks;
+  const int64_t waves = int64_t(nchunks) * tiles;
+  if (waves <= waves_per_round) return nchunks;
+  const int64_t rounds = (waves + waves_per_round - 1) / waves_per_round;
+  int64_t n = (rounds * waves_per_round + tiles - 1) / tiles;
+  if (n > max_chunks) n = max_chunks;
+  return static_cast<int>(n < nchunks ? nchunks : n);
+}
+
 template <typename GT, int VEC, int NV, int R>
-static void launch_one(const SegArgs& a, dim3 grid, hipStream_t st) {
+static void launch_one(SegArgs& a, int tiles, hipStream_t st) {
   constexpr int RF = rf_for<NV, R>(), T = t_for<R>();
   if constexpr (VEC >= 2) {
     if (a.fused) {
+      a.main_blocks = (a.nchunks + kFusedWaves - 1) / kFusedWaves;
       const int fix_blocks = (a.nchunks + kFusedSpan - 1) / kFusedSpan * a.fix_tiles;
       k_segsum<GT, VEC, NV, RF, R, T, kFusedThreads, true>
           <<<dim3(a.main_blocks + fix_blocks), kFusedThreads, 0, st>>>(a);
       return;
     }
   }
-  k_segsum<GT, VEC, NV, RF, R, T, kSegThreads, false><<<grid, kSegThreads, LMZ_SEG_LDS_PAD, st>>>(a);
+  auto k = k_segsum<GT, VEC, NV, RF, R, T, kSegThreads, false>;
+  static std::atomic<int> bpc{-1};
+  const int64_t room =
+      int64_t(blocks_per_cu(k, kSegThreads, LMZ_SEG_LDS_PAD, bpc)) * kSegWaves * device_cus();
+  a.nchunks = whole_rounds(a.nchunks, tiles, room, a.max_chunks);
+  const dim3 grid((a.nchunks + kSegWaves - 1) / kSegWaves, tiles);
+  k<<<grid, kSegThreads, LMZ_SEG_LDS_PAD, st>>>(a);
 }
 
 template <typename GT, int VEC, int NV>
-static hipError_t launch_r(const SegArgs& a, hipStream_t st) {
+static hipError_t launch_r(SegArgs& a, hipStream_t st) {
   constexpr int CT = NV * kWave * VEC;
-  dim3 grid((a.nchunks + kSegWaves - 1) / kSegWaves, (a.D + CT - 1) / CT);
+  const int tiles = (a.D + CT - 1) / CT;
   switch (a.R) {
-    case 16: launch_one<GT, VEC, NV, 16>(a, grid, st); break;
-    case 32: launch_one<GT, VEC, NV, 32>(a, grid, st); break;
-    case 64: launch_one<GT, VEC, NV, 64>(a, grid, st); break;
-    case 128: launch_one<GT, VEC, NV, 128>(a, grid, st); break;
-    case 256: launch_one<GT, VEC, NV, 256>(a, grid, st); break;
-    default: launch_one<GT, VEC, NV, 512>(a, grid, st); break;
+    case 16: launch_one<GT, VEC, NV, 16>(a, tiles, st); break;
+    case 32: launch_one<GT, VEC, NV, 32>(a, tiles, st); break;
+    case 64: launch_one<GT, VEC, NV, 64>(a, tiles, st); break;
+    case 128: launch_one<GT, VEC, NV, 128>(a, tiles, st); break;
+    case 256: launch_one<GT, VEC, NV, 256>(a, tiles, st); break;
+    default: launch_one<GT, VEC, NV, 512>(a, tiles, st); break;
   }
   return hipGetLastError();
 }
 
 template <typename GT, int VEC>
-static hipError_t dispatch_nv(const SegArgs& a, int nv_max, hipStream_t st) {
+static hipError_t dispatch_nv(SegArgs& a, int nv_max, hipStream_t st) {
   const int per = kWave * VEC;
   int nv = (a.D + per - 1) / per;
   if (nv > nv_max) nv = nv_max;
@@ -836,6 +902,7 @@ int segsum_run(const void* grad, int gtype, int64_t K, int64_t D, int64_t ld_gra
   a.rw = read_cost(gtype);
   a.ww = write_cost(gtype);
   a.nchunks = static_cast<int>(chunks_for(K, L.R, a.rw, a.ww, u_cap));
+  a.max_chunks = L.max_chunks;
   a.dev_err = dev_err;
 
   const bool out_vec = al16(out) && ld_out % 4 == 0 && D % 4 == 0;
@@ -862,7 +929,6 @@ int segsum_run(const void* grad, int gtype, int64_t K, int64_t D, int64_t ld_gra
     const bool fail = g_force_wait_failure.load(std::memory_order_relaxed);
     a.wait_epoch = fail ? a.epoch ^ (uint64_t(1) << 63) : a.epoch;
     a.spin_limit = fail ? g_forced_spin_limit.load(std::memory_order_relaxed) : kSpinLimit;
-    a.main_blocks = (a.nchunks + kFusedWaves - 1) / kFusedWaves;
     a.fix_tiles = static_cast<int>((D + kFusedCols - 1) / kFusedCols);
   }
   hipError_t e;
