@@ -168,7 +168,7 @@ int lm_unique_noalloc(const void* ids, int32_t idtype, int64_t K, int64_t V,
  * ws         device workspace of lm_segsum_workspace_bytes(K, D) bytes,
  *            256-byte aligned; no initial contents are required.
  *
- * With D <= 1024 on the 16-byte vector path, the segments that span the
+ * With D <= 4096 on the 16-byte vector path, the segments that span the
  * walk's chunks are summed by workgroups of the same launch, which wait for
  * per-chunk flags tagged with a per-call value from a process-wide counter
  * (bounded waits; LM_DEVERR_SPIN if one gave up, which a correct call never

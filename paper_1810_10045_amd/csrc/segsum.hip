@@ -29,9 +29,10 @@
 //   sums part_start[c] and part_cont[c + 1 .. c + npieces[c]] in order: one
 //   wave per column tile for a segment of fewer than 16 further pieces, all
 //   waves of a workgroup (fixed stride split of the pieces, fixed-order
-//   combine in LDS) for a head. Where the walk has one column tile, the same
-//   fix-up runs as workgroups of the walk's own launch, each waiting for the
-//   flags of the chunks it reads (the fused launch below).
+//   combine in LDS) for a head. On the 16-byte vector path (rows of up to
+//   LMZ_SEG_FUSED_MAX_D columns) the same fix-up runs as workgroups of the
+//   walk's own launch, each waiting for the flags of the chunks and column
+//   tiles it reads (the fused launch below).
 // A chunk holds at most R positions (N is sized for U = min(K, u_cap)) and
 // reads at most R + T - 1 rows.
 //
@@ -86,6 +87,9 @@ namespace lmz {
 #ifndef LMZ_SEG_FUSED
 #define LMZ_SEG_FUSED 1              // fix-up workgroups in the walk's launch (one column tile)
 #endif
+#ifndef LMZ_SEG_FUSED_MAX_D
+#define LMZ_SEG_FUSED_MAX_D 4096     // widest rows walked and fixed up in one launch
+#endif
 #ifndef LMZ_SEG_LDS_PAD
 #define LMZ_SEG_LDS_PAD 0            // LDS bytes reserved per workgroup (caps waves per CU)
 #endif
@@ -108,12 +112,13 @@ struct SegArgs {
   float* part_start;
   int32_t* desc;
   int32_t* npieces;
-  uint64_t* flags;   // fused launch: flags[c] == epoch once chunk c's descriptor and
-  uint64_t epoch;    // partial rows are visible to every workgroup
+  uint64_t* flags;   // fused launch: flags[c * tiles + t] == epoch once column tile t of
+  uint64_t epoch;    // chunk c (and, for t = 0, its descriptor) is visible everywhere
   uint64_t wait_epoch;  // the value the fix-up waits for: epoch (or, with the
                         // failure-path test hook, one no walk writes)
   uint32_t spin_limit;  // polls of a flag before the wait gives up
   int main_blocks, fix_tiles, fused;
+  int tiles, tile_cols;    // column tiles of the walk and the columns of one
   int R, nchunks, rw, ww;  // cost of a position / of a segment end
   int max_chunks;          // chunks the workspace holds
   int32_t* dev_err;
@@ -158,7 +163,7 @@ static SegLayout seg_layout(int64_t K, int64_t D) {
   L.start = off;    off += a256(n * D * 4);
   L.desc = off;     off += a256(n * 4);
   L.npieces = off;  off += a256(n * 4);
-  L.flags = off;    off += a256(n * 8);
+  L.flags = off;    off += a256(n * size_t((D + 1023) / 1024) * 8);  // per chunk and column tile
   L.total = off;
   return L;
 }
@@ -228,6 +233,11 @@ __device__ __forceinline__ void chunk_bounds(const int32_t* __restrict__ offsets
 // L2s), the walk waits for them before it sets its flag to the call's
 // epoch, and the fix-up reads them with agent-scope loads once the flag
 // holds that epoch: no workspace contents need clearing between calls.
+// Rows wider than one walk tile (1024 columns) take one flag per chunk and
+// tile: workgroup b of the walk is column tile b % tiles of chunks
+// (b / tiles) * 4 ..., and a fix-up tile of 256 columns, which lies inside
+// one walk tile, waits for that tile's flags (tile 0's also covers the
+// chunk's descriptor).
 // ---------------------------------------------------------------------------
 constexpr int kFusedThreads = 256;
 constexpr int kFusedWaves = kFusedThreads / kWave;
@@ -293,6 +303,11 @@ __device__ __forceinline__ void fused_fix(const SegArgs& a) {
   const int D = a.D;
   const int col = (f % a.fix_tiles) * kFusedCols + lane * 4;
   const int col_ld = col < D ? col : D - 4;  // past the end: a valid, unstored vector
+  // The walk's column tile these columns belong to (a fix-up tile of
+  // kFusedCols columns never straddles two), and the flag of chunk x's part
+  // of it; tile 0's flag also covers x's descriptor.
+  const int wt = (f % a.fix_tiles) * kFusedCols / a.tile_cols;
+  auto flag_of = [&](int x, int t) { return x * a.tiles + t; };
   const int U = first_lane(static_cast<int>(*a.num_unique));
 
   // Wave 0 waits for the span and reads its descriptors once; every wave
@@ -301,7 +316,7 @@ __device__ __forceinline__ void fused_fix(const SegArgs& a) {
   const bool mine = lane < nc;
   const int ci = c0 + (mine ? lane : 0);
   if (wave == 0) {
-    wait_flags(a, ci, mine);
+    wait_flags(a, flag_of(ci, 0), mine);
     s_desc[lane] = mine ? ld_agent(a.desc + ci) : -1;
     s_np[lane] = mine ? ld_agent(a.npieces + ci) : 0;
   }
@@ -321,7 +336,7 @@ __device__ __forceinline__ void fused_fix(const SegArgs& a) {
     if (j % kFusedWaves != wave) continue;
     const int i = __builtin_ctzll(m);
     const int cs = c0 + i, s = read_lane(sd, i), P = read_lane(np, i);
-    wait_flags(a, cs + (lane <= P ? lane : 0), lane <= P);
+    wait_flags(a, flag_of(cs + (lane <= P ? lane : 0), wt), lane <= P);
     float acc[4] = {0.f, 0.f, 0.f, 0.f};
     for (int t0 = 0; t0 <= P; t0 += RF) {
       float buf[RF][4];
@@ -343,7 +358,7 @@ __device__ __forceinline__ void fused_fix(const SegArgs& a) {
     float acc[4] = {0.f, 0.f, 0.f, 0.f};
     for (int t0 = wave; t0 <= P; t0 += kFusedWaves * RF) {
       const int tl = t0 + (lane < RF ? lane : 0) * kFusedWaves;  // lane r: piece t0 + r * W
-      wait_flags(a, cs + (tl <= P ? tl : 0), lane < RF && tl <= P);
+      wait_flags(a, flag_of(cs + (tl <= P ? tl : 0), wt), lane < RF && tl <= P);
       float buf[RF][4];
 #pragma unroll
       for (int r = 0; r < RF; ++r) {
@@ -387,7 +402,11 @@ __global__ __launch_bounds__(NTHR) void k_segsum(SegArgs a) {
   constexpr int NW = windows_for<R, T>();
 
   const int lane = lane_id();
-  const int c = first_lane(blockIdx.x * (NTHR / kWave) + (threadIdx.x >> 6));  // one chunk per wave
+  // One chunk and column tile per wave: the fused grid is one-dimensional,
+  // column tile = block % tiles; otherwise the tile is blockIdx.y.
+  const int blk = FUSED ? static_cast<int>(blockIdx.x) / a.tiles : static_cast<int>(blockIdx.x);
+  const int ct = FUSED ? static_cast<int>(blockIdx.x) % a.tiles : static_cast<int>(blockIdx.y);
+  const int c = first_lane(blk * (NTHR / kWave) + static_cast<int>(threadIdx.x >> 6));
   if (c >= a.nchunks) return;
   // Fused launch: once this chunk's descriptor and partial rows are visible
   // at agent scope (written with agent-scope stores, then waited for),
@@ -395,10 +414,9 @@ __global__ __launch_bounds__(NTHR) void k_segsum(SegArgs a) {
   auto publish = [&]() {
     if constexpr (FUSED) {
       asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-      if (lane_id() == 0) st_agent(a.flags + c, a.epoch);
+      if (lane_id() == 0) st_agent(a.flags + size_t(c) * a.tiles + ct, a.epoch);
     }
   };
-  const int ct = blockIdx.y;
   const int K = a.K, D = a.D;
 
   // 0. This chunk's positions [p0, p1): equal shares of the cost rw * K + ww * U.
@@ -768,22 +786,22 @@ static int blocks_per_cu(Kern k, int threads, size_t lds, std::atomic<int>& cach
 }
 
 // Whole rounds of waves. The walk's waves (chunks x column tiles) of equal
-// cost run in rounds of as many waves as fit on the device at once. Where
-// they take more than one round, a last round of a few waves runs nearly
-// alone, far below the memory system's rate: the chunk count grows (so the
+// cost run in rounds of as many waves as fit on the device at once. Where a
+// last round would be less than half full, its few waves run nearly alone,
+// far below the memory system's rate: the chunk count then grows (so the
 // chunks shrink) until the last round is full, at most to the workspace's
-// capacity (a chunk count above the minimum only shortens chunks). Measured
-// at K = 1,048,576, D = 2048 fp32 (two column tiles, room for 2,048 waves):
-// 2,088 chunks (4,176 waves) 1,591 us, 3,072 chunks 1,488 us. Applied to
-// the two-launch form only: in the one-launch form (one column tile) it
-// changed nothing measurable where the last round was half full or more
-// (the bf16 merge: 10,347 waves on room for 4,096), and more chunks than
-// one round made the 2M vocabulary 2% slower; inputs of less than one round
-// are left as they are.
+// capacity (a chunk count above the minimum only shortens chunks).
+// Measured at K = 1,048,576, D = 2048 fp32 (two column tiles, room for
+// 2,048 waves): 2,088 chunks (4,176 waves) 1,591 us, 3,072 chunks 1,488 us.
+// Where the last round was half full or more (the bf16 merge: 10,347 waves
+// on room for 4,096) rounding up changed nothing measurable, and inputs of
+// less than one round are left as they are (more chunks made the 2M
+// vocabulary 2% slower).
 static int whole_rounds(int nchunks, int tiles, int64_t waves_per_round, int max_chunks) {
   if (waves_per_round <= 0 || tiles <= 0) return nchunks;
   const int64_t waves = int64_t(nchunks) * tiles;
-  if (waves <= waves_per_round) return nchunks;
+  const int64_t last = waves % waves_per_round;
+  if (waves <= waves_per_round || last == 0 || 2 * last >= waves_per_round) return nchunks;
   const int64_t rounds = (waves + waves_per_round - 1) / waves_per_round;
   int64_t n = (rounds * waves_per_round + tiles - 1) / tiles;
   if (n > max_chunks) n = max_chunks;
@@ -793,12 +811,17 @@ static int whole_rounds(int nchunks, int tiles, int64_t waves_per_round, int max
 template <typename GT, int VEC, int NV, int R>
 static void launch_one(SegArgs& a, int tiles, hipStream_t st) {
   constexpr int RF = rf_for<NV, R>(), T = t_for<R>();
+  a.tiles = tiles;
+  a.tile_cols = NV * kWave * VEC;
   if constexpr (VEC >= 2) {
     if (a.fused) {
-      a.main_blocks = (a.nchunks + kFusedWaves - 1) / kFusedWaves;
+      auto k = k_segsum<GT, VEC, NV, RF, R, T, kFusedThreads, true>;
+      static std::atomic<int> bpc{-1};
+      const int64_t room = int64_t(blocks_per_cu(k, kFusedThreads, 0, bpc)) * kFusedWaves * device_cus();
+      a.nchunks = whole_rounds(a.nchunks, tiles, room, a.max_chunks);
+      a.main_blocks = (a.nchunks + kFusedWaves - 1) / kFusedWaves * tiles;
       const int fix_blocks = (a.nchunks + kFusedSpan - 1) / kFusedSpan * a.fix_tiles;
-      k_segsum<GT, VEC, NV, RF, R, T, kFusedThreads, true>
-          <<<dim3(a.main_blocks + fix_blocks), kFusedThreads, 0, st>>>(a);
+      k<<<dim3(a.main_blocks + fix_blocks), kFusedThreads, 0, st>>>(a);
       return;
     }
   }
@@ -908,10 +931,12 @@ int segsum_run(const void* grad, int gtype, int64_t K, int64_t D, int64_t ld_gra
   const bool out_vec = al16(out) && ld_out % 4 == 0 && D % 4 == 0;
   const bool vec = gtype == LM_F32 ? out_vec && al16(grad) && ld_grad % 4 == 0
                                    : out_vec && al16(grad) && ld_grad % 8 == 0 && D % 8 == 0;
-  // One launch for the walk and the fix-up where the walk has one column
-  // tile (vector path, D <= 1024).
-  a.fused = LMZ_SEG_FUSED != 0 && vec && D <= 1024 && (LMZ_SEG_NV_MAX >= 4 || gtype != LM_F32) &&
-            !two_launches();
+  // One launch for the walk and the fix-up on the vector path. Measured at
+  // K = 1,048,576, D = 2048 fp32 (two column tiles): 1,490 us as the walk
+  // and a separate fix-up kernel, 1,411 us in one launch, the fix-up
+  // workgroups running in the walk's last round.
+  a.fused = LMZ_SEG_FUSED != 0 && vec && D <= LMZ_SEG_FUSED_MAX_D &&
+            (LMZ_SEG_NV_MAX >= 4 || gtype != LM_F32) && !two_launches();
   // A captured launch would replay with this call's epoch every time, and a
   // replay could take the previous replay's flags for its own: under stream
   // capture the fix-up is a second launch, which keeps no state across calls.

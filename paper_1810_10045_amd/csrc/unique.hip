@@ -34,7 +34,10 @@
 
 namespace lmz {
 
-constexpr int kHistThreads = 1024;
+#ifndef LMZ_UNIQUE_HIST_THREADS
+#define LMZ_UNIQUE_HIST_THREADS 1024
+#endif
+constexpr int kHistThreads = LMZ_UNIQUE_HIST_THREADS;
 #ifndef LMZ_UNIQUE_SMALL_TILE_MAX_K
 #define LMZ_UNIQUE_SMALL_TILE_MAX_K (1 << 14)  // up to this K, 256-thread tiles
 #endif
@@ -81,7 +84,15 @@ constexpr int kGatherSmallTileKeys = 1024;  // keys per 256-thread tile-local wo
 #ifndef LMZ_UNIQUE_LARGE_ITEMS4_MAX_K
 #define LMZ_UNIQUE_LARGE_ITEMS4_MAX_K (3 << 19)
 #endif
+#ifndef LMZ_UNIQUE_LARGE256_MIN_K
+#define LMZ_UNIQUE_LARGE256_MIN_K 0    // > 0: above this K, 256-thread tiles again
+#endif
+#ifndef LMZ_UNIQUE_LARGE256_ITEMS
+#define LMZ_UNIQUE_LARGE256_ITEMS 8    // keys per thread of those tiles (4, 8 or 16)
+#endif
 static inline int items_for(int64_t K, int nt) {
+  if (nt == 256 && LMZ_UNIQUE_LARGE256_MIN_K > 0 && K > LMZ_UNIQUE_LARGE256_MIN_K)
+    return LMZ_UNIQUE_LARGE256_ITEMS;
   if (nt == 256) return K <= LMZ_UNIQUE_SMALL_ITEMS2_MAX_K ? 2 : 4;
   return K <= LMZ_UNIQUE_LARGE_ITEMS2_MAX_K ? 2 : (K <= LMZ_UNIQUE_LARGE_ITEMS4_MAX_K ? 4 : 8);
 }
@@ -142,6 +153,7 @@ static UniqueLayout unique_layout(int64_t K, int idtype, int64_t V) {
   // 26 against 29 us), 1024-thread tiles above (64K ids: 37 against 43 us;
   // 131K ids: 43 against 51 us).
   L.nt = K <= LMZ_UNIQUE_SMALL_TILE_MAX_K ? 256 : 1024;
+  if (LMZ_UNIQUE_LARGE256_MIN_K > 0 && K > LMZ_UNIQUE_LARGE256_MIN_K) L.nt = 256;
   // One workgroup holds up to 1024 * 8 keys (8 per thread keep the ranking
   // and dedup state in registers).
   L.block_items = 0;
@@ -1336,7 +1348,10 @@ static int run_unique(const KeyT* ids, int K, int64_t V, KeyT* uniq, int32_t* co
     };
     auto by_items = [&](auto rb, auto nt) {
       if constexpr (decltype(nt)::value == 256)
-        return L.items == 2 ? pass(rb, nt, I<2>{}) : pass(rb, nt, I<4>{});
+        return L.items == 2 ? pass(rb, nt, I<2>{})
+                            : (L.items == 4 ? pass(rb, nt, I<4>{})
+                                            : (L.items == 8 ? pass(rb, nt, I<8>{})
+                                                            : pass(rb, nt, I<16>{})));
       else
         return L.items == 2 ? pass(rb, nt, I<2>{})
                             : (L.items == 4 ? pass(rb, nt, I<4>{}) : pass(rb, nt, I<8>{}));
@@ -1365,7 +1380,9 @@ static int run_unique(const KeyT* ids, int K, int64_t V, KeyT* uniq, int32_t* co
   };
   if (L.nt == 256) {
     if (L.items == 2) dedup(I<256>{}, I<2>{});
-    else dedup(I<256>{}, I<4>{});
+    else if (L.items == 4) dedup(I<256>{}, I<4>{});
+    else if (L.items == 8) dedup(I<256>{}, I<8>{});
+    else dedup(I<256>{}, I<16>{});
   } else {
     if (L.items == 2) dedup(I<1024>{}, I<2>{});
     else if (L.items == 4) dedup(I<1024>{}, I<4>{});

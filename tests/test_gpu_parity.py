@@ -263,6 +263,10 @@ SEG_CASES = [
     (5000, 100, 1.2, 64, "bf16", 43), (20_000, 300, 1.2, 1024, "bf16", 44),
     (70_000, 800_000, 1.0, 1024, "bf16", 45), (9000, 500, 1.0, 100, "bf16", 46),
     (2000, 50, 1.0, 7, "bf16", 47),
+    # rows wider than one 1024-column tile, walked and fixed up in one launch
+    # (ragged last tiles, bf16 too), and wider than that one launch takes
+    (40_000, 300, 1.2, 2048, "bf16", 48), (12_000, 800, 1.0, 1536, "bf16", 49),
+    (4000, 100, 1.0, 5000, "f32", 50),
 ]
 
 
