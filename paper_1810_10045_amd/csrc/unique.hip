@@ -34,10 +34,10 @@
 
 namespace lmz {
 
-#ifndef LMZ_UNIQUE_HIST_THREADS
-#define LMZ_UNIQUE_HIST_THREADS 1024
+#ifndef LMZ_UNIQUE_HIST_RUNS_MIN_K
+#define LMZ_UNIQUE_HIST_RUNS_MIN_K (1 << 18)  // above this K, lanes' digit runs share an atomic
 #endif
-constexpr int kHistThreads = LMZ_UNIQUE_HIST_THREADS;
+constexpr int kHistThreads = 1024;
 #ifndef LMZ_UNIQUE_SMALL_TILE_MAX_K
 #define LMZ_UNIQUE_SMALL_TILE_MAX_K (1 << 14)  // up to this K, 256-thread tiles
 #endif
@@ -84,15 +84,7 @@ constexpr int kGatherSmallTileKeys = 1024;  // keys per 256-thread tile-local wo
 #ifndef LMZ_UNIQUE_LARGE_ITEMS4_MAX_K
 #define LMZ_UNIQUE_LARGE_ITEMS4_MAX_K (3 << 19)
 #endif
-#ifndef LMZ_UNIQUE_LARGE256_MIN_K
-#define LMZ_UNIQUE_LARGE256_MIN_K 0    // > 0: above this K, 256-thread tiles again
-#endif
-#ifndef LMZ_UNIQUE_LARGE256_ITEMS
-#define LMZ_UNIQUE_LARGE256_ITEMS 8    // keys per thread of those tiles (4, 8 or 16)
-#endif
 static inline int items_for(int64_t K, int nt) {
-  if (nt == 256 && LMZ_UNIQUE_LARGE256_MIN_K > 0 && K > LMZ_UNIQUE_LARGE256_MIN_K)
-    return LMZ_UNIQUE_LARGE256_ITEMS;
   if (nt == 256) return K <= LMZ_UNIQUE_SMALL_ITEMS2_MAX_K ? 2 : 4;
   return K <= LMZ_UNIQUE_LARGE_ITEMS2_MAX_K ? 2 : (K <= LMZ_UNIQUE_LARGE_ITEMS4_MAX_K ? 4 : 8);
 }
@@ -153,7 +145,6 @@ static UniqueLayout unique_layout(int64_t K, int idtype, int64_t V) {
   // 26 against 29 us), 1024-thread tiles above (64K ids: 37 against 43 us;
   // 131K ids: 43 against 51 us).
   L.nt = K <= LMZ_UNIQUE_SMALL_TILE_MAX_K ? 256 : 1024;
-  if (LMZ_UNIQUE_LARGE256_MIN_K > 0 && K > LMZ_UNIQUE_LARGE256_MIN_K) L.nt = 256;
   // One workgroup holds up to 1024 * 8 keys (8 per thread keep the ranking
   // and dedup state in registers).
   L.block_items = 0;
@@ -265,7 +256,7 @@ __device__ __forceinline__ uint32_t digit_of(KeyT k, int shift, uint32_t mask) {
 // pass p is d (rows of rstride slots per pass). Also clears the tickets and the
 // look-back status words of this call.
 // ---------------------------------------------------------------------------
-template <typename KeyT>
+template <typename KeyT, bool RUNS>
 __global__ __launch_bounds__(kHistThreads) void k_hist(
     const KeyT* __restrict__ keys, int K, uint64_t V, int passes, int rstride, PassBits pb,
     uint32_t* __restrict__ bhist, uint32_t* __restrict__ clear, int64_t clear_words,
@@ -288,11 +279,31 @@ __global__ __launch_bounds__(kHistThreads) void k_hist(
     }
 #pragma unroll
     for (int j = 0; j < kHistItems; ++j) {
-      if (i0 + j * stride < K) {
-        const uint64_t kb = key_bits(kv[j]);
-        bad |= kb >= V;
-        for (int p = 0; p < passes; ++p) {
-          const uint32_t d = static_cast<uint32_t>(kb >> pb.shift[p]) & ((1u << pb.nbits[p]) - 1);
+      const bool in = i0 + j * stride < K;
+      const uint64_t kb = key_bits(kv[j]);
+      bad |= in && kb >= V;
+      // the lanes past K are the last ones of the wave
+      const int nact = RUNS ? __popcll(ballot(in)) : 0;
+      for (int p = 0; p < passes; ++p) {
+        const uint32_t d = static_cast<uint32_t>(kb >> pb.shift[p]) & ((1u << pb.nbits[p]) - 1);
+        if constexpr (RUNS) {
+          // Lanes hold consecutive ids: a run of lanes with the same digit
+          // adds its length with one atomic. Zipf heads put long runs of the
+          // heaviest digit on adjacent lanes, whose LDS atomics on one address
+          // would otherwise serialise: measured at 1,048,576 ids over 20K
+          // words 78.3 -> 71.4 us per Unique call, 2M ids 126.6 -> 124.4 us;
+          // at 262,144 ids (32 workgroups, less skew) 60.0 -> 62.0 us, so
+          // only inputs above LMZ_UNIQUE_HIST_RUNS_MIN_K take it.
+          const uint32_t up = static_cast<uint32_t>(__shfl_up(static_cast<int>(d), 1, kWave));
+          const int ln = lane_id();
+          const bool head = in && (ln == 0 || up != d);
+          const uint64_t heads = ballot(head);
+          if (head) {
+            const uint64_t above = ln < 63 ? heads & ~((2ull << ln) - 1ull) : 0ull;
+            const int next = above ? __builtin_ctzll(above) : nact;
+            atomicAdd(&sh[p * rstride + d], static_cast<uint32_t>(next - ln));
+          }
+        } else if (in) {
           atomicAdd(&sh[p * rstride + d], 1u);
         }
       }
@@ -541,6 +552,9 @@ __global__ __launch_bounds__(NT) void k_onesweep(
 // adds up the counts of every tile (one column of words per digit) instead.
 // ---------------------------------------------------------------------------
 constexpr uint32_t kRunCountMask = 0xFFFFu;
+#ifndef LMZ_UNIQUE_RUN_U
+#define LMZ_UNIQUE_RUN_U 16            // run words a thread loads per round in run_total
+#endif
 
 // Keys of digit d over every tile of the previous pass, for thread d < R (0
 // for the others); R is a power of two. The threads split the rows: thread
@@ -554,7 +568,9 @@ __device__ __forceinline__ uint32_t run_total(const uint32_t* __restrict__ runs,
   const int d = tid & (R - 1), g = tid / R;
   uint32_t part = 0;
   if (g < G) {
-    constexpr int kU = 8;  // loads in flight per round
+    // Loads in flight per round: 16 measured 1.6 us faster per call than 8
+    // at 65,536 ids (three gathering kernels), 32 slower than 8.
+    constexpr int kU = LMZ_UNIQUE_RUN_U;
     for (int t0 = g; t0 < tiles; t0 += kU * G) {
       uint32_t w[kU];
 #pragma unroll
@@ -1330,9 +1346,14 @@ static int run_unique(const KeyT* ids, int K, int64_t V, KeyT* uniq, int32_t* co
     return launch_status(L.nt == 256 ? passes(I<256>{}) : passes(I<1024>{}));
   }
   const size_t hist_lds = size_t(L.passes) * L.rstride * 4;
-  k_hist<KeyT><<<L.hist_blocks, kHistThreads, hist_lds, st>>>(
-      ids, K, static_cast<uint64_t>(V), L.passes, L.rstride, pb, bhist, tickets, clear_words,
-      dev_err);
+  if (K > LMZ_UNIQUE_HIST_RUNS_MIN_K)
+    k_hist<KeyT, true><<<L.hist_blocks, kHistThreads, hist_lds, st>>>(
+        ids, K, static_cast<uint64_t>(V), L.passes, L.rstride, pb, bhist, tickets, clear_words,
+        dev_err);
+  else
+    k_hist<KeyT, false><<<L.hist_blocks, kHistThreads, hist_lds, st>>>(
+        ids, K, static_cast<uint64_t>(V), L.passes, L.rstride, pb, bhist, tickets, clear_words,
+        dev_err);
   if (hipError_t e = hipGetLastError(); e != hipSuccess) return launch_status(e);
 
   const KeyT* kin = ids;
@@ -1348,10 +1369,7 @@ static int run_unique(const KeyT* ids, int K, int64_t V, KeyT* uniq, int32_t* co
     };
     auto by_items = [&](auto rb, auto nt) {
       if constexpr (decltype(nt)::value == 256)
-        return L.items == 2 ? pass(rb, nt, I<2>{})
-                            : (L.items == 4 ? pass(rb, nt, I<4>{})
-                                            : (L.items == 8 ? pass(rb, nt, I<8>{})
-                                                            : pass(rb, nt, I<16>{})));
+        return L.items == 2 ? pass(rb, nt, I<2>{}) : pass(rb, nt, I<4>{});
       else
         return L.items == 2 ? pass(rb, nt, I<2>{})
                             : (L.items == 4 ? pass(rb, nt, I<4>{}) : pass(rb, nt, I<8>{}));
@@ -1380,9 +1398,7 @@ static int run_unique(const KeyT* ids, int K, int64_t V, KeyT* uniq, int32_t* co
   };
   if (L.nt == 256) {
     if (L.items == 2) dedup(I<256>{}, I<2>{});
-    else if (L.items == 4) dedup(I<256>{}, I<4>{});
-    else if (L.items == 8) dedup(I<256>{}, I<8>{});
-    else dedup(I<256>{}, I<16>{});
+    else dedup(I<256>{}, I<4>{});
   } else {
     if (L.items == 2) dedup(I<1024>{}, I<2>{});
     else if (L.items == 4) dedup(I<1024>{}, I<4>{});
