@@ -362,11 +362,33 @@ __global__ __launch_bounds__(NT) void k_onesweep(
     }
   };
   fetch(int64_t(blockIdx.x) * kTile);
-  // Totals of this thread's digits over the whole input.
+  // Totals of this thread's digits over the whole input (the histogram
+  // rows of every k_hist workgroup). Where the threads outnumber the digits
+  // (8-bit digits on 1024 threads), kRowGroups threads share a digit, each
+  // summing every kRowGroups-th row, so the rows take one round of loads
+  // instead of two: measured 72.0 -> 69.9 us per call at 1,048,576 ids over
+  // 20K words (64 rows, 8-bit digits).
+  constexpr int kRowGroups = kDigitThreads < NT ? NT / kDigitThreads : 1;
+  __shared__ uint32_t s_rows[kRowGroups > 1 ? kRowGroups : 1][kRowGroups > 1 ? kDigitThreads : 1];
   uint32_t dig_total[DPT];
 #pragma unroll
   for (int i = 0; i < DPT; ++i) dig_total[i] = 0;
-  if (owner) {
+  if constexpr (kRowGroups > 1) {
+    const int d = tid % kDigitThreads, g = tid / kDigitThreads;
+    constexpr int kHistRows = 16;  // rows in flight per round
+    uint32_t part = 0;
+    for (int b = g; b < hist_blocks; b += kRowGroups * kHistRows) {
+      uint32_t h[kHistRows];
+#pragma unroll
+      for (int r = 0; r < kHistRows; ++r) {
+        const int br = b + r * kRowGroups < hist_blocks ? b + r * kRowGroups : g;  // valid, unused
+        h[r] = bhist[size_t(br) * hist_stride + d];
+      }
+#pragma unroll
+      for (int r = 0; r < kHistRows; ++r) part += b + r * kRowGroups < hist_blocks ? h[r] : 0u;
+    }
+    s_rows[g][d] = part;
+  } else if (owner) {
     // Rows in flight per round: 16 with 256-thread tiles (at most 32 rows),
     // 32 with 1024-thread tiles (32 or 64 rows).
     constexpr int kHistRows = NT == 256 ? 16 : 32;
@@ -388,6 +410,11 @@ __global__ __launch_bounds__(NT) void k_onesweep(
   for (int i = tid; i < kWaves * kRadix / 2; i += NT)
     reinterpret_cast<uint32_t*>(&s_cnt[0][0])[i] = 0;
   __syncthreads();
+  if constexpr (kRowGroups > 1) {
+    if (owner)
+#pragma unroll
+      for (int g = 0; g < kRowGroups; ++g) dig_total[0] += s_rows[g][tid];
+  }
   const int tile = first_lane(static_cast<int>(s_tile));
   const int64_t base = int64_t(tile) * kTile;
   if (tile != static_cast<int>(blockIdx.x)) fetch(base);
