@@ -193,6 +193,28 @@ class Pipeline:
             mdt = torch.float16 if w.step == "expand_f16" else torch.float32
             st["M"] = torch.empty((cap, D), dtype=mdt, device=dev)
         self.sets = None
+        # SCATTER into the dense table: Seg-Sum writes each type's row to its
+        # table row itself (lm_segsum_rows), unless `fused` is cleared (then
+        # lm_segsum into `out`, and lm_fill_values SCATTER from there).
+        self.fused = w.step == "scatter"
+
+    def reduce(self, bt, ures, err):
+        """Seg-Sum of batch bt from Unique outputs ures: into `out`, or with
+        `fused`, straight into the table rows of the types (SCATTER done)."""
+        w, lz, st = self.w, self.lz, self.state
+        if self.fused:
+            lz.segsum_rows(bt.grad, ures.perm, ures.inverse, ures.offsets, ures.num_unique,
+                           ures.uniq, st["table"], dev_err=err, ws=self.ws)
+        else:
+            lz.segsum(bt.grad, ures.perm, ures.inverse, ures.offsets, ures.num_unique,
+                      out=self.out, dev_err=err, ws=self.ws)
+
+    def reduced_rows(self, U):
+        """The U reduced rows of the last step, in type order (from the table
+        when the SCATTER was fused into Seg-Sum)."""
+        if self.fused:
+            return self.state["table"][self.ures.uniq[:U].long()]
+        return self.out[:U]
 
     def enable_overlap(self, nsets=4):
         """nsets sets of Unique outputs and a Unique workspace of their own,
@@ -231,8 +253,7 @@ class Pipeline:
         bt = self.batches[b % len(self.batches)]
         ures, u0 = self.sets[j]
         err = ures.dev_err
-        lz.segsum(bt.grad, ures.perm, ures.inverse, ures.offsets, ures.num_unique, out=self.out,
-                  dev_err=err, ws=self.ws)
+        self.reduce(bt, ures, err)
         if w.step in ("sgd", "softmax_sgd"):
             lz.sparse_apply(st["table"], ures.uniq, ures.num_unique, self.out, "sgd", lr=w.lr,
                             dev_err=err)
@@ -241,7 +262,7 @@ class Pipeline:
             lz.sparse_apply(st["table"], ures.uniq, ures.num_unique, self.out, "adam", lr=w.lr,
                             beta1=b1, beta2=b2, eps=eps, step=1 + b, m=st["m"], v=st["v"],
                             dev_err=err)
-        elif w.step == "scatter":
+        elif w.step == "scatter" and not self.fused:
             lz.fill_values(self.out, ures.uniq, ures.num_unique, st["table"], None, None,
                            "scatter", dev_err=err)
         elif w.step in ("expand", "expand_f16"):
@@ -287,8 +308,7 @@ class Pipeline:
             lz.sample_ids(bt.words, w.V, out=bt.ids[:w.shards * w.samples])
         lz.unique(bt.ids, w.V, out=ures, ws=self.ws)
         if ev: ev(1)
-        lz.segsum(bt.grad, ures.perm, ures.inverse, ures.offsets, ures.num_unique, out=self.out,
-                  dev_err=err, ws=self.ws)
+        self.reduce(bt, ures, err)
         if ev: ev(2)
         if w.step in ("sgd", "softmax_sgd"):
             lz.sparse_apply(st["table"], ures.uniq, ures.num_unique, self.out, "sgd", lr=w.lr,
@@ -298,7 +318,7 @@ class Pipeline:
             lz.sparse_apply(st["table"], ures.uniq, ures.num_unique, self.out, "adam", lr=w.lr,
                             beta1=b1, beta2=b2, eps=eps, step=1 + b, m=st["m"], v=st["v"],
                             dev_err=err)
-        elif w.step == "scatter":
+        elif w.step == "scatter" and not self.fused:
             lz.fill_values(self.out, ures.uniq, ures.num_unique, st["table"], None, None,
                            "scatter", dev_err=err)
         elif w.step in ("expand", "expand_f16"):
@@ -404,6 +424,29 @@ def run_gpu(w, steps, warmup, nbatch, torch, lz, host):
     st = np.array([[ev.ms(4 * i, 4 * i + 1), ev.ms(4 * i + 1, 4 * i + 2), ev.ms(4 * i + 2, 4 * i + 3)]
                    for i in range(steps)])
     ev.close()
+    unfused = None
+    if pipe.fused:
+        # For comparison, passes 1 and 2 again with the SCATTER as its own
+        # call after lm_segsum (the stage the fused call replaces).
+        pipe.fused = False
+        for i in range(warmup):
+            step(i)
+        ev = HipEvents(2 + 4 * steps)
+        torch.cuda.synchronize()
+        ev.record(0, stream)
+        for i in range(steps):
+            step(i)
+        ev.record(1, stream)
+        torch.cuda.synchronize()
+        for i in range(steps):
+            step(i, lambda k, i=i: ev.record(2 + 4 * i + k, stream))
+        torch.cuda.synchronize()
+        lz.check(dev_err)
+        ust = np.array([[ev.ms(2 + 4 * i + k, 2 + 4 * i + k + 1) for k in range(3)]
+                        for i in range(steps)])
+        unfused = dict(serial_ms=ev.ms(0, 1), stage_ms=ust.mean(axis=0).tolist())
+        ev.close()
+        pipe.fused = True
     # Pass 3, the headline: the same K steps with the Unique calls on a
     # second stream (default priority, like the first), running ahead.
     pipe.enable_overlap()
@@ -417,20 +460,27 @@ def run_gpu(w, steps, warmup, nbatch, torch, lz, host):
     outputs = dict(U=U0, uniq=ures.uniq[:U0].cpu().numpy().astype(np.int64),
                    counts=ures.counts[:U0].cpu().numpy(), offsets=ures.offsets[:U0 + 1].cpu().numpy(),
                    inverse=ures.inverse[:K].cpu().numpy(), perm=ures.perm[:K].cpu().numpy(),
-                   out=pipe.out[:U0].cpu().numpy())
+                   out=pipe.reduced_rows(U0).cpu().numpy())
+    fused = pipe.fused
     del pipe, batches
     torch.cuda.empty_cache()
     gb = 2 if w.grad_dtype == "bf16" else 4
     ib = 8 if w.id_dtype == "i64" else 4
     Us = [U_of[i % nbatch] for i in range(steps)]
-    seg_bytes = np.mean([segsum_bytes(K, D, U, gb) for U in Us])
+    # the fused call also reads the U row ids
+    seg_bytes = np.mean([segsum_bytes(K, D, U, gb) + (U * ib if fused else 0) for U in Us])
     seg_ms = float(st[:, 1].mean())
     uniq_bytes = float(np.mean([unique_bytes(K, U, ib) for U in Us]))
     rows = AFTER_ROWS.get(w.step)
     after_bytes = float(np.mean([rows * U * D * 4 for U in Us])) if rows else None
+    if unfused:
+        ub = float(np.mean([segsum_bytes(K, D, U, gb) for U in Us]))
+        unfused.update(seg_bytes=ub, seg_gbps=ub / (unfused["stage_ms"][1] / 1e3) / 1e9,
+                       ms_per_step=unfused["serial_ms"] / steps,
+                       value=K / (unfused["serial_ms"] / steps / 1e3))
     return dict(total_ms=total_ms, overlap_ms=overlap_ms, stage_ms=st.mean(axis=0).tolist(), seg_ms=seg_ms,
                 seg_bytes=float(seg_bytes), uniq_bytes=uniq_bytes, after_bytes=after_bytes,
-                U=U_of, outputs=outputs)
+                U=U_of, outputs=outputs, fused=fused, unfused=unfused)
 
 
 def host_threads() -> int:
@@ -576,10 +626,34 @@ def copy_calibration(torch, reps=3):
     torch.cuda.empty_cache()
 
 
-def segsum_kernels(w):
-    """The kernels of one lm_segsum call at this workload's shape (rows of up
-    to 4096 columns on the 16-byte path: one launch)."""
-    return SEGSUM_KERNELS if w.D <= 4096 else "lm_segsum (k_segsum walk, then k_segsum_fix)"
+def segsum_kernels(w, fused=False):
+    """The kernels of one lm_segsum (or, fused with SCATTER, lm_segsum_rows)
+    call at this workload's shape (rows of up to 4096 columns on the 16-byte
+    path: one launch)."""
+    name = "lm_segsum_rows" if fused else "lm_segsum"
+    k = (SEGSUM_KERNELS if w.D <= 4096 else "lm_segsum (k_segsum walk, then k_segsum_fix)")
+    k = k.replace("lm_segsum", name, 1)
+    return k + (", each type row written to its table row" if fused else "")
+
+
+def stages(w, r):
+    """Per-stage ms of the event pass, named for what each stage runs."""
+    ms = r["stage_ms"]
+    if r["fused"]:
+        return {"unique": ms[0], "segsum_rows (segsum + scatter)": ms[1]}
+    return {"unique": ms[0], "segsum": ms[1], w.step: ms[2]}
+
+
+def unfused_entry(w, r):
+    """The same workload with SCATTER as its own call after lm_segsum."""
+    u = r["unfused"]
+    if not u:
+        return None
+    return {"value": u["value"], "ms_per_step": u["ms_per_step"],
+            "stages_ms": {"unique": u["stage_ms"][0], "segsum": u["stage_ms"][1],
+                          "scatter": u["stage_ms"][2]},
+            "segsum_gbps": u["seg_gbps"], "segsum_frac": u["seg_gbps"] / HBM_PEAK_GBPS,
+            "schedule": "one stream; lm_segsum into a U x D buffer, then lm_fill_values SCATTER"}
 
 
 def measure(w, args, torch, lz, cpu_budget):
@@ -631,14 +705,14 @@ def workload_summary(res):
         "types_batch0": r["U"][0],
         "value": res["value"], "ms_per_step": res["ms"],
         "serial_value": w.tokens / (res["serial_ms"] / 1e3), "serial_ms_per_step": res["serial_ms"],
-        "stages_ms": {"unique": r["stage_ms"][0], "segsum": r["stage_ms"][1],
-                      w.step: r["stage_ms"][2]},
-        "segsum": {"kernels": segsum_kernels(w), "achieved_gbps": res["achieved"],
+        "stages_ms": stages(w, r),
+        "segsum": {"kernels": segsum_kernels(w, r["fused"]), "achieved_gbps": res["achieved"],
                    "frac": res["achieved"] / HBM_PEAK_GBPS, "bytes_per_launch": r["seg_bytes"],
                    "avg_launch_ms": r["seg_ms"], "traffic": res["traffic"]},
         "cpu_tokens_per_s": {str(k): v["value"] for k, v in legs.items()},
         "gpu_over_cpu_all_cores": (res["value"] / legs[max(legs)]["value"]) if legs else None,
         "oracle_check": res["check"],
+        "unfused_serial": unfused_entry(w, r),
     }
 
 
@@ -704,14 +778,15 @@ def main():
                    **({"gpus_simulated": w.shards, "samples_per_gpu": w.samples,
                        "seed_rule": w.seed_rule} if w.samples else {}),
                    "resident_batches": head["nbatch"], "types_per_batch": r["U"]},
-        "stages_ms": {"unique": r["stage_ms"][0], "segsum": r["stage_ms"][1],
-                      w.step: r["stage_ms"][2]},
+        "stages_ms": stages(w, r),
         # algorithmic bytes of each stage / its event-measured time (GB/s)
-        "stages_gbps": {"unique": r["uniq_bytes"] / (r["stage_ms"][0] / 1e3) / 1e9,
-                        "segsum": head["achieved"],
-                        w.step: (r["after_bytes"] / (r["stage_ms"][2] / 1e3) / 1e9
-                                 if r["after_bytes"] else None)},
-        "roofline": {"bound": "hbm", "kernel": segsum_kernels(w),
+        "stages_gbps": ({"unique": r["uniq_bytes"] / (r["stage_ms"][0] / 1e3) / 1e9,
+                         "segsum_rows (segsum + scatter)": head["achieved"]} if r["fused"] else
+                        {"unique": r["uniq_bytes"] / (r["stage_ms"][0] / 1e3) / 1e9,
+                         "segsum": head["achieved"],
+                         w.step: (r["after_bytes"] / (r["stage_ms"][2] / 1e3) / 1e9
+                                  if r["after_bytes"] else None)}),
+        "roofline": {"bound": "hbm", "kernel": segsum_kernels(w, r["fused"]),
                      "achieved": head["achieved"], "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                      "frac": head["achieved"] / HBM_PEAK_GBPS,
                      "bytes_per_launch": r["seg_bytes"], "avg_launch_ms": r["seg_ms"],
@@ -721,6 +796,7 @@ def main():
         "schedule": "unique on a second stream, up to 3 steps ahead (4 sets of its outputs)",
         "serial": {"value": w.tokens / (head["serial_ms"] / 1e3), "ms_per_step": head["serial_ms"],
                    "schedule": "one stream, the steps one after another"},
+        "unfused_serial": unfused_entry(w, r),
         "workloads": table,
     }
     print(json.dumps(line), flush=True)

@@ -3,8 +3,9 @@ reference rates of plain memory patterns on the same shapes (one GPU).
 
 Per entry point (default mode). For each workload, each stage of the step
 (Unique; Seg-Sum; the stage after it: the apply, SCATTER or the merge's
-EXPAND) is timed on its own, with HIP events on the launch stream around
-just that stage:
+EXPAND; where the step is a SCATTER into a dense table, also
+lm_segsum_rows, which does Seg-Sum and the SCATTER in one call) is timed on
+its own, with HIP events on the launch stream around just that stage:
 
   cold  before every timed rep, a 1 GiB buffer is read, which leaves nothing
         of the inputs in the 256 MB Infinity Cache or the L2s (read, not
@@ -16,7 +17,8 @@ just that stage:
 Each is 5 untimed reps, then --reps timed ones; the table gives the median,
 10th and 90th percentile in microseconds, Seg-Sum's algorithmic GB/s and its
 fraction of the 8 TB/s HBM peak (from the median), and tokens/s = K / the sum
-of the three cold medians.
+of the cold medians of the step's stages (Unique and lm_segsum_rows where
+the SCATTER is fused).
 
 Ceilings (--ceilings). Plain torch operations on a workload's shapes (its K
 gradient rows of D fp32, its U types), each rep on the next of several
@@ -100,9 +102,15 @@ def run_calls(workload, reps, torch, lz, synth):
     scratch = torch.empty(EVICT_BYTES // 4, dtype=torch.int32, device=dev).fill_(1)
     stream = torch.cuda.current_stream()
     res = {}
+    fused = pipe.fused
     for mode, cold in (("cold", True), ("warm", False)):
+        pipe.fused = False
         for s, name in enumerate(STAGES):
             res[(mode, name)] = time_stage(pipe, s, cold, reps, nbatch, torch, scratch, stream)
+        if fused:
+            pipe.fused = True
+            res[(mode, "rows")] = time_stage(pipe, 1, cold, reps, nbatch, torch, scratch, stream)
+    pipe.fused = fused
     lz.check(pipe.dev_err)
     del scratch
     seg_cold = np.mean([bench.segsum_bytes(w.tokens, w.D, u, gb) for u in U])
@@ -112,22 +120,29 @@ def run_calls(workload, reps, torch, lz, synth):
 
 def calls_table(w, U, res, seg_cold, seg_warm):
     pct = lambda a: (np.median(a), np.percentile(a, 10), np.percentile(a, 90))
+    fused = ("cold", "rows") in res
     lines = [f"### {w.name}: K = {w.tokens:,}, V = {w.V:,}, D = {w.D}, {w.grad_dtype} gradients, "
              f"{w.id_dtype} ids, after Seg-Sum: {w.step}; U per batch {min(U):,}..{max(U):,}",
              "", "| stage | cold median | cold p10 | cold p90 | warm median | warm p10 | warm p90 |",
              "|---|---|---|---|---|---|---|"]
-    for name in STAGES:
+    for name in STAGES + (("rows",) if fused else ()):
         c, h = pct(res[("cold", name)]), pct(res[("warm", name)])
-        label = w.step if name == "after" else name
+        label = {"after": w.step, "rows": "segsum_rows (segsum + scatter)"}.get(name, name)
         lines.append(f"| {label} | {c[0]:.1f} | {c[1]:.1f} | {c[2]:.1f} | {h[0]:.1f} | {h[1]:.1f} | "
                      f"{h[2]:.1f} |")
     sc, sw = np.median(res[("cold", "segsum")]), np.median(res[("warm", "segsum")])
     gbc, gbw = seg_cold / sc / 1e3, seg_warm / sw / 1e3
-    step = sum(np.median(res[("cold", n)]) for n in STAGES)
+    step = sum(np.median(res[("cold", n)]) for n in (("unique", "rows") if fused else STAGES))
     lines += ["", f"Seg-Sum: {seg_cold / 1e6:.1f} MB algorithmic per call; cold {gbc:,.0f} GB/s "
               f"(frac {gbc / bench.HBM_PEAK_GBPS:.3f}), warm {gbw:,.0f} GB/s "
               f"(frac {gbw / bench.HBM_PEAK_GBPS:.3f}). Cold step {step:.1f} us: "
               f"{w.tokens / step * 1e6 / 1e6:,.1f} M tokens/s.", ""]
+    if fused:
+        ib = 8 if w.id_dtype == "i64" else 4
+        rb = seg_cold + np.mean(U) * ib  # the row ids too
+        rc = rb / np.median(res[("cold", "rows")]) / 1e3
+        lines[-1:-1] = [f"segsum_rows: {rb / 1e6:.1f} MB algorithmic per call (Seg-Sum's and the "
+                        f"U row ids); cold {rc:,.0f} GB/s (frac {rc / bench.HBM_PEAK_GBPS:.3f})."]
     return "\n".join(lines)
 
 

@@ -152,7 +152,9 @@ int lm_unique_noalloc(const void* ids, int32_t idtype, int64_t K, int64_t V,
  * one row of E, so the reverse map is an accumulation):
  *     out[u, :] = sum over i in [offsets[u], offsets[u+1]) of grad[perm[i], :]
  * for u < U = *num_unique, accumulated in fp32 in a fixed order, so repeated
- * calls give bit-identical results.
+ * calls give bit-identical results. The order depends on K, D, u_cap (the
+ * walk's chunks are sized from min(K, u_cap)) and the launch form, not on
+ * the values.
  *
  * grad       device, K rows of D values of dtype `gtype` (LM_F32 / LM_BF16),
  *            row stride ld_grad elements.
@@ -184,11 +186,41 @@ int lm_segsum(const void* grad, int32_t gtype, int64_t K, int64_t D,
               float* out, int64_t ld_out, int32_t* dev_err, void* ws,
               size_t ws_bytes, void* stream);
 
-/* The one-launch form of lm_segsum relies on the hardware starting the
- * walk's workgroups before the fix-up workgroups that wait on them (they come
- * first in the grid). lm_segsum_set_two_launches(1) makes every later call
- * in the process use the two-launch form instead (the walk, then a separate
- * fix-up kernel: no workgroup ever waits on another), the fallback should a
+/* ------------------------------------------------------------------------
+ * Seg-Sum into chosen rows — Sec. III-A steps 2 and 5 in one pass on one
+ * GPU: the same sums as lm_segsum, but type u's row goes to row row_ids[u]
+ * of `out` instead of row u:
+ *     out[row_ids[u], :] = sum over i in [offsets[u], offsets[u+1]) of
+ *                          grad[perm[i], :]          for u < *num_unique,
+ * with the same fixed summation order (so bit-identical to lm_segsum with
+ * u_cap = rows_cap, in the same launch form, followed by a row copy). With
+ * row_ids = uniq from lm_unique and `out` a
+ * dense V x D table, this is Seg-Sum followed by Fill-Values SCATTER
+ * (lm_fill_values, LM_FILL_SCATTER, dst_ids NULL) without writing and
+ * re-reading the U x D intermediate; rows of `out` that no type names are
+ * left untouched.
+ *
+ * row_ids    device, rows_cap ids of dtype `idtype`, the first *num_unique
+ *            used; they must be distinct (lm_unique's uniq are). An id
+ *            outside [0, out_rows) sets LM_DEVERR_ID_RANGE and that type is
+ *            not written. *num_unique > rows_cap sets LM_DEVERR_CAPACITY and
+ *            only the first rows_cap types are written.
+ * out        device, out_rows x D fp32 (out_rows < 2^31), row stride ld_out.
+ * The other arguments, the workspace (lm_segsum_workspace_bytes(K, D)) and
+ * the launch forms are those of lm_segsum.
+ * ------------------------------------------------------------------------ */
+int lm_segsum_rows(const void* grad, int32_t gtype, int64_t K, int64_t D, int64_t ld_grad,
+                   const int32_t* perm, const int32_t* inverse, const int32_t* offsets,
+                   const int64_t* num_unique, const void* row_ids, int32_t idtype,
+                   int64_t rows_cap, float* out, int64_t out_rows, int64_t ld_out,
+                   int32_t* dev_err, void* ws, size_t ws_bytes, void* stream);
+
+/* The one-launch form of lm_segsum (and lm_segsum_rows) relies on the
+ * hardware starting the walk's workgroups before the fix-up workgroups that
+ * wait on them (they come first in the grid). lm_segsum_set_two_launches(1)
+ * makes every later call in the process use the two-launch form instead
+ * (the walk, then a separate fix-up kernel: no workgroup ever waits on
+ * another), the fallback should a
  * device break that order; 0 restores the default. The environment variable
  * LMZIPF_SEGSUM_TWO_LAUNCHES=1, read at the first lm_segsum call, sets it
  * too. Results agree with the one-launch form within the Seg-Sum tolerance

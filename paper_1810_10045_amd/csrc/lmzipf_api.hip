@@ -13,7 +13,8 @@ size_t segsum_workspace_bytes(int64_t K, int64_t D);
 int segsum_run(const void* grad, int gtype, int64_t K, int64_t D, int64_t ld_grad,
                const int32_t* perm, const int32_t* inverse, const int32_t* offsets,
                const int64_t* num_unique, int64_t u_cap, float* out, int64_t ld_out,
-               int32_t* dev_err, void* ws, size_t ws_bytes, hipStream_t st);
+               int32_t* dev_err, void* ws, size_t ws_bytes, hipStream_t st,
+               const void* row_ids = nullptr, int row_ids64 = 0, int64_t out_rows = 0);
 int map_run(const void* sub, const int64_t* n_sub, int64_t sub_cap, const void* sup,
             const int64_t* n_sup, int64_t sup_cap, int idtype, int32_t* map, int32_t* dev_err,
             hipStream_t st);
@@ -133,6 +134,27 @@ int lm_segsum(const void* grad, int32_t gtype, int64_t K, int64_t D, int64_t ld_
   if (ws_bytes < segsum_workspace_bytes(K, D)) return LM_E_WORKSPACE;
   return segsum_run(grad, gtype, K, D, ld_grad, perm, inverse, offsets, num_unique, u_cap, out,
                     ld_out, dev_err, ws, ws_bytes, static_cast<hipStream_t>(stream));
+}
+
+int lm_segsum_rows(const void* grad, int32_t gtype, int64_t K, int64_t D, int64_t ld_grad,
+                   const int32_t* perm, const int32_t* inverse, const int32_t* offsets,
+                   const int64_t* num_unique, const void* row_ids, int32_t idtype,
+                   int64_t rows_cap, float* out, int64_t out_rows, int64_t ld_out,
+                   int32_t* dev_err, void* ws, size_t ws_bytes, void* stream) {
+  if (gtype != LM_F32 && gtype != LM_BF16) return LM_E_UNSUPPORTED;
+  if (!valid_idtype(idtype)) return LM_E_UNSUPPORTED;
+  if (K < 0 || D < 0 || rows_cap < 0 || out_rows < 0 || ld_grad < D || ld_out < D)
+    return LM_E_INVAL;
+  if (K >= LM_MAX_K || D > (int64_t(1) << 24) || out_rows > INT32_MAX) return LM_E_UNSUPPORTED;
+  if (K > 0 && D > 0 && rows_cap > 0 &&
+      (!grad || !perm || !inverse || !offsets || !num_unique || !row_ids || !out || !dev_err ||
+       !ws))
+    return LM_E_INVAL;
+  if (ws && (reinterpret_cast<uintptr_t>(ws) & 255)) return LM_E_INVAL;
+  if (ws_bytes < segsum_workspace_bytes(K, D)) return LM_E_WORKSPACE;
+  return segsum_run(grad, gtype, K, D, ld_grad, perm, inverse, offsets, num_unique, rows_cap,
+                    out, ld_out, dev_err, ws, ws_bytes, static_cast<hipStream_t>(stream),
+                    row_ids, idtype == LM_I64 ? 1 : 0, out_rows);
 }
 
 int lm_map_ids(const void* sub_ids, const int64_t* n_sub, int64_t sub_cap, const void* sup_ids,

@@ -121,6 +121,9 @@ struct SegArgs {
   int tiles, tile_cols;    // column tiles of the walk and the columns of one
   int R, nchunks, rw, ww;  // cost of a position / of a segment end
   int max_chunks;          // chunks the workspace holds
+  const void* row_ids;     // lm_segsum_rows: type u goes to out row row_ids[u]
+  int row_ids64;           //   (int64 ids when nonzero), < out_rows; nullptr: row u
+  int64_t out_rows;
   int32_t* dev_err;
 };
 
@@ -254,6 +257,20 @@ constexpr int kFusedSpan = LMZ_SEG_FUSED_SPAN;
 constexpr int kFusedCols = kWave * 4;  // columns of a fused fix-up tile
 static_assert(kFusedSpan <= kWave, "one descriptor per lane");
 
+// The output row of type s: s itself, or row_ids[s] for lm_segsum_rows
+// (-1 when that id lies outside [0, out_rows); LM_DEVERR_ID_RANGE is raised
+// and the row is not written).
+__device__ __forceinline__ int64_t out_row_of(const SegArgs& a, int s) {
+  if (!a.row_ids) return s;
+  const int64_t r = a.row_ids64 ? static_cast<const int64_t*>(a.row_ids)[s]
+                                : static_cast<const int32_t*>(a.row_ids)[s];
+  if (r < 0 || r >= a.out_rows) {
+    raise_err(a.dev_err, LM_DEVERR_ID_RANGE);
+    return -1;
+  }
+  return r;
+}
+
 template <int VEC>
 __device__ __forceinline__ void store_vec_agent(float* p, const float* v) {
   static_assert(VEC % 2 == 0, "pairs of fp32 values");
@@ -348,7 +365,8 @@ __device__ __forceinline__ void fused_fix(const SegArgs& a) {
 #pragma unroll
           for (int e = 0; e < 4; ++e) acc[e] += buf[r][e];
     }
-    if (col < D) store_vec<4>(a.out + static_cast<int64_t>(s) * a.ld_out + col, acc);
+    const int64_t orow = out_row_of(a, s);
+    if (col < D && orow >= 0) store_vec<4>(a.out + orow * a.ld_out + col, acc);
   }
 
   // Heads, one after the other, all waves: wave w adds pieces w, w + W, ...
@@ -374,13 +392,14 @@ __device__ __forceinline__ void fused_fix(const SegArgs& a) {
 #pragma unroll
     for (int e = 0; e < 4; ++e) s_part[wave][lane * 4 + e] = acc[e];
     __syncthreads();
+    const int64_t orow = out_row_of(a, s);
     for (int x = threadIdx.x; x < kFusedCols; x += kFusedThreads) {
       const int cx = (f % a.fix_tiles) * kFusedCols + x;
-      if (cx < D) {
+      if (cx < D && orow >= 0) {
         float sum = 0.f;
 #pragma unroll
         for (int w = 0; w < kFusedWaves; ++w) sum += s_part[w][x];
-        a.out[static_cast<int64_t>(s) * a.ld_out + cx] = sum;
+        a.out[orow * a.ld_out + cx] = sum;
       }
     }
     __syncthreads();
@@ -524,6 +543,20 @@ __global__ __launch_bounds__(NTHR) void k_segsum(SegArgs a) {
     if (lane == kWave - 1) nxt = w + 1 < NW ? read_lane(sw[w + 1 < NW ? w + 1 : w], 0) : -3;
     ends[w] = ballot(sw[w] != nxt);
   }
+  // lm_segsum_rows: the output row of every position's type, gathered with
+  // the windows (the first segment end needs it, not the first row loads);
+  // -1 marks an id outside [0, out_rows) (and clamped positions).
+  int orw[NW];
+  const bool rows = a.row_ids != nullptr;
+  if (rows) {
+#pragma unroll
+    for (int w = 0; w < NW; ++w) {
+      const int sv = sw[w] >= 0 && sw[w] < a.u_cap ? sw[w] : 0;
+      const int64_t r = a.row_ids64 ? static_cast<const int64_t*>(a.row_ids)[sv]
+                                    : static_cast<const int32_t*>(a.row_ids)[sv];
+      orw[w] = r >= 0 && r < a.out_rows ? static_cast<int>(r) : -1;
+    }
+  }
 
   // 3. Walk rows q .. q_end - 1, window by window. Lanes past the last column
   //    load a valid vector of the same row (col_ld) and never store it, so
@@ -538,6 +571,7 @@ __global__ __launch_bounds__(NTHR) void k_segsum(SegArgs a) {
     col_ld[v] = col < D ? col : D - VEC;
   }
   const GT* __restrict__ grad = static_cast<const GT*>(a.grad);
+  bool bad_row = false;
 
   float acc[NV][VEC];
 #pragma unroll
@@ -581,7 +615,9 @@ __global__ __launch_bounds__(NTHR) void k_segsum(SegArgs a) {
             else if (!is_end) dst = a.part_start + static_cast<int64_t>(c) * D;
             else {
               part = false;
-              dst = (s >= 0 && s < a.u_cap) ? a.out + static_cast<int64_t>(s) * a.ld_out : nullptr;
+              const int64_t orow = rows ? read_lane(orw[w], j) : s;
+              bad_row |= rows && orow < 0 && s >= 0 && s < a.u_cap;
+              dst = (s >= 0 && s < a.u_cap && orow >= 0) ? a.out + orow * a.ld_out : nullptr;
             }
             if (dst) {
 #pragma unroll
@@ -610,6 +646,7 @@ __global__ __launch_bounds__(NTHR) void k_segsum(SegArgs a) {
   if (started_before) bad |= seg_before != s_f || seg_p0 != s_f;
   else bad |= seg_before == seg_p0 || seg_p0 != (p0 == A.o1 ? A.u + 1 : A.u);
   if (ballot(bad) && lane == 0) raise_err(a.dev_err, LM_DEVERR_CAPACITY);
+  if (ballot(bad_row) && lane == 0) raise_err(a.dev_err, LM_DEVERR_ID_RANGE);
   publish();
 }
 
@@ -697,7 +734,8 @@ __global__ __launch_bounds__(kFixThreads) void k_segsum_fix(SegArgs a) {
       if (r <= sP)
 #pragma unroll
         for (int e = 0; e < VEC; ++e) acc[e] += sbuf[r][e];
-    if (col < D) store_vec<VEC>(a.out + static_cast<int64_t>(ss) * a.ld_out + col, acc);
+    const int64_t orow = out_row_of(a, ss);
+    if (col < D && orow >= 0) store_vec<VEC>(a.out + orow * a.ld_out + col, acc);
   }
   if (ih < 0) return;  // the same in every wave: no barrier below is skipped by only some
   float acc[VEC];
@@ -725,13 +763,14 @@ __global__ __launch_bounds__(kFixThreads) void k_segsum_fix(SegArgs a) {
   for (int e = 0; e < VEC; ++e) s_part[wave][lane * VEC + e] = acc[e];
   __syncthreads();
   // Thread x adds column x of the tile over the waves in order.
+  const int64_t orow = out_row_of(a, hs);
   for (int x = threadIdx.x; x < kCols; x += kFixThreads) {
     const int cx = blockIdx.y * kCols + x;
-    if (cx < D) {
+    if (cx < D && orow >= 0) {
       float sum = 0.f;
 #pragma unroll
       for (int w = 0; w < kFixWaves; ++w) sum += s_part[w][x];
-      a.out[static_cast<int64_t>(hs) * a.ld_out + cx] = sum;
+      a.out[orow * a.ld_out + cx] = sum;
     }
   }
 }
@@ -899,7 +938,8 @@ int segsum_set_two_launches(bool enable) {
 int segsum_run(const void* grad, int gtype, int64_t K, int64_t D, int64_t ld_grad,
                const int32_t* perm, const int32_t* inverse, const int32_t* offsets,
                const int64_t* num_unique, int64_t u_cap, float* out, int64_t ld_out,
-               int32_t* dev_err, void* ws, size_t ws_bytes, hipStream_t st) {
+               int32_t* dev_err, void* ws, size_t ws_bytes, hipStream_t st,
+               const void* row_ids, int row_ids64, int64_t out_rows) {
   const SegLayout L = seg_layout(K, D);
   if (ws_bytes < L.total) return LM_E_WORKSPACE;
   if (K == 0 || D == 0 || u_cap == 0) return LM_OK;
@@ -917,6 +957,9 @@ int segsum_run(const void* grad, int gtype, int64_t K, int64_t D, int64_t ld_gra
   a.u_cap = u_cap;
   a.out = out;
   a.ld_out = ld_out;
+  a.row_ids = row_ids;
+  a.row_ids64 = row_ids64;
+  a.out_rows = row_ids ? out_rows : u_cap;
   a.part_cont = reinterpret_cast<float*>(w + L.cont);
   a.part_start = reinterpret_cast<float*>(w + L.start);
   a.desc = reinterpret_cast<int32_t*>(w + L.desc);

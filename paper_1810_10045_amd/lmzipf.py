@@ -64,6 +64,8 @@ def _load():
     L.lm_segsum_workspace_bytes.argtypes = [I64_, I64_]
     L.lm_segsum_workspace_bytes.restype = SZ
     L.lm_segsum.argtypes = [P, I32_, I64_, I64_, I64_, P, P, P, P, I64_, P, I64_, P, P, SZ, P]
+    L.lm_segsum_rows.argtypes = [P, I32_, I64_, I64_, I64_, P, P, P, P, P, I32_, I64_, P, I64_, I64_,
+                                 P, P, SZ, P]
     L.lm_map_ids.argtypes = [P, P, I64_, P, P, I64_, I32_, P, P, P]
     L.lm_fill_values.argtypes = [P, I64_, P, P, I64_, P, P, I32_, I64_, P, I64_, I64_, I32_, P, P]
     L.lm_sparse_apply.argtypes = [P, I64_, I64_, I64_, P, I32_, P, I64_, P, I64_, I32_,
@@ -76,7 +78,7 @@ def _load():
     L.lm_segsum_set_two_launches.argtypes = [I32_]
     L.lm_test_force_wait_failure.argtypes = [I32_, ctypes.c_uint32]
     for f in ("lm_abi_version", "lm_workspace_clear", "lm_unique", "lm_unique_noalloc",
-              "lm_segsum", "lm_map_ids",
+              "lm_segsum", "lm_segsum_rows", "lm_map_ids",
               "lm_fill_values", "lm_sparse_apply", "lm_fill_values_f16", "lm_sparse_apply_f16",
               "lm_sample_ids", "lm_segsum_set_two_launches", "lm_test_force_wait_failure"):
         getattr(L, f).restype = ctypes.c_int
@@ -281,6 +283,35 @@ def segsum(grad: torch.Tensor, perm: torch.Tensor, inverse: torch.Tensor, offset
     _call(_lib.lm_segsum(_ptr(grad), _gtype(grad), K, D, ld, _ptr(perm), _ptr(inverse), _ptr(offsets),
                          _ptr(num_unique), u_cap, _ptr(out), ld_out, _ptr(dev_err), _ptr(buf),
                          buf.numel(), _stream(stream)), "lm_segsum")
+    return out
+
+
+def segsum_rows(grad: torch.Tensor, perm: torch.Tensor, inverse: torch.Tensor,
+                offsets: torch.Tensor, num_unique: torch.Tensor, row_ids: torch.Tensor,
+                out: torch.Tensor, dev_err: Optional[torch.Tensor] = None,
+                ws: Optional[Workspace] = None, stream=None) -> torch.Tensor:
+    """lm_segsum_rows: Sec. III-A steps 2 and 5 in one pass: type u's sum goes
+    to row row_ids[u] of `out` (e.g. the uniq ids into a dense V x D table);
+    other rows of `out` are untouched. Returns `out`."""
+    _dev(grad, "grad")
+    _dev(row_ids, "row_ids")
+    K, D = grad.shape
+    ld = _rows(grad, "grad")
+    if perm.numel() < K or inverse.numel() < K or offsets.numel() < 1:
+        raise LmError("perm and inverse must hold K entries")
+    if out.dim() != 2 or out.shape[1] != D or out.dtype != torch.float32:
+        raise LmError("out must be an fp32 matrix with D columns")
+    if not row_ids.is_contiguous():
+        raise LmError("row_ids must be contiguous")
+    ld_out = _rows(out, "out")
+    if dev_err is None:
+        dev_err = torch.zeros(1, dtype=torch.int32, device=grad.device)
+    ws = ws or default_workspace(grad.device)
+    buf = ws.get(_lib.lm_segsum_workspace_bytes(K, D))
+    _call(_lib.lm_segsum_rows(_ptr(grad), _gtype(grad), K, D, ld, _ptr(perm), _ptr(inverse),
+                              _ptr(offsets), _ptr(num_unique), _ptr(row_ids), _idtype(row_ids),
+                              row_ids.numel(), _ptr(out), out.shape[0], ld_out, _ptr(dev_err),
+                              _ptr(buf), buf.numel(), _stream(stream)), "lm_segsum_rows")
     return out
 
 

@@ -9,8 +9,8 @@ very launches that bench.py times (its Batch and Pipeline, batch 0).
 * Map J^ -> I^ at the merge's real shape (shard 0's types into the merged
   list), bit-exact.
 * What follows Seg-Sum, end to end from the oracle's own sums: SCATTER into a
-  dense table (against the dense per-token scatter-add for the 100K x 512
-  case), SGD, the first lazy-Adam step (moments too, every touched row),
+  dense table, done by Seg-Sum's own writes (lm_segsum_rows; against the
+  dense per-token scatter-add for the 100K x 512 case), SGD, the first lazy-Adam step (moments too, every touched row),
   EXPAND of shard 0 into the merged type list; rows the step must not touch
   are compared exactly.
 """
@@ -68,8 +68,10 @@ def _release(pipe):
 
 
 def test_full_word_tiny_8k(lz):
-    """8,192 tokens over 100K words, D = 512: Seg-Sum on every row and the
-    dense V x 512 table filled by SCATTER against the per-token scatter-add."""
+    """8,192 tokens over 100K words, D = 512: Seg-Sum with the SCATTER into
+    the dense V x 512 table in the same call (lm_segsum_rows), every written
+    row against the oracle's Seg-Sum and the whole table against the
+    per-token scatter-add."""
     w = synth.WORKLOADS["word_tiny_8k"]
     ids, g = w.ids(), w.grads()
     pipe = _run(lz, w, ids, g)
@@ -77,7 +79,7 @@ def test_full_word_tiny_8k(lz):
     U = len(o[0])
     S = oracle.segsum(g, o[3], U)
     sq = H.sum_of_squares(g, o[3], U, oracle)
-    got = pipe.out[:U].cpu().numpy()
+    got = pipe.reduced_rows(U).cpu().numpy()
     H.check_rows(got, S, sq)
     H.assert_single_rows_exact(got, S, o[1])
     dense = oracle.dense_scatter(g, ids, w.V)
@@ -101,7 +103,7 @@ def test_full_word_step_64k(lz, name):
     U = len(o[0])
     S = oracle.segsum(g, o[3], U)
     sq = H.sum_of_squares(g, o[3], U, oracle)
-    got = pipe.out[:U].cpu().numpy()
+    got = pipe.reduced_rows(U).cpu().numpy()
     H.check_rows(got, S, sq)
     H.assert_single_rows_exact(got, S, o[1])
     lr = _f32(w.lr)
@@ -132,7 +134,7 @@ def test_full_merge_64x32k_bf16(lz, name):
     o = H.assert_unique_matches(pipe.ures, ids, w.V, oracle, w.name)
     UG = len(o[0])
     S = oracle.segsum_threads(g, o[3], UG, THREADS)
-    got = pipe.out[:UG].cpu().numpy()
+    got = pipe.reduced_rows(UG).cpu().numpy()
     H.check_rows(got, S, None, w.grad_dtype, "merged rows")
     H.assert_single_rows_exact(got, S, o[1], "merged rows")
     del S, got
@@ -177,8 +179,8 @@ def test_full_merge_64x32k_bf16(lz, name):
 
 def test_full_char_heavy_1m(lz):
     """1,048,576 tokens over 20K characters (Zipf 1.2, the top type holds
-    about a fifth of the tokens), D = 2048: every Seg-Sum row, then SCATTER
-    into the dense 20K x 2048 table. No floor on the row scale here: with
+    about a fifth of the tokens), D = 2048: every Seg-Sum row, written into
+    the dense 20K x 2048 table by the same call (lm_segsum_rows). No floor on the row scale here: with
     2048 columns the largest |sum| always exceeds the rms of the summands."""
     w = synth.WORKLOADS["char_heavy_1m"]
     ids, g = w.ids(), w.grads()
@@ -186,7 +188,7 @@ def test_full_char_heavy_1m(lz):
     o = H.assert_unique_matches(pipe.ures, ids, w.V, oracle, w.name)
     U = len(o[0])
     S = oracle.segsum_threads(g, o[3], U, THREADS)
-    got = pipe.out[:U].cpu().numpy()
+    got = pipe.reduced_rows(U).cpu().numpy()
     H.check_rows(got, S)
     H.assert_single_rows_exact(got, S, o[1])
     T = pipe.state["table"].cpu().numpy()
@@ -208,7 +210,7 @@ def test_full_vocab2m_adam_i64(lz):
     o = H.assert_unique_matches(pipe.ures, ids, w.V, oracle, w.name)
     U = len(o[0])
     S = oracle.segsum_threads(g, o[3], U, THREADS)
-    got = pipe.out[:U].cpu().numpy()
+    got = pipe.reduced_rows(U).cpu().numpy()
     H.check_rows(got, S)
     H.assert_single_rows_exact(got, S, o[1])
     del got
@@ -274,7 +276,7 @@ def test_full_sampled_softmax(lz, rule):
     U = len(o[0])
     S = oracle.segsum(g, o[3], U)
     sq = H.sum_of_squares(g, o[3], U, oracle)
-    got = pipe.out[:U].cpu().numpy()
+    got = pipe.reduced_rows(U).cpu().numpy()
     H.check_rows(got, S, sq)
     H.assert_single_rows_exact(got, S, o[1])
     lr = _f32(w.lr)

@@ -535,6 +535,143 @@ def test_segsum_strided_and_capacity(lz):
     assert int(err2.item()) == lz.DEVERR_CAPACITY
 
 
+ROWS_CASES = [
+    # (K, V, s, D, grad dtype, id dtype, seed): one-workgroup Unique and a
+    # 512-column walk; rows of two 1024-column tiles in one launch (f32 and
+    # bf16, int64 row ids); narrow rows; rows wider than the one-launch form
+    # takes (walk, then the separate fix-up); a single token.
+    (8192, 100_000, 1.0, 512, "f32", np.int32, 131),
+    (60_000, 20_000, 1.2, 2048, "f32", np.int32, 132),
+    (40_000, 300, 1.2, 2048, "bf16", np.int64, 133),
+    (20_000, 300, 1.2, 96, "f32", np.int64, 134),
+    (4000, 100, 1.0, 5000, "f32", np.int32, 135),
+    (1, 5, 1.0, 16, "f32", np.int32, 136),
+]
+
+
+def _rows_case(lz, K, V, s, D, gdt, dt, seed):
+    ids = synth.zipf_ids(K, V, s, seed, dt)
+    g32 = synth.normal_rows(K, D, seed + 1000)
+    grad = synth.bf16_bits(g32) if gdt == "bf16" else g32
+    tgrad = _t(g32).to(torch.bfloat16) if gdt == "bf16" else _t(g32)
+    res = lz.unique(_t(ids), V)
+    return ids, grad, tgrad, res
+
+
+@pytest.mark.parametrize("K,V,s,D,gdt,dt,seed", ROWS_CASES,
+                         ids=[f"K{c[0]}-V{c[1]}-D{c[3]}-{c[4]}-{np.dtype(c[5]).name}"
+                              for c in ROWS_CASES])
+def test_segsum_rows_is_segsum_then_scatter(lz, K, V, s, D, gdt, dt, seed):
+    """lm_segsum_rows into a dense V x D table with row_ids = uniq: the same
+    table, bit for bit, as lm_segsum followed by Fill-Values SCATTER (each
+    launch form against lm_segsum in that form: the forms group the heads'
+    partial rows differently); the written rows match the oracle's steps 2
+    and 5; every other row keeps its value."""
+    _say(f"segsum_rows K={K} V={V} D={D} {gdt} {np.dtype(dt).name}")
+    ids, grad, tgrad, res = _rows_case(lz, K, V, s, D, gdt, dt, seed)
+    base = _t(synth.normal_rows(V, D, seed + 2000))
+    out = lz.segsum(tgrad, res.perm, res.inverse, res.offsets, res.num_unique, dev_err=res.dev_err)
+    want = base.clone()
+    lz.fill_values(out, res.uniq, res.num_unique, want, None, None, "scatter", dev_err=res.dev_err)
+    got = base.clone()
+    lz.segsum_rows(tgrad, res.perm, res.inverse, res.offsets, res.num_unique, res.uniq, got,
+                   dev_err=res.dev_err)
+    assert lz.segsum_two_launches(True) is False
+    try:
+        out2 = lz.segsum(tgrad, res.perm, res.inverse, res.offsets, res.num_unique,
+                         dev_err=res.dev_err)
+        want2 = base.clone()
+        lz.fill_values(out2, res.uniq, res.num_unique, want2, None, None, "scatter",
+                       dev_err=res.dev_err)
+        got2 = base.clone()
+        lz.segsum_rows(tgrad, res.perm, res.inverse, res.offsets, res.num_unique, res.uniq, got2,
+                       dev_err=res.dev_err)
+        torch.cuda.synchronize()
+    finally:
+        assert lz.segsum_two_launches(False) is True
+    lz.check(res.dev_err)
+    o = H.assert_unique_matches(res, ids, V, oracle)
+    U = len(o[0])
+    assert torch.equal(got, want), "not the table of lm_segsum + SCATTER"
+    assert torch.equal(got2, want2), "two-launch form: not lm_segsum + SCATTER"
+    touched = torch.zeros(V, dtype=torch.bool, device=DEV)
+    touched[_t(o[0].astype(np.int64))] = True
+    assert torch.equal(got[~touched], base[~touched]), "a row no type names was written"
+    ref = oracle.segsum(grad, o[3], U)
+    rows = got[_t(o[0].astype(np.int64))].double().cpu().numpy()
+    H.check_rows(rows, ref, H.sum_of_squares(grad, o[3], U, oracle), gdt)
+    if V * D <= 1 << 20:  # the oracle's dense table, whole
+        dense = oracle.scatter(ref, o[0], base.double().cpu().numpy())
+        assert H.row_rel_err(got.double().cpu().numpy(), dense) <= (
+            H.TOL_BF16 if gdt == "bf16" else H.TOL_F32)
+
+
+@pytest.mark.parametrize("D,dt", [(512, np.int32), (2048, np.int64), (5000, np.int32)])
+def test_segsum_rows_any_row_map(lz, D, dt):
+    """row_ids need not be the uniq ids: type u to row U-1-u of a U-row
+    output is lm_segsum's output (u_cap = U, the same chunks) upside down,
+    bit for bit."""
+    K, V = 20_000, 3000
+    _say(f"segsum_rows reversed D={D}")
+    ids, grad, tgrad, res = _rows_case(lz, K, V, 1.0, D, "f32", dt, 141)
+    U = int(res.num_unique.item())
+    out = lz.segsum(tgrad, res.perm, res.inverse, res.offsets, res.num_unique, u_cap=U,
+                    dev_err=res.dev_err)
+    rev = torch.arange(U - 1, -1, -1, device=DEV).to(torch.int64 if dt == np.int64 else torch.int32)
+    got = torch.full((U, D), float("nan"), device=DEV)
+    lz.segsum_rows(tgrad, res.perm, res.inverse, res.offsets, res.num_unique, rev, got,
+                   dev_err=res.dev_err)
+    torch.cuda.synchronize()
+    lz.check(res.dev_err)
+    assert torch.equal(got, out[:U].flip(0))
+
+
+@pytest.mark.parametrize("D", [512, 2048, 5000])
+def test_segsum_rows_bad_row_id(lz, D):
+    """A row id outside [0, out_rows) sets LM_DEVERR_ID_RANGE and leaves that
+    type unwritten; the other types are written as usual. The longest type
+    (summed by the fix-up) and a short one (ended inside the walk), and a
+    negative id; then rows_cap below the number of types: the capacity
+    error."""
+    K, V = 30_000, 2000
+    _say(f"segsum_rows bad ids D={D}")
+    ids, grad, tgrad, res = _rows_case(lz, K, V, 1.2, D, "f32", np.int64, 151)
+    U = int(res.num_unique.item())
+    counts = res.counts[:U].cpu().numpy()
+    head, short = int(np.argmax(counts)), int(np.argmin(counts))
+    # lm_segsum with u_cap = rows_cap: the same chunks, so the same sums
+    out = lz.segsum(tgrad, res.perm, res.inverse, res.offsets, res.num_unique, u_cap=U,
+                    dev_err=res.dev_err)
+    e10 = torch.zeros(1, dtype=torch.int32, device=DEV)
+    out10 = lz.segsum(tgrad, res.perm, res.inverse, res.offsets, res.num_unique, u_cap=10,
+                      out=torch.empty((10, D), device=DEV), dev_err=e10)
+    base = _t(synth.normal_rows(V, D, 152))
+    uniq = res.uniq[:U].clone()
+    for bad_u, bad_id in ((head, V), (short, V + 99), (short, -1)):
+        rid = uniq.clone()
+        rid[bad_u] = bad_id
+        err = torch.zeros(1, dtype=torch.int32, device=DEV)
+        got = base.clone()
+        lz.segsum_rows(tgrad, res.perm, res.inverse, res.offsets, res.num_unique, rid, got,
+                       dev_err=err)
+        torch.cuda.synchronize()
+        assert int(err.item()) == lz.DEVERR_ID_RANGE, (bad_u, bad_id)
+        keep = torch.ones(U, dtype=torch.bool, device=DEV)
+        keep[bad_u] = False
+        assert torch.equal(got[uniq[keep]], out[:U][keep])
+        assert torch.equal(got[uniq[bad_u]], base[uniq[bad_u]]), "the bad type was written"
+    err = torch.zeros(1, dtype=torch.int32, device=DEV)
+    got = base.clone()
+    lz.segsum_rows(tgrad, res.perm, res.inverse, res.offsets, res.num_unique, uniq[:10].clone(),
+                   got, dev_err=err)
+    torch.cuda.synchronize()
+    assert int(err.item()) == lz.DEVERR_CAPACITY == int(e10.item())
+    assert torch.equal(got[uniq[:10]], out10)
+    rest = torch.ones(V, dtype=torch.bool, device=DEV)
+    rest[uniq[:10]] = False
+    assert torch.equal(got[rest], base[rest]), "a type past rows_cap was written"
+
+
 # ---------------------------------------------------------------------------
 # Map, Fill-Values, the G-shard merge
 # ---------------------------------------------------------------------------
