@@ -251,6 +251,35 @@ __device__ __forceinline__ uint32_t digit_of(KeyT k, int shift, uint32_t mask) {
   return static_cast<uint32_t>(key_bits(k) >> shift) & mask;
 }
 
+// gfx950's three-input bitwise op: bit (a << 2 | b << 1 | c) of the
+// immediate is the result for input bits a, b, c. This one is a & ~(b ^ c).
+constexpr int kBitop3AndXnor = (1 << 4) | (1 << 7);
+
+// The lanes of this wave whose digit equals this lane's, among the lanes of
+// `valid`: one ballot per digit bit, and a lane keeps the lanes whose bit
+// agrees with its own, peers &= ~(bits ^ mine) with its bit spread over the
+// word (0 or ~0). Digits have no bits at or above RB on valid lanes, so bits
+// past a pass's width (zero in every lane) leave the mask unchanged and the
+// loop needs no bound of its own. Four instructions per bit: the bit field
+// extract, the compare that is the ballot, and one three-input op per half
+// (the loop with a runtime bound and a select per half took about twice as
+// many, with a branch per bit).
+template <int RB>
+__device__ __forceinline__ uint64_t match_digit(uint32_t dig, uint64_t valid) {
+  uint32_t lo = static_cast<uint32_t>(valid), hi = static_cast<uint32_t>(valid >> 32);
+#pragma unroll
+  for (int b = 0; b < RB; ++b) {
+    uint32_t mine = static_cast<uint32_t>(__builtin_amdgcn_sbfe(static_cast<int>(dig), b, 1));
+    // Opaque to the optimiser, so that the ballot compares this value
+    // instead of deriving the bit again with a shift and a compare.
+    __asm__("" : "+v"(mine));
+    const uint64_t bits = ballot(mine != 0u);
+    lo = __builtin_amdgcn_bitop3_b32(lo, static_cast<uint32_t>(bits), mine, kBitop3AndXnor);
+    hi = __builtin_amdgcn_bitop3_b32(hi, static_cast<uint32_t>(bits >> 32), mine, kBitop3AndXnor);
+  }
+  return (uint64_t(hi) << 32) | lo;
+}
+
 // ---------------------------------------------------------------------------
 // k_hist: bhist[b][p][d] = number of keys read by workgroup b whose digit of
 // pass p is d (rows of rstride slots per pass). Also clears the tickets and the
@@ -431,15 +460,7 @@ __global__ __launch_bounds__(NT) void k_onesweep(
 #pragma unroll
   for (int i = 0; i < kItems; ++i) {
     const bool ok = dig[i] < kRadix;
-    uint64_t peers = ballot(ok);
-#pragma unroll
-    for (int b = 0; b < RB; ++b) {
-      if (b < nbits) {
-        const bool bit = (dig[i] >> b) & 1u;
-        const uint64_t bb = ballot(bit);
-        peers &= bit ? bb : ~bb;
-      }
-    }
+    const uint64_t peers = match_digit<RB>(dig[i], ballot(ok));
     uint32_t prior = 0;
     if (ok) prior = s_cnt[wave][dig[i]];
     const uint32_t below = popc_below(peers);
@@ -795,15 +816,7 @@ __global__ __launch_bounds__(NT) void k_sort_local(
 #pragma unroll
   for (int i = 0; i < kItems; ++i) {
     const bool ok = dig[i] < kRadix;
-    uint64_t peers = ballot(ok);
-#pragma unroll
-    for (int b = 0; b < RB; ++b) {
-      if (b < nbits) {
-        const bool bit = (dig[i] >> b) & 1u;
-        const uint64_t bb = ballot(bit);
-        peers &= bit ? bb : ~bb;
-      }
-    }
+    const uint64_t peers = match_digit<RB>(dig[i], ballot(ok));
     uint32_t prior = 0;
     if (ok) prior = s_cnt[wave][dig[i]];
     const uint32_t below = popc_below(peers);
@@ -1136,15 +1149,7 @@ __global__ __launch_bounds__(kBlockThreads) void k_unique_block(
 #pragma unroll
     for (int i = 0; i < ITEMS; ++i) {
       const bool ok = dig[i] < kRadix;
-      uint64_t peers = ballot(ok);
-#pragma unroll
-      for (int b = 0; b < RB; ++b) {
-        if (b < nbits) {
-          const bool bit = (dig[i] >> b) & 1u;
-          const uint64_t bb = ballot(bit);
-          peers &= bit ? bb : ~bb;
-        }
-      }
+      const uint64_t peers = match_digit<RB>(dig[i], ballot(ok));
       uint32_t prior = 0;
       if (ok) prior = s_cnt[wave][dig[i]];
       const uint32_t below = popc_below(peers);
