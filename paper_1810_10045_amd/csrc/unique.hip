@@ -280,6 +280,144 @@ __device__ __forceinline__ uint64_t match_digit(uint32_t dig, uint64_t valid) {
   return (uint64_t(hi) << 32) | lo;
 }
 
+// Wave and block scans for Unique's kernels. Within a wave they use DPP
+// (lanes read other lanes' registers inside the ALU op: row shifts by 1, 2
+// and 3, then by 4 and 8 on the upper banks of each 16-lane row, then the
+// broadcasts of lanes 15 and 31 to the rows after them), not LDS permutes:
+// a 64-lane scan is seven dependent ALU ops instead of six LDS round trips.
+// `id` is the operation's identity, which a lane takes where its source
+// lies outside its row or its row or bank is masked off.
+struct OpAdd {
+  __device__ int operator()(int a, int b) const { return a + b; }
+};
+struct OpMax {
+  __device__ int operator()(int a, int b) const { return a > b ? a : b; }
+};
+
+template <typename Op>
+__device__ __forceinline__ int dpp_incl_scan(int v, Op op, int id) {
+  int a = op(v, __builtin_amdgcn_update_dpp(id, v, 0x111, 0xf, 0xf, false));  // row_shr:1
+  a = op(a, __builtin_amdgcn_update_dpp(id, v, 0x112, 0xf, 0xf, false));      // row_shr:2
+  a = op(a, __builtin_amdgcn_update_dpp(id, v, 0x113, 0xf, 0xf, false));      // row_shr:3
+  a = op(a, __builtin_amdgcn_update_dpp(id, a, 0x114, 0xf, 0xe, false));      // row_shr:4
+  a = op(a, __builtin_amdgcn_update_dpp(id, a, 0x118, 0xf, 0xc, false));      // row_shr:8
+  a = op(a, __builtin_amdgcn_update_dpp(id, a, 0x142, 0xa, 0xf, false));      // row_bcast:15
+  a = op(a, __builtin_amdgcn_update_dpp(id, a, 0x143, 0xc, 0xf, false));      // row_bcast:31
+  return a;
+}
+
+// The value of the lane below this one (`id` on lane 0): DPP wave_shr:1.
+__device__ __forceinline__ int dpp_lane_below(int v, int id) {
+  return __builtin_amdgcn_update_dpp(id, v, 0x138, 0xf, 0xf, false);
+}
+
+__device__ __forceinline__ uint32_t wave_sum(uint32_t v) {
+  return static_cast<uint32_t>(
+      read_lane(dpp_incl_scan(static_cast<int>(v), OpAdd(), 0), kWave - 1));
+}
+
+// Exclusive sums over a block of NW waves of two values at once (one pair
+// of barriers for both); lds holds 2 * NW words. t0, t1: the block totals.
+template <int NW>
+__device__ __forceinline__ void blk_excl_sum2(uint32_t v0, uint32_t v1, uint32_t* lds,
+                                              uint32_t& e0, uint32_t& t0, uint32_t& e1,
+                                              uint32_t& t1) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const uint32_t i0 = static_cast<uint32_t>(dpp_incl_scan(static_cast<int>(v0), OpAdd(), 0));
+  const uint32_t i1 = static_cast<uint32_t>(dpp_incl_scan(static_cast<int>(v1), OpAdd(), 0));
+  if (lane == kWave - 1) {
+    lds[wave] = i0;
+    lds[NW + wave] = i1;
+  }
+  __syncthreads();
+  uint32_t b0 = 0, b1 = 0, a0 = 0, a1 = 0;
+#pragma unroll
+  for (int w = 0; w < NW; ++w) {
+    const uint32_t x0 = lds[w], x1 = lds[NW + w];
+    b0 += w < wave ? x0 : 0u;
+    b1 += w < wave ? x1 : 0u;
+    a0 += x0;
+    a1 += x1;
+  }
+  __syncthreads();
+  e0 = b0 + i0 - v0;
+  e1 = b1 + i1 - v1;
+  t0 = a0;
+  t1 = a1;
+}
+
+// Exclusive sum over a block of NW waves; lds holds NW words.
+template <int NW>
+__device__ __forceinline__ uint32_t blk_excl_sum(uint32_t v, uint32_t* lds, uint32_t& total) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const uint32_t incl = static_cast<uint32_t>(dpp_incl_scan(static_cast<int>(v), OpAdd(), 0));
+  if (lane == kWave - 1) lds[wave] = incl;
+  __syncthreads();
+  uint32_t before = 0, all = 0;
+#pragma unroll
+  for (int w = 0; w < NW; ++w) {
+    const uint32_t x = lds[w];
+    before += w < wave ? x : 0u;
+    all += x;
+  }
+  __syncthreads();
+  total = all;
+  return before + incl - v;
+}
+
+// An exclusive sum (s) and an exclusive maximum (m, values >= -1, -1 before
+// the first thread) over a block of NW waves with one pair of barriers.
+template <int NW>
+__device__ __forceinline__ void blk_excl_sum_max(uint32_t s, int m, uint32_t* lds_s, int* lds_m,
+                                                 uint32_t& es, uint32_t& ts, int& em, int& tm) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const uint32_t is = static_cast<uint32_t>(dpp_incl_scan(static_cast<int>(s), OpAdd(), 0));
+  const int im = dpp_incl_scan(m, OpMax(), -1);
+  const int prev = dpp_lane_below(im, -1);
+  if (lane == kWave - 1) {
+    lds_s[wave] = is;
+    lds_m[wave] = im;
+  }
+  __syncthreads();
+  uint32_t bs = 0, as = 0;
+  int bm = -1, am = -1;
+#pragma unroll
+  for (int w = 0; w < NW; ++w) {
+    const uint32_t x = lds_s[w];
+    const int y = lds_m[w];
+    bs += w < wave ? x : 0u;
+    as += x;
+    if (w < wave && y > bm) bm = y;
+    if (y > am) am = y;
+  }
+  __syncthreads();
+  es = bs + is - s;
+  ts = as;
+  em = prev > bm ? prev : bm;
+  tm = am;
+}
+
+// Exclusive maximum (values >= -1; -1 before the first thread) over a block
+// of NW waves; lds holds NW words.
+template <int NW>
+__device__ __forceinline__ int blk_excl_max(int v, int* lds, int& total) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int incl = dpp_incl_scan(v, OpMax(), -1);
+  const int prev = dpp_lane_below(incl, -1);
+  if (lane == kWave - 1) lds[wave] = incl;
+  __syncthreads();
+  int before = -1, all = -1;
+#pragma unroll
+  for (int w = 0; w < NW; ++w) {
+    const int x = lds[w];
+    if (w < wave && x > before) before = x;
+    if (x > all) all = x;
+  }
+  __syncthreads();
+  total = all;
+  return prev > before ? prev : before;
+}
+
 // ---------------------------------------------------------------------------
 // k_hist: bhist[b][p][d] = number of keys read by workgroup b whose digit of
 // pass p is d (rows of rstride slots per pass). Also clears the tickets and the
@@ -323,7 +461,7 @@ __global__ __launch_bounds__(kHistThreads) void k_hist(
           // words 78.3 -> 71.4 us per Unique call, 2M ids 126.6 -> 124.4 us;
           // at 262,144 ids (32 workgroups, less skew) 60.0 -> 62.0 us, so
           // only inputs above LMZ_UNIQUE_HIST_RUNS_MIN_K take it.
-          const uint32_t up = static_cast<uint32_t>(__shfl_up(static_cast<int>(d), 1, kWave));
+          const uint32_t up = static_cast<uint32_t>(dpp_lane_below(static_cast<int>(d), static_cast<int>(d)));
           const int ln = lane_id();
           const bool head = in && (ln == 0 || up != d);
           const uint64_t heads = ballot(head);
@@ -368,7 +506,7 @@ __global__ __launch_bounds__(NT) void k_onesweep(
   __shared__ uint16_t s_cnt[kWaves][kRadix];         // per-wave digit counts, then offsets
   __shared__ int32_t s_shift[kRadix];                // global position - local position
   __shared__ int32_t s_local[kRadix];                // tile-local start of each digit
-  __shared__ uint32_t s_scan[kWaves];
+  __shared__ uint32_t s_scan[2 * kWaves];  // two block sums at once
   __shared__ uint32_t s_tile;
 
   const int tid = threadIdx.x, lane = tid & 63;
@@ -491,9 +629,8 @@ __global__ __launch_bounds__(NT) void k_onesweep(
       st_agent(status + size_t(tile) * kRadix + d, (tile == 0 ? kFlagPrefix : kFlagAgg) | t);
     }
   }
-  uint32_t tile_sum, all_sum;
-  uint32_t local = block_excl_sum<kWaves, uint32_t>(tsum, s_scan, tile_sum);
-  uint32_t gbase = block_excl_sum<kWaves, uint32_t>(gsum, s_scan, all_sum);
+  uint32_t tile_sum, all_sum, local, gbase;
+  blk_excl_sum2<kWaves>(tsum, gsum, s_scan, local, tile_sum, gbase, all_sum);
 
   // Decoupled look-back for this thread's digits, W predecessors per round.
   uint32_t excl[DPT];
@@ -665,7 +802,8 @@ __device__ __forceinline__ void mark_runs(const uint32_t* __restrict__ runs, int
   const int dhi = first_lane(s_lohi[1] < R ? s_lohi[1] : R - 1);
   auto place = [&](uint32_t w, uint32_t dstart) {
     const uint32_t c = w & kRunCountMask;
-    const int64_t g = int64_t(dstart) + (wave_incl_sum(c) - c);
+    const int64_t g =
+        int64_t(dstart) + (static_cast<uint32_t>(dpp_incl_scan(static_cast<int>(c), OpAdd(), 0)) - c);
     const int64_t lo = g > gs ? g : gs;
     const int64_t hi = g + c < gs + m ? g + c : gs + m;
     if (lo < hi) {
@@ -700,7 +838,7 @@ __device__ __forceinline__ void spread_marks(int* s_mark, int m, int* s_maxs) {
     run = v[c] > run ? v[c] : run;
   }
   int total;
-  int before = block_excl_max<kWaves>(run, s_maxs, total);
+  int before = blk_excl_max<kWaves>(run, s_maxs, total);
 #pragma unroll
   for (int c = 0; c < CH; ++c) {
     before = v[c] > before ? v[c] : before;
@@ -786,7 +924,7 @@ __global__ __launch_bounds__(NT) void k_sort_local(
     const int R = 1 << prev_nbits;
     const uint32_t tot = run_total<NT>(prev_runs, gridDim.x, rstride, R, s_dstart);
     uint32_t all;
-    const uint32_t start = block_excl_sum<kWaves, uint32_t>(tot, s_scan, all);
+    const uint32_t start = blk_excl_sum<kWaves>(tot, s_scan, all);
     mark_runs<NT>(prev_runs, gridDim.x, rstride, kTile, R, tot, start, base, n, s_mark, s_src,
                   s_dstart, s_lohi);
     spread_marks<NT, kItems>(s_mark, n, s_maxs);
@@ -836,7 +974,7 @@ __global__ __launch_bounds__(NT) void k_sort_local(
     }
   }
   uint32_t tile_sum;
-  const uint32_t local = block_excl_sum<kWaves, uint32_t>(tot, s_scan, tile_sum);
+  const uint32_t local = blk_excl_sum<kWaves>(tot, s_scan, tile_sum);
   if (tid < kRadix) {
     s_local[tid] = static_cast<int32_t>(local);
     runs[size_t(tile) * rstride + tid] = (local << 16) | tot;
@@ -930,7 +1068,7 @@ __global__ __launch_bounds__(NT) void k_dedup(
     const int R = 1 << runs_nbits;
     const uint32_t tot = run_total<NT>(runs, gridDim.x, rstride, R, s_dstart);
     uint32_t all;
-    const uint32_t start = block_excl_sum<kWaves, uint32_t>(tot, s_scan, all);
+    const uint32_t start = blk_excl_sum<kWaves>(tot, s_scan, all);
     tile = first_lane(static_cast<int>(s_tile));
     const int64_t base = int64_t(tile) * kTile;
     const int64_t gs = base > 0 ? base - 1 : 0;
@@ -1004,10 +1142,10 @@ __global__ __launch_bounds__(NT) void k_dedup(
   }
   const uint32_t nheads = static_cast<uint32_t>(__popc(hmask));
   const int last_head = hmask ? static_cast<int>(p0) + (31 - __clz(static_cast<int>(hmask))) : -1;
-  uint32_t tile_heads;
-  const uint32_t heads_before = block_excl_sum<kWaves, uint32_t>(nheads, s_scan, tile_heads);
-  int tile_last;
-  const int last_before = block_excl_max<kWaves>(last_head, s_maxs, tile_last);
+  uint32_t tile_heads, heads_before;
+  int tile_last, last_before;
+  blk_excl_sum_max<kWaves>(nheads, last_head, s_scan, s_maxs, heads_before, tile_heads,
+                           last_before, tile_last);
 
   // Wave 0: publish the tile aggregate, then look back 64 tiles per round.
   if (wave == 0) {
@@ -1031,9 +1169,7 @@ __global__ __launch_bounds__(NT) void k_dedup(
         const int take = done ? first_px + 1 : first_nr;  // lanes [0, take) are consumed
         const bool mine = lane < take;
         uint32_t h = mine ? static_cast<uint32_t>((s >> 31) & kD31) : 0u;
-#pragma unroll
-        for (int off = 32; off >= 1; off >>= 1) h += __shfl_xor(h, off, kWave);
-        eh += h;
+        eh += wave_sum(h);
         // the nearest consumed predecessor that has a head holds the last one
         const int pl = static_cast<int>(s & kD31) - 1;
         const uint64_t has = ballot(mine && pl >= 0);
@@ -1101,6 +1237,7 @@ __global__ __launch_bounds__(NT) void k_dedup(
 // ---------------------------------------------------------------------------
 constexpr int kBlockThreads = kBlockThreadsHost;
 constexpr int kBlockWaves = kBlockThreads / kWave;
+constexpr size_t kLdsBytes = 160 * 1024 - 4096;  // gfx950's 160 KiB, less a margin
 
 template <typename KeyT, int ITEMS, int RB>
 __global__ __launch_bounds__(kBlockThreads) void k_unique_block(
@@ -1113,7 +1250,14 @@ __global__ __launch_bounds__(kBlockThreads) void k_unique_block(
   constexpr int kN = kBlockThreads * ITEMS;
   __shared__ KeyT s_keys[kN];
   __shared__ int32_t s_vals[kN + 1];                // + 1: the end offset of the last type
-  __shared__ uint16_t s_cnt[kBlockWaves][kRadix];  // per-wave digit counts, then offsets
+  // Per-wave digit counts, then offsets. Where the LDS holds two sets, pass
+  // p uses set p & 1 and the next pass's counters are cleared while this
+  // pass still runs; otherwise each pass clears the one set first.
+  constexpr size_t kCntBytes = sizeof(uint16_t) * kBlockWaves * kRadix;
+  constexpr size_t kLdsRest = sizeof(KeyT) * kN + sizeof(int32_t) * (kN + 1) +
+                              sizeof(uint32_t) * (kRadix + kBlockWaves);
+  constexpr int kCntSets = kLdsRest + 2 * kCntBytes <= kLdsBytes ? 2 : 1;
+  __shared__ uint16_t s_cnt[kCntSets][kBlockWaves][kRadix];
   __shared__ uint32_t s_start[kRadix];             // first sorted position of each digit
   __shared__ uint32_t s_scan[kBlockWaves];
   const int tid = threadIdx.x, lane = tid & 63;
@@ -1129,16 +1273,27 @@ __global__ __launch_bounds__(kBlockThreads) void k_unique_block(
     const int pos = wave * (ITEMS * kWave) + i * kWave + lane;
     key[i] = pos < K ? ids[pos] : KeyT(0);
     val[i] = pos;
+  }
+  // The first pass's counters, cleared while the ids are in flight.
+  for (int j = tid; j < kBlockWaves * kRadix / 2; j += kBlockThreads)
+    reinterpret_cast<uint32_t*>(&s_cnt[0][0][0])[j] = 0;
+#pragma unroll
+  for (int i = 0; i < ITEMS; ++i) {
+    const int pos = wave * (ITEMS * kWave) + i * kWave + lane;
     bad |= pos < K && key_bits(key[i]) >= V;
   }
   if (ballot(bad) && lane == 0) raise_err(dev_err, LM_DEVERR_ID_RANGE);
+  __syncthreads();
 
   for (int p = 0; p < passes; ++p) {
     const int shift = pb.shift[p], nbits = pb.nbits[p];
     const uint32_t mask = nbits > 0 ? (1u << nbits) - 1 : 0u;
-    for (int j = tid; j < kBlockWaves * kRadix / 2; j += kBlockThreads)
-      reinterpret_cast<uint32_t*>(&s_cnt[0][0])[j] = 0;
-    __syncthreads();
+    uint16_t (*cnt)[kRadix] = s_cnt[p % kCntSets];
+    if (kCntSets == 1 && p > 0) {
+      for (int j = tid; j < kBlockWaves * kRadix / 2; j += kBlockThreads)
+        reinterpret_cast<uint32_t*>(&cnt[0][0])[j] = 0;
+      __syncthreads();
+    }
     uint32_t dig[ITEMS], rank[ITEMS];
 #pragma unroll
     for (int i = 0; i < ITEMS; ++i) {
@@ -1151,11 +1306,16 @@ __global__ __launch_bounds__(kBlockThreads) void k_unique_block(
       const bool ok = dig[i] < kRadix;
       const uint64_t peers = match_digit<RB>(dig[i], ballot(ok));
       uint32_t prior = 0;
-      if (ok) prior = s_cnt[wave][dig[i]];
+      if (ok) prior = cnt[wave][dig[i]];
       const uint32_t below = popc_below(peers);
       rank[i] = prior + below;
-      if (ok && below == 0) s_cnt[wave][dig[i]] = static_cast<uint16_t>(prior + __popcll(peers));
+      if (ok && below == 0) cnt[wave][dig[i]] = static_cast<uint16_t>(prior + __popcll(peers));
     }
+    // The next pass's counters: their last reader, the pass before this
+    // one, finished before this pass began.
+    if (kCntSets == 2 && p + 1 < passes)
+      for (int j = tid; j < kBlockWaves * kRadix / 2; j += kBlockThreads)
+        reinterpret_cast<uint32_t*>(&s_cnt[(p + 1) % kCntSets][0][0])[j] = 0;
     __syncthreads();
     // Thread d < kRadix: per-wave offsets within digit d and its total; a
     // block scan of the totals gives each digit's first sorted position.
@@ -1163,19 +1323,19 @@ __global__ __launch_bounds__(kBlockThreads) void k_unique_block(
     if (tid < kRadix) {
 #pragma unroll
       for (int w = 0; w < kBlockWaves; ++w) {
-        const uint32_t c = s_cnt[w][tid];
-        s_cnt[w][tid] = static_cast<uint16_t>(tot);
+        const uint32_t c = cnt[w][tid];
+        cnt[w][tid] = static_cast<uint16_t>(tot);
         tot += c;
       }
     }
     uint32_t all;
-    const uint32_t start = block_excl_sum<kBlockWaves, uint32_t>(tot, s_scan, all);
+    const uint32_t start = blk_excl_sum<kBlockWaves>(tot, s_scan, all);
     if (tid < kRadix) s_start[tid] = start;
     __syncthreads();
 #pragma unroll
     for (int i = 0; i < ITEMS; ++i) {
       if (dig[i] < kRadix) {
-        const int dst = static_cast<int>(s_start[dig[i]] + s_cnt[wave][dig[i]] + rank[i]);
+        const int dst = static_cast<int>(s_start[dig[i]] + cnt[wave][dig[i]] + rank[i]);
         s_keys[dst] = key[i];
         s_vals[dst] = val[i];
       }
