@@ -3,18 +3,22 @@
 One step = one pass of the whole path over one batch of synthetic tokens
 already resident in HBM:
     Unique (lm_unique) -> Seg-Sum (lm_segsum) -> Fill-Values / update
-(SGD or Adam via lm_sparse_apply, SCATTER into a dense table or EXPAND into
-the merged type list via lm_fill_values, by workload). The headline workload
-is the largest one with fp32 gradients: K = 1,048,576 Zipf(1.2) token ids
-over a 20K character vocabulary, 2048-wide fp32 gradients (8 GiB per batch),
-SCATTER of the U reduced rows into the dense 20K x 2048 table. Steps cycle
+(SGD or Adam via lm_sparse_apply, EXPAND into the merged type list via
+lm_fill_values, by workload; a SCATTER into a dense table is done by Seg-Sum
+itself, lm_segsum_rows writing each type's row to its table row). The
+headline workload is the largest one with fp32 gradients: K = 1,048,576
+Zipf(1.2) token ids over a 20K character vocabulary, 2048-wide fp32
+gradients (8 GiB per batch), the U reduced rows written into the dense
+20K x 2048 table. Steps cycle
 through resident batches (at least 2 GiB of gradients in all) so that the
 gradient rows are not served from the 256 MB Infinity Cache.
 
 The headline runs the Unique calls on a second stream, up to three steps
 ahead of Seg-Sum and the update (Unique reads only the token ids, which a
 trainer has before the gradients exist); every step still does all of its
-work. The serial schedule (one stream) is timed too and printed beside it.
+work. The serial schedule (one stream) is timed too and printed beside it,
+and for the SCATTER workloads also the serial schedule with the SCATTER as
+a call of its own after lm_segsum (`unfused_serial`).
 
 Prints one JSON line: tokens/s, ms per step, the Seg-Sum roofline (algorithmic
 bytes per lm_segsum call / its average duration from HIP events on the launch
