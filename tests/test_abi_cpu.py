@@ -39,8 +39,9 @@ def test_test_hook_is_not_in_the_training_header():
 
 def test_header_declares_the_boundary():
     names = declared_functions()
-    for n in ("lm_unique", "lm_segsum", "lm_fill_values", "lm_sparse_apply", "lm_map_ids",
-              "lm_unique_workspace_bytes", "lm_segsum_workspace_bytes", "lm_status_string"):
+    for n in ("lm_unique", "lm_segsum", "lm_segsum_rows", "lm_fill_values", "lm_sparse_apply",
+              "lm_map_ids", "lm_unique_workspace_bytes", "lm_segsum_workspace_bytes",
+              "lm_status_string"):
         assert n in names
 
 
@@ -100,6 +101,18 @@ def test_argument_errors_return_before_any_launch(lib):
     assert lib.lm_segsum(_v(), 0, 10, 4, 4, _v(), _v(), _v(), _v(), 10, _v(), 2, _v(), _v(), 1 << 20, None) == 1
     assert lib.lm_segsum(None, 0, 10, 4, 4, _v(), _v(), _v(), _v(), 10, _v(), 4, _v(), _v(), 1 << 20, None) == 1
     assert lib.lm_segsum(_v(), 0, 10, 4, 4, _v(), _v(), _v(), _v(), 10, _v(), 4, _v(), _v(), 8, None) == 3
+    lib.lm_segsum_rows.argtypes = [P, I32, I64, I64, I64, P, P, P, P, P, I32, I64, P, I64, I64,
+                                   P, P, SZ, P]
+
+    def rows(gtype=0, idtype=0, rows_cap=10, row_ids=_v(), out_rows=100, ld_out=4, ws=_v(),
+             ws_bytes=1 << 20):
+        return lib.lm_segsum_rows(_v(), gtype, 10, 4, 4, _v(), _v(), _v(), _v(), row_ids, idtype,
+                                  rows_cap, _v(), out_rows, ld_out, _v(), ws, ws_bytes, None)
+    # unknown gradient or id dtype, an output of 2^31 rows, ld_out < D, NULL or
+    # negative row ids, a misaligned or short workspace
+    assert rows(gtype=2) == 5 and rows(idtype=7) == 5 and rows(out_rows=1 << 31) == 5
+    assert rows(ld_out=3) == 1 and rows(row_ids=None) == 1 and rows(rows_cap=-1) == 1
+    assert rows(ws=_v(0x1010)) == 1 and rows(ws_bytes=8) == 3
     lib.lm_fill_values.argtypes = [P, I64, P, P, I64, P, P, I32, I64, P, I64, I64, I32, P, P]
     assert lib.lm_fill_values(_v(), 4, _v(), _v(), 10, _v(), _v(), 0, 4, _v(), 10, 4, 9, _v(), None) == 5
     assert lib.lm_fill_values(_v(), 4, _v(), _v(), 10, None, None, 0, 4, _v(), 10, 4, 0, _v(), None) == 1
