@@ -23,6 +23,17 @@
 //               predecessors per round) carrying (number of heads, position of
 //               the last head), then writes uniq, offsets, counts, inverse and
 //               num_unique.
+// Where the ids are narrower (V <= LMZ_UNIQUE_KEYCOUNT_MAX_V), the types
+// come from a count per id instead of the sorted keys, and no dedup runs:
+//   k_key_hist  the count of every id value in LDS, one row per workgroup;
+//               clears the tickets and status words like k_hist.
+//   k_key_scan  the rows added up per id, then a block scan and a decoupled
+//               look-back over the ids in ascending order give uniq, counts,
+//               offsets, num_unique and each id's type (its rank among the
+//               ids present); also the digit counts of the radix passes.
+//   k_onesweep  the passes as above; the first one, which reads the ids in
+//               token order, also writes inverse[token] = rank[id], and the
+//               last writes the permutation.
 // Tiles take their index from an atomic ticket, so a tile only waits on
 // tiles that already hold a workgroup: every look-back makes progress. A
 // tile's inputs are fetched for tile = blockIdx.x while the ticket is in
@@ -63,6 +74,9 @@ constexpr int kBlockThreadsHost = 1024;  // threads of k_unique_block
 #ifndef LMZ_UNIQUE_GATHER_DIGIT_BITS
 #define LMZ_UNIQUE_GATHER_DIGIT_BITS 9 // widest digit of the tile-local passes
 #endif
+#ifndef LMZ_UNIQUE_KEYCOUNT_MAX_V
+#define LMZ_UNIQUE_KEYCOUNT_MAX_V (1 << 15)  // up to this V (and past one workgroup), counts per id
+#endif
 #ifndef LMZ_UNIQUE_LOOKBACK_W
 #define LMZ_UNIQUE_LOOKBACK_W 4        // predecessor tiles a look-back round reads
 #endif
@@ -89,6 +103,9 @@ static inline int items_for(int64_t K, int nt) {
   return K <= LMZ_UNIQUE_LARGE_ITEMS2_MAX_K ? 2 : (K <= LMZ_UNIQUE_LARGE_ITEMS4_MAX_K ? 4 : 8);
 }
 constexpr int kHistItems = 16;             // keys per thread per histogram round
+// ids per k_key_scan workgroup: 256 measured 1.2 us faster per call than
+// 1024 at 1,048,576 ids over 20K words (80 workgroups against 20)
+constexpr int kKeyScanThreads = 256;
 // Histogram workgroups: about K / 2048 of them, 8 to 32, up to 2^18 ids
 // (measured best: 8 at 8K ids, 32 at 64K and 262K), 64 above (larger
 // blocks serialise on LDS atomics at the Zipf heads).
@@ -122,6 +139,11 @@ struct UniqueLayout {
   int block_rb;     // its digit width (8, 9 or 10): the widest digit of its passes
   int gather;       // 1: tile-local passes (k_sort_local) and a gathering dedup; the
                     // histogram region then holds the runs of each pass and tile
+  int keycount;     // 1: a count per id (k_key_hist, k_key_scan) instead of k_hist
+                    // and k_dedup; bhist then holds a row per k_key_scan tile
+  int key_blocks;   // k_key_hist workgroups (rows of khist)
+  int scan_tiles;   // k_key_scan workgroups, kKeyScanThreads ids each
+  size_t khist, rank;
   int rstride;  // digit slots per pass in the histogram rows and status arrays
   int shift[kMaxPasses], nbits[kMaxPasses];
 };
@@ -202,6 +224,12 @@ static UniqueLayout unique_layout(int64_t K, int idtype, int64_t V) {
     if (L.block_items && L.nbits[p] > L.block_rb) L.block_rb = L.nbits[p];
   L.hist_blocks = hist_blocks_for(K);
   if (L.gather) L.hist_blocks = L.tiles;  // one row of runs per pass and tile
+  L.keycount = !L.block_items && !L.gather && V <= LMZ_UNIQUE_KEYCOUNT_MAX_V;
+  if (L.keycount) {
+    L.key_blocks = L.hist_blocks;
+    L.scan_tiles = static_cast<int>((V + kKeyScanThreads - 1) / kKeyScanThreads);
+    L.hist_blocks = L.scan_tiles;  // the passes add up one row per scan tile
+  }
   size_t off = 0;
   L.rstride = 1 << kSmallDigitBits;
   for (int p = 0; p < L.passes; ++p)
@@ -210,11 +238,16 @@ static UniqueLayout unique_layout(int64_t K, int idtype, int64_t V) {
   L.tickets = off; off += 256;
   L.status = off;  // the look-backs' words (none when the passes gather)
   if (!L.gather) off += align256(size_t(L.passes) * L.tiles * L.rstride * 4);
-  L.dstatus = off; off += align256(size_t(L.tiles) * 8);
+  L.dstatus = off;  // the dedup's (or the key scan's) look-back words
+  off += align256(size_t(L.tiles > L.scan_tiles ? L.tiles : L.scan_tiles) * 8);
   L.keys0 = off;   off += align256(size_t(K) * ks);
   L.keys1 = off;   off += align256(size_t(K) * ks);
   L.vals0 = off;   off += align256(size_t(K) * 4);
   L.vals1 = off;   off += align256(size_t(K) * 4);
+  if (L.keycount) {
+    L.khist = off; off += align256(size_t(L.key_blocks) * V * 4);
+    L.rank = off;  off += align256(size_t(V) * 4);
+  }
   L.total = off;
   return L;
 }
@@ -483,6 +516,170 @@ __global__ __launch_bounds__(kHistThreads) void k_hist(
 }
 
 // ---------------------------------------------------------------------------
+// k_key_hist: khist[b][v] = number of keys read by workgroup b equal to v,
+// for every v < V (V <= LMZ_UNIQUE_KEYCOUNT_MAX_V: a counter per id in LDS).
+// Like k_hist, lanes hold consecutive ids and a run of lanes with the same
+// id adds its length with one atomic; it also clears the call's tickets and
+// look-back status words. Ids outside [0, V) raise LM_DEVERR_ID_RANGE and
+// are not counted.
+// ---------------------------------------------------------------------------
+template <typename KeyT>
+__global__ __launch_bounds__(kHistThreads) void k_key_hist(
+    const KeyT* __restrict__ keys, int K, int V, uint32_t* __restrict__ khist,
+    uint32_t* __restrict__ clear, int64_t clear_words, int32_t* __restrict__ dev_err) {
+  extern __shared__ uint32_t sh[];  // V counters (at most 128 KiB)
+  for (int i = threadIdx.x; i < V; i += kHistThreads) sh[i] = 0;
+  for (int64_t i = blockIdx.x * int64_t(kHistThreads) + threadIdx.x; i < clear_words;
+       i += int64_t(gridDim.x) * kHistThreads)
+    clear[i] = 0;
+  __syncthreads();
+  bool bad = false;
+  const int ln = lane_id();
+  const int64_t stride = int64_t(gridDim.x) * kHistThreads;
+  for (int64_t i0 = blockIdx.x * int64_t(kHistThreads) + threadIdx.x; i0 < K;
+       i0 += stride * kHistItems) {
+    KeyT kv[kHistItems];  // all loads of a round in flight together
+#pragma unroll
+    for (int j = 0; j < kHistItems; ++j) {
+      const int64_t i = i0 + j * stride;
+      kv[j] = i < K ? keys[i] : KeyT(0);
+    }
+#pragma unroll
+    for (int j = 0; j < kHistItems; ++j) {
+      const bool in = i0 + j * stride < K;
+      const uint64_t kb = key_bits(kv[j]);
+      bad |= in && kb >= static_cast<uint64_t>(V);
+      const bool ok = in && kb < static_cast<uint64_t>(V);
+      const int v = ok ? static_cast<int>(kb) : -1;
+      const int up = dpp_lane_below(v, -2);
+      const bool head = ok && up != v;
+      // a run ends before the next head or the next lane that counts nothing
+      const uint64_t stops = ballot(head) | ~ballot(ok);
+      if (head) {
+        const uint64_t above = ln < 63 ? stops & ~((2ull << ln) - 1ull) : 0ull;
+        const int next = above ? __builtin_ctzll(above) : kWave;
+        atomicAdd(&sh[v], static_cast<uint32_t>(next - ln));
+      }
+    }
+  }
+  if (ballot(bad) && ln == 0) raise_err(dev_err, LM_DEVERR_ID_RANGE);
+  __syncthreads();
+  uint32_t* row = khist + size_t(blockIdx.x) * V;
+  for (int i = threadIdx.x; i < V; i += kHistThreads) row[i] = sh[i];
+}
+
+// ---------------------------------------------------------------------------
+// k_key_scan: tile `tile` (by ticket) owns the ids v = tile * NT + tid. An
+// id's count is the sum of its khist rows; the ids with a count are the
+// types, in ascending order. A block scan of (count, has a count) and a
+// decoupled look-back over the tiles (64 predecessors per round, the pair
+// (types, tokens) before each tile in one 64-bit status word) give every
+// type its index and CSR offset: uniq, counts, offsets, rank[v] = the type
+// of id v, num_unique and offsets[U] = K. Each workgroup also writes its
+// ids' counts per digit of every radix pass as a row of bhist, which the
+// passes add up like k_hist's rows.
+// ---------------------------------------------------------------------------
+template <typename KeyT, int NT>
+__global__ __launch_bounds__(NT) void k_key_scan(
+    const uint32_t* __restrict__ khist, int rows, int V, int K, int passes, int rstride,
+    PassBits pb, uint32_t* __restrict__ bhist, KeyT* __restrict__ uniq,
+    int32_t* __restrict__ counts, int32_t* __restrict__ offsets, int32_t* __restrict__ rank,
+    int64_t* __restrict__ num_unique, uint64_t* __restrict__ status,
+    uint32_t* __restrict__ ticket, int32_t* __restrict__ dev_err, WaitCfg wc) {
+  constexpr int kWaves = NT / kWave;
+  constexpr int kDigSlots = 2 * (1 << kLargeDigitBits);  // passes * rstride at most
+  __shared__ uint32_t s_dig[kDigSlots];
+  __shared__ uint32_t s_scan[2 * kWaves];
+  __shared__ uint32_t s_tile, s_excl_types, s_excl_tokens;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = first_lane(tid >> 6);
+  if (tid == 0) s_tile = add_agent(ticket, 1u);
+  for (int i = tid; i < passes * rstride; i += NT) s_dig[i] = 0;
+  __syncthreads();
+  const int tile = first_lane(static_cast<int>(s_tile));
+  const int v = tile * NT + tid;
+
+  // This id's count: its rows, 16 loads in flight per round.
+  uint32_t c = 0;
+  if (v < V) {
+    constexpr int kRows = 16;
+    for (int b = 0; b < rows; b += kRows) {
+      uint32_t h[kRows];
+#pragma unroll
+      for (int r = 0; r < kRows; ++r) h[r] = khist[size_t(b + r < rows ? b + r : b) * V + v];
+#pragma unroll
+      for (int r = 0; r < kRows; ++r) c += b + r < rows ? h[r] : 0u;
+    }
+  }
+  if (c > 0)
+    for (int p = 0; p < passes; ++p)
+      atomicAdd(&s_dig[p * rstride + ((static_cast<uint32_t>(v) >> pb.shift[p]) &
+                                      ((1u << pb.nbits[p]) - 1))],
+                c);
+  const uint32_t nz = c > 0 ? 1u : 0u;
+  uint32_t c_before, tile_tokens, t_before, tile_types;
+  blk_excl_sum2<kWaves>(c, nz, s_scan, c_before, tile_tokens, t_before, tile_types);
+  uint32_t* row = bhist + size_t(blockIdx.x) * passes * rstride;
+  for (int i = tid; i < passes * rstride; i += NT) row[i] = s_dig[i];
+
+  // Wave 0: publish the tile aggregate, then look back 64 tiles per round.
+  if (wave == 0) {
+    uint64_t* my = status + tile;
+    const uint64_t agg = (uint64_t(tile_types) << 31) | uint64_t(tile_tokens);
+    if (lane == 0) st_agent(my, (tile == 0 ? kDFlagPrefix : kDFlagAgg) | agg);
+    uint32_t et = 0, ek = 0;
+    if (tile > 0) {
+      int j = tile - 1;
+      uint32_t spins = 0;
+      while (true) {
+        const int pos = j - lane;
+        const uint64_t st = pos >= 0 ? ld_agent(status + pos) : kDFlagPrefix;
+        const uint64_t f = wc.force_fail ? 0 : st & kDFlags;
+        const uint64_t notready = ballot(f == 0);
+        const uint64_t prefix = ballot(f == kDFlagPrefix);
+        const int first_nr = notready ? __builtin_ctzll(notready) : kWave;
+        const int first_px = prefix ? __builtin_ctzll(prefix) : kWave;
+        const bool done = first_px < first_nr;
+        const int take = done ? first_px + 1 : first_nr;  // lanes [0, take) are consumed
+        const bool mine = lane < take;
+        et += wave_sum(mine ? static_cast<uint32_t>((st >> 31) & kD31) : 0u);
+        ek += wave_sum(mine ? static_cast<uint32_t>(st & kD31) : 0u);
+        if (done) break;
+        j -= take;
+        if (take == 0) {
+          if (++spins > wc.spin_limit) {
+            if (lane == 0) raise_err(dev_err, LM_DEVERR_SPIN);
+            break;
+          }
+          __builtin_amdgcn_s_sleep(1);
+        }
+      }
+      if (lane == 0)
+        st_agent(my, kDFlagPrefix | ((uint64_t(et + tile_types) & kD31) << 31) |
+                         ((uint64_t(ek) + tile_tokens) & kD31));
+    }
+    if (lane == 0) {
+      s_excl_types = et;
+      s_excl_tokens = ek;
+    }
+  }
+  __syncthreads();
+  const uint32_t types_before = s_excl_types, tokens_before = s_excl_tokens;
+  if (nz) {
+    const int seg = static_cast<int>(types_before + t_before);
+    uniq[seg] = static_cast<KeyT>(v);
+    counts[seg] = static_cast<int32_t>(c);
+    offsets[seg] = static_cast<int32_t>(tokens_before + c_before);
+    rank[v] = seg;
+  }
+  if (tile == static_cast<int>(gridDim.x) - 1 && tid == 0) {
+    const uint32_t U = types_before + tile_types;
+    *num_unique = U;
+    offsets[U] = K;
+  }
+}
+
+// ---------------------------------------------------------------------------
 // k_onesweep: one stable LSD pass over the digit (key >> shift) & (2^nbits-1),
 // nbits <= RB. Thread t answers for digits t*DPT .. t*DPT+DPT-1 (DPT = 2 for
 // 11-bit digits; for 8-bit digits threads 0..255 answer for one each).
@@ -493,7 +690,8 @@ __global__ __launch_bounds__(NT) void k_onesweep(
     KeyT* __restrict__ keys_out, int32_t* __restrict__ vals_out, int K, int shift, int nbits,
     const uint32_t* __restrict__ bhist, int hist_blocks, int hist_stride,
     uint32_t* __restrict__ status, uint32_t* __restrict__ ticket, int32_t* __restrict__ dev_err,
-    WaitCfg wc) {
+    WaitCfg wc, const int32_t* __restrict__ type_of_id, uint32_t n_ids,
+    int32_t* __restrict__ inverse) {
   constexpr int kWaves = NT / kWave;
   constexpr int kItems = ITEMS;
   constexpr int kTile = NT * kItems;
@@ -591,6 +789,18 @@ __global__ __launch_bounds__(NT) void k_onesweep(
   for (int i = 0; i < kItems; ++i) {
     const int64_t pos = base + int64_t(wave) * (kItems * kWave) + i * kWave + lane;
     dig[i] = pos < K ? digit_of(key[i], shift, mask) : kRadix;
+  }
+  // With the key counts (the first pass, ids in token order): each token's
+  // type, loaded now and stored at the end, so that the loads fly during
+  // the ranking and the look-back.
+  int32_t type_of[kItems];
+  if (inverse) {
+#pragma unroll
+    for (int i = 0; i < kItems; ++i) {
+      const int64_t pos = base + int64_t(wave) * (kItems * kWave) + i * kWave + lane;
+      const uint64_t kb = key_bits(key[i]);
+      type_of[i] = pos < K && kb < n_ids ? type_of_id[kb] : 0;
+    }
   }
 
   // Rank every key among the equal-digit keys before it in its wave.
@@ -720,6 +930,13 @@ __global__ __launch_bounds__(NT) void k_onesweep(
         keys_out[gp] = k;
         vals_out[gp] = s_vals[jj];
       }
+    }
+  }
+  if (inverse) {
+#pragma unroll
+    for (int i = 0; i < kItems; ++i) {
+      const int64_t pos = base + int64_t(wave) * (kItems * kWave) + i * kWave + lane;
+      if (pos < K) inverse[pos] = type_of[i];
     }
   }
 }
@@ -1442,11 +1659,12 @@ template <typename KeyT, int RB, int NT, int ITEMS>
 static hipError_t launch_pass(const UniqueLayout& L, int p, const KeyT* kin, const int32_t* vin,
                               KeyT* kout, int32_t* vout, int K, uint32_t* bhist,
                               uint32_t* status, uint32_t* tickets, int32_t* dev_err,
+                              const int32_t* type_of_id, uint32_t n_ids, int32_t* inverse,
                               hipStream_t st) {
   k_onesweep<KeyT, RB, NT, ITEMS><<<L.tiles, NT, 0, st>>>(
       kin, vin, kout, vout, K, L.shift[p], L.nbits[p], bhist + size_t(p) * L.rstride,
       L.hist_blocks, L.passes * L.rstride, status + size_t(p) * L.tiles * L.rstride, tickets + p,
-      dev_err, wait_cfg());
+      dev_err, wait_cfg(), type_of_id, n_ids, inverse);
   return hipGetLastError();
 }
 
@@ -1537,15 +1755,29 @@ static int run_unique(const KeyT* ids, int K, int64_t V, KeyT* uniq, int32_t* co
     };
     return launch_status(L.nt == 256 ? passes(I<256>{}) : passes(I<1024>{}));
   }
-  const size_t hist_lds = size_t(L.passes) * L.rstride * 4;
-  if (K > LMZ_UNIQUE_HIST_RUNS_MIN_K)
-    k_hist<KeyT, true><<<L.hist_blocks, kHistThreads, hist_lds, st>>>(
-        ids, K, static_cast<uint64_t>(V), L.passes, L.rstride, pb, bhist, tickets, clear_words,
-        dev_err);
-  else
-    k_hist<KeyT, false><<<L.hist_blocks, kHistThreads, hist_lds, st>>>(
-        ids, K, static_cast<uint64_t>(V), L.passes, L.rstride, pb, bhist, tickets, clear_words,
-        dev_err);
+  int32_t* type_of_id = nullptr;
+  if (L.keycount) {
+    // Counts per id, then the types and each id's type; the first pass
+    // writes the inverse map and no dedup runs.
+    if (L.passes * L.rstride > 2 * (1 << kLargeDigitBits)) return LM_E_UNSUPPORTED;
+    uint32_t* khist = reinterpret_cast<uint32_t*>(ws + L.khist);
+    type_of_id = reinterpret_cast<int32_t*>(ws + L.rank);
+    k_key_hist<KeyT><<<L.key_blocks, kHistThreads, size_t(V) * 4, st>>>(
+        ids, K, static_cast<int>(V), khist, tickets, clear_words, dev_err);
+    k_key_scan<KeyT, kKeyScanThreads><<<L.scan_tiles, kKeyScanThreads, 0, st>>>(
+        khist, L.key_blocks, static_cast<int>(V), K, L.passes, L.rstride, pb, bhist, uniq, counts,
+        offsets, type_of_id, num_unique, dstatus, tickets + kMaxPasses + 1, dev_err, wait_cfg());
+  } else {
+    const size_t hist_lds = size_t(L.passes) * L.rstride * 4;
+    if (K > LMZ_UNIQUE_HIST_RUNS_MIN_K)
+      k_hist<KeyT, true><<<L.hist_blocks, kHistThreads, hist_lds, st>>>(
+          ids, K, static_cast<uint64_t>(V), L.passes, L.rstride, pb, bhist, tickets, clear_words,
+          dev_err);
+    else
+      k_hist<KeyT, false><<<L.hist_blocks, kHistThreads, hist_lds, st>>>(
+          ids, K, static_cast<uint64_t>(V), L.passes, L.rstride, pb, bhist, tickets, clear_words,
+          dev_err);
+  }
   if (hipError_t e = hipGetLastError(); e != hipSuccess) return launch_status(e);
 
   const KeyT* kin = ids;
@@ -1555,9 +1787,11 @@ static int run_unique(const KeyT* ids, int K, int64_t V, KeyT* uniq, int32_t* co
     int32_t* vout = p == L.passes - 1 ? perm : vb[p & 1];
     // The narrowest compiled digit that holds this pass's bits.
     const bool narrow = L.nbits[p] <= kSmallDigitBits;
+    const bool first = p == 0 && type_of_id;
     auto pass = [&](auto rb, auto nt, auto items) {
       return launch_pass<KeyT, decltype(rb)::value, decltype(nt)::value, decltype(items)::value>(
-          L, p, kin, vin, kout, vout, K, bhist, status, tickets, dev_err, st);
+          L, p, kin, vin, kout, vout, K, bhist, status, tickets, dev_err,
+          first ? type_of_id : nullptr, static_cast<uint32_t>(V), first ? inverse : nullptr, st);
     };
     auto by_items = [&](auto rb, auto nt) {
       if constexpr (decltype(nt)::value == 256)
@@ -1576,6 +1810,8 @@ static int run_unique(const KeyT* ids, int K, int64_t V, KeyT* uniq, int32_t* co
     kin = kout;
     vin = vout;
   }
+  if (L.keycount)  // the scan wrote the types, the first pass the inverse map
+    return launch_status(hipGetLastError());
   const bool perm_runs = (reinterpret_cast<uintptr_t>(perm) & 15) == 0;
   auto dedup = [&](auto nt, auto items) {
     constexpr int NT = decltype(nt)::value, IT = decltype(items)::value;

@@ -22,8 +22,9 @@ int unique_run(const void* ids, int idtype, int64_t K, int64_t V, void* uniq, in
 }  // namespace lmz
 
 // 12 MiB: the largest workspace lm_unique needs for LM_UNIQUE_NOALLOC_MAX_K
-// ids is 10.4 MiB (int64 ids of 61 key bits); the call checks its own need
-// against this size all the same.
+// ids is 10.7 MiB (int64 ids with V = 32,768, counted per id; 61-bit int64
+// keys need 10.4 MiB); the call checks its own need against this size all
+// the same.
 constexpr size_t kScratchBytes = size_t(12) << 20;
 static __device__ __align__(256) unsigned char scratch[kScratchBytes];
 

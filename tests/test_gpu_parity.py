@@ -118,6 +118,18 @@ UNIQUE_CASES = [
     (100_000, 1 << 17, 1.0, np.int32, 48), (100_000, 1 << 18, 1.0, np.int32, 49),
     (100_000, 1 << 18, 1.0, np.int64, 50), (131_072, 1 << 27, 0.9, np.int64, 51),
     (131_072, 2**40, 0.9, np.int64, 42),
+    # Vocabularies of at most 32,768 ids past one workgroup and outside the
+    # tile-local passes: a count per id gives the types (no dedup), and the
+    # first radix pass writes the inverse map. The char workload's shape
+    # (15-bit keys as 8 + 7 bits) at 2 and 8 keys per thread, the largest
+    # vocabulary with int64 ids at 4 keys per thread, one id (no key bits),
+    # five ids, all ids nearly uniform, 1024-thread tiles too few for the
+    # tile-local passes (9 tiles), 256-thread tiles; (12,345, 256) and
+    # (20,000, 257) above take this path too.
+    (150_000, 20_000, 1.2, np.int32, 52), (2_000_001, 20_000, 1.2, np.int32, 53),
+    (1_048_579, 32_768, 1.0, np.int64, 54), (600_001, 1, 1.0, np.int32, 55),
+    (300_000, 5, 1.0, np.int32, 56), (262_145, 32_767, 0.0, np.int32, 57),
+    (16_385, 1_000, 1.0, np.int32, 58), (9_000, 32_768, 1.0, np.int64, 59),
 ]
 
 
@@ -170,8 +182,9 @@ def test_unique_out_of_range_sets_error(lz):
 
 @pytest.mark.parametrize("K", [12_000, 70_000, 300_000])
 def test_unique_out_of_range_sets_error_multi_tile(lz, K):
-    # 256-thread tiles, tile-local passes, 1024-thread look-back passes: one
-    # id past V in the last tile, one negative id in the first
+    # 256-thread tiles, tile-local passes, 1024-thread look-back passes (the
+    # first and the last with counts per id, V = 1000): one id past V in the
+    # last tile, one negative id in the first
     ids = synth.zipf_ids(K, 1000, 1.0, 62, np.int32)
     ids[K - 1] = 1000
     res = lz.unique(_t(ids), 1000)
@@ -209,13 +222,14 @@ def test_unique_outputs_not_16_byte_aligned(lz, K, V, dt):
     H.assert_unique_matches(res, ids, V, oracle, f"unaligned K={K}")
 
 
-def test_unique_wait_failure_is_reported(lz):
+@pytest.mark.parametrize("K,V", [(70_000, 800_000), (300_000, 20_000)])
+def test_unique_wait_failure_is_reported(lz, K, V):
     """The failure path of the look-backs of the multi-workgroup Unique,
     forced from the host: with the test hook set, every predecessor reads as
     not ready, each look-back gives up after 64 polls with LM_DEVERR_SPIN,
     and the kernels still finish inside their buffers. With the hook
-    cleared, the next call on the same workspace is exact again."""
-    K, V = 70_000, 800_000
+    cleared, the next call on the same workspace is exact again. Tile-local
+    passes with the gathering dedup; look-back passes with the key scan."""
     ids = synth.zipf_ids(K, V, 1.0, 73, np.int32)
     ws = lz.Workspace(DEV)
     _say("unique with forced look-back failures")

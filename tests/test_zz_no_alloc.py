@@ -33,6 +33,8 @@ def lz():
 CALLS = [
     (262_144, 2**61, 0.9, np.int64, 301),
     (262_144, 2_000_000, 0.9, np.int64, 302),
+    (262_144, 32_768, 1.0, np.int64, 307),   # counts per id: the largest workspace
+    (200_000, 20_000, 1.2, np.int32, 308),
     (65_536, 800_000, 1.0, np.int32, 303),
     (32_768, 800_000, 1.0, np.int32, 304),
     (8_192, 100_000, 1.0, np.int32, 305),
