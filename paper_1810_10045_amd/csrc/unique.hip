@@ -1456,6 +1456,32 @@ constexpr int kBlockThreads = kBlockThreadsHost;
 constexpr int kBlockWaves = kBlockThreads / kWave;
 constexpr size_t kLdsBytes = 160 * 1024 - 4096;  // gfx950's 160 KiB, less a margin
 
+// The one workgroup's keys and values in LDS (N of each, and one value
+// more). With 4-byte keys a key and its value sit side by side, so that the
+// reorder, the read-back and the dedup move a pair with one 8-byte access;
+// 8-byte keys keep two arrays.
+template <typename KeyT, int N>
+struct BlockPairs {
+  KeyT keys[N];
+  int32_t vals[N + 1];
+  __device__ void put(int i, KeyT k, int32_t v) { keys[i] = k; vals[i] = v; }
+  __device__ void get(int i, KeyT& k, int32_t& v) const { k = keys[i]; v = vals[i]; }
+  __device__ KeyT& key(int i) { return keys[i]; }
+  __device__ int32_t& val(int i) { return vals[i]; }
+};
+template <int N>
+struct BlockPairs<int32_t, N> {
+  int2 kv[N + 1];
+  __device__ void put(int i, int32_t k, int32_t v) { kv[i] = make_int2(k, v); }
+  __device__ void get(int i, int32_t& k, int32_t& v) const {
+    const int2 t = kv[i];
+    k = t.x;
+    v = t.y;
+  }
+  __device__ int32_t& key(int i) { return kv[i].x; }
+  __device__ int32_t& val(int i) { return kv[i].y; }
+};
+
 template <typename KeyT, int ITEMS, int RB>
 __global__ __launch_bounds__(kBlockThreads) void k_unique_block(
     const KeyT* __restrict__ ids, int K, uint64_t V, int passes, PassBits pb, int cap,
@@ -1465,8 +1491,7 @@ __global__ __launch_bounds__(kBlockThreads) void k_unique_block(
   constexpr int kRadix = 1 << RB;
   static_assert(kRadix <= kBlockThreads, "one thread per digit");
   constexpr int kN = kBlockThreads * ITEMS;
-  __shared__ KeyT s_keys[kN];
-  __shared__ int32_t s_vals[kN + 1];                // + 1: the end offset of the last type
+  __shared__ BlockPairs<KeyT, kN> s_kv;  // + 1 value: the end offset of the last type
   // Per-wave digit counts, then offsets. Where the LDS holds two sets, pass
   // p uses set p & 1 and the next pass's counters are cleared while this
   // pass still runs; otherwise each pass clears the one set first.
@@ -1553,8 +1578,7 @@ __global__ __launch_bounds__(kBlockThreads) void k_unique_block(
     for (int i = 0; i < ITEMS; ++i) {
       if (dig[i] < kRadix) {
         const int dst = static_cast<int>(s_start[dig[i]] + cnt[wave][dig[i]] + rank[i]);
-        s_keys[dst] = key[i];
-        s_vals[dst] = val[i];
+        s_kv.put(dst, key[i], val[i]);
       }
     }
     __syncthreads();
@@ -1562,8 +1586,7 @@ __global__ __launch_bounds__(kBlockThreads) void k_unique_block(
 #pragma unroll
       for (int i = 0; i < ITEMS; ++i) {
         const int pos = wave * (ITEMS * kWave) + i * kWave + lane;
-        key[i] = s_keys[pos];
-        val[i] = s_vals[pos];
+        s_kv.get(pos, key[i], val[i]);
       }
       __syncthreads();  // every read done before the next pass overwrites
     }
@@ -1579,15 +1602,16 @@ __global__ __launch_bounds__(kBlockThreads) void k_unique_block(
   for (int i = 0; i < ITEMS; ++i) {
     const int pos = wave * (ITEMS * kWave) + i * kWave + lane;
     const bool ok = pos < K;
-    k[i] = ok ? s_keys[pos] : KeyT(0);
-    src[i] = ok ? s_vals[pos] : 0;
-    const KeyT before = ok && pos > 0 ? s_keys[pos - 1] : KeyT(0);
+    k[i] = KeyT(0);
+    src[i] = 0;
+    if (ok) s_kv.get(pos, k[i], src[i]);
+    const KeyT before = ok && pos > 0 ? s_kv.key(pos - 1) : KeyT(0);
     hm[i] = ballot(ok && (pos == 0 || k[i] != before));
     wave_heads += static_cast<uint32_t>(__popcll(hm[i]));
     if (ok) perm[pos] = src[i];
   }
   if (lane == 0) s_scan[wave] = wave_heads;
-  __syncthreads();  // also: every read of s_keys / s_vals is done
+  __syncthreads();  // also: every read of the pairs is done
   uint32_t heads_before = 0, U = 0;
 #pragma unroll
   for (int w = 0; w < kBlockWaves; ++w) {
@@ -1613,26 +1637,26 @@ __global__ __launch_bounds__(kBlockThreads) void k_unique_block(
   for (int i = 0; i < ITEMS; ++i) {
     const int pos = wave * (ITEMS * kWave) + i * kWave + lane;
     if (pos < K) {
-      s_vals[src[i]] = seg[i];
-      if (((hm[i] >> lane) & 1u) && seg[i] < Uc) s_keys[seg[i]] = k[i];
+      s_kv.val(src[i]) = seg[i];
+      if (((hm[i] >> lane) & 1u) && seg[i] < Uc) s_kv.key(seg[i]) = k[i];
     }
   }
   __syncthreads();
-  for (int j = tid; j < K; j += kBlockThreads) inverse[j] = s_vals[j];
-  for (int j = tid; j < Uc; j += kBlockThreads) uniq[j] = s_keys[j];
+  for (int j = tid; j < K; j += kBlockThreads) inverse[j] = s_kv.val(j);
+  for (int j = tid; j < Uc; j += kBlockThreads) uniq[j] = s_kv.key(j);
   __syncthreads();
   // Stage the first position of every type, then write offsets and counts.
 #pragma unroll
   for (int i = 0; i < ITEMS; ++i) {
     const int pos = wave * (ITEMS * kWave) + i * kWave + lane;
-    if (pos < K && ((hm[i] >> lane) & 1u) && seg[i] <= Uc) s_vals[seg[i]] = pos;
+    if (pos < K && ((hm[i] >> lane) & 1u) && seg[i] <= Uc) s_kv.val(seg[i]) = pos;
   }
-  if (tid == 0 && static_cast<int>(U) == Uc) s_vals[Uc] = K;
+  if (tid == 0 && static_cast<int>(U) == Uc) s_kv.val(Uc) = K;
   __syncthreads();
   for (int j = tid; j < Uc; j += kBlockThreads) {
-    const int o = s_vals[j];
+    const int o = s_kv.val(j);
     offsets[j] = o;
-    counts[j] = s_vals[j + 1] - o;
+    counts[j] = s_kv.val(j + 1) - o;
   }
   if (tid == 0) {
     offsets[Uc] = K;
