@@ -39,6 +39,11 @@
 // Each wave gathers whole 16-byte column vectors of RF rows at a time
 // (RF x NV x 1 KiB in flight), adds them in fp32 registers and writes a row
 // as soon as its segment ends; grad is streamed with non-temporal loads.
+//
+// lm_segsum_rows runs the same kernels with a row map: type u's sum goes to
+// row row_ids[u] of the output (the dense table of a SCATTER). The walk
+// gathers the row of each window position's type with the types; the
+// fix-up looks it up per segment. Without a row map, row u.
 #include <atomic>
 #include <cstdlib>
 
