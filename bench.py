@@ -339,6 +339,20 @@ class Pipeline:
         if ev: ev(3)
 
 
+_SIDE_STREAM = []
+
+
+def side_stream(torch, dev):
+    """The overlapped schedule's second stream (default priority, like the
+    first), created once per process and used by every workload: with a new
+    stream per pass, about one pass in six ran with the two streams on one
+    hardware queue (a process gets four), which serialises them (the word
+    step at 160.8 us per step against 130.6)."""
+    if not _SIDE_STREAM:
+        _SIDE_STREAM.append(torch.cuda.Stream(device=dev))
+    return _SIDE_STREAM[0]
+
+
 def run_overlap_pass(pipe, steps, warmup, torch, main, side):
     """Warm-up, then K timed steps of the overlapped schedule; ms in total."""
     sync = HipEvents(2 * max(steps, warmup) + 2, timing=False)
@@ -454,8 +468,7 @@ def run_gpu(w, steps, warmup, nbatch, torch, lz, host):
     # Pass 3, the headline: the same K steps with the Unique calls on a
     # second stream (default priority, like the first), running ahead.
     pipe.enable_overlap()
-    overlap_ms = run_overlap_pass(pipe, steps, warmup, torch, stream,
-                                  torch.cuda.Stream(device=dev))
+    overlap_ms = run_overlap_pass(pipe, steps, warmup, torch, stream, side_stream(torch, dev))
     # One more serial step over batch 0: the outputs the oracle checks.
     step(0)
     torch.cuda.synchronize()
@@ -751,6 +764,7 @@ def main():
     from paper_1810_10045_amd import lmzipf as lz
     from paper_1810_10045_amd import synth
 
+    side_stream(torch, torch.device("cuda:0"))  # the process's first stream
     if args.copy_calibration:
         copy_calibration(torch)
     w = synth.WORKLOADS[args.workload]
