@@ -51,7 +51,7 @@ __global__ __launch_bounds__(256) void k_clear(uint32_t* p, int64_t words, uint8
   for (int64_t i = blockIdx.x * int64_t(256) + threadIdx.x; i < words;
        i += int64_t(gridDim.x) * 256)
     p[i] = 0u;
-  if (blockIdx.x == 0 && threadIdx.x < tail_bytes) tail[threadIdx.x] = 0;
+  if (blockIdx.x == 0 && static_cast<int>(threadIdx.x) < tail_bytes) tail[threadIdx.x] = 0;
 }
 
 static bool valid_idtype(int32_t t) { return t == LM_I32 || t == LM_I64; }
