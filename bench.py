@@ -16,7 +16,9 @@ gradient rows are not served from the 256 MB Infinity Cache.
 The headline runs the Unique calls on a second stream, up to three steps
 ahead of Seg-Sum and the update (Unique reads only the token ids, which a
 trainer has before the gradients exist); every step still does all of its
-work. The serial schedule (one stream) is timed too and printed beside it,
+work. At the char-LM and 2M-vocabulary workloads the two streams run on
+disjoint CUs (CU-masked streams, SIDE_CUS); the same schedule on shared
+CUs is printed beside it (`overlapped_all_cus`). The serial schedule (one stream) is timed too and printed beside it,
 and for the SCATTER workloads also the serial schedule with the SCATTER as
 a call of its own after lm_segsum (`unfused_serial`).
 
@@ -353,6 +355,71 @@ def side_stream(torch, dev):
     return _SIDE_STREAM[0]
 
 
+# The overlapped schedule's CU split, per workload: the Unique calls run on
+# CUs [0, n) and the rest of the step on the others (two streams created
+# with CU masks), where that measured faster than two streams sharing every
+# CU: char_heavy_1m 1,427 against 1,445 us per step, vocab2m_adam_i64 1,082
+# against 1,118. On a CU of its own, a Unique kernel that needs a whole CU
+# (the 1024-thread sort tiles, the per-id counters in LDS) no longer waits
+# for the walk's waves to leave one. The word step and the merge, whose
+# Seg-Sums need every CU, measured slower split (133 -> 141 and
+# 1,480 -> 1,500 us at 32 CUs).
+SIDE_CUS = {"char_heavy_1m": 32, "vocab2m_adam_i64": 64}
+
+
+def cu_mask_words(first, count, ncu):
+    """hipExtStreamCreateWithCUMask's mask of CUs [first, first + count)
+    as 32-bit words, bit c of the mask being CU c."""
+    if count <= 0 or first < 0 or first + count > ncu:
+        raise ValueError(f"CU range [{first}, {first + count}) outside the {ncu} CUs")
+    words = [0] * ((ncu + 31) // 32)
+    for c in range(first, first + count):
+        words[c // 32] |= 1 << (c % 32)
+    return words
+
+
+class CuSplit:
+    """Two streams on disjoint CUs: `side` on CUs [0, n), `main` on
+    [n, N), both at the default priority. A mask of every eighth CU was
+    refused (hipErrorOutOfMemory), as is one that leaves an XCD without a
+    CU: the mask's bits interleave the 8 XCDs, so a contiguous range of 32*j
+    bits takes 4*j CUs of each. Other range sizes measured slower for the
+    Seg-Sum (its chunks are sized for whole rounds of waves, and an XCD
+    with a CU count not a multiple of 4 finished its share late). Created
+    for one pass and destroyed after it."""
+
+    def __init__(self, torch, n):
+        import ctypes
+        self.ct, self.torch = ctypes, torch
+        ncu = torch.cuda.get_device_properties(0).multi_processor_count
+        if n % 32 or not 0 < n < ncu:
+            raise ValueError(f"a CU split takes a multiple of 32 CUs below {ncu}, not {n}")
+        hip = ctypes.CDLL("libamdhip64.so.7")  # the runtime torch already loaded
+        hip.hipExtStreamCreateWithCUMask.argtypes = [ctypes.c_void_p, ctypes.c_uint32,
+                                                     ctypes.c_void_p]
+        hip.hipStreamDestroy.argtypes = [ctypes.c_void_p]
+        self.hip, self.handles = hip, []
+        self.side = self._stream(cu_mask_words(0, n, ncu))
+        self.main = self._stream(cu_mask_words(n, ncu - n, ncu))
+
+    def _stream(self, words):
+        ct = self.ct
+        mask = (ct.c_uint32 * len(words))(*words)
+        h = ct.c_void_p()
+        rc = self.hip.hipExtStreamCreateWithCUMask(ct.byref(h), len(words), ct.byref(mask))
+        if rc != 0:
+            self.close()
+            raise RuntimeError(f"hipExtStreamCreateWithCUMask failed ({rc})")
+        self.handles.append(h)
+        return self.torch.cuda.ExternalStream(h.value)
+
+    def close(self):
+        self.torch.cuda.synchronize()
+        for h in self.handles:
+            self.hip.hipStreamDestroy(h)
+        self.handles = []
+
+
 def run_overlap_pass(pipe, steps, warmup, torch, main, side):
     """Warm-up, then K timed steps of the overlapped schedule; ms in total."""
     sync = HipEvents(2 * max(steps, warmup) + 2, timing=False)
@@ -466,9 +533,19 @@ def run_gpu(w, steps, warmup, nbatch, torch, lz, host):
         ev.close()
         pipe.fused = True
     # Pass 3, the headline: the same K steps with the Unique calls on a
-    # second stream (default priority, like the first), running ahead.
+    # second stream (default priority, like the first), running ahead; at the
+    # workloads of SIDE_CUS with the two streams on disjoint CUs (and, for
+    # comparison, both on every CU).
     pipe.enable_overlap()
-    overlap_ms = run_overlap_pass(pipe, steps, warmup, torch, stream, side_stream(torch, dev))
+    overlap_ms = overlap_all_ms = run_overlap_pass(pipe, steps, warmup, torch, stream,
+                                                   side_stream(torch, dev))
+    side_cus = SIDE_CUS.get(w.name)
+    if side_cus:
+        split = CuSplit(torch, side_cus)
+        try:
+            overlap_ms = run_overlap_pass(pipe, steps, warmup, torch, split.main, split.side)
+        finally:
+            split.close()
     # One more serial step over batch 0: the outputs the oracle checks.
     step(0)
     torch.cuda.synchronize()
@@ -495,7 +572,8 @@ def run_gpu(w, steps, warmup, nbatch, torch, lz, host):
         unfused.update(seg_bytes=ub, seg_gbps=ub / (unfused["stage_ms"][1] / 1e3) / 1e9,
                        ms_per_step=unfused["serial_ms"] / steps,
                        value=K / (unfused["serial_ms"] / steps / 1e3))
-    return dict(total_ms=total_ms, overlap_ms=overlap_ms, stage_ms=st.mean(axis=0).tolist(), seg_ms=seg_ms,
+    return dict(total_ms=total_ms, overlap_ms=overlap_ms, overlap_all_ms=overlap_all_ms,
+                side_cus=side_cus, stage_ms=st.mean(axis=0).tolist(), seg_ms=seg_ms,
                 seg_bytes=float(seg_bytes), uniq_bytes=uniq_bytes, after_bytes=after_bytes,
                 U=U_of, outputs=outputs, fused=fused, unfused=unfused)
 
@@ -684,7 +762,7 @@ def measure(w, args, torch, lz, cpu_budget):
     ms = r["overlap_ms"] / args.steps
     serial_ms = r["total_ms"] / args.steps
     achieved = r["seg_bytes"] / (r["seg_ms"] / 1e3) / 1e9
-    res = dict(w=w, nbatch=nbatch, r=r, ms=ms, serial_ms=serial_ms, achieved=achieved,
+    res = dict(w=w, nbatch=nbatch, r=r, ms=ms, serial_ms=serial_ms, achieved=achieved, steps=args.steps,
                value=w.tokens / (ms / 1e3), traffic=load_traffic(w.name), cpu=None, check=None)
     if not args.no_cpu:
         t0 = time.time()
@@ -697,6 +775,26 @@ def measure(w, args, torch, lz, cpu_budget):
         del ora
     del host, r["outputs"]
     return res
+
+
+def schedule_text(r):
+    """The overlapped schedule the headline figure was measured with."""
+    t = "unique on a second stream, up to 3 steps ahead (4 sets of its outputs)"
+    n = r["side_cus"]
+    if n:
+        t += f"; the second stream on CUs 0-{n - 1}, the first on the others (CU-masked streams)"
+    return t
+
+
+def all_cus_entry(res):
+    """With a CU split: the same overlapped schedule with both streams on
+    every CU, for comparison."""
+    r = res["r"]
+    if not r["side_cus"]:
+        return None
+    ms = r["overlap_all_ms"] / res["steps"]
+    return {"value": res["w"].tokens / (ms / 1e3), "ms_per_step": ms,
+            "schedule": "the same, both streams on every CU"}
 
 
 def cpu_baseline_entry(res):
@@ -720,7 +818,8 @@ def workload_summary(res):
         "tokens": w.tokens, "V": w.V, "D": w.D, "zipf_s": w.s, "ids": w.id_dtype,
         "grad": w.grad_dtype, "after_segsum": w.step, "resident_batches": res["nbatch"],
         "types_batch0": r["U"][0],
-        "value": res["value"], "ms_per_step": res["ms"],
+        "value": res["value"], "ms_per_step": res["ms"], "schedule": schedule_text(r),
+        "overlapped_all_cus": all_cus_entry(res),
         "serial_value": w.tokens / (res["serial_ms"] / 1e3), "serial_ms_per_step": res["serial_ms"],
         "stages_ms": stages(w, r),
         "segsum": {"kernels": segsum_kernels(w, r["fused"]), "achieved_gbps": res["achieved"],
@@ -811,7 +910,8 @@ def main():
                      "traffic": head["traffic"]},
         "cpu_baseline": cpu_baseline_entry(head),
         "oracle_check": head["check"],
-        "schedule": "unique on a second stream, up to 3 steps ahead (4 sets of its outputs)",
+        "schedule": schedule_text(r),
+        "overlapped_all_cus": all_cus_entry(head),
         "serial": {"value": w.tokens / (head["serial_ms"] / 1e3), "ms_per_step": head["serial_ms"],
                    "schedule": "one stream, the steps one after another"},
         "unfused_serial": unfused_entry(w, r),

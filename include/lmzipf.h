@@ -153,8 +153,11 @@ int lm_unique_noalloc(const void* ids, int32_t idtype, int64_t K, int64_t V,
  *     out[u, :] = sum over i in [offsets[u], offsets[u+1]) of grad[perm[i], :]
  * for u < U = *num_unique, accumulated in fp32 in a fixed order, so repeated
  * calls give bit-identical results. The order depends on K, D, u_cap (the
- * walk's chunks are sized from min(K, u_cap)) and the launch form, not on
- * the values.
+ * walk's chunks are sized from min(K, u_cap)), the launch form and the
+ * number of compute units `stream` may use (the chunks are also sized to
+ * fill whole rounds of the waves that fit there: all of the device's, or
+ * those of a stream created with hipExtStreamCreateWithCUMask), not on the
+ * values.
  *
  * grad       device, K rows of D values of dtype `gtype` (LM_F32 / LM_BF16),
  *            row stride ld_grad elements.
@@ -193,7 +196,8 @@ int lm_segsum(const void* grad, int32_t gtype, int64_t K, int64_t D,
  *     out[row_ids[u], :] = sum over i in [offsets[u], offsets[u+1]) of
  *                          grad[perm[i], :]          for u < *num_unique,
  * with the same fixed summation order (so bit-identical to lm_segsum with
- * u_cap = rows_cap, in the same launch form, followed by a row copy). With
+ * u_cap = rows_cap, in the same launch form on a stream with the same
+ * compute units, followed by a row copy). With
  * row_ids = uniq from lm_unique and `out` a
  * dense V x D table, this is Seg-Sum followed by Fill-Values SCATTER
  * (lm_fill_values, LM_FILL_SCATTER, dst_ids NULL) without writing and

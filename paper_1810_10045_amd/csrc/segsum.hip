@@ -813,6 +813,21 @@ static int device_cus() {
   return n;
 }
 
+// Multiprocessors a launch on stream st may use: a stream created with a CU
+// mask runs its workgroups on the masked ones only. Any other stream, or a
+// failed query, gets the whole device.
+static int stream_cus(hipStream_t st) {
+  const int n = device_cus();
+  uint32_t mask[32] = {};
+  if (hipExtStreamGetCUMask(st, 32, mask) != hipSuccess) {
+    (void)hipGetLastError();
+    return n;
+  }
+  int c = 0;
+  for (uint32_t m : mask) c += __builtin_popcount(m);
+  return c > 0 && c < n ? c : n;
+}
+
 // Workgroups of kernel k that fit on one multiprocessor at once (the
 // occupancy the compiled kernel allows), cached by the caller.
 template <typename Kern>
@@ -830,7 +845,8 @@ static int blocks_per_cu(Kern k, int threads, size_t lds, std::atomic<int>& cach
 }
 
 // Whole rounds of waves. The walk's waves (chunks x column tiles) of equal
-// cost run in rounds of as many waves as fit on the device at once. Where a
+// cost run in rounds of as many waves as fit at once on the compute units
+// the launch's stream may use. Where a
 // last round would be less than half full, its few waves run nearly alone,
 // far below the memory system's rate: the chunk count then grows (so the
 // chunks shrink) until the last round is full, at most to the workspace's
@@ -861,7 +877,7 @@ static void launch_one(SegArgs& a, int tiles, hipStream_t st) {
     if (a.fused) {
       auto k = k_segsum<GT, VEC, NV, RF, R, T, kFusedThreads, true>;
       static std::atomic<int> bpc{-1};
-      const int64_t room = int64_t(blocks_per_cu(k, kFusedThreads, 0, bpc)) * kFusedWaves * device_cus();
+      const int64_t room = int64_t(blocks_per_cu(k, kFusedThreads, 0, bpc)) * kFusedWaves * stream_cus(st);
       a.nchunks = whole_rounds(a.nchunks, tiles, room, a.max_chunks);
       a.main_blocks = (a.nchunks + kFusedWaves - 1) / kFusedWaves * tiles;
       const int fix_blocks = (a.nchunks + kFusedSpan - 1) / kFusedSpan * a.fix_tiles;
@@ -872,7 +888,7 @@ static void launch_one(SegArgs& a, int tiles, hipStream_t st) {
   auto k = k_segsum<GT, VEC, NV, RF, R, T, kSegThreads, false>;
   static std::atomic<int> bpc{-1};
   const int64_t room =
-      int64_t(blocks_per_cu(k, kSegThreads, LMZ_SEG_LDS_PAD, bpc)) * kSegWaves * device_cus();
+      int64_t(blocks_per_cu(k, kSegThreads, LMZ_SEG_LDS_PAD, bpc)) * kSegWaves * stream_cus(st);
   a.nchunks = whole_rounds(a.nchunks, tiles, room, a.max_chunks);
   const dim3 grid((a.nchunks + kSegWaves - 1) / kSegWaves, tiles);
   k<<<grid, kSegThreads, LMZ_SEG_LDS_PAD, st>>>(a);

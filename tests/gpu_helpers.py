@@ -130,3 +130,31 @@ def assert_adam_first_step(got_p, got_m, got_v, ref_p, ref_m, ref_v, S_ref, lr, 
     bp = bp + 2 * U32 * np.abs(ref_p)
     bad = np.abs(got_p - ref_p) > bp * 1.01
     assert not bad.any(), f"Adam p: {int(bad.sum())} values outside the bound"
+
+
+class CuMaskedStream:
+    """A stream whose kernels run on CUs [first, first + count) only
+    (hipExtStreamCreateWithCUMask, default priority); close() destroys it."""
+
+    def __init__(self, torch, first, count):
+        import ctypes
+        self.torch, self.ct = torch, ctypes
+        hip = ctypes.CDLL("libamdhip64.so.7")  # the runtime torch already loaded
+        hip.hipExtStreamCreateWithCUMask.argtypes = [ctypes.c_void_p, ctypes.c_uint32,
+                                                     ctypes.c_void_p]
+        hip.hipStreamDestroy.argtypes = [ctypes.c_void_p]
+        self.hip = hip
+        ncu = torch.cuda.get_device_properties(0).multi_processor_count
+        assert 0 <= first and 0 < count and first + count <= ncu
+        words = [0] * ((ncu + 31) // 32)
+        for c in range(first, first + count):
+            words[c // 32] |= 1 << (c % 32)
+        mask = (ctypes.c_uint32 * len(words))(*words)
+        self.h = ctypes.c_void_p()
+        rc = hip.hipExtStreamCreateWithCUMask(ctypes.byref(self.h), len(words), ctypes.byref(mask))
+        assert rc == 0, f"hipExtStreamCreateWithCUMask failed ({rc})"
+        self.stream = torch.cuda.ExternalStream(self.h.value)
+
+    def close(self):
+        self.torch.cuda.synchronize()
+        self.hip.hipStreamDestroy(self.h)

@@ -102,3 +102,19 @@ def test_overlapped_schedule_lets_unique_run_ahead():
     # one wait for the start event, then one per step from step 4 on
     assert side_waits[0][:2] == ("wait", 0) and len(side_waits) == 1 + (8 - 4)
     assert ops["side"].index(("front", 3, 3)) < ops["side"].index(side_waits[1])
+
+
+def test_cu_mask_words():
+    """Bit c of the mask is CU c; the split's two ranges cover every CU once."""
+    assert bench.cu_mask_words(0, 32, 256) == [0xFFFFFFFF] + [0] * 7
+    assert bench.cu_mask_words(32, 224, 256) == [0] + [0xFFFFFFFF] * 7
+    assert bench.cu_mask_words(3, 2, 40) == [0b11000, 0]
+    for n in bench.SIDE_CUS.values():
+        side = bench.cu_mask_words(0, n, 256)
+        main = bench.cu_mask_words(n, 256 - n, 256)
+        assert all(a & b == 0 and a | b == 0xFFFFFFFF for a, b in zip(side, main))
+        assert n % 32 == 0
+    with pytest.raises(ValueError):
+        bench.cu_mask_words(250, 8, 256)
+    with pytest.raises(ValueError):
+        bench.cu_mask_words(0, 0, 256)

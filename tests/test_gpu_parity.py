@@ -471,6 +471,43 @@ def test_segsum_deterministic(lz):
     assert torch.equal(a[:U], b[:U])  # rows past U are never written
 
 
+@pytest.mark.parametrize("D,gdt", [(2048, "f32"), (1024, "bf16")])
+def test_segsum_on_cu_masked_stream(lz, D, gdt):
+    """On a stream limited to 32 CUs (a contiguous mask: 4 CUs of each XCD)
+    the walk's chunks are sized for whole rounds of the waves that fit on
+    those CUs, several rounds here where the whole device holds them in one.
+    Checked against the oracle, bit-identical from run to run on that
+    stream, and lm_segsum_rows bit-identical to lm_segsum then a row copy
+    there too."""
+    K, V, s, seed = 100_000, 5000, 1.2, 131
+    _say(f"segsum on a 32-CU stream K={K} D={D} {gdt}")
+    ids = synth.zipf_ids(K, V, s, seed, np.int32)
+    g32 = synth.normal_rows(K, D, seed + 1000)
+    grad = synth.bf16_bits(g32) if gdt == "bf16" else g32
+    tgrad = _t(g32).to(torch.bfloat16) if gdt == "bf16" else _t(g32)
+    res = lz.unique(_t(ids), V)
+    torch.cuda.synchronize()
+    U = int(res.num_unique.item())
+    ms = H.CuMaskedStream(torch, 0, 32)
+    try:
+        outs = [lz.segsum(tgrad, res.perm, res.inverse, res.offsets, res.num_unique,
+                          dev_err=res.dev_err, stream=ms.stream) for _ in range(2)]
+        table = torch.zeros((V, D), dtype=torch.float32, device=DEV)
+        lz.segsum_rows(tgrad, res.perm, res.inverse, res.offsets, res.num_unique, res.uniq,
+                       table, dev_err=res.dev_err, stream=ms.stream)
+        ms.stream.synchronize()
+    finally:
+        ms.close()
+    lz.check(res.dev_err)
+    o = H.assert_unique_matches(res, ids, V, oracle)
+    ref = oracle.segsum(grad, o[3], U)
+    got = outs[0][:U].double().cpu().numpy()
+    H.check_rows(got, ref, H.sum_of_squares(grad, o[3], U, oracle), gdt, "32-CU stream")
+    H.assert_single_rows_exact(got, ref, o[1])
+    assert torch.equal(outs[0][:U], outs[1][:U]), "not deterministic on the masked stream"
+    assert torch.equal(table[res.uniq[:U].long()], outs[0][:U]), "rows variant differs"
+
+
 @pytest.mark.parametrize("K,V,s,D,gdt,seed", [(65_536, 800_000, 1.0, 1024, "f32", 121),
                                                (60_000, 500, 1.2, 1024, "f32", 122),
                                                (70_000, 800_000, 1.0, 1024, "bf16", 123)])
