@@ -3,9 +3,10 @@
 One step = one pass of the whole path over one batch of synthetic tokens
 already resident in HBM:
     Unique (lm_unique) -> Seg-Sum (lm_segsum) -> Fill-Values / update
-(SGD or Adam via lm_sparse_apply, EXPAND into the merged type list via
-lm_fill_values, by workload; a SCATTER into a dense table is done by Seg-Sum
-itself, lm_segsum_rows writing each type's row to its table row). The
+(Adam via lm_sparse_apply, EXPAND into the merged type list via
+lm_fill_values, by workload; a SCATTER into a dense table and an SGD update
+are done by Seg-Sum itself: lm_segsum_rows writes each type's row to its
+table row, lm_segsum_sgd applies it there). The
 headline workload is the largest one with fp32 gradients: K = 1,048,576
 Zipf(1.2) token ids over a 20K character vocabulary, 2048-wide fp32
 gradients (8 GiB per batch), the U reduced rows written into the dense
@@ -19,8 +20,8 @@ trainer has before the gradients exist); every step still does all of its
 work. At the char-LM and 2M-vocabulary workloads the two streams run on
 disjoint CUs (CU-masked streams, SIDE_CUS); the same schedule on shared
 CUs is printed beside it (`overlapped_all_cus`). The serial schedule (one stream) is timed too and printed beside it,
-and for the SCATTER workloads also the serial schedule with the SCATTER as
-a call of its own after lm_segsum (`unfused_serial`).
+and for the SCATTER and SGD workloads also the serial schedule with that
+update as a call of its own after lm_segsum (`unfused_serial`).
 
 Prints one JSON line: tokens/s, ms per step, the Seg-Sum roofline (algorithmic
 bytes per lm_segsum call / its average duration from HIP events on the launch
@@ -91,6 +92,21 @@ def unique_bytes(K, U, id_bytes):
 # merge's EXPAND stage also runs shard 0's own Unique and Seg-Sum, so it has
 # no single byte count here.
 AFTER_ROWS = {"sgd": 3, "softmax_sgd": 3, "adam": 7, "scatter": 2}
+
+# Steps done by the Seg-Sum call itself (lm_segsum_rows, lm_segsum_sgd), and
+# the name of that fused stage.
+FUSED_STEPS = ("scatter", "sgd", "softmax_sgd")
+
+
+def fused_stage(w):
+    return ("segsum_rows (segsum + scatter)" if w.step == "scatter"
+            else "segsum_sgd (segsum + sgd)")
+
+
+def fused_extra_bytes(w, D, U, id_bytes):
+    """Bytes a fused call moves beyond lm_segsum's: the U row ids, and for
+    SGD the table rows it reads before it writes them."""
+    return U * id_bytes + (U * D * 4 if w.step != "scatter" else 0)
 
 
 class HipEvents:
@@ -176,7 +192,7 @@ class Pipeline:
     drive this same class, so they check the launches that are timed here."""
 
     def __init__(self, w, batches, torch, lz, dev, table=None):
-        self.w, self.batches, self.lz = w, batches, lz
+        self.w, self.batches, self.lz, self.torch = w, batches, lz, torch
         K, D = w.tokens, w.D
         idt = torch.int64 if w.id_dtype == "i64" else torch.int32
         self.ures = lz.unique_buffers(K, w.V, idt, dev)
@@ -199,27 +215,44 @@ class Pipeline:
             mdt = torch.float16 if w.step == "expand_f16" else torch.float32
             st["M"] = torch.empty((cap, D), dtype=mdt, device=dev)
         self.sets = None
-        # SCATTER into the dense table: Seg-Sum writes each type's row to its
-        # table row itself (lm_segsum_rows), unless `fused` is cleared (then
-        # lm_segsum into `out`, and lm_fill_values SCATTER from there).
-        self.fused = w.step == "scatter"
+        # SCATTER into the dense table and SGD: Seg-Sum writes (or applies)
+        # each type's row to its table row itself (lm_segsum_rows,
+        # lm_segsum_sgd), unless `fused` is cleared (then lm_segsum into
+        # `out`, and lm_fill_values SCATTER or lm_sparse_apply from there).
+        self.fused = w.step in FUSED_STEPS
+        self.last = None
 
     def reduce(self, bt, ures, err):
         """Seg-Sum of batch bt from Unique outputs ures: into `out`, or with
-        `fused`, straight into the table rows of the types (SCATTER done)."""
+        `fused`, straight into the table rows of the types (SCATTER or SGD
+        done)."""
         w, lz, st = self.w, self.lz, self.state
-        if self.fused:
+        self.last = (bt, ures, err)
+        if self.fused and w.step == "scatter":
             lz.segsum_rows(bt.grad, ures.perm, ures.inverse, ures.offsets, ures.num_unique,
                            ures.uniq, st["table"], dev_err=err, ws=self.ws)
+        elif self.fused:
+            lz.segsum_sgd(bt.grad, ures.perm, ures.inverse, ures.offsets, ures.num_unique,
+                          ures.uniq, st["table"], w.lr, dev_err=err, ws=self.ws)
         else:
             lz.segsum(bt.grad, ures.perm, ures.inverse, ures.offsets, ures.num_unique,
                       out=self.out, dev_err=err, ws=self.ws)
 
     def reduced_rows(self, U):
-        """The U reduced rows of the last step, in type order (from the table
-        when the SCATTER was fused into Seg-Sum)."""
-        if self.fused:
+        """The U reduced rows of the last step, in type order: from the table
+        when the SCATTER was fused into Seg-Sum; with SGD fused, from the same
+        call with lr = -1 on a zero table, where each row is 0 + 1 * sum,
+        the sum itself."""
+        if self.fused and self.w.step == "scatter":
             return self.state["table"][self.ures.uniq[:U].long()]
+        if self.fused:
+            bt, ures, err = self.last
+            z = self.torch.zeros_like(self.state["table"])
+            self.lz.segsum_sgd(bt.grad, ures.perm, ures.inverse, ures.offsets, ures.num_unique,
+                               ures.uniq, z, -1.0, dev_err=err, ws=self.ws)
+            rows = z[ures.uniq[:U].long()]
+            del z
+            return rows
         return self.out[:U]
 
     def enable_overlap(self, nsets=4):
@@ -260,7 +293,7 @@ class Pipeline:
         ures, u0 = self.sets[j]
         err = ures.dev_err
         self.reduce(bt, ures, err)
-        if w.step in ("sgd", "softmax_sgd"):
+        if w.step in ("sgd", "softmax_sgd") and not self.fused:
             lz.sparse_apply(st["table"], ures.uniq, ures.num_unique, self.out, "sgd", lr=w.lr,
                             dev_err=err)
         elif w.step == "adam":
@@ -316,7 +349,7 @@ class Pipeline:
         if ev: ev(1)
         self.reduce(bt, ures, err)
         if ev: ev(2)
-        if w.step in ("sgd", "softmax_sgd"):
+        if w.step in ("sgd", "softmax_sgd") and not self.fused:
             lz.sparse_apply(st["table"], ures.uniq, ures.num_unique, self.out, "sgd", lr=w.lr,
                             dev_err=err)
         elif w.step == "adam":
@@ -561,8 +594,9 @@ def run_gpu(w, steps, warmup, nbatch, torch, lz, host):
     gb = 2 if w.grad_dtype == "bf16" else 4
     ib = 8 if w.id_dtype == "i64" else 4
     Us = [U_of[i % nbatch] for i in range(steps)]
-    # the fused call also reads the U row ids
-    seg_bytes = np.mean([segsum_bytes(K, D, U, gb) + (U * ib if fused else 0) for U in Us])
+    # the fused call also reads the U row ids (and with SGD the table rows)
+    seg_bytes = np.mean([segsum_bytes(K, D, U, gb) + (fused_extra_bytes(w, D, U, ib) if fused else 0)
+                         for U in Us])
     seg_ms = float(st[:, 1].mean())
     uniq_bytes = float(np.mean([unique_bytes(K, U, ib) for U in Us]))
     rows = AFTER_ROWS.get(w.step)
@@ -722,33 +756,39 @@ def copy_calibration(torch, reps=3):
 
 
 def segsum_kernels(w, fused=False):
-    """The kernels of one lm_segsum (or, fused with SCATTER, lm_segsum_rows)
-    call at this workload's shape (rows of up to 4096 columns on the 16-byte
-    path: one launch)."""
-    name = "lm_segsum_rows" if fused else "lm_segsum"
+    """The kernels of one lm_segsum (or, fused with SCATTER or SGD,
+    lm_segsum_rows or lm_segsum_sgd) call at this workload's shape (rows of
+    up to 4096 columns on the 16-byte path: one launch)."""
+    name = ("lm_segsum" if not fused else
+            "lm_segsum_rows" if w.step == "scatter" else "lm_segsum_sgd")
     k = (SEGSUM_KERNELS if w.D <= 4096 else "lm_segsum (k_segsum walk, then k_segsum_fix)")
     k = k.replace("lm_segsum", name, 1)
-    return k + (", each type row written to its table row" if fused else "")
+    if not fused:
+        return k
+    return k + (", each type row written to its table row" if w.step == "scatter"
+                else ", each type row applied to its table row (SGD)")
 
 
 def stages(w, r):
     """Per-stage ms of the event pass, named for what each stage runs."""
     ms = r["stage_ms"]
     if r["fused"]:
-        return {"unique": ms[0], "segsum_rows (segsum + scatter)": ms[1]}
+        return {"unique": ms[0], fused_stage(w): ms[1]}
     return {"unique": ms[0], "segsum": ms[1], w.step: ms[2]}
 
 
 def unfused_entry(w, r):
-    """The same workload with SCATTER as its own call after lm_segsum."""
+    """The same workload with the SCATTER or SGD update as its own call after
+    lm_segsum."""
     u = r["unfused"]
     if not u:
         return None
+    then = "lm_fill_values SCATTER" if w.step == "scatter" else "lm_sparse_apply SGD"
     return {"value": u["value"], "ms_per_step": u["ms_per_step"],
             "stages_ms": {"unique": u["stage_ms"][0], "segsum": u["stage_ms"][1],
-                          "scatter": u["stage_ms"][2]},
+                          w.step: u["stage_ms"][2]},
             "segsum_gbps": u["seg_gbps"], "segsum_frac": u["seg_gbps"] / HBM_PEAK_GBPS,
-            "schedule": "one stream; lm_segsum into a U x D buffer, then lm_fill_values SCATTER"}
+            "schedule": f"one stream; lm_segsum into a U x D buffer, then {then}"}
 
 
 def measure(w, args, torch, lz, cpu_budget):
@@ -898,7 +938,7 @@ def main():
         "stages_ms": stages(w, r),
         # algorithmic bytes of each stage / its event-measured time (GB/s)
         "stages_gbps": ({"unique": r["uniq_bytes"] / (r["stage_ms"][0] / 1e3) / 1e9,
-                         "segsum_rows (segsum + scatter)": head["achieved"]} if r["fused"] else
+                         fused_stage(w): head["achieved"]} if r["fused"] else
                         {"unique": r["uniq_bytes"] / (r["stage_ms"][0] / 1e3) / 1e9,
                          "segsum": head["achieved"],
                          w.step: (r["after_bytes"] / (r["stage_ms"][2] / 1e3) / 1e9

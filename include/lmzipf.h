@@ -219,9 +219,37 @@ int lm_segsum_rows(const void* grad, int32_t gtype, int64_t K, int64_t D, int64_
                    int64_t rows_cap, float* out, int64_t out_rows, int64_t ld_out,
                    int32_t* dev_err, void* ws, size_t ws_bytes, void* stream);
 
-/* The one-launch form of lm_segsum (and lm_segsum_rows) relies on the
- * hardware starting the walk's workgroups before the fix-up workgroups that
- * wait on them (they come first in the grid). lm_segsum_set_two_launches(1)
+/* ------------------------------------------------------------------------
+ * Seg-Sum with the SGD update — Sec. III-A steps 2 and 7 in one pass on one
+ * GPU (where the exchange of steps 3 to 6 leaves the reduced rows as they
+ * are): the same sums as lm_segsum, applied to the rows of the table that
+ * row_ids names instead of written out:
+ *     table[row_ids[u], :] -= lr * (sum over i in [offsets[u], offsets[u+1])
+ *                                   of grad[perm[i], :])   for u < *num_unique,
+ * bit-identical to lm_segsum (u_cap = rows_cap, the same launch form, on a
+ * stream with the same compute units) followed by lm_sparse_apply with
+ * LM_OPT_SGD and the same lr, without writing and re-reading the U x D
+ * intermediate. Rows that no type names are left untouched.
+ *
+ * row_ids    device, rows_cap distinct ids of dtype `idtype` (lm_unique's
+ *            uniq), the first *num_unique used. An id outside [0, V) sets
+ *            LM_DEVERR_ID_RANGE and that row is not updated;
+ *            *num_unique > rows_cap sets LM_DEVERR_CAPACITY and only the
+ *            first rows_cap types are applied.
+ * table      device, V x D fp32 (V < 2^31), row stride ld_table, updated in
+ *            place.
+ * The other arguments, the workspace (lm_segsum_workspace_bytes(K, D)) and
+ * the launch forms are those of lm_segsum.
+ * ------------------------------------------------------------------------ */
+int lm_segsum_sgd(const void* grad, int32_t gtype, int64_t K, int64_t D, int64_t ld_grad,
+                  const int32_t* perm, const int32_t* inverse, const int32_t* offsets,
+                  const int64_t* num_unique, const void* row_ids, int32_t idtype,
+                  int64_t rows_cap, float* table, int64_t V, int64_t ld_table, float lr,
+                  int32_t* dev_err, void* ws, size_t ws_bytes, void* stream);
+
+/* The one-launch form of lm_segsum (and lm_segsum_rows, lm_segsum_sgd)
+ * relies on the hardware starting the walk's workgroups before the fix-up
+ * workgroups that wait on them (they come first in the grid). lm_segsum_set_two_launches(1)
  * makes every later call in the process use the two-launch form instead
  * (the walk, then a separate fix-up kernel: no workgroup ever waits on
  * another), the fallback should a

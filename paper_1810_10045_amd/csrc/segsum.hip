@@ -44,6 +44,14 @@
 // row row_ids[u] of the output (the dense table of a SCATTER). The walk
 // gathers the row of each window position's type with the types; the
 // fix-up looks it up per segment. Without a row map, row u.
+//
+// lm_segsum_sgd (the SGD instantiations) updates those rows instead of
+// writing them: row = row - lr * sum, the sum in the same order and the
+// update the same fused multiply-add as lm_sparse_apply's. The walk then
+// closes a gather batch after its second segment end and loads the table
+// rows of its (at most two) ends with its gradient rows, through buffer
+// resources whose range is empty where no row is needed (such a load reads
+// nothing and returns zeros), so an update costs no round trip of its own.
 #include <atomic>
 #include <cstdlib>
 
@@ -130,6 +138,7 @@ struct SegArgs {
   int row_ids64;           //   (int64 ids when nonzero), < out_rows; nullptr: row u
   int64_t out_rows;
   int32_t* dev_err;
+  float lr;                // lm_segsum_sgd: out rows become row - lr * sum
 };
 
 struct SegLayout {
@@ -276,6 +285,47 @@ __device__ __forceinline__ int64_t out_row_of(const SegArgs& a, int s) {
   return r;
 }
 
+// lm_segsum_sgd: a buffer resource over output row r (D fp32 values), or
+// over nothing for r < 0: loads through an empty range read no memory and
+// return zeros, so a batch loads its two table rows unconditionally.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t table_row(const SegArgs& a, int64_t r) {
+  constexpr int kRawBufferWord3 = 0x00020000;  // 32-bit data format, no swizzle
+  return __builtin_amdgcn_make_buffer_rsrc(a.out + (r >= 0 ? r : 0) * a.ld_out, 0,
+                                           r >= 0 ? a.D * 4 : 0, kRawBufferWord3);
+}
+
+// VEC fp32 values at column col of the row behind resource rs.
+template <int VEC>
+__device__ __forceinline__ void table_vec(__amdgpu_buffer_rsrc_t rs, int col, float* v) {
+  if constexpr (VEC % 4 == 0) {
+#pragma unroll
+    for (int i = 0; i < VEC; i += 4) {
+      const f32x4 x = __builtin_bit_cast(
+          f32x4, __builtin_amdgcn_raw_buffer_load_b128(rs, (col + i) * 4, 0, 0));
+      v[i] = x.x;
+      v[i + 1] = x.y;
+      v[i + 2] = x.z;
+      v[i + 3] = x.w;
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < VEC; ++i)
+      v[i] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rs, (col + i) * 4, 0, 0));
+  }
+}
+
+// Write a finished type row: out = sum, or with SGD out = out - lr * sum.
+template <int VEC, bool SGD>
+__device__ __forceinline__ void finish_row(const SegArgs& a, float* o, float* sum) {
+  if constexpr (SGD) {
+    float t[VEC];
+    load_vec<VEC>(o, t);
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) sum[e] = t[e] - a.lr * sum[e];
+  }
+  store_vec<VEC>(o, sum);
+}
+
 template <int VEC>
 __device__ __forceinline__ void store_vec_agent(float* p, const float* v) {
   static_assert(VEC % 2 == 0, "pairs of fp32 values");
@@ -313,6 +363,7 @@ __device__ __forceinline__ bool wait_flags(const SegArgs& a, int idx, bool need)
 // sums each long segment that starts there as k_segsum_fix does (one wave
 // for fewer than 16 further pieces, all waves and an LDS combine for a
 // head), waiting for each piece's flag before loading it.
+template <bool SGD>
 __device__ __forceinline__ void fused_fix(const SegArgs& a) {
   constexpr int RF = LMZ_SEG_FUSED_RF;
   constexpr int kShortMax = 16;  // further pieces below this: one wave
@@ -371,7 +422,7 @@ __device__ __forceinline__ void fused_fix(const SegArgs& a) {
           for (int e = 0; e < 4; ++e) acc[e] += buf[r][e];
     }
     const int64_t orow = out_row_of(a, s);
-    if (col < D && orow >= 0) store_vec<4>(a.out + orow * a.ld_out + col, acc);
+    if (col < D && orow >= 0) finish_row<4, SGD>(a, a.out + orow * a.ld_out + col, acc);
   }
 
   // Heads, one after the other, all waves: wave w adds pieces w, w + W, ...
@@ -404,18 +455,18 @@ __device__ __forceinline__ void fused_fix(const SegArgs& a) {
         float sum = 0.f;
 #pragma unroll
         for (int w = 0; w < kFusedWaves; ++w) sum += s_part[w][x];
-        a.out[orow * a.ld_out + cx] = sum;
+        finish_row<1, SGD>(a, a.out + orow * a.ld_out + cx, &sum);
       }
     }
     __syncthreads();
   }
 }
 
-template <typename GT, int VEC, int NV, int RF, int R, int T, int NTHR, bool FUSED>
+template <typename GT, int VEC, int NV, int RF, int R, int T, int NTHR, bool FUSED, bool SGD>
 __global__ __launch_bounds__(NTHR) void k_segsum(SegArgs a) {
   if constexpr (FUSED) {
     if (static_cast<int>(blockIdx.x) >= a.main_blocks) {
-      fused_fix(a);
+      fused_fix<SGD>(a);
       return;
     }
   }
@@ -589,8 +640,34 @@ __global__ __launch_bounds__(NTHR) void k_segsum(SegArgs a) {
     const int wbase = p0 - 1 + w * kWave;
     const int lo = q > wbase ? q - wbase : 0;
     const int hi = q_end - wbase < kWave ? q_end - wbase : kWave;
-    for (int j0 = lo; j0 < hi; j0 += RF) {
-      const int n = hi - j0 < RF ? hi - j0 : RF;
+    for (int j0 = lo; j0 < hi;) {
+      int n = hi - j0 < RF ? hi - j0 : RF;
+      // SGD: at most two segment ends per batch (bm: their bits), whose
+      // table rows load with the batch's gradient rows.
+      uint64_t bm = 0;
+      float tb[2][NV][VEC];
+      if constexpr (SGD) {
+        bm = (ends[w] >> j0) & ((uint64_t(1) << n) - 1);
+        const uint64_t m1 = bm & (bm - 1), m2 = m1 & (m1 - 1);
+        if (m2) {
+          n = __builtin_ctzll(m2);
+          bm &= (uint64_t(1) << n) - 1;
+        }
+        uint64_t mm = bm;
+#pragma unroll
+        for (int k = 0; k < 2; ++k) {
+          int64_t orow = -1;  // no row: a partial row, a type past u_cap, a bad id, no end
+          if (mm) {
+            const int j = j0 + __builtin_ctzll(mm);
+            mm &= mm - 1;
+            const int s = read_lane(sw[w], j);
+            if (!(s == s_f && started_before) && s >= 0 && s < a.u_cap) orow = read_lane(orw[w], j);
+          }
+          const __amdgpu_buffer_rsrc_t rs = table_row(a, orow);
+#pragma unroll
+          for (int v = 0; v < NV; ++v) table_vec<VEC>(rs, col_ld[v], tb[k][v]);
+        }
+      }
       // Always RF row loads (rows past n repeat row n-1, a cache hit): a load
       // under a condition makes the compiler wait for every earlier load.
       raw_t buf[RF][NV];
@@ -624,6 +701,16 @@ __global__ __launch_bounds__(NTHR) void k_segsum(SegArgs a) {
               bad_row |= rows && orow < 0 && s >= 0 && s < a.u_cap;
               dst = (s >= 0 && s < a.u_cap && orow >= 0) ? a.out + orow * a.ld_out : nullptr;
             }
+            if constexpr (SGD) {
+              if (!part) {  // the batch's first or second end: table row 0 or 1
+                const bool second = (bm & ((uint64_t(1) << (j - j0)) - 1)) != 0;
+#pragma unroll
+                for (int v = 0; v < NV; ++v)
+#pragma unroll
+                  for (int e = 0; e < VEC; ++e)
+                    acc[v][e] = (second ? tb[1][v][e] : tb[0][v][e]) - a.lr * acc[v][e];
+              }
+            }
             if (dst) {
 #pragma unroll
               for (int v = 0; v < NV; ++v) {
@@ -644,6 +731,7 @@ __global__ __launch_bounds__(NTHR) void k_segsum(SegArgs a) {
           }
         }
       }
+      j0 += n;
     }
   }
   // Report a segment map that disagrees with offsets at the chunk start.
@@ -682,7 +770,7 @@ constexpr int kFixChunks = LMZ_SEG_FIX_CHUNKS;
 static_assert(kFixChunks <= kFixWaves && kFixChunks <= LMZ_SEG_FIX_RF,
               "at most one short segment per wave and one head per workgroup");
 
-template <int VEC, int RF>
+template <int VEC, int RF, bool SGD>
 __global__ __launch_bounds__(kFixThreads) void k_segsum_fix(SegArgs a) {
   constexpr int kCols = kWave * VEC;  // columns of a tile
   __shared__ float s_part[kFixWaves][kCols];
@@ -740,7 +828,7 @@ __global__ __launch_bounds__(kFixThreads) void k_segsum_fix(SegArgs a) {
 #pragma unroll
         for (int e = 0; e < VEC; ++e) acc[e] += sbuf[r][e];
     const int64_t orow = out_row_of(a, ss);
-    if (col < D && orow >= 0) store_vec<VEC>(a.out + orow * a.ld_out + col, acc);
+    if (col < D && orow >= 0) finish_row<VEC, SGD>(a, a.out + orow * a.ld_out + col, acc);
   }
   if (ih < 0) return;  // the same in every wave: no barrier below is skipped by only some
   float acc[VEC];
@@ -775,7 +863,7 @@ __global__ __launch_bounds__(kFixThreads) void k_segsum_fix(SegArgs a) {
       float sum = 0.f;
 #pragma unroll
       for (int w = 0; w < kFixWaves; ++w) sum += s_part[w][x];
-      a.out[orow * a.ld_out + cx] = sum;
+      finish_row<1, SGD>(a, a.out + orow * a.ld_out + cx, &sum);
     }
   }
 }
@@ -868,16 +956,22 @@ static int whole_rounds(int nchunks, int tiles, int64_t waves_per_round, int max
   return static_cast<int>(n < nchunks ? nchunks : n);
 }
 
-template <typename GT, int VEC, int NV, int R>
+template <typename GT, int VEC, int NV, int R, bool SGD>
 static void launch_one(SegArgs& a, int tiles, hipStream_t st) {
   constexpr int RF = rf_for<NV, R>(), T = t_for<R>();
   a.tiles = tiles;
   a.tile_cols = NV * kWave * VEC;
+  // The rounds are those of the plain kernel (SGD false) for the SGD
+  // instantiations too: its occupancy fixes the chunks, and with them the
+  // order of every sum, so lm_segsum_sgd adds in lm_segsum's order.
   if constexpr (VEC >= 2) {
     if (a.fused) {
-      auto k = k_segsum<GT, VEC, NV, RF, R, T, kFusedThreads, true>;
+      auto k = k_segsum<GT, VEC, NV, RF, R, T, kFusedThreads, true, SGD>;
       static std::atomic<int> bpc{-1};
-      const int64_t room = int64_t(blocks_per_cu(k, kFusedThreads, 0, bpc)) * kFusedWaves * stream_cus(st);
+      const int64_t room =
+          int64_t(blocks_per_cu(k_segsum<GT, VEC, NV, RF, R, T, kFusedThreads, true, false>,
+                                kFusedThreads, 0, bpc)) *
+          kFusedWaves * stream_cus(st);
       a.nchunks = whole_rounds(a.nchunks, tiles, room, a.max_chunks);
       a.main_blocks = (a.nchunks + kFusedWaves - 1) / kFusedWaves * tiles;
       const int fix_blocks = (a.nchunks + kFusedSpan - 1) / kFusedSpan * a.fix_tiles;
@@ -885,39 +979,61 @@ static void launch_one(SegArgs& a, int tiles, hipStream_t st) {
       return;
     }
   }
-  auto k = k_segsum<GT, VEC, NV, RF, R, T, kSegThreads, false>;
+  auto k = k_segsum<GT, VEC, NV, RF, R, T, kSegThreads, false, SGD>;
   static std::atomic<int> bpc{-1};
   const int64_t room =
-      int64_t(blocks_per_cu(k, kSegThreads, LMZ_SEG_LDS_PAD, bpc)) * kSegWaves * stream_cus(st);
+      int64_t(blocks_per_cu(k_segsum<GT, VEC, NV, RF, R, T, kSegThreads, false, false>,
+                            kSegThreads, LMZ_SEG_LDS_PAD, bpc)) *
+      kSegWaves * stream_cus(st);
   a.nchunks = whole_rounds(a.nchunks, tiles, room, a.max_chunks);
   const dim3 grid((a.nchunks + kSegWaves - 1) / kSegWaves, tiles);
   k<<<grid, kSegThreads, LMZ_SEG_LDS_PAD, st>>>(a);
 }
 
-template <typename GT, int VEC, int NV>
+template <typename GT, int VEC, int NV, bool SGD>
 static hipError_t launch_r(SegArgs& a, hipStream_t st) {
   constexpr int CT = NV * kWave * VEC;
   const int tiles = (a.D + CT - 1) / CT;
   switch (a.R) {
-    case 16: launch_one<GT, VEC, NV, 16>(a, tiles, st); break;
-    case 32: launch_one<GT, VEC, NV, 32>(a, tiles, st); break;
-    case 64: launch_one<GT, VEC, NV, 64>(a, tiles, st); break;
-    case 128: launch_one<GT, VEC, NV, 128>(a, tiles, st); break;
-    case 256: launch_one<GT, VEC, NV, 256>(a, tiles, st); break;
-    default: launch_one<GT, VEC, NV, 512>(a, tiles, st); break;
+    case 16: launch_one<GT, VEC, NV, 16, SGD>(a, tiles, st); break;
+    case 32: launch_one<GT, VEC, NV, 32, SGD>(a, tiles, st); break;
+    case 64: launch_one<GT, VEC, NV, 64, SGD>(a, tiles, st); break;
+    case 128: launch_one<GT, VEC, NV, 128, SGD>(a, tiles, st); break;
+    case 256: launch_one<GT, VEC, NV, 256, SGD>(a, tiles, st); break;
+    default: launch_one<GT, VEC, NV, 512, SGD>(a, tiles, st); break;
   }
   return hipGetLastError();
 }
 
-template <typename GT, int VEC>
+template <typename GT, int VEC, bool SGD>
 static hipError_t dispatch_nv(SegArgs& a, int nv_max, hipStream_t st) {
   const int per = kWave * VEC;
   int nv = (a.D + per - 1) / per;
   if (nv > nv_max) nv = nv_max;
-  if (nv <= 1) return launch_r<GT, VEC, 1>(a, st);
-  if (nv == 2) return launch_r<GT, VEC, 2>(a, st);
-  if constexpr (sizeof(GT) == 4 || VEC == 1) return launch_r<GT, VEC, 4>(a, st);
-  return launch_r<GT, VEC, 2>(a, st);
+  if (nv <= 1) return launch_r<GT, VEC, 1, SGD>(a, st);
+  if (nv == 2) return launch_r<GT, VEC, 2, SGD>(a, st);
+  if constexpr (sizeof(GT) == 4 || VEC == 1) return launch_r<GT, VEC, 4, SGD>(a, st);
+  return launch_r<GT, VEC, 2, SGD>(a, st);
+}
+
+template <bool SGD>
+static hipError_t dispatch(SegArgs& a, int gtype, bool vec, hipStream_t st) {
+  if (gtype == LM_F32)
+    return vec ? dispatch_nv<float, 4, SGD>(a, LMZ_SEG_NV_MAX, st)
+               : dispatch_nv<float, 1, SGD>(a, 4, st);
+  return vec ? dispatch_nv<bf16_t, 8, SGD>(a, LMZ_SEG_NV_MAX < 2 ? LMZ_SEG_NV_MAX : 2, st)
+             : dispatch_nv<bf16_t, 1, SGD>(a, 4, st);
+}
+
+template <bool SGD>
+static void launch_fix(SegArgs& a, hipStream_t st) {
+  const uint32_t fix_blocks = static_cast<uint32_t>((a.nchunks + kFixChunks - 1) / kFixChunks);
+  if (a.D % 4 == 0)
+    k_segsum_fix<4, LMZ_SEG_FIX_RF, SGD>
+        <<<dim3(fix_blocks, (a.D + 255) / 256), kFixThreads, 0, st>>>(a);
+  else
+    k_segsum_fix<1, LMZ_SEG_FIX_RF, SGD>
+        <<<dim3(fix_blocks, (a.D + 63) / 64), kFixThreads, 0, st>>>(a);
 }
 
 static bool al16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
@@ -960,7 +1076,7 @@ int segsum_run(const void* grad, int gtype, int64_t K, int64_t D, int64_t ld_gra
                const int32_t* perm, const int32_t* inverse, const int32_t* offsets,
                const int64_t* num_unique, int64_t u_cap, float* out, int64_t ld_out,
                int32_t* dev_err, void* ws, size_t ws_bytes, hipStream_t st,
-               const void* row_ids, int row_ids64, int64_t out_rows) {
+               const void* row_ids, int row_ids64, int64_t out_rows, bool sgd, float lr) {
   const SegLayout L = seg_layout(K, D);
   if (ws_bytes < L.total) return LM_E_WORKSPACE;
   if (K == 0 || D == 0 || u_cap == 0) return LM_OK;
@@ -991,6 +1107,7 @@ int segsum_run(const void* grad, int gtype, int64_t K, int64_t D, int64_t ld_gra
   a.nchunks = static_cast<int>(chunks_for(K, L.R, a.rw, a.ww, u_cap));
   a.max_chunks = L.max_chunks;
   a.dev_err = dev_err;
+  a.lr = lr;
 
   const bool out_vec = al16(out) && ld_out % 4 == 0 && D % 4 == 0;
   const bool vec = gtype == LM_F32 ? out_vec && al16(grad) && ld_grad % 4 == 0
@@ -1020,19 +1137,11 @@ int segsum_run(const void* grad, int gtype, int64_t K, int64_t D, int64_t ld_gra
     a.spin_limit = fail ? g_forced_spin_limit.load(std::memory_order_relaxed) : kSpinLimit;
     a.fix_tiles = static_cast<int>((D + kFusedCols - 1) / kFusedCols);
   }
-  hipError_t e;
-  if (gtype == LM_F32)
-    e = vec ? dispatch_nv<float, 4>(a, LMZ_SEG_NV_MAX, st) : dispatch_nv<float, 1>(a, 4, st);
-  else
-    e = vec ? dispatch_nv<bf16_t, 8>(a, LMZ_SEG_NV_MAX < 2 ? LMZ_SEG_NV_MAX : 2, st)
-            : dispatch_nv<bf16_t, 1>(a, 4, st);
+  const hipError_t e = sgd ? dispatch<true>(a, gtype, vec, st) : dispatch<false>(a, gtype, vec, st);
   if (e != hipSuccess) return launch_status(e);
   if (a.fused) return LM_OK;
-  const uint32_t fix_blocks = static_cast<uint32_t>((a.nchunks + kFixChunks - 1) / kFixChunks);
-  if (D % 4 == 0)
-    k_segsum_fix<4, LMZ_SEG_FIX_RF><<<dim3(fix_blocks, (D + 255) / 256), kFixThreads, 0, st>>>(a);
-  else
-    k_segsum_fix<1, LMZ_SEG_FIX_RF><<<dim3(fix_blocks, (D + 63) / 64), kFixThreads, 0, st>>>(a);
+  if (sgd) launch_fix<true>(a, st);
+  else launch_fix<false>(a, st);
   return launch_status(hipGetLastError());
 }
 

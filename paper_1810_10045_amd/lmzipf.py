@@ -66,6 +66,8 @@ def _load():
     L.lm_segsum.argtypes = [P, I32_, I64_, I64_, I64_, P, P, P, P, I64_, P, I64_, P, P, SZ, P]
     L.lm_segsum_rows.argtypes = [P, I32_, I64_, I64_, I64_, P, P, P, P, P, I32_, I64_, P, I64_, I64_,
                                  P, P, SZ, P]
+    L.lm_segsum_sgd.argtypes = [P, I32_, I64_, I64_, I64_, P, P, P, P, P, I32_, I64_, P, I64_, I64_,
+                                F, P, P, SZ, P]
     L.lm_map_ids.argtypes = [P, P, I64_, P, P, I64_, I32_, P, P, P]
     L.lm_fill_values.argtypes = [P, I64_, P, P, I64_, P, P, I32_, I64_, P, I64_, I64_, I32_, P, P]
     L.lm_sparse_apply.argtypes = [P, I64_, I64_, I64_, P, I32_, P, I64_, P, I64_, I32_,
@@ -78,7 +80,7 @@ def _load():
     L.lm_segsum_set_two_launches.argtypes = [I32_]
     L.lm_test_force_wait_failure.argtypes = [I32_, ctypes.c_uint32]
     for f in ("lm_abi_version", "lm_workspace_clear", "lm_unique", "lm_unique_noalloc",
-              "lm_segsum", "lm_segsum_rows", "lm_map_ids",
+              "lm_segsum", "lm_segsum_rows", "lm_segsum_sgd", "lm_map_ids",
               "lm_fill_values", "lm_sparse_apply", "lm_fill_values_f16", "lm_sparse_apply_f16",
               "lm_sample_ids", "lm_segsum_set_two_launches", "lm_test_force_wait_failure"):
         getattr(L, f).restype = ctypes.c_int
@@ -313,6 +315,36 @@ def segsum_rows(grad: torch.Tensor, perm: torch.Tensor, inverse: torch.Tensor,
                               row_ids.numel(), _ptr(out), out.shape[0], ld_out, _ptr(dev_err),
                               _ptr(buf), buf.numel(), _stream(stream)), "lm_segsum_rows")
     return out
+
+
+def segsum_sgd(grad: torch.Tensor, perm: torch.Tensor, inverse: torch.Tensor,
+               offsets: torch.Tensor, num_unique: torch.Tensor, row_ids: torch.Tensor,
+               table: torch.Tensor, lr: float, dev_err: Optional[torch.Tensor] = None,
+               ws: Optional[Workspace] = None, stream=None) -> torch.Tensor:
+    """lm_segsum_sgd: Sec. III-A steps 2 and 7 in one pass on one GPU:
+    table[row_ids[u]] -= lr * (type u's sum), in place; other rows are
+    untouched. Returns `table`."""
+    _dev(grad, "grad")
+    _dev(row_ids, "row_ids")
+    K, D = grad.shape
+    ld = _rows(grad, "grad")
+    if perm.numel() < K or inverse.numel() < K or offsets.numel() < 1:
+        raise LmError("perm and inverse must hold K entries")
+    if table.dim() != 2 or table.shape[1] != D or table.dtype != torch.float32:
+        raise LmError("table must be an fp32 matrix with D columns")
+    if not row_ids.is_contiguous():
+        raise LmError("row_ids must be contiguous")
+    ld_t = _rows(table, "table")
+    if dev_err is None:
+        dev_err = torch.zeros(1, dtype=torch.int32, device=grad.device)
+    ws = ws or default_workspace(grad.device)
+    buf = ws.get(_lib.lm_segsum_workspace_bytes(K, D))
+    _call(_lib.lm_segsum_sgd(_ptr(grad), _gtype(grad), K, D, ld, _ptr(perm), _ptr(inverse),
+                             _ptr(offsets), _ptr(num_unique), _ptr(row_ids), _idtype(row_ids),
+                             row_ids.numel(), _ptr(table), table.shape[0], ld_t, float(lr),
+                             _ptr(dev_err), _ptr(buf), buf.numel(), _stream(stream)),
+          "lm_segsum_sgd")
+    return table
 
 
 def map_ids(sub_ids: torch.Tensor, n_sub: torch.Tensor, sup_ids: torch.Tensor,

@@ -39,7 +39,8 @@ def test_test_hook_is_not_in_the_training_header():
 
 def test_header_declares_the_boundary():
     names = declared_functions()
-    for n in ("lm_unique", "lm_segsum", "lm_segsum_rows", "lm_fill_values", "lm_sparse_apply",
+    for n in ("lm_unique", "lm_segsum", "lm_segsum_rows", "lm_segsum_sgd", "lm_fill_values",
+              "lm_sparse_apply",
               "lm_map_ids", "lm_unique_workspace_bytes", "lm_segsum_workspace_bytes",
               "lm_status_string"):
         assert n in names
@@ -54,7 +55,8 @@ def test_binding_names_match_the_header():
     src = open(os.path.join(ROOT, "paper_1810_10045_amd", "lmzipf.py")).read()
     for n in declared_functions():
         assert f'"{n}"' in src, n
-    for n in ("unique", "segsum", "map_ids", "fill_values", "sparse_apply", "fill_values_f16",
+    for n in ("unique", "segsum", "segsum_rows", "segsum_sgd", "map_ids", "fill_values",
+              "sparse_apply", "fill_values_f16",
               "sparse_apply_f16", "sample_ids"):
         assert re.search(rf"^def {n}\(", src, re.M), n
 
@@ -63,7 +65,7 @@ def test_status_strings(lib):
     lib.lm_status_string.restype = ctypes.c_char_p
     for code in (0, 1, 3, 4, 5, 99):
         assert lib.lm_status_string(code)
-    assert lib.lm_abi_version() == 104
+    assert lib.lm_abi_version() == 105
 
 
 def test_workspace_queries(lib):
@@ -113,6 +115,18 @@ def test_argument_errors_return_before_any_launch(lib):
     assert rows(gtype=2) == 5 and rows(idtype=7) == 5 and rows(out_rows=1 << 31) == 5
     assert rows(ld_out=3) == 1 and rows(row_ids=None) == 1 and rows(rows_cap=-1) == 1
     assert rows(ws=_v(0x1010)) == 1 and rows(ws_bytes=8) == 3
+    lib.lm_segsum_sgd.argtypes = [P, I32, I64, I64, I64, P, P, P, P, P, I32, I64, P, I64, I64,
+                                  ctypes.c_float, P, P, SZ, P]
+
+    def sgd(gtype=0, idtype=0, rows_cap=10, row_ids=_v(), V=100, ld_table=4, table=_v(), ws=_v(),
+            ws_bytes=1 << 20):
+        return lib.lm_segsum_sgd(_v(), gtype, 10, 4, 4, _v(), _v(), _v(), _v(), row_ids, idtype,
+                                 rows_cap, table, V, ld_table, 0.1, _v(), ws, ws_bytes, None)
+    # the same argument errors, and a NULL table or a negative row count
+    assert sgd(gtype=2) == 5 and sgd(idtype=7) == 5 and sgd(V=1 << 31) == 5
+    assert sgd(ld_table=3) == 1 and sgd(row_ids=None) == 1 and sgd(rows_cap=-1) == 1
+    assert sgd(table=None) == 1 and sgd(V=-1) == 1
+    assert sgd(ws=_v(0x1010)) == 1 and sgd(ws_bytes=8) == 3
     lib.lm_fill_values.argtypes = [P, I64, P, P, I64, P, P, I32, I64, P, I64, I64, I32, P, P]
     assert lib.lm_fill_values(_v(), 4, _v(), _v(), 10, _v(), _v(), 0, 4, _v(), 10, 4, 9, _v(), None) == 5
     assert lib.lm_fill_values(_v(), 4, _v(), _v(), 10, None, None, 0, 4, _v(), 10, 4, 0, _v(), None) == 1

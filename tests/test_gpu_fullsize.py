@@ -10,7 +10,9 @@ very launches that bench.py times (its Batch and Pipeline, batch 0).
   list), bit-exact.
 * What follows Seg-Sum, end to end from the oracle's own sums: SCATTER into a
   dense table, done by Seg-Sum's own writes (lm_segsum_rows; against the
-  dense per-token scatter-add for the 100K x 512 case), SGD, the first lazy-Adam step (moments too, every touched row),
+  dense per-token scatter-add for the 100K x 512 case), SGD, applied by
+  Seg-Sum itself (lm_segsum_sgd; its sums read back from the same call with
+  lr = -1 on a zero table), the first lazy-Adam step (moments too, every touched row),
   EXPAND of shard 0 into the merged type list; rows the step must not touch
   are compared exactly.
 """

@@ -723,6 +723,134 @@ def test_segsum_rows_bad_row_id(lz, D):
     assert torch.equal(got[rest], base[rest]), "a type past rows_cap was written"
 
 
+SGD_CASES = [
+    # (K, V, s, D, grad dtype, id dtype, seed): the word step's ids over a
+    # 100K vocabulary (many segment ends per gather batch); rows of two
+    # 1024-column tiles in one launch (f32, and bf16 with int64 ids); rows
+    # not a multiple of 4 wide (the scalar path); rows wider than the
+    # one-launch form takes; one-workgroup Unique; a single token.
+    (65_536, 100_000, 1.0, 1024, "f32", np.int32, 161),
+    (60_000, 20_000, 1.2, 2048, "f32", np.int32, 162),
+    (40_000, 300, 1.2, 2048, "bf16", np.int64, 163),
+    (20_000, 3000, 1.0, 97, "f32", np.int32, 164),
+    (9000, 500, 1.0, 100, "bf16", np.int64, 165),
+    (4000, 100, 1.0, 5000, "f32", np.int32, 166),
+    (8192, 100_000, 1.0, 512, "f32", np.int32, 167),
+    (1, 5, 1.0, 16, "f32", np.int32, 168),
+]
+
+
+@pytest.mark.parametrize("K,V,s,D,gdt,dt,seed", SGD_CASES,
+                         ids=[f"K{c[0]}-V{c[1]}-D{c[3]}-{c[4]}-{np.dtype(c[5]).name}"
+                              for c in SGD_CASES])
+def test_segsum_sgd_is_segsum_then_sgd(lz, K, V, s, D, gdt, dt, seed):
+    """lm_segsum_sgd on a V x D table with row_ids = uniq: the same table, bit
+    for bit, as lm_segsum followed by lm_sparse_apply SGD with the same lr
+    (each launch form against lm_segsum in that form); the updated rows match
+    the oracle's Seg-Sum and SGD; every other row keeps its value."""
+    _say(f"segsum_sgd K={K} V={V} D={D} {gdt} {np.dtype(dt).name}")
+    ids, grad, tgrad, res = _rows_case(lz, K, V, s, D, gdt, dt, seed)
+    lr = float(np.float32(0.1))
+    p0 = synth.normal_rows(V, D, seed + 2000)
+    base = _t(p0)
+
+    def both():
+        out = lz.segsum(tgrad, res.perm, res.inverse, res.offsets, res.num_unique,
+                        dev_err=res.dev_err)
+        want = base.clone()
+        lz.sparse_apply(want, res.uniq, res.num_unique, out, "sgd", lr=lr, dev_err=res.dev_err)
+        got = base.clone()
+        lz.segsum_sgd(tgrad, res.perm, res.inverse, res.offsets, res.num_unique, res.uniq, got,
+                      lr, dev_err=res.dev_err)
+        return want, got
+
+    want, got = both()
+    assert lz.segsum_two_launches(True) is False
+    try:
+        want2, got2 = both()
+        torch.cuda.synchronize()
+    finally:
+        assert lz.segsum_two_launches(False) is True
+    lz.check(res.dev_err)
+    o = H.assert_unique_matches(res, ids, V, oracle)
+    U = len(o[0])
+    assert torch.equal(got, want), "not the table of lm_segsum + lm_sparse_apply SGD"
+    assert torch.equal(got2, want2), "two-launch form: not lm_segsum + lm_sparse_apply SGD"
+    rows_t = _t(o[0].astype(np.int64))
+    touched = torch.zeros(V, dtype=torch.bool, device=DEV)
+    touched[rows_t] = True
+    assert torch.equal(got[~touched], base[~touched]), "a row no type names was updated"
+    S = oracle.segsum(grad, o[3], U)
+    sq = H.sum_of_squares(grad, o[3], U, oracle)
+    ref = oracle.sgd(p0[o[0]], S, lr)
+    H.assert_sgd_rows(got[rows_t].cpu().numpy(), ref, S, lr, H.row_delta(S, H.TOL_F32, sq))
+
+
+@pytest.mark.parametrize("D", [512, 2048, 5000])
+def test_segsum_sgd_minus_one_on_zeros_is_segsum_rows(lz, D):
+    """With lr = -1 on a zero table each updated row is 0 + 1 * sum, which
+    rounds to the sum itself: lm_segsum_rows's table, bit for bit."""
+    K, V = 30_000, 2000
+    _say(f"segsum_sgd lr=-1 D={D}")
+    ids, grad, tgrad, res = _rows_case(lz, K, V, 1.2, D, "f32", np.int32, 171)
+    want = torch.zeros((V, D), device=DEV)
+    lz.segsum_rows(tgrad, res.perm, res.inverse, res.offsets, res.num_unique, res.uniq, want,
+                   dev_err=res.dev_err)
+    got = torch.zeros((V, D), device=DEV)
+    lz.segsum_sgd(tgrad, res.perm, res.inverse, res.offsets, res.num_unique, res.uniq, got, -1.0,
+                  dev_err=res.dev_err)
+    torch.cuda.synchronize()
+    lz.check(res.dev_err)
+    assert torch.equal(got, want)
+
+
+@pytest.mark.parametrize("D", [512, 2048, 5000])
+def test_segsum_sgd_bad_row_id(lz, D):
+    """A row id outside [0, V) sets LM_DEVERR_ID_RANGE and leaves that row
+    as it was, as lm_sparse_apply does; the other rows are updated as usual.
+    The longest type (finished by the fix-up) and a short one (finished in
+    the walk); then rows_cap below the number of types: the capacity
+    error, and only the first rows_cap types are applied."""
+    K, V = 30_000, 2000
+    _say(f"segsum_sgd bad ids D={D}")
+    ids, grad, tgrad, res = _rows_case(lz, K, V, 1.2, D, "f32", np.int64, 172)
+    U = int(res.num_unique.item())
+    counts = res.counts[:U].cpu().numpy()
+    head, short = int(np.argmax(counts)), int(np.argmin(counts))
+    lr = 0.25
+    # lm_segsum with u_cap = rows_cap: the same chunks, so the same sums
+    out = lz.segsum(tgrad, res.perm, res.inverse, res.offsets, res.num_unique, u_cap=U,
+                    dev_err=res.dev_err)
+    base = _t(synth.normal_rows(V, D, 173))
+    uniq = res.uniq[:U].clone()
+    for bad_u, bad_id in ((head, V), (short, V + 99), (short, -1)):
+        rid = uniq.clone()
+        rid[bad_u] = bad_id
+        e_want = torch.zeros(1, dtype=torch.int32, device=DEV)
+        want = base.clone()
+        lz.sparse_apply(want, rid, res.num_unique, out, "sgd", lr=lr, dev_err=e_want)
+        err = torch.zeros(1, dtype=torch.int32, device=DEV)
+        got = base.clone()
+        lz.segsum_sgd(tgrad, res.perm, res.inverse, res.offsets, res.num_unique, rid, got, lr,
+                      dev_err=err)
+        torch.cuda.synchronize()
+        assert int(err.item()) == lz.DEVERR_ID_RANGE == int(e_want.item()), (bad_u, bad_id)
+        assert torch.equal(got, want)
+    e10 = torch.zeros(1, dtype=torch.int32, device=DEV)
+    out10 = lz.segsum(tgrad, res.perm, res.inverse, res.offsets, res.num_unique, u_cap=10,
+                      out=torch.empty((10, D), device=DEV), dev_err=e10)
+    want = base.clone()
+    lz.sparse_apply(want, uniq[:10].clone(), torch.tensor([10], dtype=torch.int64, device=DEV),
+                    out10, "sgd", lr=lr, dev_err=torch.zeros(1, dtype=torch.int32, device=DEV))
+    err = torch.zeros(1, dtype=torch.int32, device=DEV)
+    got = base.clone()
+    lz.segsum_sgd(tgrad, res.perm, res.inverse, res.offsets, res.num_unique, uniq[:10].clone(),
+                  got, lr, dev_err=err)
+    torch.cuda.synchronize()
+    assert int(err.item()) == lz.DEVERR_CAPACITY == int(e10.item())
+    assert torch.equal(got, want)
+
+
 # ---------------------------------------------------------------------------
 # Map, Fill-Values, the G-shard merge
 # ---------------------------------------------------------------------------
