@@ -87,6 +87,12 @@ namespace lmz {
 #ifndef LMZ_SEG_RF2_LONG
 #define LMZ_SEG_RF2_LONG 16
 #endif
+#ifndef LMZ_SEG_SGD_ENDS
+#define LMZ_SEG_SGD_ENDS 2           // lm_segsum_sgd: segment ends (table rows) per gather batch
+#endif
+#ifndef LMZ_SEG_SGD_RF4
+#define LMZ_SEG_SGD_RF4 3            // lm_segsum_sgd: rows per batch with 4 vectors per lane,
+#endif                               // chunks below LMZ_SEG_LONG_R (others as lm_segsum)
 #ifndef LMZ_SEG_NV_MAX
 #define LMZ_SEG_NV_MAX 4             // 16-byte vectors per lane per row (fp32)
 #endif
@@ -628,6 +634,8 @@ __global__ __launch_bounds__(NTHR) void k_segsum(SegArgs a) {
   }
   const GT* __restrict__ grad = static_cast<const GT*>(a.grad);
   bool bad_row = false;
+  constexpr int kEnds = SGD ? LMZ_SEG_SGD_ENDS : 1;
+  static_assert(kEnds >= 1 && kEnds <= RF, "table rows per batch");
 
   float acc[NV][VEC];
 #pragma unroll
@@ -642,20 +650,22 @@ __global__ __launch_bounds__(NTHR) void k_segsum(SegArgs a) {
     const int hi = q_end - wbase < kWave ? q_end - wbase : kWave;
     for (int j0 = lo; j0 < hi;) {
       int n = hi - j0 < RF ? hi - j0 : RF;
-      // SGD: at most two segment ends per batch (bm: their bits), whose
+      // SGD: at most kEnds segment ends per batch (bm: their bits), whose
       // table rows load with the batch's gradient rows.
       uint64_t bm = 0;
-      float tb[2][NV][VEC];
+      float tb[kEnds][NV][VEC];
       if constexpr (SGD) {
         bm = (ends[w] >> j0) & ((uint64_t(1) << n) - 1);
-        const uint64_t m1 = bm & (bm - 1), m2 = m1 & (m1 - 1);
-        if (m2) {
-          n = __builtin_ctzll(m2);
+        uint64_t past = bm;  // the ends after the first kEnds
+#pragma unroll
+        for (int k = 0; k < kEnds; ++k) past &= past - 1;
+        if (past) {
+          n = __builtin_ctzll(past);
           bm &= (uint64_t(1) << n) - 1;
         }
         uint64_t mm = bm;
 #pragma unroll
-        for (int k = 0; k < 2; ++k) {
+        for (int k = 0; k < kEnds; ++k) {
           int64_t orow = -1;  // no row: a partial row, a type past u_cap, a bad id, no end
           if (mm) {
             const int j = j0 + __builtin_ctzll(mm);
@@ -702,13 +712,17 @@ __global__ __launch_bounds__(NTHR) void k_segsum(SegArgs a) {
               dst = (s >= 0 && s < a.u_cap && orow >= 0) ? a.out + orow * a.ld_out : nullptr;
             }
             if constexpr (SGD) {
-              if (!part) {  // the batch's first or second end: table row 0 or 1
-                const bool second = (bm & ((uint64_t(1) << (j - j0)) - 1)) != 0;
+              if (!part) {  // the batch's k-th end: table row k
+                const int k = __popcll(bm & ((uint64_t(1) << (j - j0)) - 1));
 #pragma unroll
                 for (int v = 0; v < NV; ++v)
 #pragma unroll
-                  for (int e = 0; e < VEC; ++e)
-                    acc[v][e] = (second ? tb[1][v][e] : tb[0][v][e]) - a.lr * acc[v][e];
+                  for (int e = 0; e < VEC; ++e) {
+                    float t = tb[0][v][e];
+#pragma unroll
+                    for (int x = 1; x < kEnds; ++x) t = k == x ? tb[x][v][e] : t;
+                    acc[v][e] = t - a.lr * acc[v][e];
+                  }
               }
             }
             if (dst) {
@@ -882,6 +896,15 @@ constexpr int rf_for() {
                  : (R >= LMZ_SEG_LONG_R ? LMZ_SEG_RF2_LONG : LMZ_SEG_RF2);
 }
 
+// lm_segsum_sgd's rows per batch, whose table rows take registers too.
+// Measured at 65,536 ids over 800K words, D = 1024 (at most two ends per
+// batch): 3 rows 98.4 us per call, 2 rows 99-101, 4 rows (lm_segsum's) 102,
+// 5 rows 106; one end per batch 118 us with 4 rows, 111 with 3.
+template <int NV, int R>
+constexpr int rf_sgd_for() {
+  return NV >= 4 && R < LMZ_SEG_LONG_R ? LMZ_SEG_SGD_RF4 : rf_for<NV, R>();
+}
+
 // Multiprocessors of the current device (queried once per device).
 static int device_cus() {
   static std::atomic<int> cus[64];
@@ -958,7 +981,8 @@ static int whole_rounds(int nchunks, int tiles, int64_t waves_per_round, int max
 
 template <typename GT, int VEC, int NV, int R, bool SGD>
 static void launch_one(SegArgs& a, int tiles, hipStream_t st) {
-  constexpr int RF = rf_for<NV, R>(), T = t_for<R>();
+  constexpr int RFp = rf_for<NV, R>(), T = t_for<R>();
+  constexpr int RF = SGD ? rf_sgd_for<NV, R>() : RFp;
   a.tiles = tiles;
   a.tile_cols = NV * kWave * VEC;
   // The rounds are those of the plain kernel (SGD false) for the SGD
@@ -969,7 +993,7 @@ static void launch_one(SegArgs& a, int tiles, hipStream_t st) {
       auto k = k_segsum<GT, VEC, NV, RF, R, T, kFusedThreads, true, SGD>;
       static std::atomic<int> bpc{-1};
       const int64_t room =
-          int64_t(blocks_per_cu(k_segsum<GT, VEC, NV, RF, R, T, kFusedThreads, true, false>,
+          int64_t(blocks_per_cu(k_segsum<GT, VEC, NV, RFp, R, T, kFusedThreads, true, false>,
                                 kFusedThreads, 0, bpc)) *
           kFusedWaves * stream_cus(st);
       a.nchunks = whole_rounds(a.nchunks, tiles, room, a.max_chunks);
@@ -982,7 +1006,7 @@ static void launch_one(SegArgs& a, int tiles, hipStream_t st) {
   auto k = k_segsum<GT, VEC, NV, RF, R, T, kSegThreads, false, SGD>;
   static std::atomic<int> bpc{-1};
   const int64_t room =
-      int64_t(blocks_per_cu(k_segsum<GT, VEC, NV, RF, R, T, kSegThreads, false, false>,
+      int64_t(blocks_per_cu(k_segsum<GT, VEC, NV, RFp, R, T, kSegThreads, false, false>,
                             kSegThreads, LMZ_SEG_LDS_PAD, bpc)) *
       kSegWaves * stream_cus(st);
   a.nchunks = whole_rounds(a.nchunks, tiles, room, a.max_chunks);
