@@ -3,9 +3,10 @@ reference rates of plain memory patterns on the same shapes (one GPU).
 
 Per entry point (default mode). For each workload, each stage of the step
 (Unique; Seg-Sum; the stage after it: the apply, SCATTER or the merge's
-EXPAND; where the step is a SCATTER into a dense table, also
-lm_segsum_rows, which does Seg-Sum and the SCATTER in one call) is timed on
-its own, with HIP events on the launch stream around just that stage:
+EXPAND; where the step is a SCATTER into a dense table or an SGD update,
+also lm_segsum_rows or lm_segsum_sgd, which does Seg-Sum and that update in
+one call) is timed on its own, with HIP events on the launch stream around
+just that stage:
 
   cold  before every timed rep, a 1 GiB buffer is read, which leaves nothing
         of the inputs in the 256 MB Infinity Cache or the L2s (read, not
@@ -17,8 +18,8 @@ its own, with HIP events on the launch stream around just that stage:
 Each is 5 untimed reps, then --reps timed ones; the table gives the median,
 10th and 90th percentile in microseconds, Seg-Sum's algorithmic GB/s and its
 fraction of the 8 TB/s HBM peak (from the median), and tokens/s = K / the sum
-of the cold medians of the step's stages (Unique and lm_segsum_rows where
-the SCATTER is fused).
+of the cold medians of the step's stages (Unique and the fused call where
+the SCATTER or SGD is fused).
 
 Ceilings (--ceilings). Plain torch operations on a workload's shapes (its K
 gradient rows of D fp32, its U types), each rep on the next of several
@@ -127,7 +128,7 @@ def calls_table(w, U, res, seg_cold, seg_warm):
              "|---|---|---|---|---|---|---|"]
     for name in STAGES + (("rows",) if fused else ()):
         c, h = pct(res[("cold", name)]), pct(res[("warm", name)])
-        label = {"after": w.step, "rows": "segsum_rows (segsum + scatter)"}.get(name, name)
+        label = {"after": w.step, "rows": bench.fused_stage(w)}.get(name, name)
         lines.append(f"| {label} | {c[0]:.1f} | {c[1]:.1f} | {c[2]:.1f} | {h[0]:.1f} | {h[1]:.1f} | "
                      f"{h[2]:.1f} |")
     sc, sw = np.median(res[("cold", "segsum")]), np.median(res[("warm", "segsum")])
@@ -139,10 +140,14 @@ def calls_table(w, U, res, seg_cold, seg_warm):
               f"{w.tokens / step * 1e6 / 1e6:,.1f} M tokens/s.", ""]
     if fused:
         ib = 8 if w.id_dtype == "i64" else 4
-        rb = seg_cold + np.mean(U) * ib  # the row ids too
+        # the row ids too, and with SGD the table rows read before they are written
+        rb = seg_cold + np.mean([bench.fused_extra_bytes(w, w.D, u, ib) for u in U])
         rc = rb / np.median(res[("cold", "rows")]) / 1e3
-        lines[-1:-1] = [f"segsum_rows: {rb / 1e6:.1f} MB algorithmic per call (Seg-Sum's and the "
-                        f"U row ids); cold {rc:,.0f} GB/s (frac {rc / bench.HBM_PEAK_GBPS:.3f})."]
+        what = ("the U row ids" if w.step == "scatter" else
+                "the U row ids and the U table rows read before they are written")
+        lines[-1:-1] = [f"{bench.fused_stage(w).split()[0]}: {rb / 1e6:.1f} MB algorithmic per call "
+                        f"(Seg-Sum's, {what}); cold {rc:,.0f} GB/s "
+                        f"(frac {rc / bench.HBM_PEAK_GBPS:.3f})."]
     return "\n".join(lines)
 
 
