@@ -3,10 +3,10 @@
 One step = one pass of the whole path over one batch of synthetic tokens
 already resident in HBM:
     Unique (lm_unique) -> Seg-Sum (lm_segsum) -> Fill-Values / update
-(Adam via lm_sparse_apply, EXPAND into the merged type list via
-lm_fill_values, by workload; a SCATTER into a dense table and an SGD update
-are done by Seg-Sum itself: lm_segsum_rows writes each type's row to its
-table row, lm_segsum_sgd applies it there). The
+(EXPAND into the merged type list via lm_fill_values, by workload; a
+SCATTER into a dense table and an SGD or Adam update are done by Seg-Sum
+itself: lm_segsum_rows writes each type's row to its table row,
+lm_segsum_sgd and lm_segsum_adam apply it there). The
 headline workload is the largest one with fp32 gradients: K = 1,048,576
 Zipf(1.2) token ids over a 20K character vocabulary, 2048-wide fp32
 gradients (8 GiB per batch), the U reduced rows written into the dense
@@ -20,8 +20,8 @@ trainer has before the gradients exist); every step still does all of its
 work. At the char-LM and 2M-vocabulary workloads the two streams run on
 disjoint CUs (CU-masked streams, SIDE_CUS); the same schedule on shared
 CUs is printed beside it (`overlapped_all_cus`). The serial schedule (one stream) is timed too and printed beside it,
-and for the SCATTER and SGD workloads also the serial schedule with that
-update as a call of its own after lm_segsum (`unfused_serial`).
+and for the SCATTER, SGD and Adam workloads also the serial schedule with
+that update as a call of its own after lm_segsum (`unfused_serial`).
 
 Prints one JSON line: tokens/s, ms per step, the Seg-Sum roofline (algorithmic
 bytes per lm_segsum call / its average duration from HIP events on the launch
@@ -95,18 +95,20 @@ AFTER_ROWS = {"sgd": 3, "softmax_sgd": 3, "adam": 7, "scatter": 2}
 
 # Steps done by the Seg-Sum call itself (lm_segsum_rows, lm_segsum_sgd), and
 # the name of that fused stage.
-FUSED_STEPS = ("scatter", "sgd", "softmax_sgd")
+FUSED_STEPS = ("scatter", "sgd", "softmax_sgd", "adam")
 
 
 def fused_stage(w):
-    return ("segsum_rows (segsum + scatter)" if w.step == "scatter"
-            else "segsum_sgd (segsum + sgd)")
+    return ("segsum_rows (segsum + scatter)" if w.step == "scatter" else
+            "segsum_adam (segsum + adam)" if w.step == "adam" else "segsum_sgd (segsum + sgd)")
 
 
 def fused_extra_bytes(w, D, U, id_bytes):
-    """Bytes a fused call moves beyond lm_segsum's: the U row ids, and for
-    SGD the table rows it reads before it writes them."""
-    return U * id_bytes + (U * D * 4 if w.step != "scatter" else 0)
+    """Bytes a fused call moves beyond lm_segsum's: the U row ids; for SGD
+    the table rows it reads before it writes them; for Adam the parameter
+    rows read, and the m and v rows read and written."""
+    rows = {"scatter": 0, "adam": 5}.get(w.step, 1)
+    return U * id_bytes + rows * U * D * 4
 
 
 class HipEvents:
@@ -222,15 +224,20 @@ class Pipeline:
         self.fused = w.step in FUSED_STEPS
         self.last = None
 
-    def reduce(self, bt, ures, err):
+    def reduce(self, bt, ures, err, t=1):
         """Seg-Sum of batch bt from Unique outputs ures: into `out`, or with
-        `fused`, straight into the table rows of the types (SCATTER or SGD
-        done)."""
+        `fused`, straight into the table rows of the types (SCATTER, SGD or
+        Adam step t done)."""
         w, lz, st = self.w, self.lz, self.state
         self.last = (bt, ures, err)
         if self.fused and w.step == "scatter":
             lz.segsum_rows(bt.grad, ures.perm, ures.inverse, ures.offsets, ures.num_unique,
                            ures.uniq, st["table"], dev_err=err, ws=self.ws)
+        elif self.fused and w.step == "adam":
+            b1, b2, eps = w.adam
+            lz.segsum_adam(bt.grad, ures.perm, ures.inverse, ures.offsets, ures.num_unique,
+                           ures.uniq, st["table"], st["m"], st["v"], lr=w.lr, beta1=b1,
+                           beta2=b2, eps=eps, step=t, dev_err=err, ws=self.ws)
         elif self.fused:
             lz.segsum_sgd(bt.grad, ures.perm, ures.inverse, ures.offsets, ures.num_unique,
                           ures.uniq, st["table"], w.lr, dev_err=err, ws=self.ws)
@@ -242,9 +249,19 @@ class Pipeline:
         """The U reduced rows of the last step, in type order: from the table
         when the SCATTER was fused into Seg-Sum; with SGD fused, from the same
         call with lr = -1 on a zero table, where each row is 0 + 1 * sum,
-        the sum itself."""
+        the sum itself; with Adam fused, from the same call with beta1 = 0
+        on zero tables, where each m row is 0 * 0 + 1 * sum."""
         if self.fused and self.w.step == "scatter":
             return self.state["table"][self.ures.uniq[:U].long()]
+        if self.fused and self.w.step == "adam":
+            bt, ures, err = self.last
+            p, m, v = (self.torch.zeros_like(self.state["table"]) for _ in range(3))
+            self.lz.segsum_adam(bt.grad, ures.perm, ures.inverse, ures.offsets, ures.num_unique,
+                                ures.uniq, p, m, v, lr=0.0, beta1=0.0, step=1, dev_err=err,
+                                ws=self.ws)
+            rows = m[ures.uniq[:U].long()]
+            del p, m, v
+            return rows
         if self.fused:
             bt, ures, err = self.last
             z = self.torch.zeros_like(self.state["table"])
@@ -292,11 +309,11 @@ class Pipeline:
         bt = self.batches[b % len(self.batches)]
         ures, u0 = self.sets[j]
         err = ures.dev_err
-        self.reduce(bt, ures, err)
+        self.reduce(bt, ures, err, 1 + b)
         if w.step in ("sgd", "softmax_sgd") and not self.fused:
             lz.sparse_apply(st["table"], ures.uniq, ures.num_unique, self.out, "sgd", lr=w.lr,
                             dev_err=err)
-        elif w.step == "adam":
+        elif w.step == "adam" and not self.fused:
             b1, b2, eps = w.adam
             lz.sparse_apply(st["table"], ures.uniq, ures.num_unique, self.out, "adam", lr=w.lr,
                             beta1=b1, beta2=b2, eps=eps, step=1 + b, m=st["m"], v=st["v"],
@@ -347,12 +364,12 @@ class Pipeline:
             lz.sample_ids(bt.words, w.V, out=bt.ids[:w.shards * w.samples])
         lz.unique(bt.ids, w.V, out=ures, ws=self.ws)
         if ev: ev(1)
-        self.reduce(bt, ures, err)
+        self.reduce(bt, ures, err, 1 + b)
         if ev: ev(2)
         if w.step in ("sgd", "softmax_sgd") and not self.fused:
             lz.sparse_apply(st["table"], ures.uniq, ures.num_unique, self.out, "sgd", lr=w.lr,
                             dev_err=err)
-        elif w.step == "adam":
+        elif w.step == "adam" and not self.fused:
             b1, b2, eps = w.adam
             lz.sparse_apply(st["table"], ures.uniq, ures.num_unique, self.out, "adam", lr=w.lr,
                             beta1=b1, beta2=b2, eps=eps, step=1 + b, m=st["m"], v=st["v"],
@@ -756,17 +773,18 @@ def copy_calibration(torch, reps=3):
 
 
 def segsum_kernels(w, fused=False):
-    """The kernels of one lm_segsum (or, fused with SCATTER or SGD,
-    lm_segsum_rows or lm_segsum_sgd) call at this workload's shape (rows of
-    up to 4096 columns on the 16-byte path: one launch)."""
-    name = ("lm_segsum" if not fused else
-            "lm_segsum_rows" if w.step == "scatter" else "lm_segsum_sgd")
+    """The kernels of one lm_segsum (or, fused with SCATTER, SGD or Adam,
+    lm_segsum_rows, lm_segsum_sgd or lm_segsum_adam) call at this workload's
+    shape (rows of up to 4096 columns on the 16-byte path: one launch)."""
+    name = ("lm_segsum" if not fused else "lm_segsum_rows" if w.step == "scatter" else
+            "lm_segsum_adam" if w.step == "adam" else "lm_segsum_sgd")
     k = (SEGSUM_KERNELS if w.D <= 4096 else "lm_segsum (k_segsum walk, then k_segsum_fix)")
     k = k.replace("lm_segsum", name, 1)
     if not fused:
         return k
-    return k + (", each type row written to its table row" if w.step == "scatter"
-                else ", each type row applied to its table row (SGD)")
+    return k + (", each type row written to its table row" if w.step == "scatter" else
+                ", each type row applied to its table row (Adam, with its m and v rows)"
+                if w.step == "adam" else ", each type row applied to its table row (SGD)")
 
 
 def stages(w, r):
@@ -783,7 +801,8 @@ def unfused_entry(w, r):
     u = r["unfused"]
     if not u:
         return None
-    then = "lm_fill_values SCATTER" if w.step == "scatter" else "lm_sparse_apply SGD"
+    then = {"scatter": "lm_fill_values SCATTER", "adam": "lm_sparse_apply Adam"}.get(
+        w.step, "lm_sparse_apply SGD")
     return {"value": u["value"], "ms_per_step": u["ms_per_step"],
             "stages_ms": {"unique": u["stage_ms"][0], "segsum": u["stage_ms"][1],
                           w.step: u["stage_ms"][2]},

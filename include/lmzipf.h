@@ -247,9 +247,37 @@ int lm_segsum_sgd(const void* grad, int32_t gtype, int64_t K, int64_t D, int64_t
                   int64_t rows_cap, float* table, int64_t V, int64_t ld_table, float lr,
                   int32_t* dev_err, void* ws, size_t ws_bytes, void* stream);
 
-/* The one-launch form of lm_segsum (and lm_segsum_rows, lm_segsum_sgd)
- * relies on the hardware starting the walk's workgroups before the fix-up
- * workgroups that wait on them (they come first in the grid). lm_segsum_set_two_launches(1)
+/* ------------------------------------------------------------------------
+ * Seg-Sum with the lazy-Adam update — Sec. III-A steps 2 and 7 in one pass
+ * on one GPU: the step of lm_sparse_apply with LM_OPT_ADAM on the rows
+ * row_ids names, with type u's sum as the gradient of row row_ids[u]:
+ *     g = sum over i in [offsets[u], offsets[u+1]) of grad[perm[i], :]
+ *     m = beta1 m + (1 - beta1) g,  v = beta2 v + (1 - beta2) g^2,
+ *     E -= lr (m / (1 - beta1^step) / (sqrt(v / (1 - beta2^step)) + eps)
+ *              + weight_decay E),
+ * on E = table[row_ids[u], :] and the m and v rows of the same index,
+ * bit-identical to lm_segsum (u_cap = rows_cap, the same launch form, on a
+ * stream with the same compute units) followed by lm_sparse_apply with
+ * LM_OPT_ADAM and the same arguments, without the U x D intermediate. Rows
+ * that no type names are left untouched in all three arrays.
+ *
+ * m, v       device, V x D fp32 with the table's row stride, updated in
+ *            place.
+ * step       >= 1 (the bias corrections); beta1, beta2 in [0, 1).
+ * The other arguments and their errors are those of lm_segsum_sgd.
+ * ------------------------------------------------------------------------ */
+int lm_segsum_adam(const void* grad, int32_t gtype, int64_t K, int64_t D, int64_t ld_grad,
+                   const int32_t* perm, const int32_t* inverse, const int32_t* offsets,
+                   const int64_t* num_unique, const void* row_ids, int32_t idtype,
+                   int64_t rows_cap, float* table, int64_t V, int64_t ld_table, float lr,
+                   float beta1, float beta2, float eps, float weight_decay, int64_t step,
+                   float* m, float* v, int32_t* dev_err, void* ws, size_t ws_bytes,
+                   void* stream);
+
+/* The one-launch form of lm_segsum (and lm_segsum_rows, lm_segsum_sgd,
+ * lm_segsum_adam) relies on the hardware starting the walk's workgroups
+ * before the fix-up workgroups that wait on them (they come first in the
+ * grid). lm_segsum_set_two_launches(1)
  * makes every later call in the process use the two-launch form instead
  * (the walk, then a separate fix-up kernel: no workgroup ever waits on
  * another), the fallback should a

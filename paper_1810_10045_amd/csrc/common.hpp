@@ -383,6 +383,64 @@ __device__ __forceinline__ int64_t lower_bound_wave(const KeyT* a, int64_t n, Ke
   return lo;
 }
 
+// ---------------------------------------------------------------------------
+// The update of Sec. III-A step 7 on one fp32 value. lm_sparse_apply and the
+// Seg-Sum entry points that apply their sums themselves call these same
+// functions, so they round alike, bit for bit.
+// ---------------------------------------------------------------------------
+#ifndef LMZ_ADAM_HW_MATH
+#define LMZ_ADAM_HW_MATH 0
+#endif
+
+struct OptParams {
+  float lr, b1, b2, eps, wd, inv_c1, inv_c2, g_scale;
+};
+
+// Every multiply-add is an explicit fused one: left to the compiler, a sum
+// of two products (b1 * m + (1 - b1) * g) may be fused either way round, and
+// the choice can differ between the kernels that inline these functions.
+__device__ __forceinline__ void sgd_value(float& p, float g, const OptParams& o) {
+  p = __builtin_fmaf(-o.lr, g, p);
+}
+
+// Lazy Adam on a touched value: the moments, then the bias-corrected step
+// with decoupled weight decay (inv_c1, inv_c2: 1 / (1 - beta^t)).
+__device__ __forceinline__ void adam_value(float& p, float& m, float& v, float g,
+                                           const OptParams& o) {
+  m = __builtin_fmaf(o.b1, m, (1.f - o.b1) * g);
+  v = __builtin_fmaf(o.b2, v, (1.f - o.b2) * g * g);
+  const float mhat = m * o.inv_c1;
+  const float vhat = v * o.inv_c2;
+#if LMZ_ADAM_HW_MATH
+  // v_sqrt_f32 and v_rcp_f32 (about 1 ulp each) instead of the correctly
+  // rounded sequences.
+  const float step = mhat * __builtin_amdgcn_rcpf(__builtin_amdgcn_sqrtf(vhat) + o.eps);
+#else
+  const float step = mhat / (sqrtf(vhat) + o.eps);
+#endif
+  p = __builtin_fmaf(-o.lr, __builtin_fmaf(o.wd, p, step), p);
+}
+
+// The step's parameters; the bias corrections are computed once on the host
+// in double.
+static inline OptParams make_opt_params(bool adam, float lr, float beta1, float beta2, float eps,
+                                        float weight_decay, int64_t step, float g_scale) {
+  OptParams o{};
+  o.lr = lr;
+  o.b1 = beta1;
+  o.b2 = beta2;
+  o.eps = eps;
+  o.wd = weight_decay;
+  o.g_scale = g_scale;
+  if (adam) {
+    o.inv_c1 = static_cast<float>(
+        1.0 / (1.0 - __builtin_pow(static_cast<double>(beta1), static_cast<double>(step))));
+    o.inv_c2 = static_cast<float>(
+        1.0 / (1.0 - __builtin_pow(static_cast<double>(beta2), static_cast<double>(step))));
+  }
+  return o;
+}
+
 }  // namespace lmz
 
 // Host-side launch helpers (defined in lmzipf_api.hip).

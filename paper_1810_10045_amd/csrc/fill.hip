@@ -26,9 +26,6 @@ constexpr int kZeroRows = LMZ_ZERO_ROWS;
 #ifndef LMZ_ZERO_NT
 #define LMZ_ZERO_NT 1                // non-temporal stores for the zero fill
 #endif
-#ifndef LMZ_ADAM_HW_MATH
-#define LMZ_ADAM_HW_MATH 0
-#endif
 
 template <typename KeyT>
 __device__ __forceinline__ int64_t find_row(const KeyT* __restrict__ ids, int64_t n, KeyT x) {
@@ -255,11 +252,9 @@ __global__ __launch_bounds__(kFillThreads) void k_scatter_h(
 }
 
 // ---------------------------------------------------------------------------
-// Sparse apply (step 7): one wave per touched row.
+// Sparse apply (step 7): one wave per touched row (the update of each value:
+// sgd_value, adam_value).
 // ---------------------------------------------------------------------------
-struct OptParams {
-  float lr, b1, b2, eps, wd, inv_c1, inv_c2, g_scale;
-};
 
 // ValT float: fp32 gradients; ValT uint16_t: the binary16 payload of
 // Sec. III-C, each value multiplied by o.g_scale (1/F) after the up-cast.
@@ -299,23 +294,8 @@ __global__ __launch_bounds__(kFillThreads) void k_apply(
       for (int j = 0; j < NV; ++j) {
 #pragma unroll
         for (int e = 0; e < VEC; ++e) {
-          if constexpr (ADAM) {
-            const float gg = gr[j][e];
-            mr[j][e] = o.b1 * mr[j][e] + (1.f - o.b1) * gg;
-            vr[j][e] = o.b2 * vr[j][e] + (1.f - o.b2) * gg * gg;
-            const float mhat = mr[j][e] * o.inv_c1;
-            const float vhat = vr[j][e] * o.inv_c2;
-#if LMZ_ADAM_HW_MATH
-            // v_sqrt_f32 and v_rcp_f32 (about 1 ulp each) instead of the
-            // correctly rounded sequences.
-            const float den = __builtin_amdgcn_sqrtf(vhat) + o.eps;
-            pr[j][e] -= o.lr * (mhat * __builtin_amdgcn_rcpf(den) + o.wd * pr[j][e]);
-#else
-            pr[j][e] -= o.lr * (mhat / (sqrtf(vhat) + o.eps) + o.wd * pr[j][e]);
-#endif
-          } else {
-            pr[j][e] -= o.lr * gr[j][e];
-          }
+          if constexpr (ADAM) adam_value(pr[j][e], mr[j][e], vr[j][e], gr[j][e], o);
+          else sgd_value(pr[j][e], gr[j][e], o);
         }
         if (pc.ok[j]) {
           store_vec<VEC>(p + pc.col[j], pr[j]);
@@ -437,19 +417,7 @@ static hipError_t apply_launch(float* table, int64_t V, int64_t D, int64_t ld_ta
 
 static OptParams opt_params(int opt, float lr, float beta1, float beta2, float eps,
                             float weight_decay, int64_t step, float g_scale) {
-  OptParams o{};
-  o.lr = lr;
-  o.b1 = beta1;
-  o.b2 = beta2;
-  o.eps = eps;
-  o.wd = weight_decay;
-  o.g_scale = g_scale;
-  if (opt == LM_OPT_ADAM) {
-    // Bias corrections 1 - beta^t, computed once on the host in double.
-    o.inv_c1 = static_cast<float>(1.0 / (1.0 - __builtin_pow(static_cast<double>(beta1), static_cast<double>(step))));
-    o.inv_c2 = static_cast<float>(1.0 / (1.0 - __builtin_pow(static_cast<double>(beta2), static_cast<double>(step))));
-  }
-  return o;
+  return make_opt_params(opt == LM_OPT_ADAM, lr, beta1, beta2, eps, weight_decay, step, g_scale);
 }
 
 int apply_run(float* table, int64_t V, int64_t D, int64_t ld_table, const void* rows, int idtype,

@@ -15,7 +15,8 @@ int segsum_run(const void* grad, int gtype, int64_t K, int64_t D, int64_t ld_gra
                const int64_t* num_unique, int64_t u_cap, float* out, int64_t ld_out,
                int32_t* dev_err, void* ws, size_t ws_bytes, hipStream_t st,
                const void* row_ids = nullptr, int row_ids64 = 0, int64_t out_rows = 0,
-               bool sgd = false, float lr = 0.f);
+               int op = 0, const OptParams& opt = OptParams{}, float* m = nullptr,
+               float* v = nullptr);
 int map_run(const void* sub, const int64_t* n_sub, int64_t sub_cap, const void* sup,
             const int64_t* n_sup, int64_t sup_cap, int idtype, int32_t* map, int32_t* dev_err,
             hipStream_t st);
@@ -74,7 +75,7 @@ const char* lm_status_string(int status) {
   }
 }
 
-int lm_abi_version(void) { return 105; }
+int lm_abi_version(void) { return 106; }
 
 int lm_workspace_clear(void* ws, size_t bytes, void* stream) {
   if (bytes == 0) return LM_OK;
@@ -175,7 +176,32 @@ int lm_segsum_sgd(const void* grad, int32_t gtype, int64_t K, int64_t D, int64_t
   if (ws_bytes < segsum_workspace_bytes(K, D)) return LM_E_WORKSPACE;
   return segsum_run(grad, gtype, K, D, ld_grad, perm, inverse, offsets, num_unique, rows_cap,
                     table, ld_table, dev_err, ws, ws_bytes, static_cast<hipStream_t>(stream),
-                    row_ids, idtype == LM_I64 ? 1 : 0, V, true, lr);
+                    row_ids, idtype == LM_I64 ? 1 : 0, V, 1,
+                    make_opt_params(false, lr, 0.f, 0.f, 0.f, 0.f, 1, 1.f));
+}
+
+int lm_segsum_adam(const void* grad, int32_t gtype, int64_t K, int64_t D, int64_t ld_grad,
+                   const int32_t* perm, const int32_t* inverse, const int32_t* offsets,
+                   const int64_t* num_unique, const void* row_ids, int32_t idtype,
+                   int64_t rows_cap, float* table, int64_t V, int64_t ld_table, float lr,
+                   float beta1, float beta2, float eps, float weight_decay, int64_t step,
+                   float* m, float* v, int32_t* dev_err, void* ws, size_t ws_bytes,
+                   void* stream) {
+  if (gtype != LM_F32 && gtype != LM_BF16) return LM_E_UNSUPPORTED;
+  if (!valid_idtype(idtype)) return LM_E_UNSUPPORTED;
+  if (K < 0 || D < 0 || rows_cap < 0 || V < 0 || ld_grad < D || ld_table < D) return LM_E_INVAL;
+  if (K >= LM_MAX_K || D > (int64_t(1) << 24) || V > INT32_MAX) return LM_E_UNSUPPORTED;
+  if (step < 1 || !(beta1 >= 0.f && beta1 < 1.f && beta2 >= 0.f && beta2 < 1.f)) return LM_E_INVAL;
+  if (K > 0 && D > 0 && rows_cap > 0 &&
+      (!grad || !perm || !inverse || !offsets || !num_unique || !row_ids || !table || !m || !v ||
+       !dev_err || !ws))
+    return LM_E_INVAL;
+  if (ws && (reinterpret_cast<uintptr_t>(ws) & 255)) return LM_E_INVAL;
+  if (ws_bytes < segsum_workspace_bytes(K, D)) return LM_E_WORKSPACE;
+  return segsum_run(grad, gtype, K, D, ld_grad, perm, inverse, offsets, num_unique, rows_cap,
+                    table, ld_table, dev_err, ws, ws_bytes, static_cast<hipStream_t>(stream),
+                    row_ids, idtype == LM_I64 ? 1 : 0, V, 2,
+                    make_opt_params(true, lr, beta1, beta2, eps, weight_decay, step, 1.f), m, v);
 }
 
 int lm_map_ids(const void* sub_ids, const int64_t* n_sub, int64_t sub_cap, const void* sup_ids,

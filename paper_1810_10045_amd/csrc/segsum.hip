@@ -45,13 +45,14 @@
 // gathers the row of each window position's type with the types; the
 // fix-up looks it up per segment. Without a row map, row u.
 //
-// lm_segsum_sgd (the SGD instantiations) updates those rows instead of
-// writing them: row = row - lr * sum, the sum in the same order and the
-// update the same fused multiply-add as lm_sparse_apply's. The walk then
-// closes a gather batch after its second segment end and loads the table
-// rows of its (at most two) ends with its gradient rows, through buffer
-// resources whose range is empty where no row is needed (such a load reads
-// nothing and returns zeros), so an update costs no round trip of its own.
+// lm_segsum_sgd and lm_segsum_adam (the update instantiations, OP) update
+// those rows instead of writing them, the sum in the same order and the
+// update the same arithmetic as lm_sparse_apply's (sgd_value, adam_value).
+// The walk then closes a gather batch after its kEnds-th segment end and
+// loads the table rows of those ends (Adam: the parameters, m and v) with
+// its gradient rows, through buffer resources whose range is empty where no
+// row is needed (such a load reads nothing and returns zeros), so an update
+// costs no round trip of its own.
 #include <atomic>
 #include <cstdlib>
 
@@ -93,6 +94,10 @@ namespace lmz {
 #ifndef LMZ_SEG_SGD_RF4
 #define LMZ_SEG_SGD_RF4 3            // lm_segsum_sgd: rows per batch with 4 vectors per lane,
 #endif                               // chunks below LMZ_SEG_LONG_R (others as lm_segsum)
+#ifndef LMZ_SEG_ADAM_RF4
+#define LMZ_SEG_ADAM_RF4 2           // lm_segsum_adam: the same, every chunk length (one end,
+                                     // three table rows per batch; 4 at most with fewer vectors)
+#endif
 #ifndef LMZ_SEG_NV_MAX
 #define LMZ_SEG_NV_MAX 4             // 16-byte vectors per lane per row (fp32)
 #endif
@@ -144,8 +149,14 @@ struct SegArgs {
   int row_ids64;           //   (int64 ids when nonzero), < out_rows; nullptr: row u
   int64_t out_rows;
   int32_t* dev_err;
-  float lr;                // lm_segsum_sgd: out rows become row - lr * sum
+  OptParams opt;           // lm_segsum_sgd / _adam: the step (out is the table)
+  float* m;                // lm_segsum_adam: the moments, rows of out's stride
+  float* v;
 };
+
+// What a finished type row becomes: written (lm_segsum, lm_segsum_rows), or
+// applied to the table row by SGD or Adam.
+constexpr int kOpStore = 0, kOpSgd = 1, kOpAdam = 2;
 
 struct SegLayout {
   int R, max_chunks;
@@ -291,12 +302,14 @@ __device__ __forceinline__ int64_t out_row_of(const SegArgs& a, int s) {
   return r;
 }
 
-// lm_segsum_sgd: a buffer resource over output row r (D fp32 values), or
-// over nothing for r < 0: loads through an empty range read no memory and
-// return zeros, so a batch loads its two table rows unconditionally.
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t table_row(const SegArgs& a, int64_t r) {
+// The update instantiations: a buffer resource over row r (D fp32 values)
+// of base (the table, m or v, all of out's row stride), or over nothing for
+// r < 0: loads through an empty range read no memory and return zeros, so
+// a batch loads its table rows unconditionally.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t table_row(const SegArgs& a, float* base,
+                                                            int64_t r) {
   constexpr int kRawBufferWord3 = 0x00020000;  // 32-bit data format, no swizzle
-  return __builtin_amdgcn_make_buffer_rsrc(a.out + (r >= 0 ? r : 0) * a.ld_out, 0,
+  return __builtin_amdgcn_make_buffer_rsrc(base + (r >= 0 ? r : 0) * a.ld_out, 0,
                                            r >= 0 ? a.D * 4 : 0, kRawBufferWord3);
 }
 
@@ -320,16 +333,30 @@ __device__ __forceinline__ void table_vec(__amdgpu_buffer_rsrc_t rs, int col, fl
   }
 }
 
-// Write a finished type row: out = sum, or with SGD out = out - lr * sum.
-template <int VEC, bool SGD>
-__device__ __forceinline__ void finish_row(const SegArgs& a, float* o, float* sum) {
-  if constexpr (SGD) {
-    float t[VEC];
-    load_vec<VEC>(o, t);
+// Finish VEC columns from col of type row orow: out = sum, or the table
+// row (and Adam's moments) updated with it.
+template <int VEC, int OP>
+__device__ __forceinline__ void finish_row(const SegArgs& a, int64_t orow, int col, float* sum) {
+  const int64_t off = orow * a.ld_out + col;
+  if constexpr (OP == kOpSgd) {
+    float p[VEC];
+    load_vec<VEC>(a.out + off, p);
 #pragma unroll
-    for (int e = 0; e < VEC; ++e) sum[e] = t[e] - a.lr * sum[e];
+    for (int e = 0; e < VEC; ++e) sgd_value(p[e], sum[e], a.opt);
+    store_vec<VEC>(a.out + off, p);
+  } else if constexpr (OP == kOpAdam) {
+    float p[VEC], m[VEC], v[VEC];
+    load_vec<VEC>(a.out + off, p);
+    load_vec<VEC>(a.m + off, m);
+    load_vec<VEC>(a.v + off, v);
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) adam_value(p[e], m[e], v[e], sum[e], a.opt);
+    store_vec<VEC>(a.out + off, p);
+    store_vec<VEC>(a.m + off, m);
+    store_vec<VEC>(a.v + off, v);
+  } else {
+    store_vec<VEC>(a.out + off, sum);
   }
-  store_vec<VEC>(o, sum);
 }
 
 template <int VEC>
@@ -369,7 +396,7 @@ __device__ __forceinline__ bool wait_flags(const SegArgs& a, int idx, bool need)
 // sums each long segment that starts there as k_segsum_fix does (one wave
 // for fewer than 16 further pieces, all waves and an LDS combine for a
 // head), waiting for each piece's flag before loading it.
-template <bool SGD>
+template <int OP>
 __device__ __forceinline__ void fused_fix(const SegArgs& a) {
   constexpr int RF = LMZ_SEG_FUSED_RF;
   constexpr int kShortMax = 16;  // further pieces below this: one wave
@@ -428,7 +455,7 @@ __device__ __forceinline__ void fused_fix(const SegArgs& a) {
           for (int e = 0; e < 4; ++e) acc[e] += buf[r][e];
     }
     const int64_t orow = out_row_of(a, s);
-    if (col < D && orow >= 0) finish_row<4, SGD>(a, a.out + orow * a.ld_out + col, acc);
+    if (col < D && orow >= 0) finish_row<4, OP>(a, orow, col, acc);
   }
 
   // Heads, one after the other, all waves: wave w adds pieces w, w + W, ...
@@ -461,18 +488,18 @@ __device__ __forceinline__ void fused_fix(const SegArgs& a) {
         float sum = 0.f;
 #pragma unroll
         for (int w = 0; w < kFusedWaves; ++w) sum += s_part[w][x];
-        finish_row<1, SGD>(a, a.out + orow * a.ld_out + cx, &sum);
+        finish_row<1, OP>(a, orow, cx, &sum);
       }
     }
     __syncthreads();
   }
 }
 
-template <typename GT, int VEC, int NV, int RF, int R, int T, int NTHR, bool FUSED, bool SGD>
+template <typename GT, int VEC, int NV, int RF, int R, int T, int NTHR, bool FUSED, int OP>
 __global__ __launch_bounds__(NTHR) void k_segsum(SegArgs a) {
   if constexpr (FUSED) {
     if (static_cast<int>(blockIdx.x) >= a.main_blocks) {
-      fused_fix<SGD>(a);
+      fused_fix<OP>(a);
       return;
     }
   }
@@ -634,7 +661,11 @@ __global__ __launch_bounds__(NTHR) void k_segsum(SegArgs a) {
   }
   const GT* __restrict__ grad = static_cast<const GT*>(a.grad);
   bool bad_row = false;
-  constexpr int kEnds = SGD ? LMZ_SEG_SGD_ENDS : 1;
+  // Update instantiations: segment ends per batch, and table rows per end
+  // (Adam: the parameters, m and v; one end per batch, as three rows per
+  // end fill the registers).
+  constexpr int kEnds = OP == kOpSgd ? LMZ_SEG_SGD_ENDS : 1;
+  constexpr int kRows = OP == kOpAdam ? 3 : 1;
   static_assert(kEnds >= 1 && kEnds <= RF, "table rows per batch");
 
   float acc[NV][VEC];
@@ -650,11 +681,11 @@ __global__ __launch_bounds__(NTHR) void k_segsum(SegArgs a) {
     const int hi = q_end - wbase < kWave ? q_end - wbase : kWave;
     for (int j0 = lo; j0 < hi;) {
       int n = hi - j0 < RF ? hi - j0 : RF;
-      // SGD: at most kEnds segment ends per batch (bm: their bits), whose
-      // table rows load with the batch's gradient rows.
+      // Updates: at most kEnds segment ends per batch (bm: their bits),
+      // whose table rows load with the batch's gradient rows.
       uint64_t bm = 0;
-      float tb[kEnds][NV][VEC];
-      if constexpr (SGD) {
+      float tb[kEnds][kRows][NV][VEC];
+      if constexpr (OP != kOpStore) {
         bm = (ends[w] >> j0) & ((uint64_t(1) << n) - 1);
         uint64_t past = bm;  // the ends after the first kEnds
 #pragma unroll
@@ -673,9 +704,12 @@ __global__ __launch_bounds__(NTHR) void k_segsum(SegArgs a) {
             const int s = read_lane(sw[w], j);
             if (!(s == s_f && started_before) && s >= 0 && s < a.u_cap) orow = read_lane(orw[w], j);
           }
-          const __amdgpu_buffer_rsrc_t rs = table_row(a, orow);
 #pragma unroll
-          for (int v = 0; v < NV; ++v) table_vec<VEC>(rs, col_ld[v], tb[k][v]);
+          for (int x = 0; x < kRows; ++x) {
+            const __amdgpu_buffer_rsrc_t rs = table_row(a, x == 0 ? a.out : x == 1 ? a.m : a.v, orow);
+#pragma unroll
+            for (int v = 0; v < NV; ++v) table_vec<VEC>(rs, col_ld[v], tb[k][x][v]);
+          }
         }
       }
       // Always RF row loads (rows past n repeat row n-1, a cache hit): a load
@@ -711,18 +745,38 @@ __global__ __launch_bounds__(NTHR) void k_segsum(SegArgs a) {
               bad_row |= rows && orow < 0 && s >= 0 && s < a.u_cap;
               dst = (s >= 0 && s < a.u_cap && orow >= 0) ? a.out + orow * a.ld_out : nullptr;
             }
-            if constexpr (SGD) {
+            if constexpr (OP == kOpSgd) {
               if (!part) {  // the batch's k-th end: table row k
                 const int k = __popcll(bm & ((uint64_t(1) << (j - j0)) - 1));
 #pragma unroll
                 for (int v = 0; v < NV; ++v)
 #pragma unroll
                   for (int e = 0; e < VEC; ++e) {
-                    float t = tb[0][v][e];
+                    float t = tb[0][0][v][e];
 #pragma unroll
-                    for (int x = 1; x < kEnds; ++x) t = k == x ? tb[x][v][e] : t;
-                    acc[v][e] = t - a.lr * acc[v][e];
+                    for (int x = 1; x < kEnds; ++x) t = k == x ? tb[x][0][v][e] : t;
+                    sgd_value(t, acc[v][e], a.opt);
+                    acc[v][e] = t;
                   }
+              }
+            } else if constexpr (OP == kOpAdam) {
+              if (!part) {  // the batch's one end: the parameters into acc, the moments in place
+#pragma unroll
+                for (int v = 0; v < NV; ++v)
+#pragma unroll
+                  for (int e = 0; e < VEC; ++e) {
+                    adam_value(tb[0][0][v][e], tb[0][1][v][e], tb[0][2][v][e], acc[v][e], a.opt);
+                    acc[v][e] = tb[0][0][v][e];
+                  }
+                if (dst) {
+                  const int64_t off = dst - a.out;
+#pragma unroll
+                  for (int v = 0; v < NV; ++v) {
+                    if (!col_ok[v]) continue;
+                    store_vec<VEC>(a.m + off + col0 + v * kColsPerVec, tb[0][1][v]);
+                    store_vec<VEC>(a.v + off + col0 + v * kColsPerVec, tb[0][2][v]);
+                  }
+                }
               }
             }
             if (dst) {
@@ -784,7 +838,7 @@ constexpr int kFixChunks = LMZ_SEG_FIX_CHUNKS;
 static_assert(kFixChunks <= kFixWaves && kFixChunks <= LMZ_SEG_FIX_RF,
               "at most one short segment per wave and one head per workgroup");
 
-template <int VEC, int RF, bool SGD>
+template <int VEC, int RF, int OP>
 __global__ __launch_bounds__(kFixThreads) void k_segsum_fix(SegArgs a) {
   constexpr int kCols = kWave * VEC;  // columns of a tile
   __shared__ float s_part[kFixWaves][kCols];
@@ -842,7 +896,7 @@ __global__ __launch_bounds__(kFixThreads) void k_segsum_fix(SegArgs a) {
 #pragma unroll
         for (int e = 0; e < VEC; ++e) acc[e] += sbuf[r][e];
     const int64_t orow = out_row_of(a, ss);
-    if (col < D && orow >= 0) finish_row<VEC, SGD>(a, a.out + orow * a.ld_out + col, acc);
+    if (col < D && orow >= 0) finish_row<VEC, OP>(a, orow, col, acc);
   }
   if (ih < 0) return;  // the same in every wave: no barrier below is skipped by only some
   float acc[VEC];
@@ -877,7 +931,7 @@ __global__ __launch_bounds__(kFixThreads) void k_segsum_fix(SegArgs a) {
       float sum = 0.f;
 #pragma unroll
       for (int w = 0; w < kFixWaves; ++w) sum += s_part[w][x];
-      finish_row<1, SGD>(a, a.out + orow * a.ld_out + cx, &sum);
+      finish_row<1, OP>(a, orow, cx, &sum);
     }
   }
 }
@@ -903,6 +957,13 @@ constexpr int rf_for() {
 template <int NV, int R>
 constexpr int rf_sgd_for() {
   return NV >= 4 && R < LMZ_SEG_LONG_R ? LMZ_SEG_SGD_RF4 : rf_for<NV, R>();
+}
+
+// lm_segsum_adam's rows per batch: three table rows per end take registers
+// from the gradient batch, at every chunk length.
+template <int NV, int R>
+constexpr int rf_adam_for() {
+  return NV >= 4 ? LMZ_SEG_ADAM_RF4 : (rf_for<NV, R>() < 4 ? rf_for<NV, R>() : 4);
 }
 
 // Multiprocessors of the current device (queried once per device).
@@ -979,21 +1040,21 @@ static int whole_rounds(int nchunks, int tiles, int64_t waves_per_round, int max
   return static_cast<int>(n < nchunks ? nchunks : n);
 }
 
-template <typename GT, int VEC, int NV, int R, bool SGD>
+template <typename GT, int VEC, int NV, int R, int OP>
 static void launch_one(SegArgs& a, int tiles, hipStream_t st) {
   constexpr int RFp = rf_for<NV, R>(), T = t_for<R>();
-  constexpr int RF = SGD ? rf_sgd_for<NV, R>() : RFp;
+  constexpr int RF = OP == kOpSgd ? rf_sgd_for<NV, R>() : OP == kOpAdam ? rf_adam_for<NV, R>() : RFp;
   a.tiles = tiles;
   a.tile_cols = NV * kWave * VEC;
-  // The rounds are those of the plain kernel (SGD false) for the SGD
+  // The rounds are those of the plain kernel (kOpStore) for the update
   // instantiations too: its occupancy fixes the chunks, and with them the
-  // order of every sum, so lm_segsum_sgd adds in lm_segsum's order.
+  // order of every sum, so lm_segsum_sgd and _adam add in lm_segsum's order.
   if constexpr (VEC >= 2) {
     if (a.fused) {
-      auto k = k_segsum<GT, VEC, NV, RF, R, T, kFusedThreads, true, SGD>;
+      auto k = k_segsum<GT, VEC, NV, RF, R, T, kFusedThreads, true, OP>;
       static std::atomic<int> bpc{-1};
       const int64_t room =
-          int64_t(blocks_per_cu(k_segsum<GT, VEC, NV, RFp, R, T, kFusedThreads, true, false>,
+          int64_t(blocks_per_cu(k_segsum<GT, VEC, NV, RFp, R, T, kFusedThreads, true, kOpStore>,
                                 kFusedThreads, 0, bpc)) *
           kFusedWaves * stream_cus(st);
       a.nchunks = whole_rounds(a.nchunks, tiles, room, a.max_chunks);
@@ -1003,10 +1064,10 @@ static void launch_one(SegArgs& a, int tiles, hipStream_t st) {
       return;
     }
   }
-  auto k = k_segsum<GT, VEC, NV, RF, R, T, kSegThreads, false, SGD>;
+  auto k = k_segsum<GT, VEC, NV, RF, R, T, kSegThreads, false, OP>;
   static std::atomic<int> bpc{-1};
   const int64_t room =
-      int64_t(blocks_per_cu(k_segsum<GT, VEC, NV, RFp, R, T, kSegThreads, false, false>,
+      int64_t(blocks_per_cu(k_segsum<GT, VEC, NV, RFp, R, T, kSegThreads, false, kOpStore>,
                             kSegThreads, LMZ_SEG_LDS_PAD, bpc)) *
       kSegWaves * stream_cus(st);
   a.nchunks = whole_rounds(a.nchunks, tiles, room, a.max_chunks);
@@ -1014,49 +1075,49 @@ static void launch_one(SegArgs& a, int tiles, hipStream_t st) {
   k<<<grid, kSegThreads, LMZ_SEG_LDS_PAD, st>>>(a);
 }
 
-template <typename GT, int VEC, int NV, bool SGD>
+template <typename GT, int VEC, int NV, int OP>
 static hipError_t launch_r(SegArgs& a, hipStream_t st) {
   constexpr int CT = NV * kWave * VEC;
   const int tiles = (a.D + CT - 1) / CT;
   switch (a.R) {
-    case 16: launch_one<GT, VEC, NV, 16, SGD>(a, tiles, st); break;
-    case 32: launch_one<GT, VEC, NV, 32, SGD>(a, tiles, st); break;
-    case 64: launch_one<GT, VEC, NV, 64, SGD>(a, tiles, st); break;
-    case 128: launch_one<GT, VEC, NV, 128, SGD>(a, tiles, st); break;
-    case 256: launch_one<GT, VEC, NV, 256, SGD>(a, tiles, st); break;
-    default: launch_one<GT, VEC, NV, 512, SGD>(a, tiles, st); break;
+    case 16: launch_one<GT, VEC, NV, 16, OP>(a, tiles, st); break;
+    case 32: launch_one<GT, VEC, NV, 32, OP>(a, tiles, st); break;
+    case 64: launch_one<GT, VEC, NV, 64, OP>(a, tiles, st); break;
+    case 128: launch_one<GT, VEC, NV, 128, OP>(a, tiles, st); break;
+    case 256: launch_one<GT, VEC, NV, 256, OP>(a, tiles, st); break;
+    default: launch_one<GT, VEC, NV, 512, OP>(a, tiles, st); break;
   }
   return hipGetLastError();
 }
 
-template <typename GT, int VEC, bool SGD>
+template <typename GT, int VEC, int OP>
 static hipError_t dispatch_nv(SegArgs& a, int nv_max, hipStream_t st) {
   const int per = kWave * VEC;
   int nv = (a.D + per - 1) / per;
   if (nv > nv_max) nv = nv_max;
-  if (nv <= 1) return launch_r<GT, VEC, 1, SGD>(a, st);
-  if (nv == 2) return launch_r<GT, VEC, 2, SGD>(a, st);
-  if constexpr (sizeof(GT) == 4 || VEC == 1) return launch_r<GT, VEC, 4, SGD>(a, st);
-  return launch_r<GT, VEC, 2, SGD>(a, st);
+  if (nv <= 1) return launch_r<GT, VEC, 1, OP>(a, st);
+  if (nv == 2) return launch_r<GT, VEC, 2, OP>(a, st);
+  if constexpr (sizeof(GT) == 4 || VEC == 1) return launch_r<GT, VEC, 4, OP>(a, st);
+  return launch_r<GT, VEC, 2, OP>(a, st);
 }
 
-template <bool SGD>
+template <int OP>
 static hipError_t dispatch(SegArgs& a, int gtype, bool vec, hipStream_t st) {
   if (gtype == LM_F32)
-    return vec ? dispatch_nv<float, 4, SGD>(a, LMZ_SEG_NV_MAX, st)
-               : dispatch_nv<float, 1, SGD>(a, 4, st);
-  return vec ? dispatch_nv<bf16_t, 8, SGD>(a, LMZ_SEG_NV_MAX < 2 ? LMZ_SEG_NV_MAX : 2, st)
-             : dispatch_nv<bf16_t, 1, SGD>(a, 4, st);
+    return vec ? dispatch_nv<float, 4, OP>(a, LMZ_SEG_NV_MAX, st)
+               : dispatch_nv<float, 1, OP>(a, 4, st);
+  return vec ? dispatch_nv<bf16_t, 8, OP>(a, LMZ_SEG_NV_MAX < 2 ? LMZ_SEG_NV_MAX : 2, st)
+             : dispatch_nv<bf16_t, 1, OP>(a, 4, st);
 }
 
-template <bool SGD>
+template <int OP>
 static void launch_fix(SegArgs& a, hipStream_t st) {
   const uint32_t fix_blocks = static_cast<uint32_t>((a.nchunks + kFixChunks - 1) / kFixChunks);
   if (a.D % 4 == 0)
-    k_segsum_fix<4, LMZ_SEG_FIX_RF, SGD>
+    k_segsum_fix<4, LMZ_SEG_FIX_RF, OP>
         <<<dim3(fix_blocks, (a.D + 255) / 256), kFixThreads, 0, st>>>(a);
   else
-    k_segsum_fix<1, LMZ_SEG_FIX_RF, SGD>
+    k_segsum_fix<1, LMZ_SEG_FIX_RF, OP>
         <<<dim3(fix_blocks, (a.D + 63) / 64), kFixThreads, 0, st>>>(a);
 }
 
@@ -1100,7 +1161,8 @@ int segsum_run(const void* grad, int gtype, int64_t K, int64_t D, int64_t ld_gra
                const int32_t* perm, const int32_t* inverse, const int32_t* offsets,
                const int64_t* num_unique, int64_t u_cap, float* out, int64_t ld_out,
                int32_t* dev_err, void* ws, size_t ws_bytes, hipStream_t st,
-               const void* row_ids, int row_ids64, int64_t out_rows, bool sgd, float lr) {
+               const void* row_ids, int row_ids64, int64_t out_rows, int op,
+               const OptParams& opt, float* m, float* v) {
   const SegLayout L = seg_layout(K, D);
   if (ws_bytes < L.total) return LM_E_WORKSPACE;
   if (K == 0 || D == 0 || u_cap == 0) return LM_OK;
@@ -1131,7 +1193,9 @@ int segsum_run(const void* grad, int gtype, int64_t K, int64_t D, int64_t ld_gra
   a.nchunks = static_cast<int>(chunks_for(K, L.R, a.rw, a.ww, u_cap));
   a.max_chunks = L.max_chunks;
   a.dev_err = dev_err;
-  a.lr = lr;
+  a.opt = opt;
+  a.m = m;
+  a.v = v;
 
   const bool out_vec = al16(out) && ld_out % 4 == 0 && D % 4 == 0;
   const bool vec = gtype == LM_F32 ? out_vec && al16(grad) && ld_grad % 4 == 0
@@ -1161,11 +1225,14 @@ int segsum_run(const void* grad, int gtype, int64_t K, int64_t D, int64_t ld_gra
     a.spin_limit = fail ? g_forced_spin_limit.load(std::memory_order_relaxed) : kSpinLimit;
     a.fix_tiles = static_cast<int>((D + kFusedCols - 1) / kFusedCols);
   }
-  const hipError_t e = sgd ? dispatch<true>(a, gtype, vec, st) : dispatch<false>(a, gtype, vec, st);
+  const hipError_t e = op == kOpSgd    ? dispatch<kOpSgd>(a, gtype, vec, st)
+                       : op == kOpAdam ? dispatch<kOpAdam>(a, gtype, vec, st)
+                                       : dispatch<kOpStore>(a, gtype, vec, st);
   if (e != hipSuccess) return launch_status(e);
   if (a.fused) return LM_OK;
-  if (sgd) launch_fix<true>(a, st);
-  else launch_fix<false>(a, st);
+  if (op == kOpSgd) launch_fix<kOpSgd>(a, st);
+  else if (op == kOpAdam) launch_fix<kOpAdam>(a, st);
+  else launch_fix<kOpStore>(a, st);
   return launch_status(hipGetLastError());
 }
 

@@ -68,6 +68,8 @@ def _load():
                                  P, P, SZ, P]
     L.lm_segsum_sgd.argtypes = [P, I32_, I64_, I64_, I64_, P, P, P, P, P, I32_, I64_, P, I64_, I64_,
                                 F, P, P, SZ, P]
+    L.lm_segsum_adam.argtypes = [P, I32_, I64_, I64_, I64_, P, P, P, P, P, I32_, I64_, P, I64_, I64_,
+                                 F, F, F, F, F, I64_, P, P, P, P, SZ, P]
     L.lm_map_ids.argtypes = [P, P, I64_, P, P, I64_, I32_, P, P, P]
     L.lm_fill_values.argtypes = [P, I64_, P, P, I64_, P, P, I32_, I64_, P, I64_, I64_, I32_, P, P]
     L.lm_sparse_apply.argtypes = [P, I64_, I64_, I64_, P, I32_, P, I64_, P, I64_, I32_,
@@ -80,7 +82,7 @@ def _load():
     L.lm_segsum_set_two_launches.argtypes = [I32_]
     L.lm_test_force_wait_failure.argtypes = [I32_, ctypes.c_uint32]
     for f in ("lm_abi_version", "lm_workspace_clear", "lm_unique", "lm_unique_noalloc",
-              "lm_segsum", "lm_segsum_rows", "lm_segsum_sgd", "lm_map_ids",
+              "lm_segsum", "lm_segsum_rows", "lm_segsum_sgd", "lm_segsum_adam", "lm_map_ids",
               "lm_fill_values", "lm_sparse_apply", "lm_fill_values_f16", "lm_sparse_apply_f16",
               "lm_sample_ids", "lm_segsum_set_two_launches", "lm_test_force_wait_failure"):
         getattr(L, f).restype = ctypes.c_int
@@ -344,6 +346,44 @@ def segsum_sgd(grad: torch.Tensor, perm: torch.Tensor, inverse: torch.Tensor,
                              row_ids.numel(), _ptr(table), table.shape[0], ld_t, float(lr),
                              _ptr(dev_err), _ptr(buf), buf.numel(), _stream(stream)),
           "lm_segsum_sgd")
+    return table
+
+
+def segsum_adam(grad: torch.Tensor, perm: torch.Tensor, inverse: torch.Tensor,
+                offsets: torch.Tensor, num_unique: torch.Tensor, row_ids: torch.Tensor,
+                table: torch.Tensor, m: torch.Tensor, v: torch.Tensor, lr: float = 1e-3,
+                beta1: float = 0.9, beta2: float = 0.999, eps: float = 1e-8,
+                weight_decay: float = 0.0, step: int = 1, dev_err: Optional[torch.Tensor] = None,
+                ws: Optional[Workspace] = None, stream=None) -> torch.Tensor:
+    """lm_segsum_adam: Sec. III-A steps 2 and 7 in one pass on one GPU: the
+    lazy-Adam step of table[row_ids[u]] (and of its m and v rows) with type
+    u's sum as the gradient, in place; other rows are untouched. Returns
+    `table`."""
+    _dev(grad, "grad")
+    _dev(row_ids, "row_ids")
+    K, D = grad.shape
+    ld = _rows(grad, "grad")
+    if perm.numel() < K or inverse.numel() < K or offsets.numel() < 1:
+        raise LmError("perm and inverse must hold K entries")
+    if table.dim() != 2 or table.shape[1] != D or table.dtype != torch.float32:
+        raise LmError("table must be an fp32 matrix with D columns")
+    for t, n in ((m, "m"), (v, "v")):
+        if t is None or t.shape != table.shape or t.stride() != table.stride() or t.dtype != table.dtype:
+            raise LmError(f"{n} must have the table's shape, strides and dtype")
+    if not row_ids.is_contiguous():
+        raise LmError("row_ids must be contiguous")
+    ld_t = _rows(table, "table")
+    if dev_err is None:
+        dev_err = torch.zeros(1, dtype=torch.int32, device=grad.device)
+    ws = ws or default_workspace(grad.device)
+    buf = ws.get(_lib.lm_segsum_workspace_bytes(K, D))
+    _call(_lib.lm_segsum_adam(_ptr(grad), _gtype(grad), K, D, ld, _ptr(perm), _ptr(inverse),
+                              _ptr(offsets), _ptr(num_unique), _ptr(row_ids), _idtype(row_ids),
+                              row_ids.numel(), _ptr(table), table.shape[0], ld_t, float(lr),
+                              float(beta1), float(beta2), float(eps), float(weight_decay),
+                              int(step), _ptr(m), _ptr(v), _ptr(dev_err), _ptr(buf), buf.numel(),
+                              _stream(stream)),
+          "lm_segsum_adam")
     return table
 
 

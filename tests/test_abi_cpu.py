@@ -39,7 +39,8 @@ def test_test_hook_is_not_in_the_training_header():
 
 def test_header_declares_the_boundary():
     names = declared_functions()
-    for n in ("lm_unique", "lm_segsum", "lm_segsum_rows", "lm_segsum_sgd", "lm_fill_values",
+    for n in ("lm_unique", "lm_segsum", "lm_segsum_rows", "lm_segsum_sgd", "lm_segsum_adam",
+              "lm_fill_values",
               "lm_sparse_apply",
               "lm_map_ids", "lm_unique_workspace_bytes", "lm_segsum_workspace_bytes",
               "lm_status_string"):
@@ -55,7 +56,8 @@ def test_binding_names_match_the_header():
     src = open(os.path.join(ROOT, "paper_1810_10045_amd", "lmzipf.py")).read()
     for n in declared_functions():
         assert f'"{n}"' in src, n
-    for n in ("unique", "segsum", "segsum_rows", "segsum_sgd", "map_ids", "fill_values",
+    for n in ("unique", "segsum", "segsum_rows", "segsum_sgd", "segsum_adam", "map_ids",
+              "fill_values",
               "sparse_apply", "fill_values_f16",
               "sparse_apply_f16", "sample_ids"):
         assert re.search(rf"^def {n}\(", src, re.M), n
@@ -65,7 +67,7 @@ def test_status_strings(lib):
     lib.lm_status_string.restype = ctypes.c_char_p
     for code in (0, 1, 3, 4, 5, 99):
         assert lib.lm_status_string(code)
-    assert lib.lm_abi_version() == 105
+    assert lib.lm_abi_version() == 106
 
 
 def test_workspace_queries(lib):
@@ -127,6 +129,20 @@ def test_argument_errors_return_before_any_launch(lib):
     assert sgd(ld_table=3) == 1 and sgd(row_ids=None) == 1 and sgd(rows_cap=-1) == 1
     assert sgd(table=None) == 1 and sgd(V=-1) == 1
     assert sgd(ws=_v(0x1010)) == 1 and sgd(ws_bytes=8) == 3
+    F = ctypes.c_float
+    lib.lm_segsum_adam.argtypes = [P, I32, I64, I64, I64, P, P, P, P, P, I32, I64, P, I64, I64,
+                                   F, F, F, F, F, I64, P, P, P, P, SZ, P]
+
+    def adam(gtype=0, V=100, ld_table=4, b1=0.9, b2=0.999, step=1, m=_v(), v=_v(), ws=_v(),
+             ws_bytes=1 << 20):
+        return lib.lm_segsum_adam(_v(), gtype, 10, 4, 4, _v(), _v(), _v(), _v(), _v(), 0, 10,
+                                  _v(), V, ld_table, 1e-3, b1, b2, 1e-8, 0.0, step, m, v, _v(),
+                                  ws, ws_bytes, None)
+    # a bad dtype, step 0, a beta of 1 or below 0, NULL moments, ld < D, a
+    # short workspace
+    assert adam(gtype=2) == 5 and adam(step=0) == 1 and adam(b1=1.0) == 1 and adam(b2=-0.5) == 1
+    assert adam(m=None) == 1 and adam(v=None) == 1 and adam(ld_table=3) == 1
+    assert adam(V=1 << 31) == 5 and adam(ws_bytes=8) == 3
     lib.lm_fill_values.argtypes = [P, I64, P, P, I64, P, P, I32, I64, P, I64, I64, I32, P, P]
     assert lib.lm_fill_values(_v(), 4, _v(), _v(), 10, _v(), _v(), 0, 4, _v(), 10, 4, 9, _v(), None) == 5
     assert lib.lm_fill_values(_v(), 4, _v(), _v(), 10, None, None, 0, 4, _v(), 10, 4, 0, _v(), None) == 1

@@ -851,6 +851,151 @@ def test_segsum_sgd_bad_row_id(lz, D):
     assert torch.equal(got, want)
 
 
+ADAM_CASES = [
+    # (K, V, s, D, grad dtype, id dtype, seed): ids over a 100K vocabulary
+    # (a segment end on most rows); rows of two 1024-column tiles (f32, and
+    # bf16 with int64 ids); chunks of 512 positions; rows not a multiple of
+    # 4 wide (the scalar path); rows wider than the one-launch form takes; a
+    # single token.
+    (65_536, 100_000, 0.9, 1024, "f32", np.int64, 181),
+    (60_000, 20_000, 1.2, 2048, "f32", np.int32, 182),
+    (40_000, 300, 1.2, 2048, "bf16", np.int64, 183),
+    (300_000, 20_000, 1.2, 1024, "f32", np.int32, 184),
+    (20_000, 3000, 1.0, 97, "f32", np.int32, 185),
+    (4000, 100, 1.0, 5000, "f32", np.int32, 186),
+    (1, 5, 1.0, 16, "f32", np.int32, 187),
+]
+ADAM_KW = dict(lr=float(np.float32(1e-3)), beta1=float(np.float32(0.9)),
+               beta2=float(np.float32(0.999)), eps=float(np.float32(1e-8)),
+               weight_decay=float(np.float32(0.01)), step=3)
+
+
+def _adam_tables(V, D, seed):
+    """Parameters and non-zero moments, as a later step sees them."""
+    return (synth.normal_rows(V, D, seed, 0.02), synth.normal_rows(V, D, seed + 1, 0.01),
+            np.abs(synth.normal_rows(V, D, seed + 2, 0.01)))
+
+
+@pytest.mark.parametrize("K,V,s,D,gdt,dt,seed", ADAM_CASES,
+                         ids=[f"K{c[0]}-V{c[1]}-D{c[3]}-{c[4]}-{np.dtype(c[5]).name}"
+                              for c in ADAM_CASES])
+def test_segsum_adam_is_segsum_then_adam(lz, K, V, s, D, gdt, dt, seed):
+    """lm_segsum_adam on V x D parameter, m and v tables with row_ids = uniq,
+    at step 3 with weight decay: the same three tables, bit for bit, as
+    lm_segsum followed by lm_sparse_apply Adam with the same arguments (each
+    launch form against lm_segsum in that form); every row no type names
+    keeps its value in all three."""
+    _say(f"segsum_adam K={K} V={V} D={D} {gdt} {np.dtype(dt).name}")
+    ids, grad, tgrad, res = _rows_case(lz, K, V, s, D, gdt, dt, seed)
+    base = [_t(a) for a in _adam_tables(V, D, seed + 2000)]
+
+    def both():
+        out = lz.segsum(tgrad, res.perm, res.inverse, res.offsets, res.num_unique,
+                        dev_err=res.dev_err)
+        want = [b.clone() for b in base]
+        lz.sparse_apply(want[0], res.uniq, res.num_unique, out, "adam", m=want[1], v=want[2],
+                        dev_err=res.dev_err, **ADAM_KW)
+        got = [b.clone() for b in base]
+        lz.segsum_adam(tgrad, res.perm, res.inverse, res.offsets, res.num_unique, res.uniq,
+                       got[0], got[1], got[2], dev_err=res.dev_err, **ADAM_KW)
+        return want, got
+
+    want, got = both()
+    assert lz.segsum_two_launches(True) is False
+    try:
+        want2, got2 = both()
+        torch.cuda.synchronize()
+    finally:
+        assert lz.segsum_two_launches(False) is True
+    lz.check(res.dev_err)
+    o = H.assert_unique_matches(res, ids, V, oracle)
+    for name, a, b in zip("pmv", got, want):
+        assert torch.equal(a, b), f"{name}: not lm_segsum + lm_sparse_apply Adam"
+    for name, a, b in zip("pmv", got2, want2):
+        assert torch.equal(a, b), f"{name}, two-launch form: not lm_segsum + lm_sparse_apply Adam"
+    touched = torch.zeros(V, dtype=torch.bool, device=DEV)
+    touched[_t(o[0].astype(np.int64))] = True
+    for name, a, b in zip("pmv", got, base):
+        assert torch.equal(a[~touched], b[~touched]), f"{name}: a row no type names was updated"
+
+
+def test_segsum_adam_first_step_matches_oracle(lz):
+    """End to end against the oracle's Seg-Sum and lazy Adam: the first step
+    from zero moments, every touched row of the three tables within the
+    bounds that the Seg-Sum tolerance allows."""
+    K, V, D = 60_000, 20_000, 1024
+    _say("segsum_adam first step against the oracle")
+    ids, grad, tgrad, res = _rows_case(lz, K, V, 1.0, D, "f32", np.int32, 188)
+    p0 = synth.normal_rows(V, D, 189, 0.02)
+    p, m, v = _t(p0), torch.zeros((V, D), device=DEV), torch.zeros((V, D), device=DEV)
+    kw = dict(ADAM_KW, weight_decay=0.0, step=1)
+    lz.segsum_adam(tgrad, res.perm, res.inverse, res.offsets, res.num_unique, res.uniq, p, m, v,
+                   dev_err=res.dev_err, **kw)
+    torch.cuda.synchronize()
+    lz.check(res.dev_err)
+    o = H.assert_unique_matches(res, ids, V, oracle)
+    U = len(o[0])
+    S = oracle.segsum(grad, o[3], U)
+    sq = H.sum_of_squares(grad, o[3], U, oracle)
+    z = np.zeros_like(S)
+    rp, rm, rv = oracle.adam(p0[o[0]], z, z, S, kw["lr"], kw["beta1"], kw["beta2"], kw["eps"],
+                             0.0, 1)
+    sel = _t(o[0].astype(np.int64))
+    H.assert_adam_first_step(p[sel].cpu().numpy(), m[sel].cpu().numpy(), v[sel].cpu().numpy(),
+                             rp, rm, rv, S, kw["lr"], kw["beta1"], kw["beta2"], kw["eps"],
+                             H.row_delta(S, H.TOL_F32, sq))
+
+
+@pytest.mark.parametrize("D", [512, 2048, 5000])
+def test_segsum_adam_reads_back_the_sums(lz, D):
+    """With beta1 = 0 on zero tables each updated m row is 0 * 0 + 1 * sum,
+    the sum itself: lm_segsum_rows's table, bit for bit (how the bench reads
+    the sums of its fused Adam step back for the oracle check)."""
+    K, V = 30_000, 2000
+    _say(f"segsum_adam beta1=0 D={D}")
+    ids, grad, tgrad, res = _rows_case(lz, K, V, 1.2, D, "f32", np.int32, 190)
+    want = torch.zeros((V, D), device=DEV)
+    lz.segsum_rows(tgrad, res.perm, res.inverse, res.offsets, res.num_unique, res.uniq, want,
+                   dev_err=res.dev_err)
+    p, m, v = (torch.zeros((V, D), device=DEV) for _ in range(3))
+    lz.segsum_adam(tgrad, res.perm, res.inverse, res.offsets, res.num_unique, res.uniq, p, m, v,
+                   lr=0.0, beta1=0.0, step=1, dev_err=res.dev_err)
+    torch.cuda.synchronize()
+    lz.check(res.dev_err)
+    assert torch.equal(m, want)
+
+
+@pytest.mark.parametrize("D", [512, 2048])
+def test_segsum_adam_bad_row_id(lz, D):
+    """A row id outside [0, V) sets LM_DEVERR_ID_RANGE and leaves that row of
+    all three tables as it was, as lm_sparse_apply does; the other rows are
+    updated as usual (the longest type, finished by the fix-up, and a short
+    one, finished in the walk)."""
+    K, V = 30_000, 2000
+    _say(f"segsum_adam bad ids D={D}")
+    ids, grad, tgrad, res = _rows_case(lz, K, V, 1.2, D, "f32", np.int64, 191)
+    U = int(res.num_unique.item())
+    counts = res.counts[:U].cpu().numpy()
+    out = lz.segsum(tgrad, res.perm, res.inverse, res.offsets, res.num_unique, u_cap=U,
+                    dev_err=res.dev_err)
+    base = [_t(a) for a in _adam_tables(V, D, 192)]
+    for bad_u, bad_id in ((int(np.argmax(counts)), V), (int(np.argmin(counts)), -1)):
+        rid = res.uniq[:U].clone()
+        rid[bad_u] = bad_id
+        e_want = torch.zeros(1, dtype=torch.int32, device=DEV)
+        want = [b.clone() for b in base]
+        lz.sparse_apply(want[0], rid, res.num_unique, out, "adam", m=want[1], v=want[2],
+                        dev_err=e_want, **ADAM_KW)
+        err = torch.zeros(1, dtype=torch.int32, device=DEV)
+        got = [b.clone() for b in base]
+        lz.segsum_adam(tgrad, res.perm, res.inverse, res.offsets, res.num_unique, rid, got[0],
+                       got[1], got[2], dev_err=err, **ADAM_KW)
+        torch.cuda.synchronize()
+        assert int(err.item()) == lz.DEVERR_ID_RANGE == int(e_want.item()), (bad_u, bad_id)
+        for a, b in zip(got, want):
+            assert torch.equal(a, b)
+
+
 # ---------------------------------------------------------------------------
 # Map, Fill-Values, the G-shard merge
 # ---------------------------------------------------------------------------
