@@ -17,9 +17,9 @@ gradient rows are not served from the 256 MB Infinity Cache.
 The headline runs the Unique calls on a second stream, up to three steps
 ahead of Seg-Sum and the update (Unique reads only the token ids, which a
 trainer has before the gradients exist); every step still does all of its
-work. At the char-LM and 2M-vocabulary workloads the two streams run on
-disjoint CUs (CU-masked streams, SIDE_CUS); the same schedule on shared
-CUs is printed beside it (`overlapped_all_cus`). The serial schedule (one stream) is timed too and printed beside it,
+work. At the char-LM workload the two streams run on disjoint CUs
+(CU-masked streams, SIDE_CUS); the same schedule on shared CUs is printed
+beside it (`overlapped_all_cus`). The serial schedule (one stream) is timed too and printed beside it,
 and for the SCATTER, SGD and Adam workloads also the serial schedule with
 that update as a call of its own after lm_segsum (`unfused_serial`).
 
@@ -408,13 +408,14 @@ def side_stream(torch, dev):
 # The overlapped schedule's CU split, per workload: the Unique calls run on
 # CUs [0, n) and the rest of the step on the others (two streams created
 # with CU masks), where that measured faster than two streams sharing every
-# CU: char_heavy_1m 1,427 against 1,445 us per step, vocab2m_adam_i64 1,082
-# against 1,118. On a CU of its own, a Unique kernel that needs a whole CU
-# (the 1024-thread sort tiles, the per-id counters in LDS) no longer waits
-# for the walk's waves to leave one. The word step and the merge, whose
-# Seg-Sums need every CU, measured slower split (133 -> 141 and
-# 1,480 -> 1,500 us at 32 CUs).
-SIDE_CUS = {"char_heavy_1m": 32, "vocab2m_adam_i64": 64}
+# CU: char_heavy_1m 1,427 against 1,445 us per step. On a CU of its own, a
+# Unique kernel that needs a whole CU (the 1024-thread sort tiles, the
+# per-id counters in LDS) no longer waits for the walk's waves to leave
+# one. The word step and the merge, whose Seg-Sums need every CU, measured
+# slower split (133 -> 141 and 1,480 -> 1,500 us at 32 CUs), and so does
+# the 2M vocabulary since its Seg-Sum applies Adam itself (967 -> 1,328 us
+# at 64 CUs; with the separate apply it had gained, 1,118 -> 1,082).
+SIDE_CUS = {"char_heavy_1m": 32}
 
 
 def cu_mask_words(first, count, ncu):
