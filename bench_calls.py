@@ -144,6 +144,8 @@ def calls_table(w, U, res, seg_cold, seg_warm):
         rb = seg_cold + np.mean([bench.fused_extra_bytes(w, w.D, u, ib) for u in U])
         rc = rb / np.median(res[("cold", "rows")]) / 1e3
         what = ("the U row ids" if w.step == "scatter" else
+                "the U row ids, the U parameter rows read and the m and v rows read and written"
+                if w.step == "adam" else
                 "the U row ids and the U table rows read before they are written")
         lines[-1:-1] = [f"{bench.fused_stage(w).split()[0]}: {rb / 1e6:.1f} MB algorithmic per call "
                         f"(Seg-Sum's, {what}); cold {rc:,.0f} GB/s "
