@@ -1500,6 +1500,11 @@ __global__ __launch_bounds__(kBlockThreads) void k_unique_block(
                               sizeof(uint32_t) * (kRadix + kBlockWaves);
   constexpr int kCntSets = kLdsRest + 2 * kCntBytes <= kLdsBytes ? 2 : 1;
   __shared__ uint16_t s_cnt[kCntSets][kBlockWaves][kRadix];
+  // The dedup's offsets get an array of their own where the LDS has room
+  // beside the counter sets, so that they are staged together with the
+  // inverse map and the type ids (one barrier and one pass fewer).
+  constexpr bool kOffLds = kLdsRest + kCntSets * kCntBytes + sizeof(int32_t) * (kN + 1) <= kLdsBytes;
+  __shared__ int32_t s_off[kOffLds ? kN + 1 : 1];
   __shared__ uint32_t s_start[kRadix];             // first sorted position of each digit
   __shared__ uint32_t s_scan[kBlockWaves];
   const int tid = threadIdx.x, lane = tid & 63;
@@ -1631,15 +1636,36 @@ __global__ __launch_bounds__(kBlockThreads) void k_unique_block(
     seg[i] = static_cast<int>(run + popc_below(hm[i]) + (head ? 1u : 0u)) - 1;
     run += static_cast<uint32_t>(__popcll(hm[i]));
   }
-  // Stage the inverse map (by token) and the type ids in LDS, then write
-  // both out coalesced.
+  // Stage the inverse map (by token) and the type ids in LDS (and, with
+  // kOffLds, the first position of every type), then write them out
+  // coalesced.
 #pragma unroll
   for (int i = 0; i < ITEMS; ++i) {
     const int pos = wave * (ITEMS * kWave) + i * kWave + lane;
     if (pos < K) {
+      const bool head = (hm[i] >> lane) & 1u;
       s_kv.val(src[i]) = seg[i];
-      if (((hm[i] >> lane) & 1u) && seg[i] < Uc) s_kv.key(seg[i]) = k[i];
+      if (head && seg[i] < Uc) s_kv.key(seg[i]) = k[i];
+      if constexpr (kOffLds)
+        if (head && seg[i] <= Uc) s_off[seg[i]] = pos;
     }
+  }
+  if constexpr (kOffLds) {
+    if (tid == 0 && static_cast<int>(U) == Uc) s_off[Uc] = K;
+    __syncthreads();
+    for (int j = tid; j < K; j += kBlockThreads) inverse[j] = s_kv.val(j);
+    for (int j = tid; j < Uc; j += kBlockThreads) {
+      const int o = s_off[j];
+      uniq[j] = s_kv.key(j);
+      offsets[j] = o;
+      counts[j] = s_off[j + 1] - o;
+    }
+    if (tid == 0) {
+      offsets[Uc] = K;
+      *num_unique = Uc;
+      if (static_cast<int>(U) > cap) raise_err(dev_err, LM_DEVERR_CAPACITY);
+    }
+    return;
   }
   __syncthreads();
   for (int j = tid; j < K; j += kBlockThreads) inverse[j] = s_kv.val(j);
