@@ -477,8 +477,9 @@ def test_segsum_on_cu_masked_stream(lz, D, gdt):
     the walk's chunks are sized for whole rounds of the waves that fit on
     those CUs, several rounds here where the whole device holds them in one.
     Checked against the oracle, bit-identical from run to run on that
-    stream, and lm_segsum_rows bit-identical to lm_segsum then a row copy
-    there too."""
+    stream, and lm_segsum_rows, lm_segsum_sgd (lr = -1 on zeros: the sums)
+    and lm_segsum_adam (beta1 = 0 on zeros: the sums in m) bit-identical to
+    lm_segsum there too: all four size their chunks for the same CUs."""
     K, V, s, seed = 100_000, 5000, 1.2, 131
     _say(f"segsum on a 32-CU stream K={K} D={D} {gdt}")
     ids = synth.zipf_ids(K, V, s, seed, np.int32)
@@ -495,6 +496,13 @@ def test_segsum_on_cu_masked_stream(lz, D, gdt):
         table = torch.zeros((V, D), dtype=torch.float32, device=DEV)
         lz.segsum_rows(tgrad, res.perm, res.inverse, res.offsets, res.num_unique, res.uniq,
                        table, dev_err=res.dev_err, stream=ms.stream)
+        tsgd = torch.zeros((V, D), dtype=torch.float32, device=DEV)
+        lz.segsum_sgd(tgrad, res.perm, res.inverse, res.offsets, res.num_unique, res.uniq,
+                      tsgd, -1.0, dev_err=res.dev_err, stream=ms.stream)
+        pmv = [torch.zeros((V, D), dtype=torch.float32, device=DEV) for _ in range(3)]
+        lz.segsum_adam(tgrad, res.perm, res.inverse, res.offsets, res.num_unique, res.uniq,
+                       pmv[0], pmv[1], pmv[2], lr=0.0, beta1=0.0, step=1, dev_err=res.dev_err,
+                       stream=ms.stream)
         ms.stream.synchronize()
     finally:
         ms.close()
@@ -506,6 +514,8 @@ def test_segsum_on_cu_masked_stream(lz, D, gdt):
     H.assert_single_rows_exact(got, ref, o[1])
     assert torch.equal(outs[0][:U], outs[1][:U]), "not deterministic on the masked stream"
     assert torch.equal(table[res.uniq[:U].long()], outs[0][:U]), "rows variant differs"
+    assert torch.equal(tsgd, table), "SGD variant's sums differ"
+    assert torch.equal(pmv[1], table), "Adam variant's sums differ"
 
 
 @pytest.mark.parametrize("K,V,s,D,gdt,seed", [(65_536, 800_000, 1.0, 1024, "f32", 121),
