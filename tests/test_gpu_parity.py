@@ -1006,6 +1006,48 @@ def test_segsum_adam_bad_row_id(lz, D):
             assert torch.equal(a, b)
 
 
+def test_segsum_updates_special_inputs(lz):
+    """The update variants on degenerate inputs, against lm_segsum followed
+    by lm_sparse_apply: no tokens (nothing is touched), a single type (one
+    segment across every chunk: the fix-up's head), every id distinct (a
+    segment end on every row: each gather batch closes at its last end)."""
+    D = 256
+    _say("segsum_sgd / segsum_adam special inputs")
+    empty = lz.unique(torch.zeros(0, dtype=torch.int32, device=DEV), 10)
+    g0 = torch.zeros((0, D), device=DEV)
+    t = torch.ones((10, D), device=DEV)
+    lz.segsum_sgd(g0, empty.perm, empty.inverse, empty.offsets, empty.num_unique, empty.uniq, t,
+                  0.5, dev_err=empty.dev_err)
+    pmv = [torch.ones((10, D), device=DEV) for _ in range(3)]
+    lz.segsum_adam(g0, empty.perm, empty.inverse, empty.offsets, empty.num_unique, empty.uniq,
+                   pmv[0], pmv[1], pmv[2], dev_err=empty.dev_err)
+    torch.cuda.synchronize()
+    lz.check(empty.dev_err)
+    assert all(bool((x == 1).all()) for x in [t] + pmv), "no tokens, yet a row was touched"
+    K = 30_000
+    g = _t(synth.normal_rows(K, D, 63))
+    dist = np.random.Generator(np.random.PCG64(64)).permutation(K).astype(np.int32)
+    for ids, V in ((np.full(K, 3, np.int32), 10), (dist, K)):
+        res = lz.unique(_t(ids), V)
+        out = lz.segsum(g, res.perm, res.inverse, res.offsets, res.num_unique, dev_err=res.dev_err)
+        base = _t(synth.normal_rows(V, D, 65))
+        want = base.clone()
+        lz.sparse_apply(want, res.uniq, res.num_unique, out, "sgd", lr=0.1, dev_err=res.dev_err)
+        got = base.clone()
+        lz.segsum_sgd(g, res.perm, res.inverse, res.offsets, res.num_unique, res.uniq, got, 0.1,
+                      dev_err=res.dev_err)
+        wa = [base.clone(), torch.zeros_like(base), torch.zeros_like(base)]
+        lz.sparse_apply(wa[0], res.uniq, res.num_unique, out, "adam", m=wa[1], v=wa[2],
+                        dev_err=res.dev_err, **ADAM_KW)
+        ga = [base.clone(), torch.zeros_like(base), torch.zeros_like(base)]
+        lz.segsum_adam(g, res.perm, res.inverse, res.offsets, res.num_unique, res.uniq, ga[0],
+                       ga[1], ga[2], dev_err=res.dev_err, **ADAM_KW)
+        torch.cuda.synchronize()
+        lz.check(res.dev_err)
+        assert torch.equal(got, want), f"SGD, V={V}"
+        assert all(torch.equal(a, b) for a, b in zip(ga, wa)), f"Adam, V={V}"
+
+
 # ---------------------------------------------------------------------------
 # Map, Fill-Values, the G-shard merge
 # ---------------------------------------------------------------------------
