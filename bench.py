@@ -272,15 +272,18 @@ class Pipeline:
             return rows
         return self.out[:U]
 
-    def enable_overlap(self, nsets=4):
-        """nsets sets of Unique outputs and a Unique workspace of their own,
-        so that the Unique of later batches can run on a second stream while
-        batch i's Seg-Sum and update run on the first (Unique reads only the
-        token ids, which exist before the gradients do). Measured: two sets
-        keep the side stream in step with the main one (tiny workload 56 us
-        per step against 42 serial); three or four let it run ahead (34 and
-        33 us); the larger workloads time the same with 2, 3 or 4."""
+    def enable_overlap(self, group=None):
+        """2 x group sets of Unique outputs and a Unique workspace of their
+        own, so that the Unique calls of later batches can run on a second
+        stream while earlier batches' Seg-Sum and update run on the first
+        (Unique reads only the token ids, which exist before the gradients
+        do). The steps go in groups of `group` (run_overlapped): the Unique
+        calls of one group fill one half of the sets while the other half's
+        steps finish."""
         w, lz = self.w, self.lz
+        group = OVERLAP_GROUP.get(w.name, OVERLAP_GROUP_DEFAULT) if group is None else group
+        if group < 1:
+            raise ValueError(f"a group holds at least one step, not {group}")
         dev = self.ures.uniq.device
         idt = self.ures.uniq.dtype
         self.ws_u = lz.Workspace(dev)
@@ -290,7 +293,7 @@ class Pipeline:
         self.sets = [(self.ures, u0)] + [
             (lz.unique_buffers(w.tokens, w.V, idt, dev),
              lz.unique_buffers(w.K, w.V, idt, dev) if u0 is not None else None)
-            for _ in range(nsets - 1)]
+            for _ in range(2 * group - 1)]
 
     def front(self, b, j, stream):
         """The part of step b that reads only ids, into output set j."""
@@ -336,25 +339,41 @@ class Pipeline:
             self.lz.check(ures.dev_err)
 
     def run_overlapped(self, first, steps, torch, main, side, sync):
-        """Steps first .. first + steps - 1 with the Unique calls on `side`,
-        up to nsets - 1 steps ahead of the rest on `main`. With ns sets,
-        event 2i + 1 marks Unique i done (set i % ns filled) and event 2i + 2
-        marks step i done on `main` (set i % ns free again); event 0 starts
-        the side stream no earlier than what is already on `main`."""
-        ns = len(self.sets)
+        """Steps first .. first + steps - 1 in groups of G = len(sets) / 2
+        consecutive steps; step i uses set i % 2G. The Unique calls of group
+        g run on `side`, one after another, then event 2g + 1 marks them
+        done; `main` waits for that event once, runs the group's Seg-Sums and
+        updates, and event 2g + 2 marks them done, which frees the group's
+        half of the sets for group g + 2. So the side stream runs up to
+        2G - 1 steps ahead, and the streams meet once per group, not once
+        per step. Event 0 starts the side stream no earlier than what is
+        already on `main`."""
+        G = len(self.sets) // 2
+        if G < 1 or len(self.sets) != 2 * G:
+            raise ValueError(f"the grouped schedule takes an even number of sets, not {len(self.sets)}")
+        ngroups = (steps + G - 1) // G
+
+        def members(g):
+            return range(g * G, min(steps, (g + 1) * G))
+
+        def fronts(g):
+            for i in members(g):
+                self.front(first + i, i % (2 * G), side)
+            sync.record(2 * g + 1, side)
+
         sync.record(0, main)
         sync.wait(0, side)
-        self.front(first, 0, side)
-        sync.record(1, side)
-        for i in range(steps):
-            if i + 1 < steps:
-                if i + 1 >= ns:
-                    sync.wait(2 * (i + 1 - ns) + 2, side)
-                self.front(first + i + 1, (i + 1) % ns, side)
-                sync.record(2 * (i + 1) + 1, side)
-            sync.wait(2 * i + 1, main)
-            self.back(first + i, i % ns)
-            sync.record(2 * i + 2, main)
+        if ngroups:
+            fronts(0)
+        for g in range(ngroups):
+            if g + 1 < ngroups:
+                if g >= 1:
+                    sync.wait(2 * g, side)  # group g - 1 done: its sets are free
+                fronts(g + 1)
+            sync.wait(2 * g + 1, main)
+            for i in members(g):
+                self.back(first + i, i % (2 * G))
+            sync.record(2 * g + 2, main)
 
     def step(self, b, ev=None):
         w, lz, st, ures, err = self.w, self.lz, self.state, self.ures, self.dev_err
@@ -403,6 +422,18 @@ def side_stream(torch, dev):
     if not _SIDE_STREAM:
         _SIDE_STREAM.append(torch.cuda.Stream(device=dev))
     return _SIDE_STREAM[0]
+
+
+# Steps per group of the overlapped schedule (run_overlapped), per
+# workload. Each wait of one stream for the other's event leaves the
+# waiting stream idle for a few microseconds, so the streams meet once per
+# group of steps rather than once per step. Measured in one process against
+# one meeting per step with four sets (us per step): the tiny workload 26.7
+# -> 23.9 at groups of 8, the word step 109.9 -> 103.8, the 2M vocabulary
+# 972 -> 965, the merge 1,472 -> 1,466; the char workload, on its CU split,
+# 1,441 -> 1,434 at groups of 2 (1,439 at 8).
+OVERLAP_GROUP_DEFAULT = 8
+OVERLAP_GROUP = {"char_heavy_1m": 2}
 
 
 # The overlapped schedule's CU split, per workload: the Unique calls run on
@@ -584,10 +615,11 @@ def run_gpu(w, steps, warmup, nbatch, torch, lz, host):
         ev.close()
         pipe.fused = True
     # Pass 3, the headline: the same K steps with the Unique calls on a
-    # second stream (default priority, like the first), running ahead; at the
-    # workloads of SIDE_CUS with the two streams on disjoint CUs (and, for
-    # comparison, both on every CU).
+    # second stream (default priority, like the first), running ahead in
+    # groups of steps; at the workloads of SIDE_CUS with the two streams on
+    # disjoint CUs (and, for comparison, both on every CU).
     pipe.enable_overlap()
+    group = len(pipe.sets) // 2
     overlap_ms = overlap_all_ms = run_overlap_pass(pipe, steps, warmup, torch, stream,
                                                    side_stream(torch, dev))
     side_cus = SIDE_CUS.get(w.name)
@@ -631,7 +663,7 @@ def run_gpu(w, steps, warmup, nbatch, torch, lz, host):
                        ms_per_step=unfused["serial_ms"] / steps,
                        value=K / (unfused["serial_ms"] / steps / 1e3))
     return dict(total_ms=total_ms, overlap_ms=overlap_ms, overlap_all_ms=overlap_all_ms,
-                side_cus=side_cus, stage_ms=st.mean(axis=0).tolist(), seg_ms=seg_ms,
+                side_cus=side_cus, group=group, stage_ms=st.mean(axis=0).tolist(), seg_ms=seg_ms,
                 seg_bytes=float(seg_bytes), uniq_bytes=uniq_bytes, after_bytes=after_bytes,
                 U=U_of, outputs=outputs, fused=fused, unfused=unfused)
 
@@ -845,7 +877,9 @@ def measure(w, args, torch, lz, cpu_budget):
 
 def schedule_text(r):
     """The overlapped schedule the headline figure was measured with."""
-    t = "unique on a second stream, up to 3 steps ahead (4 sets of its outputs)"
+    g = r["group"]
+    t = (f"unique on a second stream, in groups of {g} steps ({2 * g} sets of its outputs): "
+         f"the streams meet once per group, the second up to {2 * g - 1} steps ahead")
     n = r["side_cus"]
     if n:
         t += f"; the second stream on CUs 0-{n - 1}, the first on the others (CU-masked streams)"

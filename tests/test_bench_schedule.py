@@ -1,9 +1,9 @@
 """Host logic of bench.py's overlapped schedule, on the CPU: the Unique calls
 of later steps run on a second stream while earlier steps' Seg-Sum and update
-run on the first, with several sets of Unique outputs. A recording stand-in
-for the streams and events checks that every ordering the events allow keeps
-each step on its own set and never lets a Unique overwrite a set that an
-earlier step still reads."""
+run on the first, in groups of steps over two halves of the sets of Unique
+outputs. A recording stand-in for the streams and events checks that every
+ordering the events allow keeps each step on its own set and never lets a
+Unique overwrite a set that an earlier step still reads."""
 import os
 import sys
 
@@ -71,7 +71,8 @@ def _earliest_times(ops):
     return t
 
 
-@pytest.mark.parametrize("nsets,steps", [(2, 1), (2, 7), (3, 2), (4, 3), (4, 7), (4, 200)])
+@pytest.mark.parametrize("nsets,steps", [(2, 1), (2, 7), (4, 2), (4, 3), (4, 7), (4, 200),
+                                         (6, 7), (16, 5), (16, 37), (16, 200)])
 def test_overlapped_schedule_orders_the_streams(nsets, steps):
     ops = _schedule(nsets, steps, first=5)
     fronts = [op for op in ops["side"] if op[0] == "front"]
@@ -95,13 +96,34 @@ def test_overlapped_schedule_orders_the_streams(nsets, steps):
 
 
 def test_overlapped_schedule_lets_unique_run_ahead():
-    """With four sets the side stream is not held back by the main one until
-    it is three steps ahead."""
+    """With groups of two steps (four sets) the side stream runs group 1's
+    Unique calls before it first waits for the main one, and then waits
+    once per group, for the group two before."""
     ops = _schedule(4, 8)
     side_waits = [op for op in ops["side"] if op[0] == "wait"]
-    # one wait for the start event, then one per step from step 4 on
-    assert side_waits[0][:2] == ("wait", 0) and len(side_waits) == 1 + (8 - 4)
+    # the start event, then one wait before each of groups 2 and 3
+    assert [op[1] for op in side_waits] == [0, 2, 4]
     assert ops["side"].index(("front", 3, 3)) < ops["side"].index(side_waits[1])
+    assert ops["side"].index(side_waits[1]) < ops["side"].index(("front", 4, 0))
+
+
+@pytest.mark.parametrize("nsets,steps", [(4, 8), (16, 37), (16, 8), (2, 5)])
+def test_overlapped_schedule_meets_once_per_group(nsets, steps):
+    """The main stream waits once per group of nsets / 2 steps (the last
+    group may be short), and never between two steps of one group."""
+    G = nsets // 2
+    ops = _schedule(nsets, steps)
+    main = ops["main"]
+    waits = [k for k, op in enumerate(main) if op[0] == "wait"]
+    assert len(waits) == (steps + G - 1) // G
+    for k in waits:
+        nxt = next(op for op in main[k + 1:] if op[0] == "back")
+        assert nxt[1] % G == 0  # a group's first step follows each wait
+
+
+def test_overlapped_schedule_rejects_odd_sets():
+    with pytest.raises(ValueError):
+        _schedule(3, 4)
 
 
 def test_cu_mask_words():

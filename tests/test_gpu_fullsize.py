@@ -310,10 +310,10 @@ def _final_state(pipe, ures):
 @pytest.mark.parametrize("name", ["word_step_64k", "sampled_softmax_64x1024_G", "merge_8x32k_bf16"])
 def test_overlapped_schedule_matches_serial(lz, name):
     """bench.py's overlapped schedule (the Unique calls on a second stream,
-    up to three steps ahead, with four sets of their outputs) leaves the
+    here in groups of two steps over four sets of their outputs) leaves the
     same result, bit for bit, as the serial steps: every Seg-Sum reads the
     Unique of its own batch and no Unique overwrites a set still in use.
-    Seven steps wrap around the four sets. The sampled-softmax case also
+    Seven steps wrap around the four sets, the last group a short one. The sampled-softmax case also
     draws its candidate ids on the second stream; the merge runs two Unique
     calls per step (the merged list and shard 0's own)."""
     import bench
@@ -330,7 +330,7 @@ def test_overlapped_schedule_matches_serial(lz, name):
     serial.check()
     want = _final_state(serial, serial.ures)
     pipe = bench.Pipeline(w, batches, torch, lz, dev, table=table0)
-    pipe.enable_overlap()
+    pipe.enable_overlap(group=2)
     main, side = torch.cuda.current_stream(), torch.cuda.Stream(device=dev)
     sync = bench.HipEvents(2 * steps + 2, timing=False)
     pipe.run_overlapped(0, steps, torch, main, side, sync)
