@@ -31,9 +31,10 @@
 //               look-back over the ids in ascending order give uniq, counts,
 //               offsets, num_unique and each id's type (its rank among the
 //               ids present); also the digit counts of the radix passes.
-//   k_onesweep  the passes as above; the first one, which reads the ids in
-//               token order, also writes inverse[token] = rank[id], and the
-//               last writes the permutation.
+//   k_onesweep  the passes as above (8 keys per thread from 512K ids on);
+//               the first one, which reads the ids in token order, also
+//               writes inverse[token] = rank[id], and the last writes the
+//               permutation only (no sorted keys).
 // Tiles take their index from an atomic ticket, so a tile only waits on
 // tiles that already hold a workgroup: every look-back makes progress. A
 // tile's inputs are fetched for tile = blockIdx.x while the ticket is in
@@ -225,6 +226,16 @@ static UniqueLayout unique_layout(int64_t K, int idtype, int64_t V) {
   L.hist_blocks = hist_blocks_for(K);
   if (L.gather) L.hist_blocks = L.tiles;  // one row of runs per pass and tile
   L.keycount = !L.block_items && !L.gather && V <= LMZ_UNIQUE_KEYCOUNT_MAX_V;
+  // With the counts per id, tiles of 8 keys per thread from 512K ids on.
+  // Alone the call times the same as with 4 (1,048,576 ids over 20K words:
+  // 54.7 against 53.9 us), but beside the Seg-Sum walk (Unique on CUs of
+  // its own) the sort passes' scattered digit runs slow the walk, and tiles
+  // twice as large write half as many runs and pass half as many tiles in
+  // the look-back: 1,434 -> 1,426 us per overlapped step at that workload.
+  if (L.keycount && L.nt == 1024 && L.items == 4) {
+    L.items = 8;
+    L.tiles = static_cast<int>((K + int64_t(L.nt) * L.items - 1) / (int64_t(L.nt) * L.items));
+  }
   if (L.keycount) {
     L.key_blocks = L.hist_blocks;
     L.scan_tiles = static_cast<int>((V + kKeyScanThreads - 1) / kKeyScanThreads);
@@ -927,7 +938,7 @@ __global__ __launch_bounds__(NT) void k_onesweep(
       // Only a look-back that gave up (LM_DEVERR_SPIN) leaves gp out of
       // range; never write outside the buffers.
       if (static_cast<uint32_t>(gp) < static_cast<uint32_t>(K)) {
-        keys_out[gp] = k;
+        if (keys_out) keys_out[gp] = k;
         vals_out[gp] = s_vals[jj];
       }
     }
@@ -1833,7 +1844,9 @@ static int run_unique(const KeyT* ids, int K, int64_t V, KeyT* uniq, int32_t* co
   const KeyT* kin = ids;
   const int32_t* vin = nullptr;
   for (int p = 0; p < L.passes; ++p) {
-    KeyT* kout = kb[p & 1];
+    // The last pass with the counts per id writes the permutation only: the
+    // types came from the counts, so nothing reads its sorted keys.
+    KeyT* kout = L.keycount && p == L.passes - 1 ? nullptr : kb[p & 1];
     int32_t* vout = p == L.passes - 1 ? perm : vb[p & 1];
     // The narrowest compiled digit that holds this pass's bits.
     const bool narrow = L.nbits[p] <= kSmallDigitBits;
