@@ -78,6 +78,19 @@ constexpr int kBlockThreadsHost = 1024;  // threads of k_unique_block
 #ifndef LMZ_UNIQUE_KEYCOUNT_MAX_V
 #define LMZ_UNIQUE_KEYCOUNT_MAX_V (1 << 15)  // up to this V (and past one workgroup), counts per id
 #endif
+// From this many ids on (and vocabularies of up to LMZ_UNIQUE_TYPEMAP_MAX_V
+// ids), the dedup writes each type once to a table indexed by id, and a
+// pass in token order writes the inverse map from it, instead of scattering
+// one 4-byte store per token to the tokens' positions. Above the largest K
+// of lm_unique_noalloc, whose fixed scratch does not hold the table.
+#ifndef LMZ_UNIQUE_TYPEMAP_MIN_K
+#define LMZ_UNIQUE_TYPEMAP_MIN_K (1 << 19)
+#endif
+#ifndef LMZ_UNIQUE_TYPEMAP_MAX_V
+#define LMZ_UNIQUE_TYPEMAP_MAX_V (int64_t(1) << 24)
+#endif
+static_assert(LMZ_UNIQUE_TYPEMAP_MIN_K > LM_UNIQUE_NOALLOC_MAX_K,
+              "the type table would not fit lm_unique_noalloc's scratch");
 #ifndef LMZ_UNIQUE_LOOKBACK_W
 #define LMZ_UNIQUE_LOOKBACK_W 4        // predecessor tiles a look-back round reads
 #endif
@@ -142,6 +155,8 @@ struct UniqueLayout {
                     // histogram region then holds the runs of each pass and tile
   int keycount;     // 1: a count per id (k_key_hist, k_key_scan) instead of k_hist
                     // and k_dedup; bhist then holds a row per k_key_scan tile
+  int typemap;      // 1: the dedup writes each id's type to a table (rank) and
+                    // k_inverse_types writes the inverse map in token order
   int key_blocks;   // k_key_hist workgroups (rows of khist)
   int scan_tiles;   // k_key_scan workgroups, kKeyScanThreads ids each
   size_t khist, rank;
@@ -232,6 +247,8 @@ static UniqueLayout unique_layout(int64_t K, int idtype, int64_t V) {
   // its own) the sort passes' scattered digit runs slow the walk, and tiles
   // twice as large write half as many runs and pass half as many tiles in
   // the look-back: 1,434 -> 1,426 us per overlapped step at that workload.
+  L.typemap = !L.block_items && !L.gather && !L.keycount && K >= LMZ_UNIQUE_TYPEMAP_MIN_K &&
+              V <= LMZ_UNIQUE_TYPEMAP_MAX_V;
   if (L.keycount && L.nt == 1024 && L.items == 4) {
     L.items = 8;
     L.tiles = static_cast<int>((K + int64_t(L.nt) * L.items - 1) / (int64_t(L.nt) * L.items));
@@ -257,6 +274,8 @@ static UniqueLayout unique_layout(int64_t K, int idtype, int64_t V) {
   L.vals1 = off;   off += align256(size_t(K) * 4);
   if (L.keycount) {
     L.khist = off; off += align256(size_t(L.key_blocks) * V * 4);
+  }
+  if (L.keycount || L.typemap) {
     L.rank = off;  off += align256(size_t(V) * 4);
   }
   L.total = off;
@@ -1268,7 +1287,7 @@ __global__ __launch_bounds__(NT) void k_dedup(
     int32_t* __restrict__ inverse, int64_t* __restrict__ num_unique,
     uint64_t* __restrict__ status, uint32_t* __restrict__ ticket, int32_t* __restrict__ dev_err,
     WaitCfg wc, const uint32_t* __restrict__ runs, int runs_nbits, int rstride,
-    int32_t* __restrict__ perm_out) {
+    int32_t* __restrict__ perm_out, int32_t* __restrict__ type_of_id, uint64_t n_ids) {
   constexpr int kWaves = NT / kWave;
   constexpr int kItems = ITEMS;
   constexpr int kTile = NT * kItems;
@@ -1439,8 +1458,9 @@ __global__ __launch_bounds__(NT) void k_dedup(
         offsets[seg] = static_cast<int32_t>(p);
       }
       if (((tmask >> i) & 1u) && in_cap) counts[seg] = static_cast<int32_t>(p + 1 - hp);
-      if (static_cast<uint32_t>(src[i]) < static_cast<uint32_t>(K)) inverse[src[i]] = seg;
-      else over = true;
+      if (static_cast<uint32_t>(src[i]) >= static_cast<uint32_t>(K)) over = true;
+      else if (!type_of_id) inverse[src[i]] = seg;
+      else if (head && in_cap && key_bits(k[i]) < n_ids) type_of_id[key_bits(k[i])] = seg;
       if constexpr (GATHER) perm_out[p] = src[i];
       if (p == K - 1) {
         *num_unique = seg + 1 < cap ? seg + 1 : cap;
@@ -1716,6 +1736,40 @@ size_t unique_workspace_bytes(int64_t K, int idtype, int64_t V) {
   return unique_layout(K, idtype, V).total;
 }
 
+// k_inverse_types: inverse[i] = type_of_id[ids[i]] in token order (after a
+// dedup that wrote each id's type to type_of_id). Four ids per thread per
+// round, with 16-byte loads and stores where ids and inverse are 16-byte
+// aligned; ids outside [0, n_ids) (an error already raised by the
+// histogram) read no table entry.
+constexpr int kInvThreads = 256;
+constexpr int kInvItems = 4;
+constexpr int kInvMaxBlocks = 2048;
+template <typename KeyT, bool VEC>
+__global__ __launch_bounds__(kInvThreads) void k_inverse_types(
+    const KeyT* __restrict__ ids, int K, uint64_t n_ids, const int32_t* __restrict__ type_of_id,
+    int32_t* __restrict__ inverse) {
+  const int64_t stride = int64_t(gridDim.x) * kInvThreads * kInvItems;
+  for (int64_t i0 = (int64_t(blockIdx.x) * kInvThreads + threadIdx.x) * kInvItems; i0 < K;
+       i0 += stride) {
+    if (VEC && i0 + kInvItems <= K) {
+      KeyT k[kInvItems];
+      load_run<KeyT, kInvItems>(ids + i0, k);
+      int32_t t[kInvItems];
+#pragma unroll
+      for (int j = 0; j < kInvItems; ++j) {
+        const uint64_t kb = key_bits(k[j]);
+        t[j] = kb < n_ids ? type_of_id[kb] : 0;
+      }
+      *reinterpret_cast<int4*>(inverse + i0) = make_int4(t[0], t[1], t[2], t[3]);
+    } else {
+      for (int j = 0; j < kInvItems && i0 + j < K; ++j) {
+        const uint64_t kb = key_bits(ids[i0 + j]);
+        inverse[i0 + j] = kb < n_ids ? type_of_id[kb] : 0;
+      }
+    }
+  }
+}
+
 template <typename KeyT, int RB, int NT, int ITEMS>
 static hipError_t launch_pass(const UniqueLayout& L, int p, const KeyT* kin, const int32_t* vin,
                               KeyT* kout, int32_t* vout, int K, uint32_t* bhist,
@@ -1811,7 +1865,7 @@ static int run_unique(const KeyT* ids, int K, int64_t V, KeyT* uniq, int32_t* co
       k_dedup<KeyT, kNT, kIT, false, true><<<L.tiles, kNT, 0, st>>>(
           kb[q & 1], vb[q & 1], K, cap, uniq, counts, offsets, inverse, num_unique, dstatus,
           tickets + kMaxPasses, dev_err, wait_cfg(), bhist + size_t(q) * L.tiles * L.rstride,
-          L.nbits[q], L.rstride, perm);
+          L.nbits[q], L.rstride, perm, nullptr, 0);
       return hipGetLastError();
     };
     return launch_status(L.nt == 256 ? passes(I<256>{}) : passes(I<1024>{}));
@@ -1876,16 +1930,19 @@ static int run_unique(const KeyT* ids, int K, int64_t V, KeyT* uniq, int32_t* co
   if (L.keycount)  // the scan wrote the types, the first pass the inverse map
     return launch_status(hipGetLastError());
   const bool perm_runs = (reinterpret_cast<uintptr_t>(perm) & 15) == 0;
+  int32_t* tmap = L.typemap ? reinterpret_cast<int32_t*>(ws + L.rank) : nullptr;
   auto dedup = [&](auto nt, auto items) {
     constexpr int NT = decltype(nt)::value, IT = decltype(items)::value;
     if (perm_runs)
       k_dedup<KeyT, NT, IT, true, false><<<L.tiles, NT, 0, st>>>(
           kin, perm, K, cap, uniq, counts, offsets, inverse, num_unique, dstatus,
-          tickets + kMaxPasses, dev_err, wait_cfg(), nullptr, 0, 0, nullptr);
+          tickets + kMaxPasses, dev_err, wait_cfg(), nullptr, 0, 0, nullptr, tmap,
+          static_cast<uint64_t>(V));
     else
       k_dedup<KeyT, NT, IT, false, false><<<L.tiles, NT, 0, st>>>(
           kin, perm, K, cap, uniq, counts, offsets, inverse, num_unique, dstatus,
-          tickets + kMaxPasses, dev_err, wait_cfg(), nullptr, 0, 0, nullptr);
+          tickets + kMaxPasses, dev_err, wait_cfg(), nullptr, 0, 0, nullptr, tmap,
+          static_cast<uint64_t>(V));
   };
   if (L.nt == 256) {
     if (L.items == 2) dedup(I<256>{}, I<2>{});
@@ -1894,6 +1951,19 @@ static int run_unique(const KeyT* ids, int K, int64_t V, KeyT* uniq, int32_t* co
     if (L.items == 2) dedup(I<1024>{}, I<2>{});
     else if (L.items == 4) dedup(I<1024>{}, I<4>{});
     else dedup(I<1024>{}, I<8>{});
+  }
+  if (tmap) {
+    if (hipError_t e = hipGetLastError(); e != hipSuccess) return launch_status(e);
+    const int64_t per_block = int64_t(kInvThreads) * kInvItems;
+    int64_t blocks = (K + per_block - 1) / per_block;
+    if (blocks > kInvMaxBlocks) blocks = kInvMaxBlocks;
+    const bool vec = ((reinterpret_cast<uintptr_t>(ids) | reinterpret_cast<uintptr_t>(inverse)) & 15) == 0;
+    if (vec)
+      k_inverse_types<KeyT, true><<<static_cast<int>(blocks), kInvThreads, 0, st>>>(
+          ids, K, static_cast<uint64_t>(V), tmap, inverse);
+    else
+      k_inverse_types<KeyT, false><<<static_cast<int>(blocks), kInvThreads, 0, st>>>(
+          ids, K, static_cast<uint64_t>(V), tmap, inverse);
   }
   return launch_status(hipGetLastError());
 }

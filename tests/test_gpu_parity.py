@@ -130,6 +130,15 @@ UNIQUE_CASES = [
     (1_048_579, 32_768, 1.0, np.int64, 54), (600_001, 1, 1.0, np.int32, 55),
     (300_000, 5, 1.0, np.int32, 56), (262_145, 32_767, 0.0, np.int32, 57),
     (16_385, 1_000, 1.0, np.int32, 58), (9_000, 32_768, 1.0, np.int64, 59),
+    # From 524,288 ids on, vocabularies of up to 2^24 ids past the counts per
+    # id: the dedup writes each type to a table indexed by id, and the
+    # inverse map is written in token order from it. 20-bit keys at 4 keys
+    # per thread, the first K to take it (21-bit int64 keys), the last K
+    # before it (the dedup's scatter of the inverse map), the largest
+    # vocabulary to take it (a 64 MiB table) and the first above it.
+    (600_000, 800_000, 1.0, np.int32, 60), (524_288, 2_000_000, 0.9, np.int64, 61),
+    (524_287, 800_000, 1.0, np.int32, 62), (600_000, 1 << 24, 1.0, np.int32, 63),
+    (600_000, (1 << 24) + 1, 1.0, np.int64, 64),
 ]
 
 
@@ -180,29 +189,34 @@ def test_unique_out_of_range_sets_error(lz):
     assert int(res.dev_err.item()) & lz.DEVERR_ID_RANGE
 
 
-@pytest.mark.parametrize("K", [12_000, 70_000, 300_000])
-def test_unique_out_of_range_sets_error_multi_tile(lz, K):
+@pytest.mark.parametrize("K,V", [(12_000, 1000), (70_000, 1000), (300_000, 1000),
+                                 (600_000, 800_000)])
+def test_unique_out_of_range_sets_error_multi_tile(lz, K, V):
     # 256-thread tiles, tile-local passes, 1024-thread look-back passes (the
-    # first and the last with counts per id, V = 1000): one id past V in the
-    # last tile, one negative id in the first
-    ids = synth.zipf_ids(K, 1000, 1.0, 62, np.int32)
-    ids[K - 1] = 1000
-    res = lz.unique(_t(ids), 1000)
+    # first and the last with counts per id, V = 1000; the last V = 800,000
+    # with the type table): one id past V in the last tile, one negative id
+    # in the first
+    ids = synth.zipf_ids(K, V, 1.0, 62, np.int32)
+    ids[K - 1] = V
+    res = lz.unique(_t(ids), V)
     ids2 = ids.copy()
     ids2[K - 1] = 7
     ids2[3] = -1
-    res2 = lz.unique(_t(ids2), 1000)
+    res2 = lz.unique(_t(ids2), V)
     torch.cuda.synchronize()
     assert int(res.dev_err.item()) & lz.DEVERR_ID_RANGE
     assert int(res2.dev_err.item()) & lz.DEVERR_ID_RANGE
 
 
 @pytest.mark.parametrize("K,V,dt", [(70_000, 800_000, np.int32), (9000, 100_000, np.int64),
-                                     (5000, 100_000, np.int32)])
+                                     (5000, 100_000, np.int32), (600_001, 800_000, np.int32),
+                                     (600_001, 2_000_000, np.int64)])
 def test_unique_outputs_not_16_byte_aligned(lz, K, V, dt):
     """Output buffers that start one element into their allocation (4- or
     8-byte aligned, not 16): the dedup then reads the permutation with
-    scalar loads, and every output lands where the caller asked."""
+    scalar loads, the inverse map from the type table (600,001 ids) is
+    written with scalar stores, and every output lands where the caller
+    asked."""
     ids = synth.zipf_ids(K, V, 1.0, 61, dt)
     tdt = torch.int64 if dt == np.int64 else torch.int32
     cap = min(K, V)
