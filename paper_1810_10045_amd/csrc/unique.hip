@@ -22,7 +22,10 @@
 //               each), a block scan plus a wave-wide decoupled look-back (64
 //               predecessors per round) carrying (number of heads, position of
 //               the last head), then writes uniq, offsets, counts, inverse and
-//               num_unique.
+//               num_unique. From LMZ_UNIQUE_TYPEMAP_MIN_K ids on (vocabularies
+//               of up to LMZ_UNIQUE_TYPEMAP_MAX_V ids) it writes each type to
+//               a table indexed by id instead of the inverse map, and
+//   k_inverse_types  writes inverse[token] = table[ids[token]] in token order.
 // Where the ids are narrower (V <= LMZ_UNIQUE_KEYCOUNT_MAX_V), the types
 // come from a count per id instead of the sorted keys, and no dedup runs:
 //   k_key_hist  the count of every id value in LDS, one row per workgroup;
