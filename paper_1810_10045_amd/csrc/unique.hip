@@ -250,12 +250,12 @@ static UniqueLayout unique_layout(int64_t K, int idtype, int64_t V) {
   // its own) the sort passes' scattered digit runs slow the walk, and tiles
   // twice as large write half as many runs and pass half as many tiles in
   // the look-back: 1,434 -> 1,426 us per overlapped step at that workload.
-  L.typemap = !L.block_items && !L.gather && !L.keycount && K >= LMZ_UNIQUE_TYPEMAP_MIN_K &&
-              V <= LMZ_UNIQUE_TYPEMAP_MAX_V;
   if (L.keycount && L.nt == 1024 && L.items == 4) {
     L.items = 8;
     L.tiles = static_cast<int>((K + int64_t(L.nt) * L.items - 1) / (int64_t(L.nt) * L.items));
   }
+  L.typemap = !L.block_items && !L.gather && !L.keycount && K >= LMZ_UNIQUE_TYPEMAP_MIN_K &&
+              V <= LMZ_UNIQUE_TYPEMAP_MAX_V;
   if (L.keycount) {
     L.key_blocks = L.hist_blocks;
     L.scan_tiles = static_cast<int>((V + kKeyScanThreads - 1) / kKeyScanThreads);
