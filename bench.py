@@ -14,10 +14,10 @@ gradients (8 GiB per batch), the U reduced rows written into the dense
 through resident batches (at least 2 GiB of gradients in all) so that the
 gradient rows are not served from the 256 MB Infinity Cache.
 
-The headline runs the Unique calls on a second stream, up to three steps
-ahead of Seg-Sum and the update (Unique reads only the token ids, which a
-trainer has before the gradients exist); every step still does all of its
-work. At the char-LM workload the two streams run on disjoint CUs
+The headline runs the Unique calls on a second stream, ahead of Seg-Sum and
+the update (Unique reads only the token ids, which a trainer has before the
+gradients exist), in groups of steps so that the two streams meet once per
+group (OVERLAP_GROUP); every step still does all of its work. At the char-LM workload the two streams run on disjoint CUs
 (CU-masked streams, SIDE_CUS); the same schedule on shared CUs is printed
 beside it (`overlapped_all_cus`). The serial schedule (one stream) is timed too and printed beside it,
 and for the SCATTER, SGD and Adam workloads also the serial schedule with
