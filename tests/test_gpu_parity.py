@@ -135,8 +135,10 @@ UNIQUE_CASES = [
     # inverse map is written in token order from it. 20-bit keys at 4 keys
     # per thread, the first K to take it (21-bit int64 keys), the last K
     # before it (the dedup's scatter of the inverse map), the largest
-    # vocabulary to take it (a 64 MiB table) and the first above it.
+    # vocabulary to take it (a 64 MiB table) and the first above it; 600,003
+    # ids write the inverse map in 16-byte stores with a scalar tail.
     (600_000, 800_000, 1.0, np.int32, 60), (524_288, 2_000_000, 0.9, np.int64, 61),
+    (600_003, 800_000, 1.0, np.int32, 65),
     (524_287, 800_000, 1.0, np.int32, 62), (600_000, 1 << 24, 1.0, np.int32, 63),
     (600_000, (1 << 24) + 1, 1.0, np.int64, 64),
 ]
