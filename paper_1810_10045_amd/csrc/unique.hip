@@ -37,7 +37,9 @@
 //   k_onesweep  the passes as above (8 keys per thread from 512K ids on);
 //               the first one, which reads the ids in token order, also
 //               writes inverse[token] = rank[id], and the last writes the
-//               permutation only (no sorted keys).
+//               permutation only (no sorted keys). With two passes over
+//               4-byte ids the first writes one word per key, the second
+//               pass's digit above the position, which the second reads.
 // Tiles take their index from an atomic ticket, so a tile only waits on
 // tiles that already hold a workgroup: every look-back makes progress. A
 // tile's inputs are fetched for tile = blockIdx.x while the ticket is in
@@ -293,6 +295,17 @@ using I = std::integral_constant<int, N>;
 struct WaitCfg {
   uint32_t spin_limit;
   int force_fail;
+};
+// Two-pass sorts with the counts per id and 4-byte ids: the first pass
+// writes, for each key, one word holding the second pass's digit above the
+// token's position (mode 1), and the second pass reads that word as its key
+// and the position from its low pos_bits bits (mode 2). That halves the
+// first pass's scattered writes and the second pass's reads.
+struct PackCfg {
+  int mode;      // 0: keys and positions apart; 1: write packed words; 2: read them
+  int shift;     // mode 1: the second pass's digit within the key
+  int nbits;     //         and its width
+  int pos_bits;  // bits of the position in a packed word
 };
 static std::atomic<bool> g_force_wait_failure{false};
 static std::atomic<uint32_t> g_forced_spin_limit{kSpinLimit};
@@ -724,7 +737,7 @@ __global__ __launch_bounds__(NT) void k_onesweep(
     const uint32_t* __restrict__ bhist, int hist_blocks, int hist_stride,
     uint32_t* __restrict__ status, uint32_t* __restrict__ ticket, int32_t* __restrict__ dev_err,
     WaitCfg wc, const int32_t* __restrict__ type_of_id, uint32_t n_ids,
-    int32_t* __restrict__ inverse) {
+    int32_t* __restrict__ inverse, PackCfg pk) {
   constexpr int kWaves = NT / kWave;
   constexpr int kItems = ITEMS;
   constexpr int kTile = NT * kItems;
@@ -757,6 +770,11 @@ __global__ __launch_bounds__(NT) void k_onesweep(
       const bool ok = pos < K;
       key[i] = ok ? keys_in[pos] : KeyT(0);
       val[i] = ok ? (vals_in ? vals_in[pos] : static_cast<int32_t>(pos)) : 0;
+    }
+    if (pk.mode == 2) {  // the position is the packed word's low bits
+      const uint32_t pm = (1u << pk.pos_bits) - 1u;
+#pragma unroll
+      for (int i = 0; i < kItems; ++i) val[i] = static_cast<int32_t>(static_cast<uint32_t>(key_bits(key[i])) & pm);
     }
   };
   fetch(int64_t(blockIdx.x) * kTile);
@@ -961,7 +979,11 @@ __global__ __launch_bounds__(NT) void k_onesweep(
       // range; never write outside the buffers.
       if (static_cast<uint32_t>(gp) < static_cast<uint32_t>(K)) {
         if (keys_out) keys_out[gp] = k;
-        vals_out[gp] = s_vals[jj];
+        int32_t v = s_vals[jj];
+        if (pk.mode == 1)
+          v = static_cast<int32_t>((digit_of(k, pk.shift, (1u << pk.nbits) - 1) << pk.pos_bits) |
+                                   static_cast<uint32_t>(v));
+        vals_out[gp] = v;
       }
     }
   }
@@ -1778,11 +1800,11 @@ static hipError_t launch_pass(const UniqueLayout& L, int p, const KeyT* kin, con
                               KeyT* kout, int32_t* vout, int K, uint32_t* bhist,
                               uint32_t* status, uint32_t* tickets, int32_t* dev_err,
                               const int32_t* type_of_id, uint32_t n_ids, int32_t* inverse,
-                              hipStream_t st) {
+                              int shift, PackCfg pk, hipStream_t st) {
   k_onesweep<KeyT, RB, NT, ITEMS><<<L.tiles, NT, 0, st>>>(
-      kin, vin, kout, vout, K, L.shift[p], L.nbits[p], bhist + size_t(p) * L.rstride,
+      kin, vin, kout, vout, K, shift, L.nbits[p], bhist + size_t(p) * L.rstride,
       L.hist_blocks, L.passes * L.rstride, status + size_t(p) * L.tiles * L.rstride, tickets + p,
-      dev_err, wait_cfg(), type_of_id, n_ids, inverse);
+      dev_err, wait_cfg(), type_of_id, n_ids, inverse, pk);
   return hipGetLastError();
 }
 
@@ -1900,18 +1922,30 @@ static int run_unique(const KeyT* ids, int K, int64_t V, KeyT* uniq, int32_t* co
 
   const KeyT* kin = ids;
   const int32_t* vin = nullptr;
+  // Counts per id, two passes and 4-byte ids: the first pass writes the
+  // second pass's digit and the position as one word (PackCfg).
+  const int pos_bits = L.passes == 2 ? 32 - L.nbits[1] : 0;
+  const bool packed = L.keycount && L.passes == 2 && sizeof(KeyT) == 4 && pos_bits < 32 &&
+                      int64_t(K) <= (int64_t(1) << pos_bits);
   for (int p = 0; p < L.passes; ++p) {
     // The last pass with the counts per id writes the permutation only: the
     // types came from the counts, so nothing reads its sorted keys.
-    KeyT* kout = L.keycount && p == L.passes - 1 ? nullptr : kb[p & 1];
+    KeyT* kout = (L.keycount && p == L.passes - 1) || (packed && p == 0) ? nullptr : kb[p & 1];
     int32_t* vout = p == L.passes - 1 ? perm : vb[p & 1];
+    int shift = L.shift[p];
+    PackCfg pk{0, 0, 0, 0};
+    if (packed) {
+      pk = p == 0 ? PackCfg{1, L.shift[1], L.nbits[1], pos_bits} : PackCfg{2, 0, 0, pos_bits};
+      if (p == 1) shift = pos_bits;  // the digit sits above the position
+    }
     // The narrowest compiled digit that holds this pass's bits.
     const bool narrow = L.nbits[p] <= kSmallDigitBits;
     const bool first = p == 0 && type_of_id;
     auto pass = [&](auto rb, auto nt, auto items) {
       return launch_pass<KeyT, decltype(rb)::value, decltype(nt)::value, decltype(items)::value>(
           L, p, kin, vin, kout, vout, K, bhist, status, tickets, dev_err,
-          first ? type_of_id : nullptr, static_cast<uint32_t>(V), first ? inverse : nullptr, st);
+          first ? type_of_id : nullptr, static_cast<uint32_t>(V), first ? inverse : nullptr,
+          shift, pk, st);
     };
     auto by_items = [&](auto rb, auto nt) {
       if constexpr (decltype(nt)::value == 256)
@@ -1927,8 +1961,8 @@ static int run_unique(const KeyT* ids, int K, int64_t V, KeyT* uniq, int32_t* co
       e = narrow ? by_items(I<kSmallDigitBits>{}, I<1024>{})
                  : by_items(I<kLargeDigitBits>{}, I<1024>{});
     if (e != hipSuccess) return launch_status(e);
-    kin = kout;
-    vin = vout;
+    kin = packed && p == 0 ? reinterpret_cast<const KeyT*>(vout) : kout;  // the packed words
+    vin = packed && p == 0 ? nullptr : vout;
   }
   if (L.keycount)  // the scan wrote the types, the first pass the inverse map
     return launch_status(hipGetLastError());
