@@ -130,6 +130,9 @@ UNIQUE_CASES = [
     (1_048_579, 32_768, 1.0, np.int64, 54), (600_001, 1, 1.0, np.int32, 55),
     (300_000, 5, 1.0, np.int32, 56), (262_145, 32_767, 0.0, np.int32, 57),
     (16_385, 1_000, 1.0, np.int32, 58), (9_000, 32_768, 1.0, np.int64, 59),
+    # Two passes over int32 ids with the counts per id write the second
+    # pass's digit and the position as one word: on 256-thread tiles too.
+    (12_000, 20_000, 1.2, np.int32, 66), (16_384, 32_768, 1.0, np.int32, 67),
     # From 524,288 ids on, vocabularies of up to 2^24 ids past the counts per
     # id: the dedup writes each type to a table indexed by id, and the
     # inverse map is written in token order from it. 20-bit keys at 4 keys
