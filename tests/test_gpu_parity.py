@@ -195,12 +195,12 @@ def test_unique_out_of_range_sets_error(lz):
 
 
 @pytest.mark.parametrize("K,V", [(12_000, 1000), (70_000, 1000), (300_000, 1000),
-                                 (600_000, 800_000)])
+                                 (300_000, 20_000), (600_000, 800_000)])
 def test_unique_out_of_range_sets_error_multi_tile(lz, K, V):
     # 256-thread tiles, tile-local passes, 1024-thread look-back passes (the
-    # first and the last with counts per id, V = 1000; the last V = 800,000
-    # with the type table): one id past V in the last tile, one negative id
-    # in the first
+    # first and the last with counts per id, V = 1000; V = 20,000 with the
+    # counts per id and the packed two passes; V = 800,000 with the type
+    # table): one id past V in the last tile, one negative id in the first
     ids = synth.zipf_ids(K, V, 1.0, 62, np.int32)
     ids[K - 1] = V
     res = lz.unique(_t(ids), V)
